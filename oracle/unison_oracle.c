@@ -1,0 +1,645 @@
+/*
+ * unison_oracle.c -- TEST INFRASTRUCTURE, not part of the product.
+ *
+ * A plain, slow, single-threaded CPU reference ("the oracle") for the UNISON
+ * residency policy: SPEAR eviction scoring (Sec. III-B), TIDE idle-window
+ * tiering (Sec. III-C), the joint event loop (Algorithm 1), the fixed-point
+ * image of the score (Sec. IV-C) and the ranking-fidelity statistics
+ * (Sec. VI-F).  Only the test-suite, the package smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no source
+ * with the HIP implementation; the two meet only in the binary trace format.
+ *
+ * Every step is written the obvious way: one loop over the events of one
+ * simulation, a full linear scan of the session table for every argmax or
+ * argmin, and the TIDE pass as a literal while-loop.  Nothing is cached,
+ * blocked or reordered.
+ *
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -shared -fPIC
+ * (no FMA contraction, IEEE float division, round-to-nearest-even).
+ *
+ * ---------------------------------------------------------------------------
+ * Readings of points the paper leaves open (both implementations follow them)
+ * ---------------------------------------------------------------------------
+ *  time      Trace times are integer nanoseconds.  The tool gap of eq. (gap)
+ *            is a_{s,k} - c_{s,k-1}: the ARRIVE time minus the time of the
+ *            session's previous GAP_START, both taken from the trace.
+ *  events    ARRIVE (turn k starts; a gap_end when k >= 1), GAP_START (turn
+ *            k ended and another follows) and DONE (the final turn ended).
+ *            The trace fixes their order; the simulator consumes it as given.
+ *  table     A session enters the register file at its first ARRIVE and
+ *            stays while it is not completed or while it still holds KV.
+ *            The per-event scan covers every table entry (the hardware scans
+ *            the whole register file, eq. (scan)).  Victims and migrants are
+ *            the residents that are not being served (an ARRIVE pins its
+ *            session until its GAP_START/DONE).
+ *  EMA       g = 0 and g_q = 0 before the first gap.  Float path, in us:
+ *            x = (float)((double)gap_ns / 1000.0); g = (3x + 7g) / 10 with
+ *            every operation rounded to fp32.  Integer path eq. (gapq) and
+ *            eq. (ema-int): x_q = min(gap_ns / tau, 2^b_g - 1),
+ *            g_q = (3 x_q + 7 g_q) / 10, floors.
+ *  hazard    t is the 0-based index of the session's latest turn.  From a
+ *            population of turn counts T: n(t) = #{T > t}, d(t) = #{T = t+1}
+ *            for t = 0..50; h = 0 where n(t) = 0.  Float LUT: (float)d /
+ *            (float)n.  Fixed LUT eq. (hq): floor(h*Lambda + 1/2) computed
+ *            exactly as (2 d Lambda + n) / (2 n).  eps = 1/100 exactly.
+ *  score     eq. (esp) with S_max = +inf for a completed session; operation
+ *            order sigma = max(0.01f, 1 - h); a = g/sigma; b = 1 - sigma;
+ *            c = b*P; s = a + c.  P is in microseconds.
+ *  keys      "larger key = evict first".  SPEAR: the fp32 score (or the
+ *            fixed-point score).  LRU/timeout: UINT64_MAX - last event time.
+ *            Belady: time of the next ARRIVE (UINT64_MAX once completed).
+ *            Ties in argmax and argmin go to the smallest session id.
+ *  capacity  eq. (cap) in bytes: a session holds len * kv_bytes_per_token.
+ *  placement On ARRIVE the request is classified by the session's tier at
+ *            arrival (SRAM hit, HBM hit, miss).  The session then holds its
+ *            new length; it prefers its current tier on a hit and SRAM on a
+ *            miss, else the other tier.  While it fits neither, the argmax
+ *            victim over all evictable residents is evicted (Alg. 1 evicts
+ *            one victim per violation; the loop repeats it).  A session that
+ *            cannot fit even an empty tier, or finds nothing left to evict,
+ *            is bypassed (served, not retained).
+ *  TIDE      On GAP_START with the DMA engine free, Delta is the session's
+ *            own gap EMA (us, truncated), budget = Delta * B in bytes
+ *            (eq. (budget), eq. (budgetq)).  Loop: p = argmin over evictable
+ *            HBM residents, stop if none or if p is completed.  If p fits in
+ *            free SRAM and in the budget: promote it alone.  Otherwise d =
+ *            argmax over evictable SRAM residents; swap when key(p) < key(d)
+ *            strictly, both fit the budget and eq. (cap) holds after the
+ *            swap.  The first move that is not legal ends the pass.  The DMA
+ *            engine is then busy for ceil(moved * 1000 / B) ns.
+ *  timeout   Before an event is written, every resident that has been idle
+ *            longer than the TTL expires (its timer fired since the last event).
+ *  account   eq. (hr-amat), eq. (prered): SRAM hit amat += len*kvb*t_s,
+ *            ttft += len_prev*kvb*t_s + dlen*t_p, computed += dlen; HBM hit
+ *            likewise with t_h; miss amat += len*t_p, ttft += len*t_p,
+ *            computed += len, extra prefill += len_prev.  f64, event order.
+ *  digest    Each decision (event index, op, sid a, sid b or tier) -- place,
+ *            evict, expire, bypass, promote, swap -- is hashed with the
+ *            SplitMix64 finaliser (Steele, Lea and Flood, 2014) and the
+ *            hashes are summed mod 2^64, so the digest does not depend on
+ *            the order in which one event's decisions are listed.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <time.h>
+
+#define NONE_ID 0xFFFFFFFFu
+#define LUT_LEN 51 /* t = 0..50, eq. (hazard) */
+
+enum { K_ARRIVE = 0, K_GAP_START = 1, K_DONE = 2 };
+enum { P_SPEAR = 0, P_LRU = 1, P_TIMEOUT = 2, P_BELADY = 3 };
+enum { T_NONE = 0, T_SRAM = 1, T_HBM = 2 };
+enum { PH_UNSEEN = 0, PH_SERVING = 1, PH_GAP = 2, PH_DONE = 3 };
+enum { OP_EVICT = 1, OP_EXPIRE = 2, OP_BYPASS = 3, OP_PROMOTE = 4, OP_SWAP = 5, OP_VICTIM = 6,
+       OP_PLACE = 7 };
+
+enum { ORC_OK = 0, ORC_E_INVALID = -1, ORC_E_BAD_TRACE = -2 };
+
+typedef struct {
+  uint32_t policy;      /* P_SPEAR .. P_BELADY */
+  uint32_t tide;        /* 1: run the TIDE pass on GAP_START */
+  uint32_t score_mode;  /* 0: fp32 score, 1: fixed-point score (SPEAR only) */
+  uint32_t lut;         /* index of the hazard count table */
+  uint64_t cap_sram_B;  /* C_S in bytes */
+  uint64_t cap_hbm_B;   /* C_H in bytes */
+  uint64_t n_slots;     /* N_sess */
+  uint64_t dma_B_per_us;/* logical DMA bandwidth B */
+  uint64_t ttl_ns;      /* timeout policy TTL */
+  double t_s_ns_per_B;  /* SRAM read cost */
+  double t_h_ns_per_B;  /* HBM read cost */
+  double t_p_ns_per_tok;/* prefill cost */
+  float penalty_us;     /* P of eq. (esp) */
+  uint32_t b_h;         /* hazard fraction bits */
+  uint32_t b_g;         /* gap register bits */
+  uint32_t pad0;
+  uint64_t tau_ns;      /* gap time divisor */
+  uint64_t p_z;         /* integer penalty P_Z */
+} orc_params;
+
+typedef struct {
+  uint64_t requests, hit_sram, hit_hbm, miss, bypass, evict, expire, promote, swap;
+  uint64_t dma_bytes, tide_passes, tokens_total, tokens_computed, extra_prefill_tok;
+  uint64_t score_evals, resident_evals, digest, victim_digest, events, error;
+  double amat_sum_ns, ttft_sum_ns;
+} orc_counters;
+
+typedef struct {
+  uint32_t ev, op, a, b;
+} orc_rec;
+
+typedef struct {
+  uint64_t used_sram, used_hbm;
+  uint32_t n_res, n_table;
+  uint32_t victim;      /* this event's scan result: argmax evictable key */
+  uint32_t tide_ran;
+  uint64_t tide_budget, tide_moved;
+} orc_state;
+
+/* ---------------------------------------------------------------- helpers */
+
+static uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+  return z ^ (z >> 31);
+}
+
+static uint64_t rec_hash(uint32_t ev, uint32_t op, uint32_t a, uint32_t b) {
+  uint64_t w0 = ((uint64_t)ev << 8) | (uint64_t)op;
+  uint64_t w1 = ((uint64_t)a << 32) | (uint64_t)b;
+  return mix64(w0 ^ mix64(w1));
+}
+
+static uint64_t sat_u64(unsigned __int128 x) {
+  return x > (unsigned __int128)UINT64_MAX ? UINT64_MAX : (uint64_t)x;
+}
+
+/* ---------------------------------------------------- hazard, eq. (hazard) */
+
+void orc_hazard_counts(const uint32_t* T, uint32_t n_sessions, uint32_t* d_out,
+                       uint32_t* n_out) {
+  for (uint32_t t = 0; t < LUT_LEN; t++) {
+    uint32_t d = 0, n = 0;
+    for (uint32_t i = 0; i < n_sessions; i++) {
+      if (T[i] > t) n++;        /* still live at turn t */
+      if (T[i] == t + 1) d++;   /* its last turn is t */
+    }
+    d_out[t] = d;
+    n_out[t] = n;
+  }
+}
+
+/* float hazard h(t) = d(t)/n(t) */
+void orc_lut_f32(const uint32_t* d, const uint32_t* n, float* hf) {
+  for (int t = 0; t < LUT_LEN; t++)
+    hf[t] = n[t] ? (float)d[t] / (float)n[t] : 0.0f;
+}
+
+/* eq. (uq) applied to h = d/n: floor(d/n * Lambda + 1/2), clipped to Lambda. */
+static uint64_t quantize_ratio(uint64_t d, uint64_t n, uint64_t lambda) {
+  if (n == 0) return 0;
+  unsigned __int128 num = (unsigned __int128)2 * d * lambda + n;
+  uint64_t q = (uint64_t)(num / ((unsigned __int128)2 * n));
+  return q > lambda ? lambda : q;
+}
+
+void orc_lut_q(const uint32_t* d, const uint32_t* n, uint32_t b_h, uint64_t* hq) {
+  uint64_t lambda = (1ULL << b_h) - 1;
+  for (int t = 0; t < LUT_LEN; t++) hq[t] = quantize_ratio(d[t], n[t], lambda);
+}
+
+/* ------------------------------------------------------ scores, eq. (esp) */
+
+static float spear_f32(uint32_t turn, float g, int done, const float* hf, float P) {
+  if (done) return INFINITY; /* S_max */
+  uint32_t t = turn < 50 ? turn : 50;
+  float sigma = fmaxf(0.01f, 1.0f - hf[t]); /* eq. (surv) */
+  float a = g / sigma;
+  float b = 1.0f - sigma;
+  float c = b * P;
+  return a + c;
+}
+
+/* eq. (hq), eq. (survq), eq. (t1), eq. (t2), eq. (scoreq) with b_s = 64 */
+static uint64_t spear_fixed(uint32_t turn, uint64_t gq, int done, const uint64_t* hq,
+                            uint32_t b_h, uint64_t p_z) {
+  if (done) return UINT64_MAX; /* 2^b_s - 1 */
+  uint64_t lambda = (1ULL << b_h) - 1;
+  uint32_t t = turn < 50 ? turn : 50;
+  uint64_t eps_q = (lambda + 50) / 100; /* floor(Lambda/100 + 1/2) */
+  uint64_t h = hq[t];
+  uint64_t sigma_q = lambda - h;
+  if (sigma_q < eps_q) sigma_q = eps_q;
+  unsigned __int128 t1 = ((unsigned __int128)gq * lambda) / sigma_q;
+  unsigned __int128 t2 = ((unsigned __int128)(lambda - sigma_q) * p_z) / lambda;
+  return sat_u64(t1 + t2);
+}
+
+void orc_score_f32(uint32_t n, const uint8_t* turn, const float* g, const uint8_t* done,
+                   const float* hf, float P, float* out) {
+  for (uint32_t i = 0; i < n; i++) out[i] = spear_f32(turn[i], g[i], done[i], hf, P);
+}
+
+void orc_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
+                     const uint8_t* done, const uint64_t* hq, uint32_t b_h, uint64_t p_z,
+                     uint64_t* out) {
+  for (uint32_t i = 0; i < n; i++)
+    out[i] = spear_fixed(turn[i], gq[i], done[i], hq, b_h, p_z);
+}
+
+/* ----------------------------------------------------------- EMA updates */
+
+static float ema_f32(float g, uint64_t gap_ns) {
+  float x = (float)((double)gap_ns / 1000.0);
+  float a = 3.0f * x;
+  float b = 7.0f * g;
+  return (a + b) / 10.0f; /* eq. (ema) */
+}
+
+static uint64_t ema_int(uint64_t gq, uint64_t gap_ns, uint32_t b_g, uint64_t tau) {
+  uint64_t cap = b_g >= 64 ? UINT64_MAX : ((1ULL << b_g) - 1);
+  uint64_t x = gap_ns / tau; /* eq. (gapq) */
+  if (x > cap) x = cap;
+  unsigned __int128 s = (unsigned __int128)3 * x + (unsigned __int128)7 * gq;
+  return (uint64_t)(s / 10); /* eq. (ema-int) */
+}
+
+/* Replays a gap history per session through both EMAs. gaps is [n][max_hist]. */
+void orc_ema_replay(uint32_t n, uint32_t max_hist, const uint64_t* gaps_ns,
+                    const uint8_t* n_hist, uint32_t b_g, uint64_t tau, float* g_out,
+                    uint64_t* gq_out) {
+  for (uint32_t i = 0; i < n; i++) {
+    float g = 0.0f;
+    uint64_t gq = 0;
+    for (uint32_t k = 0; k < n_hist[i] && k < max_hist; k++) {
+      g = ema_f32(g, gaps_ns[(uint64_t)i * max_hist + k]);
+      gq = ema_int(gq, gaps_ns[(uint64_t)i * max_hist + k], b_g, tau);
+    }
+    g_out[i] = g;
+    gq_out[i] = gq;
+  }
+}
+
+/* --------------------------------------------- Kendall tau-b pair counts */
+
+/* counts = {concordant, discordant, tied in x only, tied in y only, tied in
+ * both} over all pairs i < j of each snapshot; top1[s] = 1 when the argmax of
+ * x and the argmax of y (ties to the earlier position) coincide.  idx maps
+ * snapshot positions to entries of x and y; NULL means contiguous rows. */
+void orc_kendall(uint32_t n_snap, uint32_t n_per, const float* x, const uint64_t* y,
+                 const uint32_t* idx, uint64_t* counts, uint8_t* top1) {
+  for (uint32_t s = 0; s < n_snap; s++) {
+    uint64_t c = 0, d = 0, tx = 0, ty = 0, txy = 0;
+    uint32_t bx = 0, by = 0;
+    for (uint32_t i = 0; i < n_per; i++) {
+      uint64_t ei = idx ? idx[(uint64_t)s * n_per + i] : (uint64_t)s * n_per + i;
+      float xi = x[ei];
+      uint64_t yi = y[ei];
+      uint64_t eb = idx ? idx[(uint64_t)s * n_per + bx] : (uint64_t)s * n_per + bx;
+      uint64_t ec = idx ? idx[(uint64_t)s * n_per + by] : (uint64_t)s * n_per + by;
+      if (xi > x[eb]) bx = i;
+      if (yi > y[ec]) by = i;
+      for (uint32_t j = i + 1; j < n_per; j++) {
+        uint64_t ej = idx ? idx[(uint64_t)s * n_per + j] : (uint64_t)s * n_per + j;
+        int sx = (xi > x[ej]) - (xi < x[ej]);
+        int sy = (yi > y[ej]) - (yi < y[ej]);
+        if (sx == 0 && sy == 0) txy++;
+        else if (sx == 0) tx++;
+        else if (sy == 0) ty++;
+        else if (sx == sy) c++;
+        else d++;
+      }
+    }
+    counts[(uint64_t)s * 5 + 0] = c;
+    counts[(uint64_t)s * 5 + 1] = d;
+    counts[(uint64_t)s * 5 + 2] = tx;
+    counts[(uint64_t)s * 5 + 3] = ty;
+    counts[(uint64_t)s * 5 + 4] = txy;
+    top1[s] = (uint8_t)(bx == by);
+  }
+}
+
+/* ------------------------------------------------- the event simulation */
+
+typedef struct {
+  uint32_t phase, tier, turn, len;
+  float g;
+  uint64_t gq, last_ns, next_ns;
+} sess_t;
+
+typedef struct {
+  const orc_params* p;
+  sess_t* s;
+  const uint32_t* kvb;
+  uint32_t n_sess;
+  float hf[LUT_LEN];
+  uint64_t hq[LUT_LEN];
+  uint64_t used[3]; /* indexed by tier */
+  uint64_t n_res, n_table;
+  uint64_t dma_free_at;
+  orc_counters* c;
+  orc_rec* log;
+  uint32_t log_cap, log_len;
+  uint32_t ev;
+} sim_t;
+
+static void emit(sim_t* m, uint32_t op, uint32_t a, uint32_t b) {
+  m->c->digest += rec_hash(m->ev, op, a, b);
+  if (m->log && m->log_len < m->log_cap) {
+    orc_rec r = {m->ev, op, a, b};
+    m->log[m->log_len] = r;
+  }
+  if (m->log) m->log_len++;
+}
+
+static int evictable(const sess_t* e) { return e->tier != T_NONE && e->phase != PH_SERVING; }
+
+static uint64_t size_of(const sim_t* m, uint32_t i) {
+  return (uint64_t)m->s[i].len * (uint64_t)m->kvb[i];
+}
+
+/* "larger = evict first" key of one table entry */
+static uint64_t key_of(const sim_t* m, uint32_t i) {
+  const sess_t* e = &m->s[i];
+  switch (m->p->policy) {
+    case P_SPEAR:
+      if (m->p->score_mode == 1)
+        return spear_fixed(e->turn, e->gq, e->phase == PH_DONE, m->hq, m->p->b_h, m->p->p_z);
+      else {
+        float f = spear_f32(e->turn, e->g, e->phase == PH_DONE, m->hf, m->p->penalty_us);
+        uint32_t bits;
+        memcpy(&bits, &f, 4); /* non-negative floats order like their bit patterns */
+        return bits;
+      }
+    case P_LRU:
+    case P_TIMEOUT:
+      return UINT64_MAX - e->last_ns;
+    default:
+      return e->next_ns;
+  }
+}
+
+static uint64_t done_key(const sim_t* m) {
+  if (m->p->policy == P_SPEAR) return m->p->score_mode == 1 ? UINT64_MAX : 0x7F800000u;
+  if (m->p->policy == P_BELADY) return UINT64_MAX;
+  return 0; /* recency keys have no completion value */
+}
+
+/* argmax over evictable residents in tier `tier` (T_NONE = any tier) */
+static uint32_t argmax_key(const sim_t* m, uint32_t tier) {
+  uint32_t best = NONE_ID;
+  uint64_t bk = 0;
+  for (uint32_t i = 0; i < m->n_sess; i++) {
+    if (!evictable(&m->s[i])) continue;
+    if (tier != T_NONE && m->s[i].tier != tier) continue;
+    uint64_t k = key_of(m, i);
+    if (best == NONE_ID || k > bk) { best = i; bk = k; }
+  }
+  return best;
+}
+
+static uint32_t argmin_key(const sim_t* m, uint32_t tier) {
+  uint32_t best = NONE_ID;
+  uint64_t bk = 0;
+  for (uint32_t i = 0; i < m->n_sess; i++) {
+    if (!evictable(&m->s[i])) continue;
+    if (tier != T_NONE && m->s[i].tier != tier) continue;
+    uint64_t k = key_of(m, i);
+    if (best == NONE_ID || k < bk) { best = i; bk = k; }
+  }
+  return best;
+}
+
+static void release(sim_t* m, uint32_t i) {
+  m->used[m->s[i].tier] -= size_of(m, i);
+  m->s[i].tier = T_NONE;
+  m->n_res--;
+  if (m->s[i].phase == PH_DONE) m->n_table--; /* a completed session leaves the table */
+}
+
+static void put(sim_t* m, uint32_t i, uint32_t tier) {
+  m->s[i].tier = tier;
+  m->used[tier] += size_of(m, i);
+  m->n_res++;
+}
+
+static int fits(const sim_t* m, uint32_t tier, uint64_t size) {
+  uint64_t cap = tier == T_SRAM ? m->p->cap_sram_B : m->p->cap_hbm_B;
+  return m->used[tier] + size <= cap && m->n_res + 1 <= m->p->n_slots;
+}
+
+/* Algorithm 1, capacity branch: place the arriving session, evicting the
+ * argmax victim while eq. (cap) would be violated. */
+static void place(sim_t* m, uint32_t sid, uint32_t pref) {
+  uint64_t size = size_of(m, sid);
+  uint32_t other = pref == T_SRAM ? T_HBM : T_SRAM;
+  if (size > m->p->cap_sram_B && size > m->p->cap_hbm_B) {
+    emit(m, OP_BYPASS, sid, NONE_ID);
+    m->c->bypass++;
+    return;
+  }
+  for (;;) {
+    if (fits(m, pref, size)) { put(m, sid, pref); emit(m, OP_PLACE, sid, pref); return; }
+    if (fits(m, other, size)) { put(m, sid, other); emit(m, OP_PLACE, sid, other); return; }
+    uint32_t v = argmax_key(m, T_NONE);
+    if (v == NONE_ID) {
+      emit(m, OP_BYPASS, sid, NONE_ID);
+      m->c->bypass++;
+      return;
+    }
+    emit(m, OP_EVICT, v, NONE_ID);
+    m->c->evict++;
+    release(m, v);
+  }
+}
+
+/* Algorithm 1, tiering branch: eq. (budget), eq. (promote), eq. (demote). */
+static void tide(sim_t* m, uint32_t sid, uint64_t now, orc_state* st) {
+  const orc_params* p = m->p;
+  uint64_t delta_us;
+  if (p->policy == P_SPEAR && p->score_mode == 1)
+    delta_us = sat_u64(((unsigned __int128)m->s[sid].gq * p->tau_ns) / 1000);
+  else
+    delta_us = (uint64_t)m->s[sid].g;
+  uint64_t budget = sat_u64((unsigned __int128)delta_us * p->dma_B_per_us);
+  uint64_t left = budget, moved = 0;
+  uint64_t inf = done_key(m);
+  int has_inf = p->policy == P_SPEAR || p->policy == P_BELADY;
+  m->c->tide_passes++;
+  for (;;) {
+    uint32_t pid = argmin_key(m, T_HBM);
+    if (pid == NONE_ID) break;
+    uint64_t kp = key_of(m, pid);
+    if (has_inf && kp == inf) break;
+    uint64_t sp = size_of(m, pid);
+    if (m->used[T_SRAM] + sp <= p->cap_sram_B && sp <= left) {
+      m->used[T_HBM] -= sp;
+      m->used[T_SRAM] += sp;
+      m->s[pid].tier = T_SRAM;
+      left -= sp;
+      moved += sp;
+      emit(m, OP_PROMOTE, pid, NONE_ID);
+      m->c->promote++;
+      continue;
+    }
+    uint32_t did = argmax_key(m, T_SRAM);
+    if (did == NONE_ID) break;
+    uint64_t kd = key_of(m, did);
+    uint64_t sd = size_of(m, did);
+    int legal = kp < kd && sp <= left && sd <= left - sp &&
+                m->used[T_SRAM] - sd + sp <= p->cap_sram_B &&
+                m->used[T_HBM] - sp + sd <= p->cap_hbm_B;
+    if (!legal) break;
+    m->used[T_SRAM] = m->used[T_SRAM] - sd + sp;
+    m->used[T_HBM] = m->used[T_HBM] - sp + sd;
+    m->s[pid].tier = T_SRAM;
+    m->s[did].tier = T_HBM;
+    left -= sp + sd;
+    moved += sp + sd;
+    emit(m, OP_SWAP, pid, did);
+    m->c->swap++;
+  }
+  if (moved) {
+    unsigned __int128 ns = ((unsigned __int128)moved * 1000 + p->dma_B_per_us - 1) / p->dma_B_per_us;
+    m->dma_free_at = sat_u64((unsigned __int128)now + ns);
+  }
+  m->c->dma_bytes += moved;
+  if (st) { st->tide_ran = 1; st->tide_budget = budget; st->tide_moved = moved; }
+}
+
+/*
+ * Runs one simulation over one trace.
+ *   ev_*       the trace's events (already in order), n_events long
+ *   kvb        bytes per token of each of the trace's n_sess sessions
+ *   lut_d/n    the hazard counts d(t), n(t) of this simulation's table
+ *   max_events stop after this many events (UINT64_MAX = all)
+ *   log/states optional outputs (NULL to skip); states has one entry per event
+ *   elapsed_ns wall time of the event loop alone (optional)
+ * Returns ORC_OK, ORC_E_INVALID or ORC_E_BAD_TRACE (counters.error = event+1).
+ */
+int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
+            const uint32_t* ev_sid, const uint32_t* ev_info, const uint32_t* ev_len,
+            const uint64_t* ev_next, uint32_t n_sess, const uint32_t* kvb,
+            const uint32_t* lut_d, const uint32_t* lut_n, uint64_t max_events,
+            orc_counters* out, orc_rec* log, uint32_t log_cap, uint32_t* log_len,
+            orc_state* states, uint64_t* elapsed_ns) {
+  if (!p || !out || p->policy > P_BELADY || p->dma_B_per_us == 0 || p->n_slots == 0 ||
+      p->tau_ns == 0 || p->b_h < 1 || p->b_h > 32 || p->b_g < 1 || p->b_g > 64 ||
+      !(p->penalty_us >= 0.0f))
+    return ORC_E_INVALID;
+  memset(out, 0, sizeof *out);
+  sim_t m;
+  memset(&m, 0, sizeof m);
+  m.p = p;
+  m.kvb = kvb;
+  m.n_sess = n_sess;
+  m.c = out;
+  m.log = log;
+  m.log_cap = log_cap;
+  m.s = (sess_t*)calloc(n_sess ? n_sess : 1, sizeof(sess_t));
+  if (!m.s) return ORC_E_INVALID;
+  orc_lut_f32(lut_d, lut_n, m.hf);
+  orc_lut_q(lut_d, lut_n, p->b_h, m.hq);
+  int rc = ORC_OK;
+  uint64_t n_run = n_events < max_events ? n_events : max_events;
+  struct timespec t0, t1;
+  clock_gettime(CLOCK_MONOTONIC, &t0);
+  uint64_t prev_t = 0;
+  for (uint64_t e = 0; e < n_run; e++) {
+    m.ev = (uint32_t)e;
+    uint64_t now = ev_t[e];
+    uint32_t sid = ev_sid[e];
+    uint32_t kind = ev_info[e] >> 24;
+    uint32_t turn = ev_info[e] & 0xFFFFFFu;
+    orc_state* st = states ? &states[e] : NULL;
+    if (st) memset(st, 0, sizeof *st);
+    if (sid >= n_sess || now < prev_t || kind > K_DONE) { rc = ORC_E_BAD_TRACE; out->error = e + 1; break; }
+    prev_t = now;
+    sess_t* x = &m.s[sid];
+
+    /* timeout policy: the TTL timers that fired since the previous event
+     * expire idle residents (the arriving session included), in ascending id */
+    if (p->policy == P_TIMEOUT) {
+      for (uint32_t i = 0; i < n_sess; i++) {
+        if (evictable(&m.s[i]) && now - m.s[i].last_ns > p->ttl_ns) {
+          emit(&m, OP_EXPIRE, i, NONE_ID);
+          out->expire++;
+          release(&m, i);
+        }
+      }
+    }
+
+    /* Alg. 1: write e into R; on gap_end update the EMA (eq. (gap), eq. (ema)) */
+    uint32_t len_prev = x->len;
+    if (kind == K_ARRIVE) {
+      if (turn == 0) {
+        if (x->phase != PH_UNSEEN) { rc = ORC_E_BAD_TRACE; out->error = e + 1; break; }
+        x->g = 0.0f;
+        x->gq = 0;
+        x->len = 0;
+        len_prev = 0;
+        m.n_table++;
+      } else {
+        if (x->phase != PH_GAP || turn != x->turn + 1 || ev_len[e] < x->len) {
+          rc = ORC_E_BAD_TRACE; out->error = e + 1; break;
+        }
+        uint64_t gap = now - x->last_ns;
+        x->g = ema_f32(x->g, gap);
+        x->gq = ema_int(x->gq, gap, p->b_g, p->tau_ns);
+      }
+      x->turn = turn;
+      x->phase = PH_SERVING;
+      x->last_ns = now;
+    } else {
+      if (x->phase != PH_SERVING) { rc = ORC_E_BAD_TRACE; out->error = e + 1; break; }
+      x->last_ns = now;
+      if (kind == K_GAP_START) {
+        x->phase = PH_GAP;
+        x->next_ns = ev_next[e];
+      } else {
+        x->phase = PH_DONE;
+        x->next_ns = UINT64_MAX;
+      }
+    }
+
+    /* the per-event scan of the register file (eq. (pipe)): every table entry
+     * is scored; its result is this event's victim index */
+    out->score_evals += m.n_table;
+    out->resident_evals += m.n_res;
+    uint32_t v0 = argmax_key(&m, T_NONE);
+    out->victim_digest += rec_hash(m.ev, OP_VICTIM, v0, NONE_ID);
+
+    if (kind == K_ARRIVE) {
+      /* eq. (hr-amat), eq. (prered), eq. (reuse) */
+      uint64_t len = ev_len[e];
+      uint64_t dlen = len - len_prev;
+      uint64_t kb = kvb[sid];
+      out->requests++;
+      out->tokens_total += len;
+      uint32_t tier0 = x->tier;
+      if (tier0 == T_SRAM || tier0 == T_HBM) {
+        double t_mem = tier0 == T_SRAM ? p->t_s_ns_per_B : p->t_h_ns_per_B;
+        if (tier0 == T_SRAM) out->hit_sram++; else out->hit_hbm++;
+        double a = (double)(len * kb) * t_mem;
+        double b = (double)(len_prev * kb) * t_mem;
+        double c = (double)dlen * p->t_p_ns_per_tok;
+        out->amat_sum_ns += a;
+        out->ttft_sum_ns += b + c;
+        out->tokens_computed += dlen;
+        release(&m, sid);
+      } else {
+        out->miss++;
+        double a = (double)len * p->t_p_ns_per_tok;
+        out->amat_sum_ns += a;
+        out->ttft_sum_ns += a;
+        out->tokens_computed += len;
+        out->extra_prefill_tok += len_prev;
+      }
+      x->len = (uint32_t)len;
+      place(&m, sid, tier0 == T_HBM ? T_HBM : T_SRAM);
+    } else if (kind == K_GAP_START) {
+      if (p->tide && now >= m.dma_free_at) tide(&m, sid, now, st);
+    } else {
+      if (x->tier == T_NONE) m.n_table--;
+    }
+
+    if (st) {
+      st->used_sram = m.used[T_SRAM];
+      st->used_hbm = m.used[T_HBM];
+      st->n_res = (uint32_t)m.n_res;
+      st->n_table = (uint32_t)m.n_table;
+      st->victim = v0;
+    }
+    out->events++;
+  }
+  clock_gettime(CLOCK_MONOTONIC, &t1);
+  if (elapsed_ns)
+    *elapsed_ns = (uint64_t)(t1.tv_sec - t0.tv_sec) * 1000000000ULL + (uint64_t)(t1.tv_nsec - t0.tv_nsec);
+  if (log_len) *log_len = m.log_len;
+  free(m.s);
+  return rc;
+}
+
+/* Layout version of the structs above. */
+uint32_t orc_version(void) { return 1; }
