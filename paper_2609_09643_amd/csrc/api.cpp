@@ -1,0 +1,398 @@
+// api.cpp -- host side of the libunison C ABI (see include/unison.h).
+//
+// Validates arguments, carves the caller's workspace into the simulation
+// state regions, copies the small host-side tables (offsets, parameters) into
+// it and launches the kernels on the caller's stream.  No device memory is
+// allocated here and no exception crosses the ABI.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "unison_device.h"
+
+namespace unison {
+hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream, int force_variant);
+uint32_t sim_variant_capacity(int v);
+hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
+                                hipStream_t stream);
+hipError_t launch_ema_replay(uint32_t n, uint32_t max_hist, const uint64_t* gaps,
+                             const uint8_t* n_hist, uint32_t b_g, uint64_t tau, float* g,
+                             uint64_t* gq, hipStream_t s);
+hipError_t launch_score_fp32(uint32_t n, const uint8_t* turn, const float* g, const uint8_t* done,
+                             const uint32_t* d, const uint32_t* nn, float P, float* out,
+                             hipStream_t s);
+hipError_t launch_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
+                              const uint8_t* done, const uint32_t* d, const uint32_t* nn,
+                              uint32_t b_h, uint64_t p_z, uint64_t* out, hipStream_t s);
+hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const float* x,
+                          const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1,
+                          hipStream_t s);
+uint32_t kendall_max_per();
+}  // namespace unison
+
+using namespace unison;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Workspace layout; offsets in bytes from the workspace base.
+struct Layout {
+  size_t params, ev_off, sess_off, lut_d, lut_n, state, counters, mg, gq, len, last, next, log, total;
+};
+
+bool make_layout(const unison_dims& d, Layout& L) {
+  const size_t entries = (size_t)d.n_sims * d.max_sessions;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.params = take(sizeof(unison_sim_params) * d.n_sims);
+  L.ev_off = take(sizeof(uint64_t) * (d.n_traces + 1));
+  L.sess_off = take(sizeof(uint64_t) * (d.n_traces + 1));
+  L.lut_d = take(sizeof(uint32_t) * kLut * d.n_luts);
+  L.lut_n = take(sizeof(uint32_t) * kLut * d.n_luts);
+  L.state = take(sizeof(SimState) * d.n_sims);
+  L.counters = take(sizeof(unison_counters) * d.n_sims);
+  L.mg = take(sizeof(uint64_t) * entries);
+  L.gq = take(sizeof(uint64_t) * entries);
+  L.len = take(sizeof(uint32_t) * entries);
+  L.last = take(sizeof(uint64_t) * entries);
+  L.next = take(sizeof(uint64_t) * entries);
+  L.log = take(sizeof(unison_record) * (size_t)d.log_cap * d.n_sims);
+  L.total = off;
+  return true;
+}
+
+bool dims_ok(const unison_dims* d) {
+  return d && d->n_sims >= 1 && d->n_traces >= 1 && d->n_luts >= 1 && d->max_sessions >= 1 &&
+         d->max_sessions <= UNISON_MAX_SESSIONS;
+}
+
+}  // namespace
+
+struct unison_ctx {
+  unison_dims dims;
+  hipStream_t stream;
+  char* ws;
+  size_t ws_bytes;
+  Layout L;
+  unison_trace_batch tb;
+  std::vector<uint64_t> h_ev_off, h_sess_off;
+  std::vector<unison_sim_params> h_params;
+  std::vector<uint8_t> lut_set;
+  bool traces_loaded = false, params_set = false, ran = false;
+  uint32_t max_sess_batch = 0;
+  int force_variant = -1;
+  char err[512];
+
+  template <class T>
+  T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+
+  int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(err, sizeof err, fmt, ap);
+    va_end(ap);
+    return code;
+  }
+  int hip(hipError_t e, const char* what) {
+    if (e == hipSuccess) return UNISON_OK;
+    return fail(UNISON_E_HIP, "%s: %s", what, hipGetErrorString(e));
+  }
+};
+
+extern "C" {
+
+uint32_t unison_version(void) { return 1u; }
+
+const char* unison_strerror(int code) {
+  switch (code) {
+    case UNISON_OK: return "ok";
+    case UNISON_E_INVALID: return "invalid argument";
+    case UNISON_E_BAD_TRACE: return "trace breaks the event format";
+    case UNISON_E_CAPACITY: return "session count above the supported maximum";
+    case UNISON_E_HIP: return "HIP runtime error";
+    case UNISON_E_NOT_READY: return "traces, hazard tables or parameters missing";
+    default: return "unknown error";
+  }
+}
+
+const char* unison_last_error(const unison_ctx* ctx) { return ctx ? ctx->err : "null context"; }
+
+int unison_workspace_size(const unison_dims* d, size_t* bytes) {
+  if (!dims_ok(d) || !bytes) return UNISON_E_INVALID;
+  Layout L;
+  make_layout(*d, L);
+  *bytes = L.total;
+  return UNISON_OK;
+}
+
+int unison_create(unison_ctx** out, const unison_dims* d, void* hip_stream, void* workspace,
+                  size_t workspace_bytes) {
+  if (!out || !dims_ok(d) || !workspace) return UNISON_E_INVALID;
+  *out = nullptr;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign) return UNISON_E_INVALID;
+  Layout L;
+  make_layout(*d, L);
+  if (workspace_bytes < L.total) return UNISON_E_INVALID;
+  unison_ctx* c = new (std::nothrow) unison_ctx();
+  if (!c) return UNISON_E_INVALID;
+  c->dims = *d;
+  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  c->ws = reinterpret_cast<char*>(workspace);
+  c->ws_bytes = workspace_bytes;
+  c->L = L;
+  c->lut_set.assign(d->n_luts, 0);
+  c->err[0] = 0;
+  std::memset(&c->tb, 0, sizeof c->tb);
+  *out = c;
+  return UNISON_OK;
+}
+
+void unison_destroy(unison_ctx* ctx) { delete ctx; }
+
+int unison_set_stream(unison_ctx* ctx, void* hip_stream) {
+  if (!ctx) return UNISON_E_INVALID;
+  ctx->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  return UNISON_OK;
+}
+
+int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
+  if (!ctx || !tb) return UNISON_E_INVALID;
+  const uint32_t nt = tb->n_traces;
+  if (nt != ctx->dims.n_traces)
+    return ctx->fail(UNISON_E_INVALID, "n_traces %u differs from dims %u", nt, ctx->dims.n_traces);
+  if (!tb->ev_offset || !tb->sess_offset || !tb->ev_t_ns || !tb->ev_sid || !tb->ev_info ||
+      !tb->ev_len || !tb->ev_next_ns || !tb->sess_kvb)
+    return ctx->fail(UNISON_E_INVALID, "null trace array");
+  for (uint32_t i = 0; i < nt; ++i) {
+    if (tb->ev_offset[i + 1] < tb->ev_offset[i] || tb->sess_offset[i + 1] < tb->sess_offset[i])
+      return ctx->fail(UNISON_E_INVALID, "trace %u: offsets decrease", i);
+    if (tb->ev_offset[i + 1] - tb->ev_offset[i] > 0xFFFFFFFFull)
+      return ctx->fail(UNISON_E_INVALID, "trace %u: more than 2^32-1 events", i);
+    const uint64_t ns = tb->sess_offset[i + 1] - tb->sess_offset[i];
+    if (ns > ctx->dims.max_sessions)
+      return ctx->fail(UNISON_E_CAPACITY, "trace %u has %llu sessions > max_sessions %u", i,
+                       (unsigned long long)ns, ctx->dims.max_sessions);
+  }
+  ctx->tb = *tb;
+  ctx->h_ev_off.assign(tb->ev_offset, tb->ev_offset + nt + 1);
+  ctx->h_sess_off.assign(tb->sess_offset, tb->sess_offset + nt + 1);
+  int rc = ctx->hip(hipMemcpyAsync(ctx->at<uint64_t>(ctx->L.ev_off), ctx->h_ev_off.data(),
+                                   sizeof(uint64_t) * (nt + 1), hipMemcpyHostToDevice, ctx->stream),
+                    "copy event offsets");
+  if (rc) return rc;
+  rc = ctx->hip(hipMemcpyAsync(ctx->at<uint64_t>(ctx->L.sess_off), ctx->h_sess_off.data(),
+                               sizeof(uint64_t) * (nt + 1), hipMemcpyHostToDevice, ctx->stream),
+                "copy session offsets");
+  if (rc) return rc;
+  rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise after offsets");
+  if (rc) return rc;
+  ctx->traces_loaded = true;
+  return UNISON_OK;
+}
+
+int unison_hazard_counts(void* hip_stream, const uint32_t* turns, uint32_t n, uint32_t* d_out,
+                         uint32_t* n_out) {
+  if ((!turns && n) || !d_out || !n_out) return UNISON_E_INVALID;
+  hipError_t e = launch_hazard_counts(turns, n, d_out, n_out, reinterpret_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? UNISON_OK : UNISON_E_HIP;
+}
+
+int unison_set_hazard(unison_ctx* ctx, uint32_t lut, const uint32_t* d, const uint32_t* n) {
+  if (!ctx || !d || !n) return UNISON_E_INVALID;
+  if (lut >= ctx->dims.n_luts) return ctx->fail(UNISON_E_INVALID, "lut %u >= n_luts", lut);
+  int rc = ctx->hip(hipMemcpyAsync(ctx->at<uint32_t>(ctx->L.lut_d) + (size_t)lut * kLut, d,
+                                   sizeof(uint32_t) * kLut, hipMemcpyDeviceToDevice, ctx->stream),
+                    "copy hazard d");
+  if (rc) return rc;
+  rc = ctx->hip(hipMemcpyAsync(ctx->at<uint32_t>(ctx->L.lut_n) + (size_t)lut * kLut, n,
+                               sizeof(uint32_t) * kLut, hipMemcpyDeviceToDevice, ctx->stream),
+                "copy hazard n");
+  if (rc) return rc;
+  ctx->lut_set[lut] = 1;
+  return UNISON_OK;
+}
+
+int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
+  if (!ctx || !params) return UNISON_E_INVALID;
+  if (!ctx->traces_loaded) return ctx->fail(UNISON_E_NOT_READY, "load traces before parameters");
+  uint32_t max_sess = 0;
+  for (uint32_t i = 0; i < ctx->dims.n_sims; ++i) {
+    const unison_sim_params& p = params[i];
+    if (p.policy > UNISON_POLICY_BELADY || p.tide > 1 || p.score_mode > 1 ||
+        p.lut >= ctx->dims.n_luts || p.trace >= ctx->dims.n_traces || p.b_h < 1 || p.b_h > 16 ||
+        p.b_g < 1 || p.b_g > 64 || p.tau_ns < 1 || p.n_slots < 1 || p.dma_B_per_us < 1 ||
+        !(p.penalty_us >= 0.0f) || std::isinf(p.penalty_us) || !std::isfinite(p.t_s_ns_per_B) ||
+        !std::isfinite(p.t_h_ns_per_B) || !std::isfinite(p.t_p_ns_per_tok))
+      return ctx->fail(UNISON_E_INVALID, "parameter row %u out of range", i);
+    const uint64_t ns = ctx->h_sess_off[p.trace + 1] - ctx->h_sess_off[p.trace];
+    max_sess = std::max<uint32_t>(max_sess, (uint32_t)ns);
+  }
+  ctx->h_params.assign(params, params + ctx->dims.n_sims);
+  int rc = ctx->hip(hipMemcpyAsync(ctx->at<unison_sim_params>(ctx->L.params), ctx->h_params.data(),
+                                   sizeof(unison_sim_params) * ctx->dims.n_sims,
+                                   hipMemcpyHostToDevice, ctx->stream),
+                    "copy parameters");
+  if (rc) return rc;
+  rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise after parameters");
+  if (rc) return rc;
+  ctx->max_sess_batch = max_sess;
+  ctx->params_set = true;
+  return UNISON_OK;
+}
+
+int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64_t max_events) {
+  if (!ctx) return UNISON_E_INVALID;
+  if (!ctx->traces_loaded || !ctx->params_set)
+    return ctx->fail(UNISON_E_NOT_READY, "traces and parameters must be set before a run");
+  for (const auto& p : ctx->h_params)
+    if (!ctx->lut_set[p.lut]) return ctx->fail(UNISON_E_NOT_READY, "hazard table %u not set", p.lut);
+  if (policy_override != UNISON_POLICY_PARAMS && policy_override > UNISON_POLICY_BELADY)
+    return ctx->fail(UNISON_E_INVALID, "policy %u", policy_override);
+  if (flags & ~(UNISON_RUN_CONTINUE | UNISON_RUN_LOG)) return ctx->fail(UNISON_E_INVALID, "flags");
+  if ((flags & UNISON_RUN_CONTINUE) && !ctx->ran)
+    return ctx->fail(UNISON_E_NOT_READY, "UNISON_RUN_CONTINUE before any run on this context");
+  SimArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.params = ctx->at<unison_sim_params>(ctx->L.params);
+  a.ev_off = ctx->at<uint64_t>(ctx->L.ev_off);
+  a.sess_off = ctx->at<uint64_t>(ctx->L.sess_off);
+  a.ev_t = ctx->tb.ev_t_ns;
+  a.ev_sid = ctx->tb.ev_sid;
+  a.ev_info = ctx->tb.ev_info;
+  a.ev_len = ctx->tb.ev_len;
+  a.ev_next = ctx->tb.ev_next_ns;
+  a.sess_kvb = ctx->tb.sess_kvb;
+  a.lut_d = ctx->at<uint32_t>(ctx->L.lut_d);
+  a.lut_n = ctx->at<uint32_t>(ctx->L.lut_n);
+  a.state = ctx->at<SimState>(ctx->L.state);
+  a.counters = ctx->at<unison_counters>(ctx->L.counters);
+  a.t_mg = ctx->at<uint64_t>(ctx->L.mg);
+  a.t_gq = ctx->at<uint64_t>(ctx->L.gq);
+  a.t_len = ctx->at<uint32_t>(ctx->L.len);
+  a.t_last = ctx->at<uint64_t>(ctx->L.last);
+  a.t_next = ctx->at<uint64_t>(ctx->L.next);
+  a.log = ctx->dims.log_cap ? ctx->at<unison_record>(ctx->L.log) : nullptr;
+  a.max_events = max_events;
+  a.n_sims = ctx->dims.n_sims;
+  a.max_sessions = ctx->dims.max_sessions;
+  a.log_cap = ctx->dims.log_cap;
+  a.flags = flags;
+  a.policy_override = policy_override;
+  int v = ctx->force_variant;
+  if (v >= 0 && sim_variant_capacity(v) < ctx->max_sess_batch)
+    return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds %u sessions < %u", v,
+                     sim_variant_capacity(v), ctx->max_sess_batch);
+  int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->stream, v), "launch simulation");
+  if (rc == UNISON_OK) ctx->ran = true;
+  return rc;
+}
+
+int unison_read_counters(unison_ctx* ctx, unison_counters* dst, uint32_t first, uint32_t n) {
+  if (!ctx || (!dst && n)) return UNISON_E_INVALID;
+  if ((uint64_t)first + n > ctx->dims.n_sims) return ctx->fail(UNISON_E_INVALID, "range");
+  int rc = ctx->hip(hipMemcpyAsync(dst, ctx->at<unison_counters>(ctx->L.counters) + first,
+                                   sizeof(unison_counters) * n, hipMemcpyDeviceToHost, ctx->stream),
+                    "copy counters");
+  if (rc) return rc;
+  rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise counters");
+  if (rc) return rc;
+  for (uint32_t i = 0; i < n; ++i)
+    if (dst[i].error) return ctx->fail(UNISON_E_BAD_TRACE, "simulation %u stopped at event %llu", first + i,
+                                       (unsigned long long)(dst[i].error - 1));
+  return UNISON_OK;
+}
+
+int unison_counters_device(unison_ctx* ctx, const unison_counters** out) {
+  if (!ctx || !out) return UNISON_E_INVALID;
+  *out = ctx->at<unison_counters>(ctx->L.counters);
+  return UNISON_OK;
+}
+
+int unison_read_log(unison_ctx* ctx, uint32_t sim, unison_record* dst, uint32_t cap, uint64_t* n_total) {
+  if (!ctx || !n_total || (!dst && cap)) return UNISON_E_INVALID;
+  if (sim >= ctx->dims.n_sims) return ctx->fail(UNISON_E_INVALID, "sim %u", sim);
+  SimState st;
+  int rc = ctx->hip(hipMemcpyAsync(&st, ctx->at<SimState>(ctx->L.state) + sim, sizeof st,
+                                   hipMemcpyDeviceToHost, ctx->stream),
+                    "copy state");
+  if (rc) return rc;
+  rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise state");
+  if (rc) return rc;
+  *n_total = st.log_len;
+  const uint64_t kept = std::min<uint64_t>(st.log_len, ctx->dims.log_cap);
+  const uint64_t n = std::min<uint64_t>(kept, cap);
+  if (n) {
+    rc = ctx->hip(hipMemcpyAsync(dst, ctx->at<unison_record>(ctx->L.log) + (size_t)sim * ctx->dims.log_cap,
+                                 sizeof(unison_record) * n, hipMemcpyDeviceToHost, ctx->stream),
+                  "copy log");
+    if (rc) return rc;
+    rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise log");
+  }
+  return rc;
+}
+
+// Test hook: pin the simulation kernel variant (-1 = automatic).
+int unison_debug_force_variant(unison_ctx* ctx, int variant) {
+  if (!ctx) return UNISON_E_INVALID;
+  ctx->force_variant = variant;
+  return UNISON_OK;
+}
+
+int unison_ema_replay(void* hip_stream, uint32_t n, uint32_t max_hist, const uint64_t* gaps_ns,
+                      const uint8_t* n_hist, uint32_t b_g, uint64_t tau_ns, float* g_out,
+                      uint64_t* gq_out) {
+  if (n && (!gaps_ns || !n_hist || !g_out || !gq_out)) return UNISON_E_INVALID;
+  if (max_hist == 0 || b_g < 1 || b_g > 64 || tau_ns < 1) return UNISON_E_INVALID;
+  return launch_ema_replay(n, max_hist, gaps_ns, n_hist, b_g, tau_ns, g_out, gq_out,
+                           reinterpret_cast<hipStream_t>(hip_stream)) == hipSuccess
+             ? UNISON_OK
+             : UNISON_E_HIP;
+}
+
+int unison_score_fp32(void* hip_stream, uint32_t n, const uint8_t* turn, const float* g,
+                      const uint8_t* done, const uint32_t* lut_d, const uint32_t* lut_n,
+                      float penalty_us, float* out) {
+  if (n && (!turn || !g || !done || !out)) return UNISON_E_INVALID;
+  if (!lut_d || !lut_n || !(penalty_us >= 0.0f) || std::isinf(penalty_us)) return UNISON_E_INVALID;
+  return launch_score_fp32(n, turn, g, done, lut_d, lut_n, penalty_us, out,
+                           reinterpret_cast<hipStream_t>(hip_stream)) == hipSuccess
+             ? UNISON_OK
+             : UNISON_E_HIP;
+}
+
+int unison_score_fixed(void* hip_stream, uint32_t n, const uint8_t* turn, const uint64_t* gq,
+                       const uint8_t* done, const uint32_t* lut_d, const uint32_t* lut_n,
+                       uint32_t b_h, uint64_t p_z, uint64_t* out) {
+  if (n && (!turn || !gq || !done || !out)) return UNISON_E_INVALID;
+  if (!lut_d || !lut_n || b_h < 1 || b_h > 16) return UNISON_E_INVALID;
+  return launch_score_fixed(n, turn, gq, done, lut_d, lut_n, b_h, p_z, out,
+                            reinterpret_cast<hipStream_t>(hip_stream)) == hipSuccess
+             ? UNISON_OK
+             : UNISON_E_HIP;
+}
+
+int unison_kendall(void* hip_stream, uint32_t n_snap, uint32_t n_per, uint64_t n_x, const float* x,
+                   const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1) {
+  if (n_snap && (!x || !y || !counts || !top1)) return UNISON_E_INVALID;
+  if (n_per < 2 || n_per > kendall_max_per()) return UNISON_E_INVALID;
+  if (!idx && (uint64_t)n_snap * n_per > n_x) return UNISON_E_INVALID;
+  return launch_kendall(n_snap, n_per, n_x, x, y, idx, counts, top1,
+                        reinterpret_cast<hipStream_t>(hip_stream)) == hipSuccess
+             ? UNISON_OK
+             : UNISON_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,226 @@
+// rank.hip -- register-file EMA replay, the two scorers and the batched
+// Kendall tau-b statistics of the ranking-fidelity study (Sec. IV-C, Sec. VI-F).
+//
+// The scorers are elementwise and HBM-bound (one thread per session, coalesced
+// loads, the hazard table in LDS).  The Kendall kernel gives each snapshot one
+// workgroup: the snapshot's (x, y) pairs are gathered into LDS once, each
+// thread owns rows i and walks j > i with all lanes of a wave reading the same
+// LDS word (a broadcast), so the O(n^2) pair classification runs from LDS at
+// VALU rate.
+#include <hip/hip_runtime.h>
+
+#include "unison_device.h"
+
+#pragma clang fp contract(off)
+
+namespace unison {
+
+__global__ __launch_bounds__(256) void ema_replay_kernel(uint32_t n, uint32_t max_hist,
+                                                         const uint64_t* gaps, const uint8_t* n_hist,
+                                                         uint32_t b_g, uint64_t tau, float* g_out,
+                                                         uint64_t* gq_out) {
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t k_end = n_hist[i] < max_hist ? n_hist[i] : max_hist;
+  float g = 0.0f;
+  uint64_t gq = 0;
+  for (uint32_t k = 0; k < k_end; ++k) {
+    const uint64_t gap = gaps[(size_t)i * max_hist + k];
+    g = ema_f32(g, gap);
+    gq = ema_int(gq, gap, b_g, tau);
+  }
+  g_out[i] = g;
+  gq_out[i] = gq;
+}
+
+__global__ __launch_bounds__(256) void score_fp32_kernel(uint32_t n, const uint8_t* turn,
+                                                         const float* g, const uint8_t* done,
+                                                         const uint32_t* lut_d, const uint32_t* lut_n,
+                                                         float P, float* out) {
+  __shared__ float hf[52];
+  if (threadIdx.x < kLut) hf[threadIdx.x] = hazard_f32(lut_d[threadIdx.x], lut_n[threadIdx.x]);
+  __syncthreads();
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t t = turn[i] < 50u ? turn[i] : 50u;
+  const float s = spear_f32(hf[t], g[i], P);
+  out[i] = done[i] ? __uint_as_float(0x7F800000u) : s;
+}
+
+__global__ __launch_bounds__(256) void score_fixed_kernel(uint32_t n, const uint8_t* turn,
+                                                          const uint64_t* gq, const uint8_t* done,
+                                                          const uint32_t* lut_d,
+                                                          const uint32_t* lut_n, uint32_t b_h,
+                                                          uint64_t p_z, uint64_t* out) {
+  __shared__ uint32_t hq[52];
+  const uint32_t lambda = (1u << b_h) - 1u;
+  if (threadIdx.x < kLut) hq[threadIdx.x] = hazard_q(lut_d[threadIdx.x], lut_n[threadIdx.x], lambda);
+  __syncthreads();
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t t = turn[i] < 50u ? turn[i] : 50u;
+  const uint64_t s = spear_fixed(hq[t], gq[i], lambda, p_z);
+  out[i] = done[i] ? ~0ull : s;
+}
+
+constexpr int kKendallBlock = 256;
+constexpr uint32_t kKendallMax = 4096;  // 12 B of LDS per entry: 48 KiB per snapshot
+
+__device__ __forceinline__ bool fbetter(float a, uint32_t ia, float b, uint32_t ib) {
+  return a > b || (a == b && ia < ib);
+}
+__device__ __forceinline__ bool ubetter(uint64_t a, uint32_t ia, uint64_t b, uint32_t ib) {
+  return a > b || (a == b && ia < ib);
+}
+
+__global__ __launch_bounds__(kKendallBlock) void kendall_kernel(uint32_t n_per, uint64_t n_x,
+                                                                const float* x, const uint64_t* y,
+                                                                const uint32_t* idx,
+                                                                uint64_t* counts, uint8_t* top1) {
+  extern __shared__ uint64_t s_dyn[];
+  uint64_t* s_y = s_dyn;                                   // [n_per]
+  float* s_x = reinterpret_cast<float*>(s_dyn + n_per);    // [n_per]
+  __shared__ uint64_t s_cnt[4][kKendallBlock / 64];
+  __shared__ float s_bx[kKendallBlock / 64];
+  __shared__ uint32_t s_bxi[kKendallBlock / 64], s_byi[kKendallBlock / 64];
+  __shared__ uint64_t s_by[kKendallBlock / 64];
+  __shared__ uint32_t s_bad;
+  const uint32_t snap = blockIdx.x;
+  const uint32_t tid = threadIdx.x;
+  const size_t base = (size_t)snap * n_per;
+
+  // gather the snapshot into LDS and find both argmaxes
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  float bx = 0.0f;
+  uint32_t bxi = kNone, byi = kNone;
+  uint64_t by = 0;
+  for (uint32_t i = tid; i < n_per; i += kKendallBlock) {
+    size_t e = idx ? (size_t)idx[base + i] : base + i;
+    if (e >= n_x) {  // an index outside x / y: flag the snapshot, read entry 0
+      s_bad = 1;
+      e = 0;
+    }
+    const float xv = x[e];
+    const uint64_t yv = y[e];
+    s_x[i] = xv;
+    s_y[i] = yv;
+    if (bxi == kNone || fbetter(xv, i, bx, bxi)) { bx = xv; bxi = i; }
+    if (byi == kNone || ubetter(yv, i, by, byi)) { by = yv; byi = i; }
+  }
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    const float ox = __shfl_xor(bx, m);
+    const uint32_t oxi = __shfl_xor(bxi, m);
+    const uint64_t oy = __shfl_xor(by, m);
+    const uint32_t oyi = __shfl_xor(byi, m);
+    if (oxi != kNone && (bxi == kNone || fbetter(ox, oxi, bx, bxi))) { bx = ox; bxi = oxi; }
+    if (oyi != kNone && (byi == kNone || ubetter(oy, oyi, by, byi))) { by = oy; byi = oyi; }
+  }
+  if ((tid & 63u) == 0) {
+    s_bx[tid >> 6] = bx;
+    s_bxi[tid >> 6] = bxi;
+    s_by[tid >> 6] = by;
+    s_byi[tid >> 6] = byi;
+  }
+  __syncthreads();
+
+  // pair classification: discordant, tied in x only, tied in y only, both
+  uint32_t nd = 0, ntx = 0, nty = 0, nb = 0;
+  const uint32_t wave0 = tid & ~63u;
+  for (uint32_t r = 0; r * kKendallBlock < n_per; ++r) {
+    const uint32_t i = r * kKendallBlock + tid;
+    const uint32_t first = r * kKendallBlock + wave0;  // smallest row of this wave
+    if (first >= n_per) break;
+    const bool row = i < n_per;
+    const float xa = s_x[row ? i : 0];
+    const uint64_t ya = s_y[row ? i : 0];
+    for (uint32_t j = first + 1; j < n_per; ++j) {
+      const float xb = s_x[j];
+      const uint64_t yb = s_y[j];
+      const bool on = row && j > i;
+      const bool tx = xa == xb;
+      const bool ty = ya == yb;
+      const bool gx = xa > xb;
+      const bool gy = ya > yb;
+      nb += (on && tx && ty) ? 1u : 0u;
+      ntx += (on && tx && !ty) ? 1u : 0u;
+      nty += (on && !tx && ty) ? 1u : 0u;
+      nd += (on && !tx && !ty && gx != gy) ? 1u : 0u;
+    }
+  }
+  uint64_t v[4] = {nd, ntx, nty, nb};
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) v[c] += __shfl_xor(v[c], m);
+    if ((tid & 63u) == 0) s_cnt[c][tid >> 6] = v[c];
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t tot[4] = {0, 0, 0, 0};
+    for (int w = 0; w < kKendallBlock / 64; ++w)
+      for (int c = 0; c < 4; ++c) tot[c] += s_cnt[c][w];
+    const uint64_t pairs = (uint64_t)n_per * (n_per - 1) / 2;
+    counts[(size_t)snap * 5 + 0] = pairs - tot[0] - tot[1] - tot[2] - tot[3];
+    counts[(size_t)snap * 5 + 1] = tot[0];
+    counts[(size_t)snap * 5 + 2] = tot[1];
+    counts[(size_t)snap * 5 + 3] = tot[2];
+    counts[(size_t)snap * 5 + 4] = tot[3];
+    float fx = s_bx[0];
+    uint32_t fxi = s_bxi[0], fyi = s_byi[0];
+    uint64_t fy = s_by[0];
+    for (int w = 1; w < kKendallBlock / 64; ++w) {
+      if (s_bxi[w] != kNone && (fxi == kNone || fbetter(s_bx[w], s_bxi[w], fx, fxi))) {
+        fx = s_bx[w];
+        fxi = s_bxi[w];
+      }
+      if (s_byi[w] != kNone && (fyi == kNone || ubetter(s_by[w], s_byi[w], fy, fyi))) {
+        fy = s_by[w];
+        fyi = s_byi[w];
+      }
+    }
+    top1[snap] = s_bad ? (uint8_t)255 : (uint8_t)(fxi == fyi);
+  }
+}
+
+hipError_t launch_ema_replay(uint32_t n, uint32_t max_hist, const uint64_t* gaps,
+                             const uint8_t* n_hist, uint32_t b_g, uint64_t tau, float* g,
+                             uint64_t* gq, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(ema_replay_kernel, dim3((n + 255) / 256), dim3(256), 0, s, n, max_hist, gaps,
+                     n_hist, b_g, tau, g, gq);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_fp32(uint32_t n, const uint8_t* turn, const float* g, const uint8_t* done,
+                             const uint32_t* d, const uint32_t* nn, float P, float* out,
+                             hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(score_fp32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, n, turn, g, done, d,
+                     nn, P, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
+                              const uint8_t* done, const uint32_t* d, const uint32_t* nn,
+                              uint32_t b_h, uint64_t p_z, uint64_t* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(score_fixed_kernel, dim3((n + 255) / 256), dim3(256), 0, s, n, turn, gq, done,
+                     d, nn, b_h, p_z, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const float* x,
+                          const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1,
+                          hipStream_t s) {
+  if (n_snap == 0) return hipSuccess;
+  const size_t lds = (size_t)(n_per ? n_per : 1) * (sizeof(uint64_t) + sizeof(float));
+  hipLaunchKernelGGL(kendall_kernel, dim3(n_snap), dim3(kKendallBlock), lds, s, n_per, n_x, x, y,
+                     idx, counts, top1);
+  return hipGetLastError();
+}
+
+uint32_t kendall_max_per() { return kKendallMax; }
+
+}  // namespace unison

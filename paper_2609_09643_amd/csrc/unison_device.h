@@ -1,0 +1,173 @@
+// unison_device.h -- device-side arithmetic and layouts of libunison (gfx950).
+//
+// The session register file of one simulation is a struct-of-arrays table
+// indexed by session id.  Each entry holds:
+//   mg    u64  low 32 bits: meta = phase | tier << 2 | turn << 4
+//              high 32 bits: the fp32 gap EMA g in microseconds (eq. (ema))
+//   gq    u64  the integer gap EMA g_q (eq. (gapq), eq. (ema-int))
+//   len   u32  resident KV length of the latest turn, tokens
+//   last  u64  time of the session's latest event, ns
+//   next  u64  time of its next arrival (Belady key), ns
+// A scan of SPEAR keys reads only mg: 8 bytes per table entry.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/unison.h"
+
+#pragma clang fp contract(off)
+
+namespace unison {
+
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr uint32_t kLut = 51;  // t = 0..50, eq. (hazard)
+
+enum : uint32_t { kArrive = 0, kGapStart = 1, kDone = 2 };
+enum : uint32_t { kSpear = 0, kLru = 1, kTimeout = 2, kBelady = 3 };
+enum : uint32_t { kTierNone = 0, kTierSram = 1, kTierHbm = 2 };
+enum : uint32_t { kUnseen = 0, kServing = 1, kGap = 2, kDoneP = 3 };
+enum : uint32_t { kOpEvict = 1, kOpExpire = 2, kOpBypass = 3, kOpPromote = 4, kOpSwap = 5,
+                  kOpVictim = 6, kOpPlace = 7 };
+
+__host__ __device__ __forceinline__ uint32_t meta_phase(uint32_t m) { return m & 3u; }
+__host__ __device__ __forceinline__ uint32_t meta_tier(uint32_t m) { return (m >> 2) & 3u; }
+__host__ __device__ __forceinline__ uint32_t meta_turn(uint32_t m) { return m >> 4; }
+__host__ __device__ __forceinline__ uint32_t make_meta(uint32_t ph, uint32_t tier, uint32_t turn) {
+  return ph | (tier << 2) | (turn << 4);
+}
+__host__ __device__ __forceinline__ uint32_t with_tier(uint32_t m, uint32_t tier) {
+  return (m & ~0xCu) | (tier << 2);
+}
+// A resident that is not being served may be evicted or migrated.
+__device__ __forceinline__ bool evictable(uint32_t m) {
+  return meta_tier(m) != kTierNone && meta_phase(m) != kServing;
+}
+
+// SplitMix64 finaliser (Steele, Lea and Flood, 2014).
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+// Hash of one decision record (event, op, a, b); digests sum these mod 2^64.
+__device__ __forceinline__ uint64_t rec_hash(uint32_t ev, uint32_t op, uint32_t a, uint32_t b) {
+  uint64_t w0 = ((uint64_t)ev << 8) | (uint64_t)op;
+  uint64_t w1 = ((uint64_t)a << 32) | (uint64_t)b;
+  return mix64(w0 ^ mix64(w1));
+}
+
+__device__ __forceinline__ uint64_t sat_add(uint64_t a, uint64_t b) {
+  uint64_t s = a + b;
+  return s < a ? ~0ull : s;
+}
+
+// a * b saturated to 2^64 - 1.
+__device__ __forceinline__ uint64_t sat_mul(uint64_t a, uint64_t b) {
+  return __umul64hi(a, b) ? ~0ull : a * b;
+}
+
+// eq. (ema) on the fp32 register, in microseconds, every operation rounded.
+__device__ __forceinline__ float ema_f32(float g, uint64_t gap_ns) {
+  float x = (float)((double)gap_ns / 1000.0);
+  float a = 3.0f * x;
+  float b = 7.0f * g;
+  return (a + b) / 10.0f;
+}
+
+// eq. (gapq) then eq. (ema-int) on the integer register.
+__device__ __forceinline__ uint64_t ema_int(uint64_t gq, uint64_t gap_ns, uint32_t b_g, uint64_t tau) {
+  uint64_t cap = b_g >= 64 ? ~0ull : ((1ull << b_g) - 1ull);
+  uint64_t x = gap_ns / tau;
+  if (x > cap) x = cap;
+  if (x < (1ull << 60) && gq < (1ull << 60)) return (3ull * x + 7ull * gq) / 10ull;
+  unsigned __int128 s = (unsigned __int128)3 * x + (unsigned __int128)7 * gq;
+  return (uint64_t)(s / 10u);
+}
+
+// Float hazard h(t) = d(t) / n(t) (eq. (hazard)); 0 where n(t) = 0.
+__device__ __forceinline__ float hazard_f32(uint32_t d, uint32_t n) {
+  return n ? (float)d / (float)n : 0.0f;
+}
+
+// eq. (uq) of h = d/n with Lambda = 2^b_h - 1: floor(d/n * Lambda + 1/2),
+// computed exactly as (2 d Lambda + n) / (2 n) and clipped to Lambda.
+__device__ __forceinline__ uint32_t hazard_q(uint32_t d, uint32_t n, uint32_t lambda) {
+  if (n == 0) return 0;
+  uint64_t q = (2ull * d * lambda + n) / (2ull * n);
+  return q > lambda ? lambda : (uint32_t)q;
+}
+
+// eq. (surv) + eq. (esp) for a live session.
+__device__ __forceinline__ float spear_f32(float h, float g, float P) {
+  float sigma = fmaxf(0.01f, 1.0f - h);
+  float a = g / sigma;
+  float b = 1.0f - sigma;
+  float c = b * P;
+  return a + c;
+}
+
+// eq. (survq), eq. (t1), eq. (t2), eq. (scoreq) for a live session, b_s = 64.
+__device__ __forceinline__ uint64_t spear_fixed(uint32_t hq, uint64_t gq, uint32_t lambda,
+                                                uint64_t p_z) {
+  uint32_t eps_q = (lambda + 50u) / 100u;  // floor(Lambda/100 + 1/2)
+  uint32_t sigma = lambda - hq;
+  if (sigma < eps_q) sigma = eps_q;
+  uint64_t t1, t2;
+  if (gq < (1ull << 47)) {
+    t1 = (gq * lambda) / sigma;
+  } else {
+    unsigned __int128 q = ((unsigned __int128)gq * lambda) / sigma;
+    t1 = q > (unsigned __int128)~0ull ? ~0ull : (uint64_t)q;  // saturates like the sum
+  }
+  uint64_t m = lambda - sigma;
+  if (p_z < (1ull << 47)) {
+    t2 = (m * p_z) / lambda;
+  } else {
+    t2 = (uint64_t)(((unsigned __int128)m * p_z) / lambda);
+  }
+  return sat_add(t1, t2);
+}
+
+// Device copy of the workspace regions one kernel launch needs.
+struct SimState {
+  uint64_t next_event;   // events of the trace already processed
+  uint64_t prev_t;       // time of the last processed event
+  uint64_t used_s, used_h, dma_free_at;
+  uint32_t n_res, n_table;
+  uint64_t log_len;
+  uint32_t hi;           // 1 + largest session id seen so far
+  uint32_t pad;
+};
+
+struct SimArgs {
+  const unison_sim_params* params;
+  const uint64_t* ev_off;
+  const uint64_t* sess_off;
+  const uint64_t* ev_t;
+  const uint32_t* ev_sid;
+  const uint32_t* ev_info;
+  const uint32_t* ev_len;
+  const uint64_t* ev_next;
+  const uint32_t* sess_kvb;
+  const uint32_t* lut_d;   // [n_luts][51]
+  const uint32_t* lut_n;
+  SimState* state;
+  unison_counters* counters;
+  uint64_t* t_mg;          // tables [n_sims][max_sessions]
+  uint64_t* t_gq;
+  uint32_t* t_len;
+  uint64_t* t_last;
+  uint64_t* t_next;
+  unison_record* log;
+  uint64_t max_events;
+  uint32_t n_sims;
+  uint32_t max_sessions;
+  uint32_t log_cap;
+  uint32_t flags;
+  uint32_t policy_override;
+  uint32_t pad;
+};
+
+}  // namespace unison

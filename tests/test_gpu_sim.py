@@ -1,0 +1,209 @@
+"""GPU parity of the batched simulation (libunison through its C ABI) against
+the CPU oracle: every counter, both digests and the full decision logs."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_09643_amd import synth
+from paper_2609_09643_amd.synth import POLICY_BELADY, POLICY_LRU, POLICY_SPEAR, POLICY_TIMEOUT
+from parity import compare_counters, oracle_counters, oracle_log, same_log
+from tracekit import trace_from_events
+
+pytestmark = pytest.mark.gpu
+
+VARIANTS = (0, 1, 2, 3, 4, 5)
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def Sim(*a, **k):
+    from paper_2609_09643_amd.unison import Simulator
+    return Simulator(*a, **k)
+
+
+def subset(w, sims):
+    return synth.Workload(w.name, w.traces, w.lut_pops, w.params[np.asarray(sims)].copy(),
+                          w.flat_luts)
+
+
+@pytest.fixture(scope="module")
+def c3():
+    return synth.c3_sweep()
+
+
+@pytest.fixture(scope="module")
+def c3_want(c3):
+    return oracle_counters(c3)
+
+
+def test_c1_counters_and_decision_logs():
+    w = synth.c1_tiny()
+    say("c1: 2 sims, 384 events")
+    s = Sim(w, log_cap=4096)
+    s.run(flags=2)
+    compare_counters(s.counters(), oracle_counters(w), label="c1")
+    for i in range(w.n_sims):
+        assert same_log(s.log(i), oracle_log(w, i)), "c1 sim %d decision log" % i
+
+
+def test_c3_full_sweep(c3, c3_want):
+    say("c3: %d sims" % c3.n_sims)
+    s = Sim(c3)
+    s.run()
+    compare_counters(s.counters(), c3_want, label="c3")
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_c3_every_kernel_variant(c3, c3_want, variant):
+    sims = list(range(0, c3.n_sims, 29))            # all policies, traces, pools
+    w = subset(c3, sims)
+    say("c3 variant %d: %d sims" % (variant, w.n_sims))
+    s = Sim(w, variant=variant)
+    s.run()
+    compare_counters(s.counters(), [c3_want[i] for i in sims], label="variant %d" % variant)
+
+
+def test_c3_decision_logs(c3):
+    sims = list(range(3, c3.n_sims, 257))
+    w = subset(c3, sims)
+    say("c3 logs: %d sims" % w.n_sims)
+    s = Sim(w, log_cap=8192)
+    s.run(flags=2)
+    for k, i in enumerate(sims):
+        assert same_log(s.log(k), oracle_log(c3, i)), "c3 sim %d log" % i
+
+
+@pytest.mark.parametrize("variant", [None, 3])
+def test_continue_matches_single_run(c3, c3_want, variant):
+    sims = list(range(5, c3.n_sims, 61))
+    w = subset(c3, sims)
+    say("continue: %d sims, variant %s" % (w.n_sims, variant))
+    s = Sim(w, variant=variant)
+    s.run(max_events=100)
+    compare_counters(s.counters(), oracle_counters(w, max_events=100), label="prefix 100")
+    s.run(flags=1, max_events=150)
+    compare_counters(s.counters(), oracle_counters(w, max_events=250), label="prefix 250")
+    s.run(flags=1)
+    compare_counters(s.counters(), [c3_want[i] for i in sims], label="resumed")
+
+
+def test_determinism(c3):
+    w = subset(c3, list(range(0, c3.n_sims, 7)))
+    s = Sim(w)
+    s.run()
+    a = s.counters().copy()
+    s.run()
+    b = s.counters()
+    assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+
+
+def test_c2_paper_scale():
+    w = synth.c2_paper_scale()
+    say("c2: 4 sims x %d events" % w.traces[0].n_events)
+    s = Sim(w, log_cap=1 << 17)
+    s.run(flags=2)
+    compare_counters(s.counters(), oracle_counters(w), label="c2")
+    assert same_log(s.log(0), oracle_log(w, 0, log_cap=1 << 17)), "c2 SPEAR log"
+
+
+def test_c4_large_live_set_prefix():
+    w = synth.c4_large(n_traces=1)
+    sims = [0, 3]
+    ww = subset(w, sims)
+    n1, n2 = 6000, 9000
+    say("c4: %d sims, 65,536 sessions, prefixes %d / %d events" % (len(sims), n1, n2))
+    s = Sim(ww)
+    s.run(max_events=n1)
+    compare_counters(s.counters(), oracle_counters(ww, max_events=n1), label="c4 prefix")
+    s.run(flags=1, max_events=n2 - n1)
+    got = s.counters()
+    compare_counters(got, oracle_counters(ww, max_events=n2), label="c4 resumed prefix")
+    assert int(got[0]["evict"]) > 0 and int(got[0]["score_evals"]) > 10_000_000
+
+
+def edge_workload(traces, rows):
+    luts = [np.array([1, 2, 2, 3, 30, 51, 60], np.uint32), None]
+    return synth.Workload("edge", traces, luts, rows, flat_luts=[(1, 3, 7)])
+
+
+def edge_rows(n_traces, rng):
+    rows = []
+    for ti in range(n_traces):
+        for pol in (POLICY_SPEAR, POLICY_LRU, POLICY_TIMEOUT, POLICY_BELADY):
+            for k in range(3):
+                p = synth.default_params(1)
+                p["policy"], p["trace"], p["lut"] = pol, ti, int(rng.integers(0, 2))
+                p["tide"] = int(rng.integers(0, 2))
+                p["score_mode"] = int(pol == POLICY_SPEAR and k == 2)
+                p["b_h"] = int(rng.choice([8, 12, 16]))
+                p["cap_sram_B"] = int(rng.choice([0, 1, 64, 300])) * synth.MIB
+                p["cap_hbm_B"] = int(rng.choice([0, 1, 2, 8])) * synth.GIB
+                p["n_slots"] = int(rng.choice([1, 2, 5, 1000]))
+                p["ttl_ns"] = int(rng.choice([1, 2, 10])) * synth.NS
+                p["dma_B_per_us"] = int(rng.choice([1, 1000, 100_000]))
+                rows.append(p[0])
+    return np.array(rows, dtype=synth.SIM_PARAMS_DTYPE)
+
+
+@pytest.mark.parametrize("n_sess", [1, 5, 16, 17, 33, 64, 65, 100, 256, 257, 300])
+def test_ragged_session_counts(n_sess):
+    rng = np.random.default_rng(n_sess)
+    tr = synth.tiny_trace(seed=900 + n_sess, n_sessions=n_sess, turns=int(rng.integers(1, 6)))
+    rows = edge_rows(1, rng)
+    w = edge_workload([tr], rows)
+    say("ragged: %d sessions, %d events, %d sims" % (n_sess, tr.n_events, w.n_sims))
+    s = Sim(w, log_cap=1 << 14)
+    s.run(flags=2)
+    compare_counters(s.counters(), oracle_counters(w), label="ragged %d" % n_sess)
+    for i in range(0, w.n_sims, 5):
+        assert same_log(s.log(i), oracle_log(w, i)), "ragged %d sim %d" % (n_sess, i)
+
+
+def test_mixed_traces_and_empty_trace():
+    rng = np.random.default_rng(77)
+    empty = trace_from_events([], 1)
+    trs = [synth.tiny_trace(seed=5, n_sessions=12, turns=4), empty,
+           synth.tiny_trace(seed=6, n_sessions=9, turns=7)]
+    w = edge_workload(trs, edge_rows(3, rng))
+    for v in (None, 3):
+        s = Sim(w, variant=v)
+        s.run()
+        got = s.counters()
+        compare_counters(got, oracle_counters(w), label="mixed variant %s" % v)
+        assert int(got[12]["events"]) == 0
+
+
+def test_bad_trace_is_reported():
+    from paper_2609_09643_amd.unison import E_BAD_TRACE, UnisonError
+    A, G = synth.KIND_ARRIVE, synth.KIND_GAP_START
+    ev = [(10, 0, A, 0, 3), (20, 0, G, 0, 0), (30, 1, A, 0, 4), (40, 1, G, 0, 0),
+          (50, 0, A, 2, 5), (60, 0, G, 2, 0)]           # turn 2 after turn 0
+    tr = trace_from_events(ev, 2)
+    p = synth.default_params(2)
+    p["policy"] = [POLICY_LRU, POLICY_SPEAR]
+    p["cap_sram_B"], p["cap_hbm_B"] = 1 << 20, 1 << 30
+    w = synth.Workload("bad", [tr], [tr.turns], p)
+    s = Sim(w)
+    s.run()
+    with pytest.raises(UnisonError) as e:
+        s.counters()
+    assert e.value.code == E_BAD_TRACE
+    got = s.counters(check=False)
+    want = oracle_counters_allow_error(w)
+    compare_counters(got, want, label="bad trace")
+    assert int(got[0]["error"]) == 5
+
+
+def oracle_counters_allow_error(w):
+    D, N = oracle.luts_for(w)
+    out = []
+    for i in range(w.n_sims):
+        row = w.params[i]
+        rc, cnt, _, _, _ = oracle.run(w.traces[0], row, D[int(row["lut"])], N[int(row["lut"])])
+        assert rc == -2
+        out.append(cnt)
+    return out
