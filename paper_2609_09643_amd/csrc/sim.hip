@@ -10,19 +10,21 @@
 // The event loop of a simulation is sequential; parallelism comes from
 // running many simulations at once and from the scan inside each event.
 // Two table layouts share one event engine:
-//   RegTable<G, EPL>  a group of G lanes (a quarter, half or whole wave) per
-//                     simulation; each lane owns EPL sessions (sid = j*G +
-//                     lane) and keeps their register-file entries in VGPRs.
-//                     Scores are computed per entry and reduced with
-//                     cross-lane shuffles inside the group: no LDS traffic
-//                     and no barriers for the table.
+//   RegTable<G, EPL>  a group of G lanes (4 to 64) per simulation; each lane
+//                     owns EPL sessions (sid = j*G + lane) and keeps their
+//                     register-file entries in VGPRs.  Keys are computed per
+//                     entry and reduced with DPP butterflies inside the
+//                     group (quad_perm, row_half_mirror, row_mirror, then
+//                     ds_swizzle / bpermute across rows): no LDS traffic and
+//                     no barriers for the table.
 //   MemTable<BLOCK>   one workgroup per simulation; the table lives in the
 //                     workspace (HBM / L2 / MALL) and each event streams the
 //                     populated window of it with coalesced 8-byte loads;
 //                     block reductions go through LDS.
-// All per-simulation scalars (capacities in use, DMA state, counters) are
-// replicated in every lane of the group and updated identically, so control
-// flow is uniform within a group.
+// The engine is instantiated per policy and score mode, so each simulation
+// keeps only the register-file fields its keys read.  All per-simulation
+// scalars are replicated in every lane of the group and updated identically,
+// so control flow is uniform within a group.
 #include <hip/hip_runtime.h>
 
 #include "unison_device.h"
@@ -30,6 +32,25 @@
 #pragma clang fp contract(off)
 
 namespace unison {
+
+// ------------------------------------------------------- cross-lane moves
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+// Partner value for butterfly step M.  Before step M every aligned block of
+// M lanes holds one value; the partner lane lies in the sibling block.
+template <int M>
+__device__ __forceinline__ uint32_t xchg(uint32_t v) {
+  if constexpr (M == 1) return dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  else if constexpr (M == 2) return dpp<0x4E>(v);  // quad_perm [2,3,0,1]
+  else if constexpr (M == 4) return dpp<0x141>(v);  // row_half_mirror
+  else if constexpr (M == 8) return dpp<0x140>(v);  // row_mirror
+  else if constexpr (M == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F);  // xor 16
+  else return (uint32_t)__shfl_xor((int)v, 32);
+}
 
 struct Cand {
   uint64_t key;
@@ -45,26 +66,79 @@ __device__ __forceinline__ bool min_better(uint64_t ka, uint32_t sa, uint64_t kb
 __device__ __forceinline__ Cand cand_none_max() { return Cand{0ull, kNone}; }
 __device__ __forceinline__ Cand cand_none_min() { return Cand{~0ull, kNone}; }
 
-// Butterfly reduction over aligned groups of W lanes; every lane of the
-// group ends with the same winner (ties to the smaller session id).
+template <int W, int M, bool MAX>
+__device__ __forceinline__ void reduce_step(Cand& c) {
+  if constexpr (M < W) {
+    const uint32_t klo = xchg<M>((uint32_t)c.key);
+    const uint32_t khi = xchg<M>((uint32_t)(c.key >> 32));
+    const uint32_t s = xchg<M>(c.sid);
+    const uint64_t k = ((uint64_t)khi << 32) | klo;
+    const bool take = MAX ? max_better(k, s, c.key, c.sid) : min_better(k, s, c.key, c.sid);
+    c.key = take ? k : c.key;
+    c.sid = take ? s : c.sid;
+    reduce_step<W, M * 2, MAX>(c);
+  }
+}
+
+// Every lane of an aligned group of W lanes ends with the winner (ties to
+// the smaller session id).
 template <int W, bool MAX>
 __device__ __forceinline__ Cand reduce_group(Cand c) {
-#pragma unroll
-  for (int m = 1; m < W; m <<= 1) {
-    uint64_t ok = __shfl_xor(c.key, m, W);
-    uint32_t os = __shfl_xor(c.sid, m, W);
-    bool take = MAX ? max_better(ok, os, c.key, c.sid) : min_better(ok, os, c.key, c.sid);
-    c.key = take ? ok : c.key;
-    c.sid = take ? os : c.sid;
-  }
+  reduce_step<W, 1, MAX>(c);
   return c;
 }
 
-template <int W>
-__device__ __forceinline__ uint64_t reduce_sum_group(uint64_t v) {
-#pragma unroll
-  for (int m = 1; m < W; m <<= 1) v += __shfl_xor(v, m, W);
-  return v;
+__device__ __forceinline__ uint32_t uni32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+__device__ __forceinline__ uint64_t uni64(uint64_t v) {
+  return ((uint64_t)uni32((uint32_t)(v >> 32)) << 32) | uni32((uint32_t)v);
+}
+
+// ------------------------------------------------------------ keys
+
+template <uint32_t POL, uint32_t SMODE>
+struct Pol {
+  static constexpr bool spear = POL == kSpear;
+  static constexpr bool fixed = spear && SMODE == 1;
+  static constexpr bool belady = POL == kBelady;
+  static constexpr bool timeout = POL == kTimeout;
+  static constexpr bool recency = POL == kLru || POL == kTimeout;
+  static constexpr bool has_inf = spear || belady;
+  static constexpr uint64_t inf_key = (spear && !fixed) ? 0x7F800000ull : ~0ull;
+};
+
+struct KeyCtx {
+  const float* hf;      // LDS [52]
+  const uint32_t* hq;   // LDS [52]
+  float P;
+  uint32_t lambda;
+  uint64_t p_z;
+};
+
+// "Larger key = evict first".  SPEAR: the score (eq. (esp) or eq. (scoreq));
+// completed sessions take S_max.  LRU / timeout: older last event first.
+// Belady: later next arrival first.
+template <uint32_t POL, uint32_t SMODE>
+__device__ __forceinline__ uint64_t key_of(const KeyCtx& K, uint32_t meta, float g, uint64_t gq,
+                                           uint64_t last, uint64_t next) {
+  using PT = Pol<POL, SMODE>;
+  if constexpr (PT::spear) {
+    uint32_t t = meta_turn(meta);
+    t = t < 50u ? t : 50u;
+    const bool done = meta_phase(meta) == kDoneP;
+    if constexpr (PT::fixed) {
+      const uint64_t s = spear_fixed(K.hq[t], gq, K.lambda, K.p_z);
+      return done ? ~0ull : s;
+    } else {
+      const float s = spear_f32(K.hf[t], g, K.P);
+      return done ? 0x7F800000ull : (uint64_t)__float_as_uint(s);
+    }
+  } else if constexpr (PT::belady) {
+    return next;
+  } else {
+    return ~0ull - last;
+  }
 }
 
 struct Entry {
@@ -77,41 +151,11 @@ struct Entry {
   uint64_t next;
 };
 
-// What a key needs besides the entry: policy, hazard table, penalty.
-struct KeyCtx {
-  uint32_t pol;
-  uint32_t smode;
-  const float* hf;      // LDS [52]
-  const uint32_t* hq;   // LDS [52]
-  float P;
-  uint32_t lambda;
-  uint64_t p_z;
-};
+// ------------------------------------------------------------ tables
 
-// "Larger key = evict first".  SPEAR: the score (eq. (esp) or eq. (scoreq));
-// completed sessions take S_max.  LRU / timeout: older last event first.
-// Belady: later next arrival first.
-__device__ __forceinline__ uint64_t key_of(const KeyCtx& K, uint32_t meta, float g, uint64_t gq,
-                                           uint64_t last, uint64_t next) {
-  if (K.pol == kSpear) {
-    uint32_t t = meta_turn(meta);
-    t = t < 50u ? t : 50u;
-    bool done = meta_phase(meta) == kDoneP;
-    if (K.smode) {
-      uint64_t s = spear_fixed(K.hq[t], gq, K.lambda, K.p_z);
-      return done ? ~0ull : s;
-    }
-    float s = spear_f32(K.hf[t], g, K.P);
-    return done ? 0x7F800000ull : (uint64_t)__float_as_uint(s);
-  }
-  if (K.pol == kBelady) return next;
-  return ~0ull - last;
-}
-
-// ------------------------------------------------------------------ tables
-
-template <int G, int EPL>
+template <int G, int EPL, uint32_t POL, uint32_t SMODE>
 struct RegTable {
+  using PT = Pol<POL, SMODE>;
   uint32_t lane;
   uint32_t meta[EPL];
   float g[EPL];
@@ -131,48 +175,49 @@ struct RegTable {
     for (int j = 1; j < EPL; ++j) v = (js == (uint32_t)j) ? a[j] : v;
     return v;
   }
+  template <class T>
+  __device__ __forceinline__ T bcast(const T (&a)[EPL], uint32_t sid) const {
+    return __shfl(pick(a, sid / G), sid % G, G);
+  }
 
   __device__ __forceinline__ void event_begin() {}
   __device__ __forceinline__ void grow(uint32_t) {}
 
   __device__ __forceinline__ Entry read(uint32_t sid) const {
-    uint32_t owner = sid % G, js = sid / G;
     Entry e;
-    e.meta = __shfl(pick(meta, js), owner, G);
-    e.g = __shfl(pick(g, js), owner, G);
-    e.gq = __shfl(pick(gq, js), owner, G);
-    e.len = __shfl(pick(len, js), owner, G);
-    e.kvb = __shfl(pick(kvb, js), owner, G);
-    e.last = __shfl(pick(last, js), owner, G);
-    e.next = __shfl(pick(next, js), owner, G);
+    e.meta = bcast(meta, sid);
+    e.g = bcast(g, sid);
+    e.gq = PT::fixed ? bcast(gq, sid) : 0ull;
+    e.len = bcast(len, sid);
+    e.kvb = bcast(kvb, sid);
+    e.last = bcast(last, sid);
+    e.next = PT::belady ? bcast(next, sid) : ~0ull;
     return e;
   }
-  // size in bytes and meta of one entry
   __device__ __forceinline__ void read_size(uint32_t sid, uint64_t& size, uint32_t& m) const {
-    uint32_t owner = sid % G, js = sid / G;
-    uint32_t l = __shfl(pick(len, js), owner, G);
-    uint32_t k = __shfl(pick(kvb, js), owner, G);
-    m = __shfl(pick(meta, js), owner, G);
+    const uint32_t l = bcast(len, sid);
+    const uint32_t k = bcast(kvb, sid);
+    m = bcast(meta, sid);
     size = (uint64_t)l * k;
   }
 
   __device__ __forceinline__ void write(uint32_t sid, const Entry& e) {
-    uint32_t owner = sid % G, js = sid / G;
-    bool mine = lane == owner;
+    const uint32_t js = sid / G;
+    const bool mine = lane == sid % G;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
-      bool w = mine && js == (uint32_t)j;
+      const bool w = mine && js == (uint32_t)j;
       meta[j] = w ? e.meta : meta[j];
       g[j] = w ? e.g : g[j];
-      gq[j] = w ? e.gq : gq[j];
+      if constexpr (PT::fixed) gq[j] = w ? e.gq : gq[j];
       len[j] = w ? e.len : len[j];
       last[j] = w ? e.last : last[j];
-      next[j] = w ? e.next : next[j];
+      if constexpr (PT::belady) next[j] = w ? e.next : next[j];
     }
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) {
-    uint32_t owner = sid % G, js = sid / G;
-    bool mine = lane == owner;
+    const uint32_t js = sid / G;
+    const bool mine = lane == sid % G;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) meta[j] = (mine && js == (uint32_t)j) ? m : meta[j];
   }
@@ -180,7 +225,9 @@ struct RegTable {
   // The per-event scan: every entry's key, kept for this event's reductions.
   __device__ __forceinline__ void scan(const KeyCtx& K) {
 #pragma unroll
-    for (int j = 0; j < EPL; ++j) key[j] = key_of(K, meta[j], g[j], gq[j], last[j], next[j]);
+    for (int j = 0; j < EPL; ++j)
+      key[j] = key_of<POL, SMODE>(K, meta[j], g[j], PT::fixed ? gq[j] : 0ull, last[j],
+                                  PT::belady ? next[j] : 0ull);
   }
 
   // argmax / argmin of the keys over evictable entries in `tier` (0 = any).
@@ -189,26 +236,25 @@ struct RegTable {
     Cand c = MAX ? cand_none_max() : cand_none_min();
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
-      bool ok = evictable(meta[j]) && (tier == 0 || meta_tier(meta[j]) == tier);
-      uint32_t s = sid_of(j);
-      bool take = ok && (MAX ? max_better(key[j], s, c.key, c.sid) : min_better(key[j], s, c.key, c.sid));
+      const bool ok = evictable(meta[j]) && (tier == 0 || meta_tier(meta[j]) == tier);
+      const uint32_t s = sid_of(j);
+      const bool take =
+          ok && (MAX ? max_better(key[j], s, c.key, c.sid) : min_better(key[j], s, c.key, c.sid));
       c.key = take ? key[j] : c.key;
       c.sid = take ? s : c.sid;
     }
     return reduce_group<G, MAX>(c);
   }
-  __device__ __forceinline__ Cand argmax_first(uint32_t tier, const KeyCtx& K) const {
-    return select<true>(tier, K);
-  }
+  __device__ __forceinline__ Cand argmax_first(const KeyCtx& K) const { return select<true>(0, K); }
 
   // Smallest evictable session idle for longer than ttl (timeout policy).
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) const {
     Cand c = cand_none_min();
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
-      bool ok = evictable(meta[j]) && now - last[j] > ttl;
-      uint32_t s = sid_of(j);
-      bool take = ok && s < c.sid;
+      const bool ok = evictable(meta[j]) && now - last[j] > ttl;
+      const uint32_t s = sid_of(j);
+      const bool take = ok && s < c.sid;
       c.sid = take ? s : c.sid;
       c.key = take ? 0ull : c.key;
     }
@@ -216,10 +262,14 @@ struct RegTable {
   }
 };
 
-// Table in the workspace, one workgroup per simulation.
-template <int BLOCK>
+// Table in the workspace, one workgroup per simulation.  Uniform values read
+// from memory or LDS go through readfirstlane so the engine's scalars live in
+// SGPRs.
+template <int BLOCK, uint32_t POL, uint32_t SMODE>
 struct MemTable {
+  using PT = Pol<POL, SMODE>;
   static constexpr int NW = BLOCK / 64;
+  static constexpr int UNROLL = 4;
   uint64_t* mg;
   uint64_t* gq;
   uint32_t* len;
@@ -238,20 +288,20 @@ struct MemTable {
   // any wave goes on to overwrite it.
   __device__ __forceinline__ Entry read(uint32_t sid) const {
     Entry e;
-    uint64_t x = mg[sid];
+    const uint64_t x = uni64(mg[sid]);
     e.meta = (uint32_t)x;
     e.g = __uint_as_float((uint32_t)(x >> 32));
-    e.gq = gq[sid];
-    e.len = len[sid];
-    e.kvb = kvb[sid];
-    e.last = last[sid];
-    e.next = next[sid];
+    e.gq = PT::fixed ? uni64(gq[sid]) : 0ull;
+    e.len = uni32(len[sid]);
+    e.kvb = uni32(kvb[sid]);
+    e.last = uni64(last[sid]);
+    e.next = PT::belady ? uni64(next[sid]) : ~0ull;
     __syncthreads();
     return e;
   }
   __device__ __forceinline__ void read_size(uint32_t sid, uint64_t& size, uint32_t& m) const {
-    m = (uint32_t)mg[sid];
-    size = (uint64_t)len[sid] * kvb[sid];
+    m = uni32((uint32_t)mg[sid]);
+    size = (uint64_t)uni32(len[sid]) * uni32(kvb[sid]);
     __syncthreads();
   }
   // Every thread stores the same values, so each thread's later loads see
@@ -259,13 +309,13 @@ struct MemTable {
   // writes an entry that another wave has still to read.
   __device__ __forceinline__ void write(uint32_t sid, const Entry& e) {
     mg[sid] = (uint64_t)e.meta | ((uint64_t)__float_as_uint(e.g) << 32);
-    gq[sid] = e.gq;
+    if constexpr (PT::fixed) gq[sid] = e.gq;
     len[sid] = e.len;
     last[sid] = e.last;
-    next[sid] = e.next;
+    if constexpr (PT::belady) next[sid] = e.next;
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) {
-    uint64_t x = mg[sid];
+    const uint64_t x = mg[sid];
     mg[sid] = (x & 0xFFFFFFFF00000000ull) | m;
   }
 
@@ -281,45 +331,53 @@ struct MemTable {
     Cand r = buf[0];
 #pragma unroll
     for (int w = 1; w < NW; ++w) {
-      Cand o = buf[w];
-      bool take = MAX ? max_better(o.key, o.sid, r.key, r.sid) : min_better(o.key, o.sid, r.key, r.sid);
+      const Cand o = buf[w];
+      const bool take = MAX ? max_better(o.key, o.sid, r.key, r.sid) : min_better(o.key, o.sid, r.key, r.sid);
       r = take ? o : r;
     }
+    r.key = uni64(r.key);
+    r.sid = uni32(r.sid);
     return r;
+  }
+
+  __device__ __forceinline__ uint64_t key_at(const KeyCtx& K, uint32_t i, uint64_t x) const {
+    const uint32_t m = (uint32_t)x;
+    const float gv = __uint_as_float((uint32_t)(x >> 32));
+    return key_of<POL, SMODE>(K, m, gv, PT::fixed ? gq[i] : 0ull, PT::recency ? last[i] : 0ull,
+                              PT::belady ? next[i] : 0ull);
   }
 
   // Streams the window and reduces the keys of evictable entries in `tier`.
   template <bool MAX>
   __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx& K) {
     Cand c = MAX ? cand_none_max() : cand_none_min();
-    const bool need_gq = K.pol == kSpear && K.smode;
-    for (uint32_t i = tid; i < hi; i += BLOCK) {
-      uint64_t x = mg[i];
-      uint32_t m = (uint32_t)x;
-      float gv = __uint_as_float((uint32_t)(x >> 32));
-      uint64_t k;
-      if (K.pol == kSpear && !need_gq) {
-        k = key_of(K, m, gv, 0, 0, 0);
-      } else {
-        k = key_of(K, m, gv, need_gq ? gq[i] : 0ull, K.pol != kBelady ? last[i] : 0ull,
-                   K.pol == kBelady ? next[i] : 0ull);
+    for (uint32_t base = tid; base < hi; base += UNROLL * BLOCK) {
+      uint64_t x[UNROLL];
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        const uint32_t i = base + u * BLOCK;
+        x[u] = i < hi ? mg[i] : 0ull;
       }
-      bool ok = evictable(m) && (tier == 0 || meta_tier(m) == tier);
-      bool take = ok && (MAX ? max_better(k, i, c.key, c.sid) : min_better(k, i, c.key, c.sid));
-      c.key = take ? k : c.key;
-      c.sid = take ? i : c.sid;
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        const uint32_t i = base + u * BLOCK;
+        const uint32_t m = (uint32_t)x[u];
+        const bool ok = i < hi && evictable(m) && (tier == 0 || meta_tier(m) == tier);
+        const uint64_t k = key_at(K, i < hi ? i : 0u, x[u]);
+        const bool take = ok && (MAX ? max_better(k, i, c.key, c.sid) : min_better(k, i, c.key, c.sid));
+        c.key = take ? k : c.key;
+        c.sid = take ? i : c.sid;
+      }
     }
     return block_reduce<MAX>(c);
   }
   // The first reduction of an event is the full-table scan.
-  __device__ __forceinline__ Cand argmax_first(uint32_t tier, const KeyCtx& K) {
-    return select<true>(tier, K);
-  }
+  __device__ __forceinline__ Cand argmax_first(const KeyCtx& K) { return select<true>(0, K); }
 
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) {
     Cand c = cand_none_min();
     for (uint32_t i = tid; i < hi; i += BLOCK) {
-      uint32_t m = (uint32_t)mg[i];
+      const uint32_t m = (uint32_t)mg[i];
       if (evictable(m) && now - last[i] > ttl && i < c.sid) {
         c.sid = i;
         c.key = 0;
@@ -336,14 +394,77 @@ struct Scalars {
   uint32_t n_res, n_table, hi;
 };
 
+// Counters as kept during a run: event-bounded counts in 32 bits.
+struct Cnt {
+  uint32_t requests, hit_sram, hit_hbm, miss, bypass, evict, expire, promote, swap, tide_passes,
+      events;
+  uint64_t dma_bytes, tokens_total, tokens_computed, extra_prefill, score_evals, resident_evals,
+      digest, victim_digest, error;
+  double amat, ttft;
+};
+
+__device__ __forceinline__ Cnt cnt_from(const unison_counters& c) {
+  Cnt k;
+  k.requests = (uint32_t)c.requests;
+  k.hit_sram = (uint32_t)c.hit_sram;
+  k.hit_hbm = (uint32_t)c.hit_hbm;
+  k.miss = (uint32_t)c.miss;
+  k.bypass = (uint32_t)c.bypass;
+  k.evict = (uint32_t)c.evict;
+  k.expire = (uint32_t)c.expire;
+  k.promote = (uint32_t)c.promote;
+  k.swap = (uint32_t)c.swap;
+  k.tide_passes = (uint32_t)c.tide_passes;
+  k.events = (uint32_t)c.events;
+  k.dma_bytes = c.dma_bytes;
+  k.tokens_total = c.tokens_total;
+  k.tokens_computed = c.tokens_computed;
+  k.extra_prefill = c.extra_prefill_tok;
+  k.score_evals = c.score_evals;
+  k.resident_evals = c.resident_evals;
+  k.digest = c.digest;
+  k.victim_digest = c.victim_digest;
+  k.error = c.error;
+  k.amat = c.amat_sum_ns;
+  k.ttft = c.ttft_sum_ns;
+  return k;
+}
+
+__device__ __forceinline__ unison_counters cnt_to(const Cnt& k) {
+  unison_counters c;
+  c.requests = k.requests;
+  c.hit_sram = k.hit_sram;
+  c.hit_hbm = k.hit_hbm;
+  c.miss = k.miss;
+  c.bypass = k.bypass;
+  c.evict = k.evict;
+  c.expire = k.expire;
+  c.promote = k.promote;
+  c.swap = k.swap;
+  c.dma_bytes = k.dma_bytes;
+  c.tide_passes = k.tide_passes;
+  c.tokens_total = k.tokens_total;
+  c.tokens_computed = k.tokens_computed;
+  c.extra_prefill_tok = k.extra_prefill;
+  c.score_evals = k.score_evals;
+  c.resident_evals = k.resident_evals;
+  c.digest = k.digest;
+  c.victim_digest = k.victim_digest;
+  c.events = k.events;
+  c.error = k.error;
+  c.amat_sum_ns = k.amat;
+  c.ttft_sum_ns = k.ttft;
+  return c;
+}
+
 struct LogSink {
   unison_record* rec;  // this simulation's records, or null
   uint32_t cap;
   bool lead;           // the one lane that stores records
 };
 
-__device__ __forceinline__ void emit(unison_counters& C, Scalars& S, const LogSink& L, uint32_t ev,
-                                     uint32_t op, uint32_t a, uint32_t b) {
+__device__ __forceinline__ void emit(Cnt& C, Scalars& S, const LogSink& L, uint32_t ev, uint32_t op,
+                                     uint32_t a, uint32_t b) {
   C.digest += rec_hash(ev, op, a, b);
   if (L.rec) {
     if (L.lead && S.log_len < L.cap) {
@@ -368,6 +489,23 @@ struct TraceView {
   uint32_t n_sess;
 };
 
+struct Ev {
+  uint64_t t;
+  uint32_t sid, info, len;
+  uint64_t next;
+};
+
+template <bool NEXT>
+__device__ __forceinline__ Ev load_ev(const TraceView& tr, uint64_t e) {
+  Ev v;
+  v.t = tr.t[e];
+  v.sid = tr.sid[e];
+  v.info = tr.info[e];
+  v.len = tr.len[e];
+  v.next = NEXT ? tr.next[e] : ~0ull;
+  return v;
+}
+
 template <class Tab>
 __device__ __forceinline__ void release(Tab& T, Scalars& S, uint32_t sid) {
   uint64_t size;
@@ -379,22 +517,23 @@ __device__ __forceinline__ void release(Tab& T, Scalars& S, uint32_t sid) {
   T.set_meta(sid, with_tier(m, kTierNone));
 }
 
-// Algorithm 1 over events [S.next, end) of one simulation.
-template <class Tab>
+// Algorithm 1 over the simulation's events [next_event, next_event + max_events).
+template <uint32_t POL, uint32_t SMODE, class Tab>
 __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
-                           Scalars& S, unison_counters& C, const LogSink& L, uint64_t& next_event,
+                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& next_event,
                            uint64_t max_events) {
-  const uint32_t pol = K.pol;
-  const bool has_inf = pol == kSpear || pol == kBelady;
-  const uint64_t inf_key = (pol == kSpear && !K.smode) ? 0x7F800000ull : ~0ull;
+  using PT = Pol<POL, SMODE>;
   uint64_t e = next_event;
-  uint64_t end = tr.n_ev - e < max_events ? tr.n_ev : e + max_events;
+  const uint64_t end = (e >= tr.n_ev || tr.n_ev - e < max_events) ? tr.n_ev : e + max_events;
+  if (e >= end) return;
+  Ev cur = load_ev<PT::belady>(tr, e);
   for (; e < end; ++e) {
+    // the next event's record is in flight while this one is processed
+    const Ev nxt = load_ev<PT::belady>(tr, e + 1 < end ? e + 1 : e);
     T.event_begin();
-    const uint64_t now = tr.t[e];
-    const uint32_t sid = tr.sid[e];
-    const uint32_t info = tr.info[e];
-    const uint32_t kind = info >> 24, turn = info & 0xFFFFFFu;
+    const uint64_t now = cur.t;
+    const uint32_t sid = cur.sid;
+    const uint32_t kind = cur.info >> 24, turn = cur.info & 0xFFFFFFu;
     const uint32_t ev = (uint32_t)e;
     if (sid >= tr.n_sess || now < S.prev_t || kind > kDone) {
       C.error = e + 1;
@@ -403,9 +542,9 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     S.prev_t = now;
 
     // timeout policy: TTL timers that fired since the previous event
-    if (pol == kTimeout) {
+    if constexpr (PT::timeout) {
       for (;;) {
-        uint32_t v = T.first_idle(now, P.ttl_ns);
+        const uint32_t v = T.first_idle(now, P.ttl_ns);
         if (v == kNone) break;
         emit(C, S, L, ev, kOpExpire, v, kNone);
         C.expire++;
@@ -426,16 +565,16 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         x.len = 0;
         len_prev = 0;
       } else {
-        bad = ph != kGap || turn != meta_turn(x.meta) + 1 || tr.len[e] < x.len;
-        uint64_t gap = now - x.last;  // eq. (gap)
+        bad = ph != kGap || turn != meta_turn(x.meta) + 1 || cur.len < x.len;
+        const uint64_t gap = now - x.last;  // eq. (gap)
         x.g = ema_f32(x.g, gap);
-        x.gq = ema_int(x.gq, gap, P.b_g, P.tau_ns);
+        if constexpr (PT::fixed) x.gq = ema_int(x.gq, gap, P.b_g, P.tau_ns);
       }
       x.meta = make_meta(kServing, tier0, turn);
     } else {
       bad = ph != kServing;
       x.meta = make_meta(kind == kGapStart ? kGap : kDoneP, tier0, meta_turn(x.meta));
-      x.next = kind == kGapStart ? tr.next[e] : ~0ull;
+      x.next = kind == kGapStart ? cur.next : ~0ull;
     }
     if (bad) {
       C.error = e + 1;
@@ -454,12 +593,12 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     C.score_evals += S.n_table;
     C.resident_evals += S.n_res;
     T.scan(K);
-    const Cand v0 = T.argmax_first(0, K);
+    const Cand v0 = T.argmax_first(K);
     C.victim_digest += rec_hash(ev, kOpVictim, v0.sid, kNone);
 
     if (kind == kArrive) {
       // eq. (hr-amat), eq. (prered), eq. (reuse)
-      const uint64_t ln = tr.len[e];
+      const uint64_t ln = cur.len;
       const uint64_t dlen = ln - len_prev;
       const uint64_t kb = x.kvb;
       C.requests++;
@@ -470,8 +609,8 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         const double a = (double)(ln * kb) * t_mem;
         const double b = (double)((uint64_t)len_prev * kb) * t_mem;
         const double c = (double)dlen * P.t_p_ns_per_tok;
-        C.amat_sum_ns += a;
-        C.ttft_sum_ns += b + c;
+        C.amat += a;
+        C.ttft += b + c;
         C.tokens_computed += dlen;
         const uint64_t old = (uint64_t)len_prev * kb;
         if (tier0 == kTierSram) S.used_s -= old; else S.used_h -= old;
@@ -479,10 +618,10 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
       } else {
         C.miss++;
         const double a = (double)ln * P.t_p_ns_per_tok;
-        C.amat_sum_ns += a;
-        C.ttft_sum_ns += a;
+        C.amat += a;
+        C.ttft += a;
         C.tokens_computed += ln;
-        C.extra_prefill_tok += len_prev;
+        C.extra_prefill += len_prev;
       }
       x.len = (uint32_t)ln;
       x.meta = with_tier(x.meta, kTierNone);
@@ -529,8 +668,8 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
       if (P.tide && now >= S.dma_free_at) {
         // eq. (budget) / eq. (budgetq): Delta is the session's gap EMA in us
         uint64_t delta_us;
-        if (pol == kSpear && K.smode) {
-          unsigned __int128 d = ((unsigned __int128)x.gq * P.tau_ns) / 1000u;
+        if constexpr (PT::fixed) {
+          const unsigned __int128 d = ((unsigned __int128)x.gq * P.tau_ns) / 1000u;
           delta_us = d > (unsigned __int128)~0ull ? ~0ull : (uint64_t)d;
         } else {
           delta_us = (uint64_t)x.g;
@@ -541,7 +680,7 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         for (;;) {
           const Cand p = T.template select<false>(kTierHbm, K);  // eq. (promote)
           if (p.sid == kNone) break;
-          if (has_inf && p.key == inf_key) break;
+          if (PT::has_inf && p.key == PT::inf_key) break;
           uint64_t sp;
           uint32_t mp;
           T.read_size(p.sid, sp, mp);
@@ -574,8 +713,9 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         }
         if (moved) {
           // DMA busy for ceil(moved * 1000 / B) ns
-          unsigned __int128 ns = ((unsigned __int128)moved * 1000u + P.dma_B_per_us - 1u) / P.dma_B_per_us;
-          unsigned __int128 fin = (unsigned __int128)now + ns;
+          const unsigned __int128 ns =
+              ((unsigned __int128)moved * 1000u + P.dma_B_per_us - 1u) / P.dma_B_per_us;
+          const unsigned __int128 fin = (unsigned __int128)now + ns;
           S.dma_free_at = fin > (unsigned __int128)~0ull ? ~0ull : (uint64_t)fin;
         }
         C.dma_bytes += moved;
@@ -584,6 +724,7 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
       if (tier0 == kTierNone) S.n_table--;
     }
     C.events++;
+    cur = nxt;
   }
   next_event = e;
 }
@@ -624,7 +765,75 @@ __device__ __forceinline__ uint32_t sim_policy(const SimArgs& a, const unison_si
   return a.policy_override == UNISON_POLICY_PARAMS ? P.policy : a.policy_override;
 }
 
-// --------------------------------------------------------------- kernels
+// ------------------------------------------------- register-table kernels
+
+template <int G, int EPL, uint32_t POL, uint32_t SMODE>
+__device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_t lane,
+                                      const unison_sim_params& P, const KeyCtx& K) {
+  using PT = Pol<POL, SMODE>;
+  const uint64_t eb = a.ev_off[P.trace], ee = a.ev_off[P.trace + 1];
+  const uint64_t sb = a.sess_off[P.trace];
+  const uint32_t n_sess = (uint32_t)(a.sess_off[P.trace + 1] - sb);
+  const TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb,
+                     ee - eb, n_sess};
+  const size_t tb = (size_t)sim * a.max_sessions;
+  const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
+
+  RegTable<G, EPL, POL, SMODE> T;
+  T.lane = lane;
+#pragma unroll
+  for (int j = 0; j < EPL; ++j) {
+    const uint32_t s = (uint32_t)j * G + lane;
+    const bool in = s < n_sess;
+    T.kvb[j] = in ? a.sess_kvb[sb + s] : 0u;
+    const bool ld = cont && in;
+    const uint64_t x = ld ? a.t_mg[tb + s] : 0ull;
+    T.meta[j] = (uint32_t)x;
+    T.g[j] = __uint_as_float((uint32_t)(x >> 32));
+    if constexpr (PT::fixed) T.gq[j] = ld ? a.t_gq[tb + s] : 0ull;
+    T.len[j] = ld ? a.t_len[tb + s] : 0u;
+    T.last[j] = ld ? a.t_last[tb + s] : 0ull;
+    if constexpr (PT::belady) T.next[j] = ld ? a.t_next[tb + s] : ~0ull;
+    T.key[j] = 0;
+  }
+
+  Scalars S;
+  Cnt C;
+  uint64_t next_event = 0;
+  if (cont) {
+    load_scalars(a.state[sim], S);
+    C = cnt_from(a.counters[sim]);
+    next_event = a.state[sim].next_event;
+  } else {
+    S = Scalars{0, 0, 0, 0, 0, 0, 0, 0};
+    C = cnt_from(unison_counters{});
+  }
+  const LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
+                  a.log_cap, lane == 0};
+  if (C.error == 0) {
+    if (n_sess > (uint32_t)(G * EPL)) {
+      C.error = ~0ull;  // the launcher picks a variant that holds the trace
+    } else {
+      run_events<POL, SMODE>(T, P, K, tr, S, C, L, next_event, a.max_events);
+    }
+  }
+
+#pragma unroll
+  for (int j = 0; j < EPL; ++j) {
+    const uint32_t s = (uint32_t)j * G + lane;
+    if (s < n_sess) {
+      a.t_mg[tb + s] = (uint64_t)T.meta[j] | ((uint64_t)__float_as_uint(T.g[j]) << 32);
+      if constexpr (PT::fixed) a.t_gq[tb + s] = T.gq[j];
+      a.t_len[tb + s] = T.len[j];
+      a.t_last[tb + s] = T.last[j];
+      if constexpr (PT::belady) a.t_next[tb + s] = T.next[j];
+    }
+  }
+  if (lane == 0) {
+    store_scalars(a.state[sim], S, next_event);
+    a.counters[sim] = cnt_to(C);
+  }
+}
 
 template <int G, int EPL>
 __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
@@ -643,101 +852,33 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
            s_hq[grp], lane, G);
   __syncthreads();
   if (!live) return;
-
-  const uint64_t eb = a.ev_off[P.trace], ee = a.ev_off[P.trace + 1];
-  const uint64_t sb = a.sess_off[P.trace];
-  const uint32_t n_sess = (uint32_t)(a.sess_off[P.trace + 1] - sb);
-  TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb, ee - eb,
-               n_sess};
-  const size_t tb = (size_t)sim * a.max_sessions;
-  const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
-
-  RegTable<G, EPL> T;
-  T.lane = lane;
-#pragma unroll
-  for (int j = 0; j < EPL; ++j) {
-    const uint32_t s = (uint32_t)j * G + lane;
-    const bool in = s < n_sess;
-    T.kvb[j] = in ? a.sess_kvb[sb + s] : 0u;
-    if (cont && in) {
-      const uint64_t x = a.t_mg[tb + s];
-      T.meta[j] = (uint32_t)x;
-      T.g[j] = __uint_as_float((uint32_t)(x >> 32));
-      T.gq[j] = a.t_gq[tb + s];
-      T.len[j] = a.t_len[tb + s];
-      T.last[j] = a.t_last[tb + s];
-      T.next[j] = a.t_next[tb + s];
-    } else {
-      T.meta[j] = 0;
-      T.g[j] = 0.0f;
-      T.gq[j] = 0;
-      T.len[j] = 0;
-      T.last[j] = 0;
-      T.next[j] = ~0ull;
-    }
-    T.key[j] = 0;
-  }
-
-  Scalars S;
-  unison_counters C;
-  uint64_t next_event = 0;
-  if (cont) {
-    load_scalars(a.state[sim], S);
-    C = a.counters[sim];
-    next_event = a.state[sim].next_event;
-  } else {
-    S = Scalars{0, 0, 0, 0, 0, 0, 0, 0};
-    C = unison_counters{};
-  }
-  KeyCtx K{sim_policy(a, P), P.score_mode, s_hf[grp], s_hq[grp], P.penalty_us, lambda, P.p_z};
-  LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
-            a.log_cap, lane == 0};
-  if (C.error == 0) {
-    if (n_sess > (uint32_t)(G * EPL)) {
-      C.error = ~0ull;  // the launcher picks a variant that holds the trace
-    } else {
-      run_events(T, P, K, tr, S, C, L, next_event, a.max_events);
-    }
-  }
-
-#pragma unroll
-  for (int j = 0; j < EPL; ++j) {
-    const uint32_t s = (uint32_t)j * G + lane;
-    if (s < n_sess) {
-      a.t_mg[tb + s] = (uint64_t)T.meta[j] | ((uint64_t)__float_as_uint(T.g[j]) << 32);
-      a.t_gq[tb + s] = T.gq[j];
-      a.t_len[tb + s] = T.len[j];
-      a.t_last[tb + s] = T.last[j];
-      a.t_next[tb + s] = T.next[j];
-    }
-  }
-  if (lane == 0) {
-    store_scalars(a.state[sim], S, next_event);
-    a.counters[sim] = C;
+  const KeyCtx K{s_hf[grp], s_hq[grp], P.penalty_us, lambda, P.p_z};
+  switch (sim_policy(a, P)) {
+    case kSpear:
+      if (P.score_mode) regs_run<G, EPL, kSpear, 1>(a, sim, lane, P, K);
+      else regs_run<G, EPL, kSpear, 0>(a, sim, lane, P, K);
+      break;
+    case kLru: regs_run<G, EPL, kLru, 0>(a, sim, lane, P, K); break;
+    case kTimeout: regs_run<G, EPL, kTimeout, 0>(a, sim, lane, P, K); break;
+    default: regs_run<G, EPL, kBelady, 0>(a, sim, lane, P, K); break;
   }
 }
 
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
-  __shared__ float s_hf[52];
-  __shared__ uint32_t s_hq[52];
-  __shared__ Cand s_red[2 * (BLOCK / 64)];
-  const uint32_t sim = blockIdx.x;
-  const uint32_t tid = threadIdx.x;
-  const unison_sim_params P = a.params[sim];
-  const uint32_t lambda = (1u << P.b_h) - 1u;
-  load_lut(a.lut_d + (size_t)P.lut * kLut, a.lut_n + (size_t)P.lut * kLut, lambda, s_hf, s_hq, tid,
-           BLOCK);
+// ------------------------------------------------- streamed-table kernel
 
+template <int BLOCK, uint32_t POL, uint32_t SMODE>
+__device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const unison_sim_params& P,
+                                       const KeyCtx& K, Cand* s_red) {
+  const uint32_t tid = threadIdx.x;
   const uint64_t eb = a.ev_off[P.trace], ee = a.ev_off[P.trace + 1];
   const uint64_t sb = a.sess_off[P.trace];
   const uint32_t n_sess = (uint32_t)(a.sess_off[P.trace + 1] - sb);
-  TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb, ee - eb,
-               n_sess};
+  const TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb,
+                     ee - eb, n_sess};
   const size_t tb = (size_t)sim * a.max_sessions;
   const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
 
-  MemTable<BLOCK> T;
+  MemTable<BLOCK, POL, SMODE> T;
   T.mg = a.t_mg + tb;
   T.gq = a.t_gq + tb;
   T.len = a.t_len + tb;
@@ -759,26 +900,48 @@ __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   __syncthreads();
 
   Scalars S;
-  unison_counters C;
+  Cnt C;
   uint64_t next_event = 0;
   if (cont) {
     load_scalars(a.state[sim], S);
-    C = a.counters[sim];
+    C = cnt_from(a.counters[sim]);
     next_event = a.state[sim].next_event;
   } else {
     S = Scalars{0, 0, 0, 0, 0, 0, 0, 0};
-    C = unison_counters{};
+    C = cnt_from(unison_counters{});
   }
   if (S.hi > n_sess) S.hi = n_sess;  // never scan past the trace's sessions
   T.hi = S.hi;
-  KeyCtx K{sim_policy(a, P), P.score_mode, s_hf, s_hq, P.penalty_us, lambda, P.p_z};
-  LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
-            a.log_cap, tid == 0};
-  if (C.error == 0) run_events(T, P, K, tr, S, C, L, next_event, a.max_events);
+  const LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
+                  a.log_cap, tid == 0};
+  if (C.error == 0) run_events<POL, SMODE>(T, P, K, tr, S, C, L, next_event, a.max_events);
   __syncthreads();
   if (tid == 0) {
     store_scalars(a.state[sim], S, next_event);
-    a.counters[sim] = C;
+    a.counters[sim] = cnt_to(C);
+  }
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
+  __shared__ float s_hf[52];
+  __shared__ uint32_t s_hq[52];
+  __shared__ Cand s_red[2 * (BLOCK / 64)];
+  const uint32_t sim = blockIdx.x;
+  const unison_sim_params P = a.params[sim];
+  const uint32_t lambda = (1u << P.b_h) - 1u;
+  load_lut(a.lut_d + (size_t)P.lut * kLut, a.lut_n + (size_t)P.lut * kLut, lambda, s_hf, s_hq,
+           threadIdx.x, BLOCK);
+  __syncthreads();
+  const KeyCtx K{s_hf, s_hq, P.penalty_us, lambda, P.p_z};
+  switch (sim_policy(a, P)) {
+    case kSpear:
+      if (P.score_mode) block_run<BLOCK, kSpear, 1>(a, sim, P, K, s_red);
+      else block_run<BLOCK, kSpear, 0>(a, sim, P, K, s_red);
+      break;
+    case kLru: block_run<BLOCK, kLru, 0>(a, sim, P, K, s_red); break;
+    case kTimeout: block_run<BLOCK, kTimeout, 0>(a, sim, P, K, s_red); break;
+    default: block_run<BLOCK, kBelady, 0>(a, sim, P, K, s_red); break;
   }
 }
 
@@ -789,7 +952,7 @@ __global__ __launch_bounds__(256) void hazard_counts_kernel(const uint32_t* turn
   for (uint32_t t = threadIdx.x; t <= kLut; t += 256) s_end[t] = 0;
   __syncthreads();
   for (uint32_t i = threadIdx.x; i < n; i += 256) {
-    uint32_t T = turns[i];
+    const uint32_t T = turns[i];
     if (T >= 1) atomicAdd(&s_end[T - 1 < kLut ? T - 1 : kLut], 1u);
   }
   __syncthreads();
@@ -804,43 +967,57 @@ __global__ __launch_bounds__(256) void hazard_counts_kernel(const uint32_t* turn
   }
 }
 
-}  // namespace unison
-
 // ------------------------------------------------------------ launchers
 
-namespace unison {
+struct Variant {
+  int g, epl;
+};
 
-hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream, int force_variant) {
-  // Variant by the largest trace: register tables while a group can hold
-  // every session, the streamed table beyond.
-  int v = force_variant;
-  if (v < 0) {
-    if (max_sess_in_batch <= 16) v = 0;
-    else if (max_sess_in_batch <= 64) v = 1;
-    else if (max_sess_in_batch <= 256) v = 2;
-    else v = 3;
-  }
-  const uint32_t n = a.n_sims;
-  switch (v) {
-    case 0: hipLaunchKernelGGL((sim_regs_kernel<16, 1>), dim3((n * 16 + 255) / 256), dim3(256), 0, stream, a); break;
-    case 1: hipLaunchKernelGGL((sim_regs_kernel<64, 1>), dim3((n * 64 + 255) / 256), dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((sim_regs_kernel<64, 4>), dim3((n * 64 + 255) / 256), dim3(256), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL((sim_regs_kernel<4, 4>), dim3((n * 4 + 255) / 256), dim3(256), 0, stream, a); break;
-    case 5: hipLaunchKernelGGL((sim_regs_kernel<8, 2>), dim3((n * 8 + 255) / 256), dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL((sim_block_kernel<256>), dim3(n), dim3(256), 0, stream, a); break;
-  }
-  return hipGetLastError();
-}
+// Register-table shapes (lanes per simulation x sessions per lane); id 3 is
+// the streamed table.
+constexpr Variant kVariants[] = {{16, 1}, {64, 1}, {64, 4}, {0, 0}, {4, 4},
+                                 {8, 2},  {64, 24}, {16, 4}, {32, 8}};
+constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
+constexpr int kBlock = 256;
 
 uint32_t sim_variant_capacity(int v) {
+  if (v < 0 || v >= kNumVariants) return 0;
+  if (kVariants[v].g == 0) return UNISON_MAX_SESSIONS;
+  return (uint32_t)(kVariants[v].g * kVariants[v].epl);
+}
+
+int sim_auto_variant(uint32_t max_sess) {
+  if (max_sess <= 16) return 5;
+  if (max_sess <= 64) return 7;
+  if (max_sess <= 256) return 8;
+  if (max_sess <= 1536) return 6;
+  return 3;
+}
+
+template <int G, int EPL>
+static void launch_regs(const SimArgs& a, hipStream_t stream) {
+  const uint32_t groups_per_block = 256 / G;
+  const uint32_t blocks = (a.n_sims + groups_per_block - 1) / groups_per_block;
+  hipLaunchKernelGGL((sim_regs_kernel<G, EPL>), dim3(blocks), dim3(256), 0, stream, a);
+}
+
+hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream,
+                      int force_variant) {
+  const int v = force_variant >= 0 ? force_variant : sim_auto_variant(max_sess_in_batch);
   switch (v) {
-    case 0: return 16;
-    case 1: return 64;
-    case 2: return 256;
-    case 4: return 16;
-    case 5: return 16;
-    default: return UNISON_MAX_SESSIONS;
+    case 0: launch_regs<16, 1>(a, stream); break;
+    case 1: launch_regs<64, 1>(a, stream); break;
+    case 2: launch_regs<64, 4>(a, stream); break;
+    case 4: launch_regs<4, 4>(a, stream); break;
+    case 5: launch_regs<8, 2>(a, stream); break;
+    case 6: launch_regs<64, 24>(a, stream); break;
+    case 7: launch_regs<16, 4>(a, stream); break;
+    case 8: launch_regs<32, 8>(a, stream); break;
+    default:
+      hipLaunchKernelGGL((sim_block_kernel<kBlock>), dim3(a.n_sims), dim3(kBlock), 0, stream, a);
+      break;
   }
+  return hipGetLastError();
 }
 
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
