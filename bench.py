@@ -180,6 +180,10 @@ def main():
     ap.add_argument("--c4-events", type=int, default=200_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", type=int, default=None)
+    ap.add_argument("--policies", default="0,1,2,3",
+                    help="policies of the sweep to include (0 SPEAR+TIDE, 1 LRU, 2 timeout, 3 Belady)")
+    ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
+                    help="only run one device-to-device copy of MIB MiB (PMC byte calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the simulations are independent and this build "
@@ -193,8 +197,16 @@ def main():
 
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs the GPU")
+    if args.copy_calib:
+        n = args.copy_calib * (1 << 20)
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n}), flush=True)
+        return
     log("generating the sweep workload")
-    w = synth.c3_sweep()
+    w = synth.c3_sweep(policies=tuple(int(x) for x in args.policies.split(",")))
     sim = U.Simulator(w, variant=args.variant)
     log("warmup %d, steps %d" % (args.warmup, args.steps))
     per, wall = time_launches(torch, sim.run, args.steps, args.warmup)

@@ -74,6 +74,9 @@ extern "C" {
 
 #define UNISON_RUN_CONTINUE 1u   /* resume every simulation where the last run stopped */
 #define UNISON_RUN_LOG 2u        /* also record decisions (see unison_read_log) */
+#define UNISON_RUN_LOG_VICTIM 4u /* with UNISON_RUN_LOG: also record each event's scan
+                                    result as a UNISON_OP_VICTIM record (a = victim or
+                                    0xFFFFFFFF), written before that event's decisions */
 
 #define UNISON_LUT_LEN 51u       /* hazard table entries, t = 0..50 (eq. (hazard)) */
 #define UNISON_MAX_SESSIONS (1u << 20) /* largest session count of one trace */
@@ -84,6 +87,7 @@ extern "C" {
 #define UNISON_OP_BYPASS 3u   /* a = arriving session served but not retained */
 #define UNISON_OP_PROMOTE 4u  /* a = HBM resident moved into free SRAM (TIDE) */
 #define UNISON_OP_SWAP 5u     /* a = promoted (eq. (promote)), b = demoted (eq. (demote)) */
+#define UNISON_OP_VICTIM 6u   /* a = the event's scan result (UNISON_RUN_LOG_VICTIM only) */
 #define UNISON_OP_PLACE 7u    /* a = arriving session, b = tier (1 SRAM, 2 HBM) */
 
 typedef struct unison_ctx unison_ctx;
@@ -132,8 +136,12 @@ typedef struct {
   uint64_t extra_prefill_tok; /* prefix tokens re-prefilled after a loss */
   uint64_t score_evals;       /* table entries scored: sum over events of |table| */
   uint64_t resident_evals;    /* sum over events of the resident count */
-  uint64_t digest;            /* sum mod 2^64 of SplitMix64 hashes of every decision */
-  uint64_t victim_digest;     /* same over each event's scan result (argmax victim) */
+  uint64_t digest;            /* sum mod 2^64 of hashes of every decision record:
+                                 mix(w0 ^ w1 * 0x9e3779b97f4a7c15), w0 = ev << 8 | op,
+                                 w1 = a << 32 | b, mix = the SplitMix64 finaliser */
+  uint64_t victim_digest;     /* sum over events e of (v + 1) * (2e + 1) * 0x9e3779b97f4a7c15
+                                 mod 2^64, v = the event's scan result (argmax victim,
+                                 0xFFFFFFFF when nothing is evictable) */
   uint64_t events;            /* events processed so far */
   uint64_t error;             /* 0, or 1 + index of the event that broke the format */
   double amat_sum_ns;         /* sum of per-request access costs, eq. (hr-amat) */
@@ -250,9 +258,11 @@ int unison_kendall(void* hip_stream, uint32_t n_snap, uint32_t n_per, uint64_t n
                    const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1);
 
 /* Test hook: pins the simulation kernel variant (-1 = chosen by the largest
- * trace; 0: 16 lanes x 1, 1: 64 x 1, 2: 64 x 4, 4: 4 x 4, 5: 8 x 2 register
- * tables; 3: workgroup with the table in the workspace).  A variant too small
- * for the traces makes unison_run return UNISON_E_CAPACITY. */
+ * trace; register tables of lanes x sessions per lane 0: 16 x 1, 1: 64 x 1,
+ * 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 6: 64 x 24, 7: 16 x 4, 8: 32 x 8; one
+ * workgroup per simulation with the table 3: streamed from the workspace,
+ * 9: held in LDS).  A variant too small for the traces, or an unknown id,
+ * makes unison_run return UNISON_E_CAPACITY. */
 int unison_debug_force_variant(unison_ctx* ctx, int variant);
 
 uint32_t unison_version(void);

@@ -33,8 +33,8 @@
  *            the residents that are not being served (an ARRIVE pins its
  *            session until its GAP_START/DONE).
  *  EMA       g = 0 and g_q = 0 before the first gap.  Float path, in us:
- *            x = (float)((double)gap_ns / 1000.0); g = (3x + 7g) / 10 with
- *            every operation rounded to fp32.  Integer path eq. (gapq) and
+ *            x = (float)min(gap_ns / 1000, 2^32 - 1) (whole microseconds);
+ *            g = (3x + 7g) / 10 with every operation rounded to fp32.  Integer path eq. (gapq) and
  *            eq. (ema-int): x_q = min(gap_ns / tau, 2^b_g - 1),
  *            g_q = (3 x_q + 7 g_q) / 10, floors.
  *  hazard    t is the 0-based index of the session's latest turn.  From a
@@ -74,10 +74,13 @@
  *            likewise with t_h; miss amat += len*t_p, ttft += len*t_p,
  *            computed += len, extra prefill += len_prev.  f64, event order.
  *  digest    Each decision (event index, op, sid a, sid b or tier) -- place,
- *            evict, expire, bypass, promote, swap -- is hashed with the
- *            SplitMix64 finaliser (Steele, Lea and Flood, 2014) and the
+ *            evict, expire, bypass, promote, swap -- is hashed: w0 = ev << 8 |
+ *            op, w1 = a << 32 | b, h = mix(w0 ^ w1 * 0x9e3779b97f4a7c15) with
+ *            mix the SplitMix64 finaliser (Steele, Lea and Flood, 2014); the
  *            hashes are summed mod 2^64, so the digest does not depend on
- *            the order in which one event's decisions are listed.
+ *            the order in which one event's decisions are listed.  The scan
+ *            result v of event e (0xFFFFFFFF when nothing is evictable) enters
+ *            a second digest as (v + 1) * ((2e + 1) * 0x9e3779b97f4a7c15).
  */
 #include <math.h>
 #include <stdint.h>
@@ -145,10 +148,12 @@ static uint64_t mix64(uint64_t z) {
   return z ^ (z >> 31);
 }
 
+/* The record's two words are combined by an odd multiplier (a bijection on
+ * w1) before one finaliser pass. */
 static uint64_t rec_hash(uint32_t ev, uint32_t op, uint32_t a, uint32_t b) {
   uint64_t w0 = ((uint64_t)ev << 8) | (uint64_t)op;
   uint64_t w1 = ((uint64_t)a << 32) | (uint64_t)b;
-  return mix64(w0 ^ mix64(w1));
+  return mix64(w0 ^ (w1 * 0x9e3779b97f4a7c15ULL));
 }
 
 static uint64_t sat_u64(unsigned __int128 x) {
@@ -230,8 +235,16 @@ void orc_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
 
 /* ----------------------------------------------------------- EMA updates */
 
+/* The gap sample is taken in whole microseconds (the tau = 10^3 resolution of
+ * eq. (lock)), clipped to 2^32 - 1 like the 32-bit gap register, so that the
+ * fp32 and the integer register see the same sample. */
+static uint32_t gap_us(uint64_t gap_ns) {
+  uint64_t us = gap_ns / 1000;
+  return us > 0xFFFFFFFFULL ? 0xFFFFFFFFu : (uint32_t)us;
+}
+
 static float ema_f32(float g, uint64_t gap_ns) {
-  float x = (float)((double)gap_ns / 1000.0);
+  float x = (float)gap_us(gap_ns);
   float a = 3.0f * x;
   float b = 7.0f * g;
   return (a + b) / 10.0f; /* eq. (ema) */
@@ -588,7 +601,8 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
     out->score_evals += m.n_table;
     out->resident_evals += m.n_res;
     uint32_t v0 = argmax_key(&m, T_NONE);
-    out->victim_digest += rec_hash(m.ev, OP_VICTIM, v0, NONE_ID);
+    /* odd weight per event: a different victim at any one event changes the sum */
+    out->victim_digest += ((uint64_t)v0 + 1) * ((2 * (uint64_t)m.ev + 1) * 0x9e3779b97f4a7c15ULL);
 
     if (kind == K_ARRIVE) {
       /* eq. (hr-amat), eq. (prered), eq. (reuse) */

@@ -21,6 +21,8 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
 uint32_t sim_variant_capacity(int v);
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
                                 hipStream_t stream);
+hipError_t launch_max_time(const uint64_t* t, const uint64_t* next, uint64_t n, uint64_t* out,
+                           hipStream_t stream);
 hipError_t launch_ema_replay(uint32_t n, uint32_t max_hist, const uint64_t* gaps,
                              const uint8_t* n_hist, uint32_t b_g, uint64_t tau, float* g,
                              uint64_t* gq, hipStream_t s);
@@ -46,7 +48,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Workspace layout; offsets in bytes from the workspace base.
 struct Layout {
-  size_t params, ev_off, sess_off, lut_d, lut_n, state, counters, mg, gq, len, last, next, log, total;
+  size_t params, ev_off, sess_off, lut_d, lut_n, state, counters, mg, gq, len, last, next, log,
+      scratch, total;
 };
 
 bool make_layout(const unison_dims& d, Layout& L) {
@@ -70,6 +73,7 @@ bool make_layout(const unison_dims& d, Layout& L) {
   L.last = take(sizeof(uint64_t) * entries);
   L.next = take(sizeof(uint64_t) * entries);
   L.log = take(sizeof(unison_record) * (size_t)d.log_cap * d.n_sims);
+  L.scratch = take(256);
   L.total = off;
   return true;
 }
@@ -92,6 +96,7 @@ struct unison_ctx {
   std::vector<unison_sim_params> h_params;
   std::vector<uint8_t> lut_set;
   bool traces_loaded = false, params_set = false, ran = false;
+  bool time44 = false;  // every trace time is below 2^44 - 1 ns
   uint32_t max_sess_batch = 0;
   int force_variant = -1;
   char err[512];
@@ -197,8 +202,18 @@ int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
                                sizeof(uint64_t) * (nt + 1), hipMemcpyHostToDevice, ctx->stream),
                 "copy session offsets");
   if (rc) return rc;
+  // the largest time decides whether recency / Belady keys pack into 44 bits
+  uint64_t* d_max = ctx->at<uint64_t>(ctx->L.scratch);
+  rc = ctx->hip(launch_max_time(tb->ev_t_ns, tb->ev_next_ns, tb->ev_offset[nt], d_max, ctx->stream),
+                "largest trace time");
+  if (rc) return rc;
+  uint64_t h_max = 0;
+  rc = ctx->hip(hipMemcpyAsync(&h_max, d_max, sizeof h_max, hipMemcpyDeviceToHost, ctx->stream),
+                "copy largest trace time");
+  if (rc) return rc;
   rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise after offsets");
   if (rc) return rc;
+  ctx->time44 = h_max < (1ull << 44) - 1;
   ctx->traces_loaded = true;
   return UNISON_OK;
 }
@@ -261,7 +276,8 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
     if (!ctx->lut_set[p.lut]) return ctx->fail(UNISON_E_NOT_READY, "hazard table %u not set", p.lut);
   if (policy_override != UNISON_POLICY_PARAMS && policy_override > UNISON_POLICY_BELADY)
     return ctx->fail(UNISON_E_INVALID, "policy %u", policy_override);
-  if (flags & ~(UNISON_RUN_CONTINUE | UNISON_RUN_LOG)) return ctx->fail(UNISON_E_INVALID, "flags");
+  if (flags & ~(UNISON_RUN_CONTINUE | UNISON_RUN_LOG | UNISON_RUN_LOG_VICTIM))
+    return ctx->fail(UNISON_E_INVALID, "flags");
   if ((flags & UNISON_RUN_CONTINUE) && !ctx->ran)
     return ctx->fail(UNISON_E_NOT_READY, "UNISON_RUN_CONTINUE before any run on this context");
   SimArgs a;
@@ -291,8 +307,9 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   a.log_cap = ctx->dims.log_cap;
   a.flags = flags;
   a.policy_override = policy_override;
+  a.time44 = ctx->time44 ? 1u : 0u;
   int v = ctx->force_variant;
-  if (v >= 0 && sim_variant_capacity(v) < ctx->max_sess_batch)
+  if (v >= 0 && (sim_variant_capacity(v) == 0 || sim_variant_capacity(v) < ctx->max_sess_batch))
     return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds %u sessions < %u", v,
                      sim_variant_capacity(v), ctx->max_sess_batch);
   int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->stream, v), "launch simulation");

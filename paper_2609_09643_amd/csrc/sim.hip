@@ -80,6 +80,17 @@ __device__ __forceinline__ void reduce_step(Cand& c) {
   }
 }
 
+template <int W, int M, bool MAX>
+__device__ __forceinline__ uint64_t reduce_packed(uint64_t c) {
+  if constexpr (M < W) {
+    const uint64_t o = ((uint64_t)xchg<M>((uint32_t)(c >> 32)) << 32) | xchg<M>((uint32_t)c);
+    c = (MAX ? o > c : o < c) ? o : c;
+    return reduce_packed<W, M * 2, MAX>(c);
+  } else {
+    return c;
+  }
+}
+
 // Every lane of an aligned group of W lanes ends with the winner (ties to
 // the smaller session id).
 template <int W, bool MAX>
@@ -114,6 +125,7 @@ struct KeyCtx {
   float P;
   uint32_t lambda;
   uint64_t p_z;
+  bool pack44;          // times fit 44 bits and ids 20 bits: recency / Belady keys pack
 };
 
 // "Larger key = evict first".  SPEAR: the score (eq. (esp) or eq. (scoreq));
@@ -200,6 +212,23 @@ struct RegTable {
     m = bcast(meta, sid);
     size = (uint64_t)l * k;
   }
+  // The fields a gap onset or completion reads: meta and the gap EMAs.
+  __device__ __forceinline__ void read_end(uint32_t sid, Entry& e) const {
+    e.meta = bcast(meta, sid);
+    e.g = bcast(g, sid);
+    e.gq = PT::fixed ? bcast(gq, sid) : 0ull;
+  }
+  __device__ __forceinline__ void write_end(uint32_t sid, uint32_t m, uint64_t t, uint64_t nx) {
+    const uint32_t js = sid / G;
+    const bool mine = lane == sid % G;
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const bool w = mine && js == (uint32_t)j;
+      meta[j] = w ? m : meta[j];
+      last[j] = w ? t : last[j];
+      if constexpr (PT::belady) next[j] = w ? nx : next[j];
+    }
+  }
 
   __device__ __forceinline__ void write(uint32_t sid, const Entry& e) {
     const uint32_t js = sid / G;
@@ -221,6 +250,16 @@ struct RegTable {
 #pragma unroll
     for (int j = 0; j < EPL; ++j) meta[j] = (mine && js == (uint32_t)j) ? m : meta[j];
   }
+  __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
+    const uint32_t js = sid / G;
+    const bool mine = lane == sid % G;
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const bool w = mine && js == (uint32_t)j;
+      meta[j] = w ? m : meta[j];
+      len[j] = w ? l : len[j];
+    }
+  }
 
   // The per-event scan: every entry's key, kept for this event's reductions.
   __device__ __forceinline__ void scan(const KeyCtx& K) {
@@ -232,7 +271,10 @@ struct RegTable {
 
   // argmax / argmin of the keys over evictable entries in `tier` (0 = any).
   template <bool MAX>
-  __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx&) const {
+  __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx& K) const {
+    if constexpr (PT::spear && !PT::fixed) return select32<MAX>(tier);
+    if constexpr (PT::recency || PT::belady)
+      if (K.pack44) return select44<MAX>(tier);
     Cand c = MAX ? cand_none_max() : cand_none_min();
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
@@ -246,6 +288,55 @@ struct RegTable {
     return reduce_group<G, MAX>(c);
   }
   __device__ __forceinline__ Cand argmax_first(const KeyCtx& K) const { return select<true>(0, K); }
+
+  // 32-bit keys (fp32 scores) reduce as one packed u64: key << 32 with the
+  // complement of the id for argmax (ties to the smaller id) and the id itself
+  // for argmin; 0 and 2^64 - 1 are the empty values.
+  template <bool MAX>
+  __device__ __forceinline__ Cand select32(uint32_t tier) const {
+    uint64_t c = MAX ? 0ull : ~0ull;
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const bool ok = evictable(meta[j]) && (tier == 0 || meta_tier(meta[j]) == tier);
+      const uint32_t s = sid_of(j);
+      const uint64_t p = (key[j] << 32) | (MAX ? (0xFFFFFFFFu - s) : s);
+      c = ok && (MAX ? p > c : p < c) ? p : c;
+    }
+    c = reduce_packed<G, 1, MAX>(c);
+    const bool none = MAX ? c == 0ull : c == ~0ull;
+    const uint32_t lo = (uint32_t)c;
+    return Cand{c >> 32, none ? kNone : (MAX ? 0xFFFFFFFFu - lo : lo)};
+  }
+
+  // Recency and Belady keys are times; below 2^44 - 1 they pack with a 20-bit
+  // id as k44 << 20 | id field.  Recency: k44 = 2^44 - 1 - last (the order of
+  // 2^64 - 1 - last); Belady: k44 = min(next, 2^44 - 1), the cap standing for
+  // "never".  The id field is 2^20 - 1 - id for argmax and id for argmin,
+  // so ties go to the smaller id; ids stay below 2^20 - 1, which keeps 0 and
+  // 2^64 - 1 free as the empty values.
+  template <bool MAX>
+  __device__ __forceinline__ Cand select44(uint32_t tier) const {
+    constexpr uint64_t kCap = (1ull << 44) - 1;
+    uint64_t c = MAX ? 0ull : ~0ull;
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const bool ok = evictable(meta[j]) && (tier == 0 || meta_tier(meta[j]) == tier);
+      const uint32_t s = sid_of(j);
+      uint64_t k44;
+      if constexpr (PT::belady) k44 = next[j] < kCap ? next[j] : kCap;
+      else k44 = kCap - last[j];
+      const uint64_t p = (k44 << 20) | (MAX ? (0xFFFFFu - s) : s);
+      c = ok && (MAX ? p > c : p < c) ? p : c;
+    }
+    c = reduce_packed<G, 1, MAX>(c);
+    const bool none = MAX ? c == 0ull : c == ~0ull;
+    const uint32_t lo = (uint32_t)c & 0xFFFFFu;
+    const uint64_t k44 = c >> 20;
+    uint64_t key;
+    if constexpr (PT::belady) key = k44 == kCap ? ~0ull : k44;
+    else key = k44 | ~kCap;
+    return Cand{key, none ? kNone : (MAX ? 0xFFFFFu - lo : lo)};
+  }
 
   // Smallest evictable session idle for longer than ttl (timeout policy).
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) const {
@@ -304,6 +395,18 @@ struct MemTable {
     size = (uint64_t)uni32(len[sid]) * uni32(kvb[sid]);
     __syncthreads();
   }
+  __device__ __forceinline__ void read_end(uint32_t sid, Entry& e) const {
+    const uint64_t x = uni64(mg[sid]);
+    e.meta = (uint32_t)x;
+    e.g = __uint_as_float((uint32_t)(x >> 32));
+    e.gq = PT::fixed ? uni64(gq[sid]) : 0ull;
+    __syncthreads();
+  }
+  __device__ __forceinline__ void write_end(uint32_t sid, uint32_t m, uint64_t t, uint64_t nx) {
+    set_meta(sid, m);
+    last[sid] = t;
+    if constexpr (PT::belady) next[sid] = nx;
+  }
   // Every thread stores the same values, so each thread's later loads see
   // them; reads end with a barrier and each event starts with one, so no wave
   // writes an entry that another wave has still to read.
@@ -317,6 +420,10 @@ struct MemTable {
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) {
     const uint64_t x = mg[sid];
     mg[sid] = (x & 0xFFFFFFFF00000000ull) | m;
+  }
+  __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
+    set_meta(sid, m);
+    len[sid] = l;
   }
 
   __device__ __forceinline__ void scan(const KeyCtx&) {}
@@ -392,6 +499,7 @@ struct MemTable {
 struct Scalars {
   uint64_t used_s, used_h, dma_free_at, prev_t, log_len;
   uint32_t n_res, n_table, hi;
+  uint64_t hit_s_bytes, hit_h_bytes, miss_tok, prev_s_bytes, prev_h_bytes;
 };
 
 // Counters as kept during a run: event-bounded counts in 32 bits.
@@ -461,6 +569,7 @@ struct LogSink {
   unison_record* rec;  // this simulation's records, or null
   uint32_t cap;
   bool lead;           // the one lane that stores records
+  bool victims;        // also record each event's scan result
 };
 
 __device__ __forceinline__ void emit(Cnt& C, Scalars& S, const LogSink& L, uint32_t ev, uint32_t op,
@@ -518,7 +627,10 @@ __device__ __forceinline__ void release(Tab& T, Scalars& S, uint32_t sid) {
 }
 
 // Algorithm 1 over the simulation's events [next_event, next_event + max_events).
-template <uint32_t POL, uint32_t SMODE, class Tab>
+// UNI: every lane replays the same trace from the same event (one simulation
+// per workgroup), so the event record is read as uniform values that live in
+// SGPRs: scalar decode and scalar branches on the event kind.
+template <uint32_t POL, uint32_t SMODE, bool UNI, class Tab>
 __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
                            Scalars& S, Cnt& C, const LogSink& L, uint64_t& next_event,
                            uint64_t max_events) {
@@ -531,9 +643,12 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     // the next event's record is in flight while this one is processed
     const Ev nxt = load_ev<PT::belady>(tr, e + 1 < end ? e + 1 : e);
     T.event_begin();
-    const uint64_t now = cur.t;
-    const uint32_t sid = cur.sid;
-    const uint32_t kind = cur.info >> 24, turn = cur.info & 0xFFFFFFu;
+    const uint64_t now = UNI ? uni64(cur.t) : cur.t;
+    const uint32_t sid = UNI ? uni32(cur.sid) : cur.sid;
+    const uint32_t info = UNI ? uni32(cur.info) : cur.info;
+    const uint32_t kind = info >> 24, turn = info & 0xFFFFFFu;
+    const uint32_t cur_len = UNI ? uni32(cur.len) : cur.len;
+    const uint64_t cur_next = (UNI && PT::belady) ? uni64(cur.next) : cur.next;
     const uint32_t ev = (uint32_t)e;
     if (sid >= tr.n_sess || now < S.prev_t || kind > kDone) {
       C.error = e + 1;
@@ -553,11 +668,14 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     }
 
     // Alg. 1: write e into R; on gap_end update the EMA
-    Entry x = T.read(sid);
-    const uint32_t ph = meta_phase(x.meta), tier0 = meta_tier(x.meta);
-    uint32_t len_prev = x.len;
-    bool bad;
+    Entry x;
+    uint32_t ph, tier0, len_prev = 0;
     if (kind == kArrive) {
+      x = T.read(sid);
+      ph = meta_phase(x.meta);
+      tier0 = meta_tier(x.meta);
+      len_prev = x.len;
+      bool bad;
       if (turn == 0) {
         bad = ph != kUnseen;
         x.g = 0.0f;
@@ -565,28 +683,34 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         x.len = 0;
         len_prev = 0;
       } else {
-        bad = ph != kGap || turn != meta_turn(x.meta) + 1 || cur.len < x.len;
+        bad = ph != kGap || turn != meta_turn(x.meta) + 1 || cur_len < x.len;
         const uint64_t gap = now - x.last;  // eq. (gap)
         x.g = ema_f32(x.g, gap);
         if constexpr (PT::fixed) x.gq = ema_int(x.gq, gap, P.b_g, P.tau_ns);
       }
+      if (bad) {
+        C.error = e + 1;
+        break;
+      }
       x.meta = make_meta(kServing, tier0, turn);
+      x.last = now;
+      if (turn == 0) {
+        S.n_table++;
+        if (sid + 1 > S.hi) S.hi = sid + 1;
+        T.grow(S.hi);
+      }
+      T.write(sid, x);
     } else {
-      bad = ph != kServing;
+      T.read_end(sid, x);
+      ph = meta_phase(x.meta);
+      tier0 = meta_tier(x.meta);
+      if (ph != kServing) {
+        C.error = e + 1;
+        break;
+      }
       x.meta = make_meta(kind == kGapStart ? kGap : kDoneP, tier0, meta_turn(x.meta));
-      x.next = kind == kGapStart ? cur.next : ~0ull;
+      T.write_end(sid, x.meta, now, kind == kGapStart ? cur_next : ~0ull);
     }
-    if (bad) {
-      C.error = e + 1;
-      break;
-    }
-    x.last = now;
-    if (kind == kArrive && turn == 0) {
-      S.n_table++;
-      if (sid + 1 > S.hi) S.hi = sid + 1;
-      T.grow(S.hi);
-    }
-    T.write(sid, x);
 
     // the register-file scan: every table entry is scored; its argmax over
     // evictable residents is this event's victim index
@@ -594,38 +718,45 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     C.resident_evals += S.n_res;
     T.scan(K);
     const Cand v0 = T.argmax_first(K);
-    C.victim_digest += rec_hash(ev, kOpVictim, v0.sid, kNone);
+    // odd weight per event: a different victim at any one event changes the sum
+    C.victim_digest += ((uint64_t)v0.sid + 1u) * ((2ull * e + 1ull) * 0x9e3779b97f4a7c15ull);
+    if (L.victims) {
+      if (L.rec && L.lead && S.log_len < L.cap) L.rec[S.log_len] = unison_record{ev, kOpVictim, v0.sid, kNone};
+      if (L.rec) S.log_len++;
+    }
 
     if (kind == kArrive) {
       // eq. (hr-amat), eq. (prered), eq. (reuse)
-      const uint64_t ln = cur.len;
+      const uint64_t ln = cur_len;
       const uint64_t dlen = ln - len_prev;
       const uint64_t kb = x.kvb;
       C.requests++;
       C.tokens_total += ln;
       if (tier0 != kTierNone) {
-        const double t_mem = tier0 == kTierSram ? P.t_s_ns_per_B : P.t_h_ns_per_B;
-        if (tier0 == kTierSram) C.hit_sram++; else C.hit_hbm++;
-        const double a = (double)(ln * kb) * t_mem;
-        const double b = (double)((uint64_t)len_prev * kb) * t_mem;
-        const double c = (double)dlen * P.t_p_ns_per_tok;
-        C.amat += a;
-        C.ttft += b + c;
-        C.tokens_computed += dlen;
+        const uint64_t now_b = ln * kb;
         const uint64_t old = (uint64_t)len_prev * kb;
-        if (tier0 == kTierSram) S.used_s -= old; else S.used_h -= old;
+        if (tier0 == kTierSram) {
+          C.hit_sram++;
+          S.hit_s_bytes += now_b;
+          S.prev_s_bytes += old;
+          S.used_s -= old;
+        } else {
+          C.hit_hbm++;
+          S.hit_h_bytes += now_b;
+          S.prev_h_bytes += old;
+          S.used_h -= old;
+        }
+        C.tokens_computed += dlen;
         S.n_res--;
       } else {
         C.miss++;
-        const double a = (double)ln * P.t_p_ns_per_tok;
-        C.amat += a;
-        C.ttft += a;
+        S.miss_tok += ln;
         C.tokens_computed += ln;
         C.extra_prefill += len_prev;
       }
       x.len = (uint32_t)ln;
       x.meta = with_tier(x.meta, kTierNone);
-      T.write(sid, x);
+      T.set_len_meta(sid, x.len, x.meta);
 
       // Alg. 1 capacity branch: evict the argmax victim until the session fits
       const uint64_t size = ln * kb;
@@ -747,6 +878,11 @@ __device__ __forceinline__ void load_scalars(const SimState& st, Scalars& S) {
   S.n_res = st.n_res;
   S.n_table = st.n_table;
   S.hi = st.hi;
+  S.hit_s_bytes = st.hit_s_bytes;
+  S.hit_h_bytes = st.hit_h_bytes;
+  S.miss_tok = st.miss_tok;
+  S.prev_s_bytes = st.prev_s_bytes;
+  S.prev_h_bytes = st.prev_h_bytes;
 }
 
 __device__ __forceinline__ void store_scalars(SimState& st, const Scalars& S, uint64_t next_event) {
@@ -759,6 +895,24 @@ __device__ __forceinline__ void store_scalars(SimState& st, const Scalars& S, ui
   st.n_res = S.n_res;
   st.n_table = S.n_table;
   st.hi = S.hi;
+  st.hit_s_bytes = S.hit_s_bytes;
+  st.hit_h_bytes = S.hit_h_bytes;
+  st.miss_tok = S.miss_tok;
+  st.prev_s_bytes = S.prev_s_bytes;
+  st.prev_h_bytes = S.prev_h_bytes;
+}
+
+// eq. (hr-amat) sums from the exact integer totals, rounded once: the same
+// quantities the per-request f64 sums approximate.
+__device__ __forceinline__ void finish_costs(const Scalars& S, const unison_sim_params& P, Cnt& C) {
+  const double a = (double)S.hit_s_bytes * P.t_s_ns_per_B;
+  const double b = (double)S.hit_h_bytes * P.t_h_ns_per_B;
+  const double c = (double)S.miss_tok * P.t_p_ns_per_tok;
+  C.amat = (a + b) + c;
+  const double d = (double)S.prev_s_bytes * P.t_s_ns_per_B;
+  const double f = (double)S.prev_h_bytes * P.t_h_ns_per_B;
+  const double h = (double)C.tokens_computed * P.t_p_ns_per_tok;
+  C.ttft = (d + f) + h;
 }
 
 __device__ __forceinline__ uint32_t sim_policy(const SimArgs& a, const unison_sim_params& P) {
@@ -805,16 +959,16 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
     C = cnt_from(a.counters[sim]);
     next_event = a.state[sim].next_event;
   } else {
-    S = Scalars{0, 0, 0, 0, 0, 0, 0, 0};
+    S = Scalars{};
     C = cnt_from(unison_counters{});
   }
   const LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
-                  a.log_cap, lane == 0};
+                  a.log_cap, lane == 0, (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
   if (C.error == 0) {
     if (n_sess > (uint32_t)(G * EPL)) {
       C.error = ~0ull;  // the launcher picks a variant that holds the trace
     } else {
-      run_events<POL, SMODE>(T, P, K, tr, S, C, L, next_event, a.max_events);
+      run_events<POL, SMODE, false>(T, P, K, tr, S, C, L, next_event, a.max_events);
     }
   }
 
@@ -830,6 +984,7 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
     }
   }
   if (lane == 0) {
+    finish_costs(S, P, C);
     store_scalars(a.state[sim], S, next_event);
     a.counters[sim] = cnt_to(C);
   }
@@ -852,7 +1007,7 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
            s_hq[grp], lane, G);
   __syncthreads();
   if (!live) return;
-  const KeyCtx K{s_hf[grp], s_hq[grp], P.penalty_us, lambda, P.p_z};
+  const KeyCtx K{s_hf[grp], s_hq[grp], P.penalty_us, lambda, P.p_z, a.time44 != 0};
   switch (sim_policy(a, P)) {
     case kSpear:
       if (P.score_mode) regs_run<G, EPL, kSpear, 1>(a, sim, lane, P, K);
@@ -866,9 +1021,12 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
 
 // ------------------------------------------------- streamed-table kernel
 
-template <int BLOCK, uint32_t POL, uint32_t SMODE>
+// One workgroup per simulation.  IN_LDS keeps the table in LDS for the whole
+// run (copied from and back to the workspace); otherwise it is streamed from
+// the workspace in place.
+template <int BLOCK, uint32_t POL, uint32_t SMODE, bool IN_LDS>
 __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const unison_sim_params& P,
-                                       const KeyCtx& K, Cand* s_red) {
+                                          const KeyCtx& K, Cand* s_red, uint64_t* s_tab) {
   const uint32_t tid = threadIdx.x;
   const uint64_t eb = a.ev_off[P.trace], ee = a.ev_off[P.trace + 1];
   const uint64_t sb = a.sess_off[P.trace];
@@ -879,22 +1037,42 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
 
   MemTable<BLOCK, POL, SMODE> T;
-  T.mg = a.t_mg + tb;
-  T.gq = a.t_gq + tb;
-  T.len = a.t_len + tb;
-  T.last = a.t_last + tb;
-  T.next = a.t_next + tb;
-  T.kvb = a.sess_kvb + sb;
   T.tid = tid;
   T.parity = 0;
   T.red = s_red;
-  if (!cont) {
-    for (uint32_t i = tid; i < n_sess; i += BLOCK) {
-      T.mg[i] = 0;
-      T.gq[i] = 0;
-      T.len[i] = 0;
-      T.last[i] = 0;
-      T.next[i] = ~0ull;
+  if constexpr (IN_LDS) {
+    const uint32_t n = n_sess;
+    T.mg = s_tab;
+    T.last = s_tab + n;
+    T.gq = s_tab + 2 * (size_t)n;
+    T.next = s_tab + 3 * (size_t)n;
+    uint32_t* s32 = reinterpret_cast<uint32_t*>(s_tab + 4 * (size_t)n);
+    T.len = s32;
+    uint32_t* kv = s32 + n;
+    T.kvb = kv;
+    for (uint32_t i = tid; i < n; i += BLOCK) {
+      T.mg[i] = cont ? a.t_mg[tb + i] : 0ull;
+      T.last[i] = cont ? a.t_last[tb + i] : 0ull;
+      T.gq[i] = cont ? a.t_gq[tb + i] : 0ull;
+      T.next[i] = cont ? a.t_next[tb + i] : ~0ull;
+      T.len[i] = cont ? a.t_len[tb + i] : 0u;
+      kv[i] = a.sess_kvb[sb + i];
+    }
+  } else {
+    T.mg = a.t_mg + tb;
+    T.gq = a.t_gq + tb;
+    T.len = a.t_len + tb;
+    T.last = a.t_last + tb;
+    T.next = a.t_next + tb;
+    T.kvb = a.sess_kvb + sb;
+    if (!cont) {
+      for (uint32_t i = tid; i < n_sess; i += BLOCK) {
+        T.mg[i] = 0;
+        T.gq[i] = 0;
+        T.len[i] = 0;
+        T.last[i] = 0;
+        T.next[i] = ~0ull;
+      }
     }
   }
   __syncthreads();
@@ -907,41 +1085,52 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
     C = cnt_from(a.counters[sim]);
     next_event = a.state[sim].next_event;
   } else {
-    S = Scalars{0, 0, 0, 0, 0, 0, 0, 0};
+    S = Scalars{};
     C = cnt_from(unison_counters{});
   }
   if (S.hi > n_sess) S.hi = n_sess;  // never scan past the trace's sessions
   T.hi = S.hi;
   const LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
-                  a.log_cap, tid == 0};
-  if (C.error == 0) run_events<POL, SMODE>(T, P, K, tr, S, C, L, next_event, a.max_events);
+                  a.log_cap, tid == 0, (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
+  if (C.error == 0) run_events<POL, SMODE, true>(T, P, K, tr, S, C, L, next_event, a.max_events);
   __syncthreads();
+  if constexpr (IN_LDS) {
+    for (uint32_t i = tid; i < n_sess; i += BLOCK) {
+      a.t_mg[tb + i] = T.mg[i];
+      a.t_last[tb + i] = T.last[i];
+      a.t_gq[tb + i] = T.gq[i];
+      a.t_next[tb + i] = T.next[i];
+      a.t_len[tb + i] = T.len[i];
+    }
+  }
   if (tid == 0) {
+    finish_costs(S, P, C);
     store_scalars(a.state[sim], S, next_event);
     a.counters[sim] = cnt_to(C);
   }
 }
 
-template <int BLOCK>
+template <int BLOCK, bool IN_LDS>
 __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   __shared__ float s_hf[52];
   __shared__ uint32_t s_hq[52];
   __shared__ Cand s_red[2 * (BLOCK / 64)];
+  extern __shared__ uint64_t s_tab[];
   const uint32_t sim = blockIdx.x;
   const unison_sim_params P = a.params[sim];
   const uint32_t lambda = (1u << P.b_h) - 1u;
   load_lut(a.lut_d + (size_t)P.lut * kLut, a.lut_n + (size_t)P.lut * kLut, lambda, s_hf, s_hq,
            threadIdx.x, BLOCK);
   __syncthreads();
-  const KeyCtx K{s_hf, s_hq, P.penalty_us, lambda, P.p_z};
+  const KeyCtx K{s_hf, s_hq, P.penalty_us, lambda, P.p_z, a.time44 != 0};
   switch (sim_policy(a, P)) {
     case kSpear:
-      if (P.score_mode) block_run<BLOCK, kSpear, 1>(a, sim, P, K, s_red);
-      else block_run<BLOCK, kSpear, 0>(a, sim, P, K, s_red);
+      if (P.score_mode) block_run<BLOCK, kSpear, 1, IN_LDS>(a, sim, P, K, s_red, s_tab);
+      else block_run<BLOCK, kSpear, 0, IN_LDS>(a, sim, P, K, s_red, s_tab);
       break;
-    case kLru: block_run<BLOCK, kLru, 0>(a, sim, P, K, s_red); break;
-    case kTimeout: block_run<BLOCK, kTimeout, 0>(a, sim, P, K, s_red); break;
-    default: block_run<BLOCK, kBelady, 0>(a, sim, P, K, s_red); break;
+    case kLru: block_run<BLOCK, kLru, 0, IN_LDS>(a, sim, P, K, s_red, s_tab); break;
+    case kTimeout: block_run<BLOCK, kTimeout, 0, IN_LDS>(a, sim, P, K, s_red, s_tab); break;
+    default: block_run<BLOCK, kBelady, 0, IN_LDS>(a, sim, P, K, s_red, s_tab); break;
   }
 }
 
@@ -974,14 +1163,31 @@ struct Variant {
 };
 
 // Register-table shapes (lanes per simulation x sessions per lane); id 3 is
-// the streamed table.
+// the streamed table, id 9 the LDS-resident table.
 constexpr Variant kVariants[] = {{16, 1}, {64, 1}, {64, 4}, {0, 0}, {4, 4},
-                                 {8, 2},  {64, 24}, {16, 4}, {32, 8}};
+                                 {8, 2},  {64, 24}, {16, 4}, {32, 8}, {0, 1}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kBlock = 256;
+constexpr int kLdsVariant = 9;
+constexpr uint32_t kLdsBytesPerSession = 4 * 8 + 2 * 4;  // mg, last, gq, next; len, kvb
+
+// Largest dynamic LDS one workgroup may take on the current device.
+static uint32_t lds_limit() {
+  static int cached = -1;
+  if (cached < 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+      v = 65536;
+    cached = v;
+  }
+  const uint32_t static_bytes = 2048;  // hazard tables, reduction slots
+  return (uint32_t)cached > static_bytes ? (uint32_t)cached - static_bytes : 0u;
+}
 
 uint32_t sim_variant_capacity(int v) {
   if (v < 0 || v >= kNumVariants) return 0;
+  if (v == kLdsVariant) return lds_limit() / kLdsBytesPerSession;
   if (kVariants[v].g == 0) return UNISON_MAX_SESSIONS;
   return (uint32_t)(kVariants[v].g * kVariants[v].epl);
 }
@@ -989,8 +1195,7 @@ uint32_t sim_variant_capacity(int v) {
 int sim_auto_variant(uint32_t max_sess) {
   if (max_sess <= 16) return 5;
   if (max_sess <= 64) return 7;
-  if (max_sess <= 256) return 8;
-  if (max_sess <= 1536) return 6;
+  if (max_sess <= sim_variant_capacity(kLdsVariant)) return kLdsVariant;
   return 3;
 }
 
@@ -1013,10 +1218,44 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
     case 6: launch_regs<64, 24>(a, stream); break;
     case 7: launch_regs<16, 4>(a, stream); break;
     case 8: launch_regs<32, 8>(a, stream); break;
+    case kLdsVariant: {
+      const size_t lds = (size_t)(max_sess_in_batch ? max_sess_in_batch : 1) * kLdsBytesPerSession;
+      hipLaunchKernelGGL((sim_block_kernel<kBlock, true>), dim3(a.n_sims), dim3(kBlock), lds, stream, a);
+      break;
+    }
     default:
-      hipLaunchKernelGGL((sim_block_kernel<kBlock>), dim3(a.n_sims), dim3(kBlock), 0, stream, a);
+      hipLaunchKernelGGL((sim_block_kernel<kBlock, false>), dim3(a.n_sims), dim3(kBlock), 0, stream, a);
       break;
   }
+  return hipGetLastError();
+}
+
+// Largest event or next-arrival time over all traces ("never" excluded).
+__global__ __launch_bounds__(256) void max_time_kernel(const uint64_t* t, const uint64_t* next,
+                                                       uint64_t n, unsigned long long* out) {
+  uint64_t m = 0;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256u + threadIdx.x; i < n; i += (uint64_t)gridDim.x * 256u) {
+    const uint64_t a = t[i];
+    const uint64_t b = next[i];
+    m = a > m ? a : m;
+    m = (b != ~0ull && b > m) ? b : m;
+  }
+#pragma unroll
+  for (int k = 1; k < 64; k <<= 1) {
+    const uint64_t o = __shfl_xor(m, k);
+    m = o > m ? o : m;
+  }
+  if ((threadIdx.x & 63u) == 0) atomicMax(out, (unsigned long long)m);
+}
+
+hipError_t launch_max_time(const uint64_t* t, const uint64_t* next, uint64_t n, uint64_t* out,
+                           hipStream_t stream) {
+  hipError_t e = hipMemsetAsync(out, 0, sizeof(uint64_t), stream);
+  if (e != hipSuccess || n == 0) return e;
+  const uint64_t want = (n + 255) / 256;
+  const uint32_t blocks = (uint32_t)(want < 4096 ? want : 4096);
+  hipLaunchKernelGGL(max_time_kernel, dim3(blocks), dim3(256), 0, stream, t, next, n,
+                     reinterpret_cast<unsigned long long*>(out));
   return hipGetLastError();
 }
 

@@ -52,10 +52,11 @@ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
 }
 
 // Hash of one decision record (event, op, a, b); digests sum these mod 2^64.
+// The second word enters through an odd multiplier, then one finaliser pass.
 __device__ __forceinline__ uint64_t rec_hash(uint32_t ev, uint32_t op, uint32_t a, uint32_t b) {
-  uint64_t w0 = ((uint64_t)ev << 8) | (uint64_t)op;
-  uint64_t w1 = ((uint64_t)a << 32) | (uint64_t)b;
-  return mix64(w0 ^ mix64(w1));
+  const uint64_t w0 = ((uint64_t)ev << 8) | (uint64_t)op;
+  const uint64_t w1 = ((uint64_t)a << 32) | (uint64_t)b;
+  return mix64(w0 ^ (w1 * 0x9e3779b97f4a7c15ull));
 }
 
 __device__ __forceinline__ uint64_t sat_add(uint64_t a, uint64_t b) {
@@ -68,11 +69,14 @@ __device__ __forceinline__ uint64_t sat_mul(uint64_t a, uint64_t b) {
   return __umul64hi(a, b) ? ~0ull : a * b;
 }
 
-// eq. (ema) on the fp32 register, in microseconds, every operation rounded.
+// eq. (ema) on the fp32 register.  The sample is the gap in whole
+// microseconds (the tau = 10^3 resolution of eq. (lock)), clipped to 32 bits;
+// every operation is rounded to fp32.
 __device__ __forceinline__ float ema_f32(float g, uint64_t gap_ns) {
-  float x = (float)((double)gap_ns / 1000.0);
-  float a = 3.0f * x;
-  float b = 7.0f * g;
+  const uint64_t us = gap_ns / 1000u;
+  const float x = (float)(us > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)us);
+  const float a = 3.0f * x;
+  const float b = 7.0f * g;
   return (a + b) / 10.0f;
 }
 
@@ -139,6 +143,10 @@ struct SimState {
   uint64_t log_len;
   uint32_t hi;           // 1 + largest session id seen so far
   uint32_t pad;
+  // exact sums behind the AMAT and TTFT counters (eq. (hr-amat)): bytes read
+  // by SRAM / HBM hits, tokens of missed requests, bytes of the previous
+  // prefix on SRAM / HBM hits
+  uint64_t hit_s_bytes, hit_h_bytes, miss_tok, prev_s_bytes, prev_h_bytes;
 };
 
 struct SimArgs {
@@ -167,7 +175,7 @@ struct SimArgs {
   uint32_t log_cap;
   uint32_t flags;
   uint32_t policy_override;
-  uint32_t pad;
+  uint32_t time44;         // every trace time is below 2^44 - 1 ns
 };
 
 }  // namespace unison

@@ -13,7 +13,7 @@ from tracekit import trace_from_events
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = (0, 1, 2, 3, 4, 5)
+VARIANTS = (0, 1, 2, 3, 4, 5, 6, 7, 8, 9)
 
 
 def say(*a):
@@ -77,7 +77,7 @@ def test_c3_decision_logs(c3):
         assert same_log(s.log(k), oracle_log(c3, i)), "c3 sim %d log" % i
 
 
-@pytest.mark.parametrize("variant", [None, 3])
+@pytest.mark.parametrize("variant", [None, 3, 9])
 def test_continue_matches_single_run(c3, c3_want, variant):
     sims = list(range(5, c3.n_sims, 61))
     w = subset(c3, sims)
@@ -157,10 +157,19 @@ def test_ragged_session_counts(n_sess):
     w = edge_workload([tr], rows)
     say("ragged: %d sessions, %d events, %d sims" % (n_sess, tr.n_events, w.n_sims))
     s = Sim(w, log_cap=1 << 14)
-    s.run(flags=2)
+    s.run(flags=2 | 4)
     compare_counters(s.counters(), oracle_counters(w), label="ragged %d" % n_sess)
-    for i in range(0, w.n_sims, 5):
-        assert same_log(s.log(i), oracle_log(w, i)), "ragged %d sim %d" % (n_sess, i)
+    D, N = oracle.luts_for(w)
+    for i in range(w.n_sims):
+        g = s.log(i)
+        row = w.params[i]
+        _, _, olog, st, _ = oracle.run(tr, row, D[int(row["lut"])], N[int(row["lut"])],
+                                       log_cap=1 << 14, states=True)
+        gv = g[g["op"] == 6]["a"]
+        bad = np.nonzero(gv != st["victim"])[0]
+        assert len(bad) == 0, "ragged %d sim %d: scan victim differs at events %s" % (
+            n_sess, i, bad[:5].tolist())
+        assert same_log(g[g["op"] != 6], olog), "ragged %d sim %d decision log" % (n_sess, i)
 
 
 def test_mixed_traces_and_empty_trace():

@@ -117,15 +117,28 @@ def test_integer_ema_gap_clip():
 
 
 def test_float_ema_within_rounding_bound():
+    """eq. (ema) on whole-microsecond samples: the fp32 register stays within
+    its rounding bound of the exact rational EMA."""
+    from fractions import Fraction
     rng = np.random.default_rng(11)
-    gaps = rng.integers(1_000_000, 300_000_000_000, (500, 8)).astype(np.uint64)
-    nh = rng.integers(0, 9, 500).astype(np.uint8)
+    gaps = rng.integers(1_000_000, 300_000_000_000, (300, 8)).astype(np.uint64)
+    gaps[0, 0] = 999           # below one microsecond: the sample is 0
+    nh = rng.integers(0, 9, 300).astype(np.uint8)
+    nh[0] = 1
     g, _ = oracle.ema_replay(gaps, nh)
-    for i in range(500):
-        ref = 0.0
+    assert float(g[0]) == 0.0
+    for i in range(300):
+        ref = Fraction(0)
         for k in range(nh[i]):
-            ref = 0.3 * (int(gaps[i, k]) / 1000.0) + 0.7 * ref
-        assert abs(float(g[i]) - ref) <= 2e-6 * max(ref, 1.0)
+            ref = (3 * Fraction(int(gaps[i, k]) // 1000) + 7 * ref) / 10
+        assert abs(float(g[i]) - float(ref)) <= 2e-6 * max(float(ref), 1.0)
+
+
+def test_ema_sample_clips_at_32_bits():
+    gaps = np.array([[(2 ** 32 + 5) * 1000, 0]], np.uint64)
+    g, gq = oracle.ema_replay(gaps, [1], b_g=32)
+    assert int(gq[0]) == (3 * (2 ** 32 - 1)) // 10
+    assert float(g[0]) == np.float32(np.float32(3.0) * np.float32(2 ** 32 - 1)) / np.float32(10)
 
 
 # ------------------------------------------------------------ fp32 score
