@@ -91,6 +91,16 @@ __device__ __forceinline__ uint64_t reduce_packed(uint64_t c) {
   }
 }
 
+template <int W, int M>
+__device__ __forceinline__ uint32_t reduce_min32(uint32_t c) {
+  if constexpr (M < W) {
+    const uint32_t o = xchg<M>(c);
+    return reduce_min32<W, M * 2>(o < c ? o : c);
+  } else {
+    return c;
+  }
+}
+
 // Every lane of an aligned group of W lanes ends with the winner (ties to
 // the smaller session id).
 template <int W, bool MAX>
@@ -128,22 +138,35 @@ struct KeyCtx {
   bool pack44;          // times fit 44 bits and ids 20 bits: recency / Belady keys pack
 };
 
-// "Larger key = evict first".  SPEAR: the score (eq. (esp) or eq. (scoreq));
-// completed sessions take S_max.  LRU / timeout: older last event first.
-// Belady: later next arrival first.
+// The hazard entry eq. (hazard) / eq. (hq) of a session at turn index t
+// (clamped to 50): fp32 bits of h for the fp32 score, h_q for the integer one.
 template <uint32_t POL, uint32_t SMODE>
-__device__ __forceinline__ uint64_t key_of(const KeyCtx& K, uint32_t meta, float g, uint64_t gq,
-                                           uint64_t last, uint64_t next) {
+__device__ __forceinline__ uint32_t hazard_of(const KeyCtx& K, uint32_t meta) {
   using PT = Pol<POL, SMODE>;
   if constexpr (PT::spear) {
     uint32_t t = meta_turn(meta);
     t = t < 50u ? t : 50u;
+    return PT::fixed ? K.hq[t] : __float_as_uint(K.hf[t]);
+  } else {
+    return 0u;
+  }
+}
+
+// "Larger key = evict first".  SPEAR: the score (eq. (esp) or eq. (scoreq))
+// from the entry's hazard value hz (hazard_of); completed sessions take
+// S_max.  LRU / timeout: older last event first.  Belady: later next arrival
+// first.
+template <uint32_t POL, uint32_t SMODE>
+__device__ __forceinline__ uint64_t key_of(const KeyCtx& K, uint32_t meta, uint32_t hz, float g,
+                                           uint64_t gq, uint64_t last, uint64_t next) {
+  using PT = Pol<POL, SMODE>;
+  if constexpr (PT::spear) {
     const bool done = meta_phase(meta) == kDoneP;
     if constexpr (PT::fixed) {
-      const uint64_t s = spear_fixed(K.hq[t], gq, K.lambda, K.p_z);
+      const uint64_t s = spear_fixed(hz, gq, K.lambda, K.p_z);
       return done ? ~0ull : s;
     } else {
-      const float s = spear_f32(K.hf[t], g, K.P);
+      const float s = spear_f32(__uint_as_float(hz), g, K.P);
       return done ? 0x7F800000ull : (uint64_t)__float_as_uint(s);
     }
   } else if constexpr (PT::belady) {
@@ -177,6 +200,7 @@ struct RegTable {
   uint64_t last[EPL];
   uint64_t next[EPL];
   uint64_t key[EPL];
+  uint32_t hz[EPL];   // hazard value at the entry's turn (hazard_of), set when the turn changes
 
   __device__ __forceinline__ uint32_t sid_of(int j) const { return (uint32_t)j * G + lane; }
 
@@ -250,6 +274,16 @@ struct RegTable {
 #pragma unroll
     for (int j = 0; j < EPL; ++j) meta[j] = (mine && js == (uint32_t)j) ? m : meta[j];
   }
+  // A new turn index: look its hazard up once instead of at every scan.
+  __device__ __forceinline__ void set_turn(uint32_t sid, uint32_t m, const KeyCtx& K) {
+    if constexpr (PT::spear) {
+      const uint32_t h = hazard_of<POL, SMODE>(K, m);
+      const uint32_t js = sid / G;
+      const bool mine = lane == sid % G;
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) hz[j] = (mine && js == (uint32_t)j) ? h : hz[j];
+    }
+  }
   __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
     const uint32_t js = sid / G;
     const bool mine = lane == sid % G;
@@ -265,7 +299,7 @@ struct RegTable {
   __device__ __forceinline__ void scan(const KeyCtx& K) {
 #pragma unroll
     for (int j = 0; j < EPL; ++j)
-      key[j] = key_of<POL, SMODE>(K, meta[j], g[j], PT::fixed ? gq[j] : 0ull, last[j],
+      key[j] = key_of<POL, SMODE>(K, meta[j], hz[j], g[j], PT::fixed ? gq[j] : 0ull, last[j],
                                   PT::belady ? next[j] : 0ull);
   }
 
@@ -338,18 +372,23 @@ struct RegTable {
     return Cand{key, none ? kNone : (MAX ? 0xFFFFFu - lo : lo)};
   }
 
-  // Smallest evictable session idle for longer than ttl (timeout policy).
+  // TIDE's two candidates, eq. (promote) and eq. (demote), from one pass.
+  __device__ __forceinline__ void select_pd(const KeyCtx& K, Cand& p, Cand& d) const {
+    p = select<false>(kTierHbm, K);
+    d = select<true>(kTierSram, K);
+  }
+
+  // Smallest evictable session idle for longer than ttl (timeout policy);
+  // kNone if there is none.
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) const {
-    Cand c = cand_none_min();
+    uint32_t c = kNone;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
       const bool ok = evictable(meta[j]) && now - last[j] > ttl;
       const uint32_t s = sid_of(j);
-      const bool take = ok && s < c.sid;
-      c.sid = take ? s : c.sid;
-      c.key = take ? 0ull : c.key;
+      c = ok && s < c ? s : c;
     }
-    return reduce_group<G, false>(c).sid;
+    return reduce_min32<G, 1>(c);
   }
 };
 
@@ -425,6 +464,7 @@ struct MemTable {
     set_meta(sid, m);
     len[sid] = l;
   }
+  __device__ __forceinline__ void set_turn(uint32_t, uint32_t, const KeyCtx&) {}
 
   __device__ __forceinline__ void scan(const KeyCtx&) {}
 
@@ -450,8 +490,8 @@ struct MemTable {
   __device__ __forceinline__ uint64_t key_at(const KeyCtx& K, uint32_t i, uint64_t x) const {
     const uint32_t m = (uint32_t)x;
     const float gv = __uint_as_float((uint32_t)(x >> 32));
-    return key_of<POL, SMODE>(K, m, gv, PT::fixed ? gq[i] : 0ull, PT::recency ? last[i] : 0ull,
-                              PT::belady ? next[i] : 0ull);
+    return key_of<POL, SMODE>(K, m, hazard_of<POL, SMODE>(K, m), gv, PT::fixed ? gq[i] : 0ull,
+                              PT::recency ? last[i] : 0ull, PT::belady ? next[i] : 0ull);
   }
 
   // Streams the window and reduces the keys of evictable entries in `tier`.
@@ -480,6 +520,38 @@ struct MemTable {
   }
   // The first reduction of an event is the full-table scan.
   __device__ __forceinline__ Cand argmax_first(const KeyCtx& K) { return select<true>(0, K); }
+
+  // TIDE's two candidates, eq. (promote) and eq. (demote), from one pass.
+  __device__ __forceinline__ void select_pd(const KeyCtx& K, Cand& p, Cand& d) {
+    Cand cp = cand_none_min(), cd = cand_none_max();
+    for (uint32_t base = tid; base < hi; base += UNROLL * BLOCK) {
+      uint64_t x[UNROLL];
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        const uint32_t i = base + u * BLOCK;
+        x[u] = i < hi ? mg[i] : 0ull;
+      }
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        const uint32_t i = base + u * BLOCK;
+        const uint32_t m = (uint32_t)x[u];
+        const bool ev = i < hi && evictable(m);
+        const bool in_h = ev && meta_tier(m) == kTierHbm;
+        const bool in_s = ev && meta_tier(m) == kTierSram;
+        if (in_h || in_s) {
+          const uint64_t k = key_at(K, i, x[u]);
+          const bool tp = in_h && min_better(k, i, cp.key, cp.sid);
+          const bool td = in_s && max_better(k, i, cd.key, cd.sid);
+          cp.key = tp ? k : cp.key;
+          cp.sid = tp ? i : cp.sid;
+          cd.key = td ? k : cd.key;
+          cd.sid = td ? i : cd.sid;
+        }
+      }
+    }
+    p = block_reduce<false>(cp);
+    d = block_reduce<true>(cd);
+  }
 
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) {
     Cand c = cand_none_min();
@@ -639,6 +711,9 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
   const uint64_t end = (e >= tr.n_ev || tr.n_ev - e < max_events) ? tr.n_ev : e + max_events;
   if (e >= end) return;
   Ev cur = load_ev<PT::belady>(tr, e);
+  // victim-digest weight of event e, (2e + 1) * 0x9e3779b97f4a7c15, stepped per event
+  constexpr uint64_t kGolden = 0x9e3779b97f4a7c15ull;
+  uint64_t vw = (2ull * e + 1ull) * kGolden;
   for (; e < end; ++e) {
     // the next event's record is in flight while this one is processed
     const Ev nxt = load_ev<PT::belady>(tr, e + 1 < end ? e + 1 : e);
@@ -700,6 +775,7 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         T.grow(S.hi);
       }
       T.write(sid, x);
+      T.set_turn(sid, x.meta, K);
     } else {
       T.read_end(sid, x);
       ph = meta_phase(x.meta);
@@ -719,7 +795,8 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     T.scan(K);
     const Cand v0 = T.argmax_first(K);
     // odd weight per event: a different victim at any one event changes the sum
-    C.victim_digest += ((uint64_t)v0.sid + 1u) * ((2ull * e + 1ull) * 0x9e3779b97f4a7c15ull);
+    C.victim_digest += ((uint64_t)v0.sid + 1u) * vw;
+    vw += 2ull * kGolden;
     if (L.victims) {
       if (L.rec && L.lead && S.log_len < L.cap) L.rec[S.log_len] = unison_record{ev, kOpVictim, v0.sid, kNone};
       if (L.rec) S.log_len++;
@@ -809,7 +886,8 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         uint64_t left = budget, moved = 0;
         C.tide_passes++;
         for (;;) {
-          const Cand p = T.template select<false>(kTierHbm, K);  // eq. (promote)
+          Cand p, d;
+          T.select_pd(K, p, d);  // eq. (promote), eq. (demote)
           if (p.sid == kNone) break;
           if (PT::has_inf && p.key == PT::inf_key) break;
           uint64_t sp;
@@ -825,7 +903,6 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
             C.promote++;
             continue;
           }
-          const Cand d = T.template select<true>(kTierSram, K);  // eq. (demote)
           if (d.sid == kNone) break;
           uint64_t sd;
           uint32_t md;
@@ -949,6 +1026,7 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
     T.last[j] = ld ? a.t_last[tb + s] : 0ull;
     if constexpr (PT::belady) T.next[j] = ld ? a.t_next[tb + s] : ~0ull;
     T.key[j] = 0;
+    T.hz[j] = hazard_of<POL, SMODE>(K, T.meta[j]);
   }
 
   Scalars S;
