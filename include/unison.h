@@ -260,8 +260,8 @@ int unison_kendall(void* hip_stream, uint32_t n_snap, uint32_t n_per, uint64_t n
 /* Test hook: pins the simulation kernel variant (-1 = chosen by the largest
  * trace; register tables of lanes x sessions per lane 0: 16 x 1, 1: 64 x 1,
  * 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 6: 64 x 24, 7: 16 x 4, 8: 32 x 8; one
- * workgroup per simulation with the table 3: streamed from the workspace,
- * 9: held in LDS).  A variant too small for the traces, or an unknown id,
+ * workgroup per simulation with the table 3: streamed from the workspace by
+ * 256 threads, 10: by 512 threads, 9: held in LDS).  A variant too small for the traces, or an unknown id,
  * makes unison_run return UNISON_E_CAPACITY. */
 int unison_debug_force_variant(unison_ctx* ctx, int variant);
 

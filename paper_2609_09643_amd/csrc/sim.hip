@@ -109,6 +109,20 @@ __device__ __forceinline__ Cand reduce_group(Cand c) {
   return c;
 }
 
+// Pins a value to a vector register.  A workgroup-per-simulation kernel keeps
+// its long-lived per-simulation state (pool usage, counters) there: held in
+// scalar registers it would exceed them and spill on every event.
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+__device__ __forceinline__ uint64_t in_vgpr(uint64_t v) {
+  return ((uint64_t)in_vgpr((uint32_t)(v >> 32)) << 32) | in_vgpr((uint32_t)v);
+}
+__device__ __forceinline__ double in_vgpr(double v) {
+  return __longlong_as_double((long long)in_vgpr((uint64_t)__double_as_longlong(v)));
+}
+
 __device__ __forceinline__ uint32_t uni32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
 }
@@ -475,16 +489,17 @@ struct MemTable {
     parity ^= 1u;
     if ((tid & 63u) == 0) buf[tid >> 6] = c;
     __syncthreads();
-    Cand r = buf[0];
+    uint64_t rk = buf[0].key;
+    uint32_t rs = buf[0].sid;
 #pragma unroll
     for (int w = 1; w < NW; ++w) {
-      const Cand o = buf[w];
-      const bool take = MAX ? max_better(o.key, o.sid, r.key, r.sid) : min_better(o.key, o.sid, r.key, r.sid);
-      r = take ? o : r;
+      const uint64_t ok = buf[w].key;
+      const uint32_t os = buf[w].sid;
+      const bool take = MAX ? max_better(ok, os, rk, rs) : min_better(ok, os, rk, rs);
+      rk = take ? ok : rk;
+      rs = take ? os : rs;
     }
-    r.key = uni64(r.key);
-    r.sid = uni32(r.sid);
-    return r;
+    return Cand{uni64(rk), uni32(rs)};
   }
 
   __device__ __forceinline__ uint64_t key_at(const KeyCtx& K, uint32_t i, uint64_t x) const {
@@ -635,6 +650,58 @@ __device__ __forceinline__ unison_counters cnt_to(const Cnt& k) {
   c.amat_sum_ns = k.amat;
   c.ttft_sum_ns = k.ttft;
   return c;
+}
+
+__device__ __forceinline__ void pin_vgpr(Scalars& S) {
+  S.used_s = in_vgpr(S.used_s);
+  S.used_h = in_vgpr(S.used_h);
+  S.dma_free_at = in_vgpr(S.dma_free_at);
+  S.prev_t = in_vgpr(S.prev_t);
+  S.log_len = in_vgpr(S.log_len);
+  S.n_res = in_vgpr(S.n_res);
+  S.n_table = in_vgpr(S.n_table);
+  S.hi = in_vgpr(S.hi);
+  S.hit_s_bytes = in_vgpr(S.hit_s_bytes);
+  S.hit_h_bytes = in_vgpr(S.hit_h_bytes);
+  S.miss_tok = in_vgpr(S.miss_tok);
+  S.prev_s_bytes = in_vgpr(S.prev_s_bytes);
+  S.prev_h_bytes = in_vgpr(S.prev_h_bytes);
+}
+
+__device__ __forceinline__ void pin_vgpr(unison_sim_params& p) {
+  p.tide = in_vgpr(p.tide);
+  p.cap_sram_B = in_vgpr(p.cap_sram_B);
+  p.cap_hbm_B = in_vgpr(p.cap_hbm_B);
+  p.n_slots = in_vgpr(p.n_slots);
+  p.dma_B_per_us = in_vgpr(p.dma_B_per_us);
+  p.ttl_ns = in_vgpr(p.ttl_ns);
+  p.b_g = in_vgpr(p.b_g);
+  p.tau_ns = in_vgpr(p.tau_ns);
+}
+
+__device__ __forceinline__ void pin_vgpr(Cnt& k) {
+  k.requests = in_vgpr(k.requests);
+  k.hit_sram = in_vgpr(k.hit_sram);
+  k.hit_hbm = in_vgpr(k.hit_hbm);
+  k.miss = in_vgpr(k.miss);
+  k.bypass = in_vgpr(k.bypass);
+  k.evict = in_vgpr(k.evict);
+  k.expire = in_vgpr(k.expire);
+  k.promote = in_vgpr(k.promote);
+  k.swap = in_vgpr(k.swap);
+  k.tide_passes = in_vgpr(k.tide_passes);
+  k.events = in_vgpr(k.events);
+  k.dma_bytes = in_vgpr(k.dma_bytes);
+  k.tokens_total = in_vgpr(k.tokens_total);
+  k.tokens_computed = in_vgpr(k.tokens_computed);
+  k.extra_prefill = in_vgpr(k.extra_prefill);
+  k.score_evals = in_vgpr(k.score_evals);
+  k.resident_evals = in_vgpr(k.resident_evals);
+  k.digest = in_vgpr(k.digest);
+  k.victim_digest = in_vgpr(k.victim_digest);
+  k.error = in_vgpr(k.error);
+  k.amat = in_vgpr(k.amat);
+  k.ttft = in_vgpr(k.ttft);
 }
 
 struct LogSink {
@@ -860,7 +927,13 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
           }
           // the event's own scan result is the first victim: the arriving
           // session was never evictable, so releasing it changed nothing
-          const Cand v = first ? v0 : T.template select<true>(0, K);
+          Cand v;
+          if (first) {
+            v.key = v0.key;
+            v.sid = v0.sid;
+          } else {
+            v = T.template select<true>(0, K);
+          }
           first = false;
           if (v.sid == kNone) {
             emit(C, S, L, ev, kOpBypass, sid, kNone);
@@ -1168,9 +1241,15 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   }
   if (S.hi > n_sess) S.hi = n_sess;  // never scan past the trace's sessions
   T.hi = S.hi;
+  pin_vgpr(S);
+  pin_vgpr(C);
   const LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
                   a.log_cap, tid == 0, (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
-  if (C.error == 0) run_events<POL, SMODE, true>(T, P, K, tr, S, C, L, next_event, a.max_events);
+  if (C.error == 0) {
+    unison_sim_params Pv = P;
+    pin_vgpr(Pv);
+    run_events<POL, SMODE, true>(T, Pv, K, tr, S, C, L, next_event, a.max_events);
+  }
   __syncthreads();
   if constexpr (IN_LDS) {
     for (uint32_t i = tid; i < n_sess; i += BLOCK) {
@@ -1240,10 +1319,10 @@ struct Variant {
   int g, epl;
 };
 
-// Register-table shapes (lanes per simulation x sessions per lane); id 3 is
-// the streamed table, id 9 the LDS-resident table.
+// Register-table shapes (lanes per simulation x sessions per lane); ids 3
+// and 10 stream the table with 256 and 512 threads, id 9 keeps it in LDS.
 constexpr Variant kVariants[] = {{16, 1}, {64, 1}, {64, 4}, {0, 0}, {4, 4},
-                                 {8, 2},  {64, 24}, {16, 4}, {32, 8}, {0, 1}};
+                                 {8, 2},  {64, 24}, {16, 4}, {32, 8}, {0, 1}, {0, 0}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kBlock = 256;
 constexpr int kLdsVariant = 9;
@@ -1274,7 +1353,7 @@ int sim_auto_variant(uint32_t max_sess) {
   if (max_sess <= 16) return 5;
   if (max_sess <= 64) return 7;
   if (max_sess <= sim_variant_capacity(kLdsVariant)) return kLdsVariant;
-  return 3;
+  return 10;
 }
 
 template <int G, int EPL>
@@ -1301,6 +1380,9 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
       hipLaunchKernelGGL((sim_block_kernel<kBlock, true>), dim3(a.n_sims), dim3(kBlock), lds, stream, a);
       break;
     }
+    case 10:
+      hipLaunchKernelGGL((sim_block_kernel<512, false>), dim3(a.n_sims), dim3(512), 0, stream, a);
+      break;
     default:
       hipLaunchKernelGGL((sim_block_kernel<kBlock, false>), dim3(a.n_sims), dim3(kBlock), 0, stream, a);
       break;

@@ -13,7 +13,7 @@ from tracekit import trace_from_events
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = (0, 1, 2, 3, 4, 5, 6, 7, 8, 9)
+VARIANTS = (0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10)
 
 
 def say(*a):
@@ -77,7 +77,7 @@ def test_c3_decision_logs(c3):
         assert same_log(s.log(k), oracle_log(c3, i)), "c3 sim %d log" % i
 
 
-@pytest.mark.parametrize("variant", [None, 3, 9])
+@pytest.mark.parametrize("variant", [None, 3, 9, 10])
 def test_continue_matches_single_run(c3, c3_want, variant):
     sims = list(range(5, c3.n_sims, 61))
     w = subset(c3, sims)
@@ -178,7 +178,7 @@ def test_mixed_traces_and_empty_trace():
     trs = [synth.tiny_trace(seed=5, n_sessions=12, turns=4), empty,
            synth.tiny_trace(seed=6, n_sessions=9, turns=7)]
     w = edge_workload(trs, edge_rows(3, rng))
-    for v in (None, 3):
+    for v in (None, 3, 10):
         s = Sim(w, variant=v)
         s.run()
         got = s.counters()
