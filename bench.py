@@ -26,10 +26,12 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "simulated session-events/s and score evals/s (1 GPU); % HBM roofline"
-# Algorithmic bytes: the session-record fields one key evaluation reads and
-# the event record one event reads ("Roofline").
-EVAL_BYTES = {0: 8, 1: 12, 2: 12, 3: 12}   # SPEAR fp32 (meta+g), LRU/timeout (meta+last), Belady (meta+next)
-EVENT_BYTES = 28                           # t 8 + sid 4 + info 4 + len 4 + next 8
+# Algorithmic bytes per unit of work: one score evaluation reads one
+# session-table record (turn, gap EMA, flags, length: 12 B), and a recency or
+# next-arrival key adds its 8-B time; one event reads its 32-B record (time,
+# session, kind and turn, length, next arrival, the session's KV bytes/token).
+EVAL_BYTES = {0: 12, 1: 20, 2: 20, 3: 20}   # SPEAR, LRU, timeout, Belady
+EVENT_BYTES = 32
 PMC_FILE = os.path.join(ROOT, "profiles", "sim_c3_pmc.txt")
 SIM_SOURCES = [os.path.join(ROOT, "paper_2609_09643_amd", "csrc", f)
                for f in ("sim.hip", "unison_device.h")]
@@ -186,8 +188,8 @@ def main():
                     help="only run one device-to-device copy of MIB MiB (PMC byte calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the simulations are independent and this build "
-              "runs on a single MI355X (see DESIGN.md for how the batch would shard)",
+        print("bench.py measures one GPU only: the simulations are independent, and a batch "
+              "would shard over GPUs as contiguous blocks of simulations with no exchange",
               file=sys.stderr)
         sys.exit(2)
 
