@@ -35,9 +35,11 @@ namespace unison {
 
 // ------------------------------------------------------- cross-lane moves
 
+// Every pattern used here reads a lane of the same row, so no lane needs a
+// fallback value (mov_dpp leaves the destination's old value unspecified).
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
 }
 
 // Partner value for butterfly step M.  Before step M every aligned block of
@@ -705,7 +707,8 @@ __device__ __forceinline__ void pin_vgpr(Cnt& k) {
 }
 
 struct LogSink {
-  unison_record* rec;  // this simulation's records, or null
+  bool on;             // logging requested (a launch-wide, uniform flag)
+  unison_record* rec;  // this simulation's records
   uint32_t cap;
   bool lead;           // the one lane that stores records
   bool victims;        // also record each event's scan result
@@ -714,7 +717,7 @@ struct LogSink {
 __device__ __forceinline__ void emit(Cnt& C, Scalars& S, const LogSink& L, uint32_t ev, uint32_t op,
                                      uint32_t a, uint32_t b) {
   C.digest += rec_hash(ev, op, a, b);
-  if (L.rec) {
+  if (L.on) {
     if (L.lead && S.log_len < L.cap) {
       unison_record r;
       r.ev = ev;
@@ -865,8 +868,8 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     C.victim_digest += ((uint64_t)v0.sid + 1u) * vw;
     vw += 2ull * kGolden;
     if (L.victims) {
-      if (L.rec && L.lead && S.log_len < L.cap) L.rec[S.log_len] = unison_record{ev, kOpVictim, v0.sid, kNone};
-      if (L.rec) S.log_len++;
+      if (L.lead && S.log_len < L.cap) L.rec[S.log_len] = unison_record{ev, kOpVictim, v0.sid, kNone};
+      S.log_len++;
     }
 
     if (kind == kArrive) {
@@ -1113,8 +1116,9 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
     S = Scalars{};
     C = cnt_from(unison_counters{});
   }
-  const LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
-                  a.log_cap, lane == 0, (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
+  const bool log_on = (a.flags & UNISON_RUN_LOG) && a.log_cap;
+  const LogSink L{log_on, log_on ? a.log + (size_t)sim * a.log_cap : nullptr, a.log_cap, lane == 0,
+                  log_on && (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
   if (C.error == 0) {
     if (n_sess > (uint32_t)(G * EPL)) {
       C.error = ~0ull;  // the launcher picks a variant that holds the trace
@@ -1243,8 +1247,9 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   T.hi = S.hi;
   pin_vgpr(S);
   pin_vgpr(C);
-  const LogSink L{(a.flags & UNISON_RUN_LOG) && a.log_cap ? a.log + (size_t)sim * a.log_cap : nullptr,
-                  a.log_cap, tid == 0, (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
+  const bool log_on = (a.flags & UNISON_RUN_LOG) && a.log_cap;
+  const LogSink L{log_on, log_on ? a.log + (size_t)sim * a.log_cap : nullptr, a.log_cap, tid == 0,
+                  log_on && (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
   if (C.error == 0) {
     unison_sim_params Pv = P;
     pin_vgpr(Pv);
