@@ -173,12 +173,45 @@ def section_c5(torch, U, synth, steps):
             "mean_tau_b": float(np.nanmean(tau)), "top1_agreement": float((top == 1).mean())}
 
 
+def section_fmt(torch):
+    """The fixed-point format sweep: 27 (b_h, b_g, tau) points x 18 (trace,
+    envelope) cells of whole-trace SPEAR+TIDE replays plus the fp32
+    reference, and ranking fidelity on 7,265 snapshots of 64 sessions."""
+    from paper_2609_09643_amd import fidelity, synth
+    fmts = synth.format_grid()
+    w, meta = synth.format_sweep(formats=fmts)
+    t0 = time.perf_counter()
+    c, d_hr, d_am, cells = fidelity.run_trajectories(w, meta, fmts)
+    torch.cuda.synchronize()
+    t_traj = time.perf_counter() - t0
+    rs = synth.fidelity_snapshots()
+    t0 = time.perf_counter()
+    rank = fidelity.ranking_fidelity(rs, fmts)
+    torch.cuda.synchronize()
+    t_rank = time.perf_counter() - t0
+    rows = []
+    for f, (bh, bg, tau) in enumerate(fmts):
+        worst = float(np.nanmax(np.abs(d_hr[f])))
+        rows.append({"format": [bh, bg, tau], "worst_hr_drift_pp": round(worst, 4),
+                     "mean_hr_drift_pp": round(float(np.nanmean(np.abs(d_hr[f]))), 4),
+                     "mean_amat_drift_pct": round(float(np.nanmean(d_am[f])), 4),
+                     "mean_tau_b": round(rank[f][0], 6), "top1": round(rank[f][2], 4),
+                     "passes": bool(worst <= fidelity.HR_GATE_PP and rank[f][2] >= fidelity.TOP1_GATE)})
+    locked = rows[fmts.index(synth.LOCKED_FORMAT)]
+    return {"workload": "format sweep: 27 formats + fp32 x 18 cells (6 traces, 1,415 sessions, "
+                        "33,596 turns; 3 envelopes), %d simulations; ranking on %d x %d snapshots"
+                        % (w.n_sims, rs.n_snap, rs.n_per),
+            "trajectory_s": t_traj, "events_per_s": float(c["events"].sum()) / t_traj,
+            "ranking_s": t_rank, "locked": locked,
+            "passing": [r["format"] for r in rows if r["passes"]], "formats": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--sections", default="c2,c5", help="comma list of c2,c4,c5 or 'none'")
+    ap.add_argument("--sections", default="c2,c5", help="comma list of c2,c4,c5,fmt or 'none'")
     ap.add_argument("--c4-events", type=int, default=200_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", type=int, default=None)
@@ -255,6 +288,9 @@ def main():
     if "c4" in secs:
         log("section c4")
         extra["c4"] = section_c4(torch, U, synth, args.c4_events)
+    if "fmt" in secs:
+        log("section fmt")
+        extra["fmt"] = section_fmt(torch)
     if extra:
         result["sections"] = extra
     if not args.no_cpu_baseline:

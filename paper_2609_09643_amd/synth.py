@@ -383,3 +383,101 @@ def c5_ranking(n_snap=10000, n_per=4096, pool=65536, max_hist=8, seed=5) -> Rank
         idx[s] = rng.choice(pool, size=n_per, replace=False)
     lut_pop = lognormal_turns(np.random.Generator(np.random.PCG64(seed + 1000)), 128)
     return RankingSet(turn, done, gaps, n_hist, idx, lut_pop)
+
+
+# ------------------------------------------------- fixed-point format sweep
+
+# Sec. IV-C: the pre-registered grid of hazard bits b_h, gap-register bits
+# b_g and time divisor tau (exact divider, b_s = 64), and the locked point of
+# eq. (lock).
+FORMAT_BH = (8, 10, 12)
+FORMAT_BG = (24, 32, 64)
+FORMAT_TAU_NS = (1, 1000, 1_000_000)
+LOCKED_FORMAT = (12, 32, 1000)
+
+# Six traces of 128..496 sessions, 1,415 sessions and 33,596 turns in all
+# (Sec. V-A); three capacity envelopes of Table VI in tokens at 128 KiB/token:
+# Edge-Tight (10K SRAM / 50K HBM) and its HBM-100K and SRAM-20K neighbours.
+FIDELITY_SESSIONS = (128, 160, 192, 215, 224, 496)
+FIDELITY_ENVELOPES = ((10_000, 50_000), (10_000, 100_000), (20_000, 50_000))
+FIDELITY_TURNS = 33_596
+
+
+def format_grid():
+    """The 27 (b_h, b_g, tau_ns) points of the format sweep."""
+    return [(bh, bg, tau) for bh in FORMAT_BH for bg in FORMAT_BG for tau in FORMAT_TAU_NS]
+
+
+def fix_total(rng, t, total, lo=1):
+    """Adds or removes single turns at random sessions until sum(t) = total."""
+    t = np.asarray(t, dtype=np.int64).copy()
+    diff = int(total - t.sum())
+    while diff != 0:
+        i = int(rng.integers(t.shape[0]))
+        if diff > 0:
+            t[i] += 1
+            diff -= 1
+        elif t[i] > lo:
+            t[i] -= 1
+            diff += 1
+    return t.astype(np.uint32)
+
+
+def fidelity_traces(seed=300, rate_per_s=0.2):
+    """The six stand-in traces: turn counts 1 + floor(lognormal(ln 16.5,
+    0.8)) (mean about 23.7, a hazard that rises with the turn index) fixed up
+    to 33,596 turns in all; Poisson arrivals at 0.2 sessions/s, which keeps
+    about 50 sessions live at once (the paper's traces stay at or below 64);
+    mixture gaps; KV 64/128/160 KiB per token in thirds."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n_all = sum(FIDELITY_SESSIONS)
+    turns = fix_total(rng, lognormal_turns(rng, n_all, median=16.5), FIDELITY_TURNS)
+    traces, at = [], 0
+    for n in FIDELITY_SESSIONS:
+        first = poisson_arrivals(rng, n, rate_per_s)
+        kvb = np.array([64, 128, 160], dtype=np.uint32)[rng.permutation(n) % 3] * KIB
+        traces.append(build_trace(rng, turns[at:at + n], first, gaps_mixture, kvb))
+        at += n
+    return traces
+
+
+FORMAT_META_DTYPE = np.dtype([("trace", np.uint32), ("envelope", np.uint32), ("fmt", np.int32)])
+
+
+def format_sweep(traces=None, envelopes=FIDELITY_ENVELOPES, formats=None, penalty_us=5e8):
+    """SPEAR+TIDE on every (trace, envelope) cell, once with the fp32 score
+    and once per fixed-point format.  Returns the workload and, per
+    simulation, its (trace, envelope, format index; -1 for fp32).  P_Z is the
+    penalty in units of tau: P_Z = P / tau (eq. (lock))."""
+    traces = fidelity_traces() if traces is None else traces
+    formats = format_grid() if formats is None else list(formats)
+    rows, meta = [], []
+    for ti in range(len(traces)):
+        for ei in range(len(envelopes)):
+            for fi in range(-1, len(formats)):
+                rows.append((ti, ei, fi))
+    p = default_params(len(rows))
+    set_policy(p, POLICY_SPEAR)
+    m = np.zeros(len(rows), dtype=FORMAT_META_DTYPE)
+    for r, (ti, ei, fi) in enumerate(rows):
+        s_tok, h_tok = envelopes[ei]
+        p[r]["trace"] = ti
+        p[r]["lut"] = ti
+        p[r]["cap_sram_B"] = s_tok * 128 * KIB
+        p[r]["cap_hbm_B"] = h_tok * 128 * KIB
+        p[r]["penalty_us"] = np.float32(penalty_us)
+        if fi >= 0:
+            bh, bg, tau = formats[fi]
+            p[r]["score_mode"] = 1
+            p[r]["b_h"], p[r]["b_g"], p[r]["tau_ns"] = bh, bg, tau
+            p[r]["p_z"] = int(round(penalty_us * 1000 / tau))
+        m[r] = (ti, ei, fi)
+    w = Workload("format_sweep", list(traces), [tr.turns for tr in traces], p)
+    return w, m
+
+
+def fidelity_snapshots(n_snap=7265, n_per=64, seed=6) -> RankingSet:
+    """Eviction-snapshot stand-ins for the format sweep's ranking gate: the
+    C5 session pool drawn into 7,265 snapshots of 64 live sessions (the
+    paper's traces keep at most 64 live)."""
+    return c5_ranking(n_snap=n_snap, n_per=n_per, seed=seed)
