@@ -206,12 +206,33 @@ def section_fmt(torch):
             "passing": [r["format"] for r in rows if r["passes"]], "formats": rows}
 
 
+def section_online(torch):
+    """Online convergence of the hazard table, eq. (attainment): per trace LRU,
+    the offline table and tables rebuilt online from the first n
+    completions, one launch."""
+    from paper_2609_09643_amd import fidelity
+    t0 = time.perf_counter()
+    curves, ref, c, w = fidelity.run_attainment()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    out = {}
+    for t, cv in curves.items():
+        lru, off = ref[t]
+        out[str(t)] = {"sessions": int(w.traces[t].n_sessions), "hr_lru": round(float(lru), 5),
+                       "hr_offline": round(float(off), 5)}
+        for kind, pts in cv.items():
+            out[str(t)]["A_" + kind] = [[n, round(a, 4)] for n, a, _ in pts]
+    return {"workload": "online hazard tables: 6 traces (1,415 sessions), Edge-Tight envelope, "
+                        "%d simulations" % w.n_sims,
+            "s": dt, "events_per_s": float(c["events"].sum()) / dt, "traces": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--sections", default="c2,c5", help="comma list of c2,c4,c5,fmt or 'none'")
+    ap.add_argument("--sections", default="c2,c5", help="comma list of c2,c4,c5,fmt,online or 'none'")
     ap.add_argument("--c4-events", type=int, default=200_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", type=int, default=None)
@@ -288,6 +309,9 @@ def main():
     if "c4" in secs:
         log("section c4")
         extra["c4"] = section_c4(torch, U, synth, args.c4_events)
+    if "online" in secs:
+        log("section online")
+        extra["online"] = section_online(torch)
     if "fmt" in secs:
         log("section fmt")
         extra["fmt"] = section_fmt(torch)

@@ -109,7 +109,11 @@ typedef struct {
   uint32_t score_mode;     /* 0: fp32 score; 1: fixed-point score_q (SPEAR only) */
   uint32_t lut;            /* hazard table index, < n_luts */
   uint32_t trace;          /* trace index, < n_traces */
-  uint32_t pad0;
+  uint32_t hazard_online;  /* 0: the table set by unison_set_hazard; 1: the table starts
+                              empty and is rebuilt from the first online_sessions
+                              completions, each DONE adding its session's turn count to
+                              the counts of eq. (hazard) before that event's scan (the
+                              online-convergence study of eq. (attainment)) */
   uint64_t cap_sram_B;     /* C_S in bytes */
   uint64_t cap_hbm_B;      /* C_H in bytes */
   uint64_t n_slots;        /* N_sess, >= 1 */
@@ -121,7 +125,7 @@ typedef struct {
   float penalty_us;        /* completion penalty P of eq. (esp), >= 0, microseconds */
   uint32_t b_h;            /* hazard bits b_h, 1..16 */
   uint32_t b_g;            /* gap register bits b_g, 1..64 */
-  uint32_t pad1;
+  uint32_t online_sessions; /* completions an online table counts (hazard_online = 1) */
   uint64_t tau_ns;         /* gap time divisor tau, >= 1 */
   uint64_t p_z;            /* integer penalty P_Z = P / tau */
 } unison_sim_params;
@@ -256,6 +260,13 @@ int unison_score_fixed(void* hip_stream, uint32_t n, const uint8_t* turn, const 
  * 2 <= n_per <= 4096. */
 int unison_kendall(void* hip_stream, uint32_t n_snap, uint32_t n_per, uint64_t n_x, const float* x,
                    const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1);
+
+/* Copies the hazard counts d(t), n(t), t = 0..50, that simulation `sim`'s
+ * table held at the end of the latest run to HOST d_out[51], n_out[51]: its
+ * fixed table's, or what its online table (hazard_online = 1) has counted.
+ * Synchronises the context's stream.  Errors: UNISON_E_INVALID (sim out of
+ * range, null pointer), UNISON_E_NOT_READY (no run yet). */
+int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t* n_out);
 
 /* Test hook: pins the simulation kernel variant (-1 = chosen by the largest
  * trace; register tables of lanes x sessions per lane 0: 16 x 1, 1: 64 x 1,

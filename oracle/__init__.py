@@ -46,7 +46,8 @@ class Params(C.Structure):
         ("n_slots", C.c_uint64), ("dma_B_per_us", C.c_uint64), ("ttl_ns", C.c_uint64),
         ("t_s_ns_per_B", C.c_double), ("t_h_ns_per_B", C.c_double),
         ("t_p_ns_per_tok", C.c_double), ("penalty_us", C.c_float), ("b_h", C.c_uint32),
-        ("b_g", C.c_uint32), ("pad0", C.c_uint32), ("tau_ns", C.c_uint64), ("p_z", C.c_uint64),
+        ("b_g", C.c_uint32), ("hazard_online", C.c_uint32), ("online_sessions", C.c_uint32),
+        ("pad0", C.c_uint32), ("tau_ns", C.c_uint64), ("p_z", C.c_uint64),
     ]
 
 
@@ -87,7 +88,7 @@ def lib():
         L.orc_run.restype = C.c_int
         L.orc_run.argtypes = [C.POINTER(Params), C.c_uint64, u64p, u32p, u32p, u32p, u64p,
                               C.c_uint32, u32p, u32p, u32p, C.c_uint64, C.POINTER(Counters),
-                              C.c_void_p, C.c_uint32, u32p, C.c_void_p, u64p]
+                              C.c_void_p, C.c_uint32, u32p, C.c_void_p, C.c_void_p, u64p]
         L.orc_hazard_counts.argtypes = [u32p, C.c_uint32, u32p, u32p]
         L.orc_lut_f32.argtypes = [u32p, u32p, f32p]
         L.orc_lut_q.argtypes = [u32p, u32p, C.c_uint32, u64p]
@@ -214,9 +215,10 @@ def params_struct(row):
     return p
 
 
-def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False):
+def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False, counts=None):
     """Runs one simulation. Returns (rc, counters dict, log or None, states or None,
-    elapsed_ns of the event loop)."""
+    elapsed_ns of the event loop).  counts: optional uint32 array [2, 51] that
+    receives the hazard counts d, n of the table at the end."""
     L = lib()
     p = params_struct(row)
     t_ns, sid = _c(trace.t_ns, np.uint64), _c(trace.sid, np.uint32)
@@ -238,6 +240,7 @@ def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False):
                    log.ctypes.data_as(C.c_void_p) if log is not None else None, log_cap,
                    _p(log_len, C.c_uint32),
                    st.ctypes.data_as(C.c_void_p) if st is not None else None,
+                   counts.ctypes.data_as(C.c_void_p) if counts is not None else None,
                    _p(el, C.c_uint64))
     if log is not None:
         log = log[:min(int(log_len[0]), log_cap)]

@@ -67,6 +67,13 @@
  *            strictly, both fit the budget and eq. (cap) holds after the
  *            swap.  The first move that is not legal ends the pass.  The DMA
  *            engine is then busy for ceil(moved * 1000 / B) ns.
+ *  online    Online hazard table (the convergence study beside eq.
+ *            (attainment)): the counts start at zero, and each DONE adds its
+ *            session (T = its turn index + 1) to eq. (hazard) -- n(t) += 1
+ *            for t < min(T, 51), d(T-1) += 1 when T - 1 <= 50 -- for the
+ *            first online_sessions completions.  The update follows the DONE's
+ *            register write, so that event's scan already uses the new table;
+ *            every score is then re-evaluated against it.
  *  timeout   Before an event is written, every resident that has been idle
  *            longer than the TTL expires (its timer fired since the last event).
  *  account   eq. (hr-amat), eq. (prered): SRAM hit amat += len*kvb*t_s,
@@ -116,6 +123,8 @@ typedef struct {
   float penalty_us;     /* P of eq. (esp) */
   uint32_t b_h;         /* hazard fraction bits */
   uint32_t b_g;         /* gap register bits */
+  uint32_t hazard_online;   /* 1: the table is rebuilt from completions */
+  uint32_t online_sessions; /* completions it counts at most */
   uint32_t pad0;
   uint64_t tau_ns;      /* gap time divisor */
   uint64_t p_z;         /* integer penalty P_Z */
@@ -328,6 +337,7 @@ typedef struct {
   uint32_t n_sess;
   float hf[LUT_LEN];
   uint64_t hq[LUT_LEN];
+  uint32_t hd[LUT_LEN], hn[LUT_LEN]; /* the counts the table is built from */
   uint64_t used[3]; /* indexed by tier */
   uint64_t n_res, n_table;
   uint64_t dma_free_at;
@@ -505,9 +515,11 @@ static void tide(sim_t* m, uint32_t sid, uint64_t now, orc_state* st) {
  * Runs one simulation over one trace.
  *   ev_*       the trace's events (already in order), n_events long
  *   kvb        bytes per token of each of the trace's n_sess sessions
- *   lut_d/n    the hazard counts d(t), n(t) of this simulation's table
+ *   lut_d/n    the hazard counts d(t), n(t) of this simulation's table (not
+ *              read when p->hazard_online: that table starts empty)
  *   max_events stop after this many events (UINT64_MAX = all)
  *   log/states optional outputs (NULL to skip); states has one entry per event
+ *   counts_out optional: the table's counts at the end, d[51] then n[51]
  *   elapsed_ns wall time of the event loop alone (optional)
  * Returns ORC_OK, ORC_E_INVALID or ORC_E_BAD_TRACE (counters.error = event+1).
  */
@@ -516,7 +528,7 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
             const uint64_t* ev_next, uint32_t n_sess, const uint32_t* kvb,
             const uint32_t* lut_d, const uint32_t* lut_n, uint64_t max_events,
             orc_counters* out, orc_rec* log, uint32_t log_cap, uint32_t* log_len,
-            orc_state* states, uint64_t* elapsed_ns) {
+            orc_state* states, uint32_t* counts_out, uint64_t* elapsed_ns) {
   if (!p || !out || p->policy > P_BELADY || p->dma_B_per_us == 0 || p->n_slots == 0 ||
       p->tau_ns == 0 || p->b_h < 1 || p->b_h > 32 || p->b_g < 1 || p->b_g > 64 ||
       !(p->penalty_us >= 0.0f))
@@ -532,8 +544,13 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
   m.log_cap = log_cap;
   m.s = (sess_t*)calloc(n_sess ? n_sess : 1, sizeof(sess_t));
   if (!m.s) return ORC_E_INVALID;
-  orc_lut_f32(lut_d, lut_n, m.hf);
-  orc_lut_q(lut_d, lut_n, p->b_h, m.hq);
+  for (int t = 0; t < LUT_LEN; t++) {
+    m.hd[t] = p->hazard_online ? 0 : lut_d[t];
+    m.hn[t] = p->hazard_online ? 0 : lut_n[t];
+  }
+  orc_lut_f32(m.hd, m.hn, m.hf);
+  orc_lut_q(m.hd, m.hn, p->b_h, m.hq);
+  uint32_t online_seen = 0;
   int rc = ORC_OK;
   uint64_t n_run = n_events < max_events ? n_events : max_events;
   struct timespec t0, t1;
@@ -593,6 +610,15 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
       } else {
         x->phase = PH_DONE;
         x->next_ns = UINT64_MAX;
+        if (p->hazard_online && online_seen < p->online_sessions) {
+          /* the completed session joins the counts of eq. (hazard) */
+          uint32_t T = x->turn + 1;
+          for (uint32_t t = 0; t < LUT_LEN && t < T; t++) m.hn[t]++;
+          if (T - 1 < LUT_LEN) m.hd[T - 1]++;
+          online_seen++;
+          orc_lut_f32(m.hd, m.hn, m.hf);
+          orc_lut_q(m.hd, m.hn, p->b_h, m.hq);
+        }
       }
     }
 
@@ -651,6 +677,11 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
   if (elapsed_ns)
     *elapsed_ns = (uint64_t)(t1.tv_sec - t0.tv_sec) * 1000000000ULL + (uint64_t)(t1.tv_nsec - t0.tv_nsec);
   if (log_len) *log_len = m.log_len;
+  if (counts_out)
+    for (int t = 0; t < LUT_LEN; t++) {
+      counts_out[t] = m.hd[t];
+      counts_out[LUT_LEN + t] = m.hn[t];
+    }
   free(m.s);
   return rc;
 }

@@ -48,8 +48,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Workspace layout; offsets in bytes from the workspace base.
 struct Layout {
-  size_t params, ev_off, sess_off, lut_d, lut_n, state, counters, mg, gq, len, last, next, log,
-      scratch, total;
+  size_t params, ev_off, sess_off, lut_d, lut_n, state, counters, hcount, mg, gq, len, last, next,
+      log, scratch, total;
 };
 
 bool make_layout(const unison_dims& d, Layout& L) {
@@ -67,6 +67,7 @@ bool make_layout(const unison_dims& d, Layout& L) {
   L.lut_n = take(sizeof(uint32_t) * kLut * d.n_luts);
   L.state = take(sizeof(SimState) * d.n_sims);
   L.counters = take(sizeof(unison_counters) * d.n_sims);
+  L.hcount = take(sizeof(uint32_t) * 2 * kLut * d.n_sims);
   L.mg = take(sizeof(uint64_t) * entries);
   L.gq = take(sizeof(uint64_t) * entries);
   L.len = take(sizeof(uint32_t) * entries);
@@ -246,7 +247,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
   uint32_t max_sess = 0;
   for (uint32_t i = 0; i < ctx->dims.n_sims; ++i) {
     const unison_sim_params& p = params[i];
-    if (p.policy > UNISON_POLICY_BELADY || p.tide > 1 || p.score_mode > 1 ||
+    if (p.policy > UNISON_POLICY_BELADY || p.tide > 1 || p.score_mode > 1 || p.hazard_online > 1 ||
         p.lut >= ctx->dims.n_luts || p.trace >= ctx->dims.n_traces || p.b_h < 1 || p.b_h > 16 ||
         p.b_g < 1 || p.b_g > 64 || p.tau_ns < 1 || p.n_slots < 1 || p.dma_B_per_us < 1 ||
         !(p.penalty_us >= 0.0f) || std::isinf(p.penalty_us) || !std::isfinite(p.t_s_ns_per_B) ||
@@ -301,6 +302,7 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   a.t_last = ctx->at<uint64_t>(ctx->L.last);
   a.t_next = ctx->at<uint64_t>(ctx->L.next);
   a.log = ctx->dims.log_cap ? ctx->at<unison_record>(ctx->L.log) : nullptr;
+  a.hcount = ctx->at<uint32_t>(ctx->L.hcount);
   a.max_events = max_events;
   a.n_sims = ctx->dims.n_sims;
   a.max_sessions = ctx->dims.max_sessions;
@@ -359,6 +361,22 @@ int unison_read_log(unison_ctx* ctx, uint32_t sim, unison_record* dst, uint32_t 
     rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise log");
   }
   return rc;
+}
+
+int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t* n_out) {
+  if (!ctx || !d_out || !n_out) return UNISON_E_INVALID;
+  if (sim >= ctx->dims.n_sims) return ctx->fail(UNISON_E_INVALID, "sim %u", sim);
+  if (!ctx->ran) return ctx->fail(UNISON_E_NOT_READY, "no run on this context yet");
+  const uint32_t* src = ctx->at<uint32_t>(ctx->L.hcount) + (size_t)sim * 2 * kLut;
+  int rc = ctx->hip(hipMemcpyAsync(d_out, src, sizeof(uint32_t) * kLut, hipMemcpyDeviceToHost,
+                                   ctx->stream),
+                    "copy hazard counts d");
+  if (rc) return rc;
+  rc = ctx->hip(hipMemcpyAsync(n_out, src + kLut, sizeof(uint32_t) * kLut, hipMemcpyDeviceToHost,
+                               ctx->stream),
+                "copy hazard counts n");
+  if (rc) return rc;
+  return ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise hazard counts");
 }
 
 // Test hook: pin the simulation kernel variant (-1 = automatic).

@@ -145,14 +145,40 @@ struct Pol {
   static constexpr uint64_t inf_key = (spear && !fixed) ? 0x7F800000ull : ~0ull;
 };
 
+// The simulation's hazard table lives in LDS: its counts d(t), n(t) of
+// eq. (hazard) and both derived forms, h as fp32 and h_q (eq. (hq)).  An
+// online table (online_cap > 0) grows by one session at each of the first
+// online_cap completions.
 struct KeyCtx {
-  const float* hf;      // LDS [52]
-  const uint32_t* hq;   // LDS [52]
+  float* hf;            // LDS [52]
+  uint32_t* hq;         // LDS [52]
+  uint32_t* hd;         // LDS [52]
+  uint32_t* hn;         // LDS [52]
   float P;
   uint32_t lambda;
   uint64_t p_z;
   bool pack44;          // times fit 44 bits and ids 20 bits: recency / Belady keys pack
+  uint32_t online_cap;  // completions an online table still may count; 0: fixed table
 };
+
+// Adds a completed session of Tn turns to the counts (n(t) += 1 for t < Tn,
+// d(Tn - 1) += 1) and rebuilds the entries it changed; t is split over
+// `width` cooperating lanes starting at `lane`.
+__device__ __forceinline__ void hazard_add_counts(const KeyCtx& K, uint32_t Tn, uint32_t lane,
+                                                  uint32_t width) {
+  for (uint32_t t = lane; t < kLut; t += width) {
+    const uint32_t dn = t < Tn ? 1u : 0u;
+    const uint32_t dd = t + 1u == Tn ? 1u : 0u;
+    if (dn | dd) {
+      const uint32_t d = K.hd[t] + dd;
+      const uint32_t n = K.hn[t] + dn;
+      K.hd[t] = d;
+      K.hn[t] = n;
+      K.hf[t] = hazard_f32(d, n);
+      K.hq[t] = hazard_q(d, n, K.lambda);
+    }
+  }
+}
 
 // The hazard entry eq. (hazard) / eq. (hq) of a session at turn index t
 // (clamped to 50): fp32 bits of h for the fp32 score, h_q for the integer one.
@@ -394,6 +420,15 @@ struct RegTable {
     d = select<true>(kTierSram, K);
   }
 
+  // Online hazard table: does it still count completions?  Then add one and
+  // refresh every entry's hazard value, so the next scan rescores them all.
+  __device__ __forceinline__ bool hazard_open(const KeyCtx& K) const { return K.hn[0] < K.online_cap; }
+  __device__ __forceinline__ void hazard_add(const KeyCtx& K, uint32_t Tn) {
+    hazard_add_counts(K, Tn, lane, G);
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) hz[j] = hazard_of<POL, SMODE>(K, meta[j]);
+  }
+
   // Smallest evictable session idle for longer than ttl (timeout policy);
   // kNone if there is none.
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) const {
@@ -568,6 +603,17 @@ struct MemTable {
     }
     p = block_reduce<false>(cp);
     d = block_reduce<true>(cd);
+  }
+
+  // Online hazard table: both calls are made by the whole workgroup.
+  __device__ __forceinline__ bool hazard_open(const KeyCtx& K) const {
+    const uint32_t seen = uni32(K.hn[0]);
+    __syncthreads();
+    return seen < K.online_cap;
+  }
+  __device__ __forceinline__ void hazard_add(const KeyCtx& K, uint32_t Tn) {
+    hazard_add_counts(K, Tn, tid, BLOCK);
+    __syncthreads();
   }
 
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) {
@@ -856,6 +902,8 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
       }
       x.meta = make_meta(kind == kGapStart ? kGap : kDoneP, tier0, meta_turn(x.meta));
       T.write_end(sid, x.meta, now, kind == kGapStart ? cur_next : ~0ull);
+      // an online hazard table counts the completed session before the scan
+      if (kind == kDone && K.online_cap && T.hazard_open(K)) T.hazard_add(K, meta_turn(x.meta) + 1u);
     }
 
     // the register-file scan: every table entry is scored; its argmax over
@@ -1013,12 +1061,33 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
   next_event = e;
 }
 
-// Hazard tables of one simulation into LDS (h as fp32 and as UQ0.b_h).
-__device__ __forceinline__ void load_lut(const uint32_t* d, const uint32_t* n, uint32_t lambda,
-                                         float* hf, uint32_t* hq, uint32_t lane, uint32_t width) {
+// The simulation's hazard table into LDS: the counts of its fixed table, or
+// of its online table so far (none on a fresh run), and h in both forms.
+__device__ __forceinline__ void load_hazard(const SimArgs& a, const unison_sim_params& P,
+                                            uint32_t sim, const KeyCtx& K, uint32_t lane,
+                                            uint32_t width) {
+  const bool online = P.hazard_online != 0;
+  const bool fresh = online && !(a.flags & UNISON_RUN_CONTINUE);
+  const uint32_t* kd = online ? a.hcount + (size_t)sim * 2 * kLut : a.lut_d + (size_t)P.lut * kLut;
+  const uint32_t* kn = online ? kd + kLut : a.lut_n + (size_t)P.lut * kLut;
   for (uint32_t t = lane; t < kLut; t += width) {
-    hf[t] = hazard_f32(d[t], n[t]);
-    hq[t] = hazard_q(d[t], n[t], lambda);
+    const uint32_t d = fresh ? 0u : kd[t];
+    const uint32_t n = fresh ? 0u : kn[t];
+    K.hd[t] = d;
+    K.hn[t] = n;
+    K.hf[t] = hazard_f32(d, n);
+    K.hq[t] = hazard_q(d, n, K.lambda);
+  }
+}
+
+// The table's counts at the end of the launch, for a later CONTINUE and for
+// unison_read_hazard.
+__device__ __forceinline__ void store_hazard(const SimArgs& a, uint32_t sim, const KeyCtx& K,
+                                             uint32_t lane, uint32_t width) {
+  uint32_t* out = a.hcount + (size_t)sim * 2 * kLut;
+  for (uint32_t t = lane; t < kLut; t += width) {
+    out[t] = K.hd[t];
+    out[kLut + t] = K.hn[t];
   }
 }
 
@@ -1138,6 +1207,7 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
       if constexpr (PT::belady) a.t_next[tb + s] = T.next[j];
     }
   }
+  store_hazard(a, sim, K, lane, G);
   if (lane == 0) {
     finish_costs(S, P, C);
     store_scalars(a.state[sim], S, next_event);
@@ -1150,6 +1220,8 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
   constexpr int GROUPS = 256 / G;
   __shared__ float s_hf[GROUPS][52];
   __shared__ uint32_t s_hq[GROUPS][52];
+  __shared__ uint32_t s_hd[GROUPS][52];
+  __shared__ uint32_t s_hn[GROUPS][52];
   const uint32_t gtid = blockIdx.x * 256u + threadIdx.x;
   const uint32_t sim = gtid / G;
   const uint32_t lane = gtid % G;
@@ -1158,11 +1230,11 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
   const uint32_t simc = live ? sim : 0u;
   const unison_sim_params P = a.params[simc];
   const uint32_t lambda = (1u << P.b_h) - 1u;
-  load_lut(a.lut_d + (size_t)P.lut * kLut, a.lut_n + (size_t)P.lut * kLut, lambda, s_hf[grp],
-           s_hq[grp], lane, G);
+  const KeyCtx K{s_hf[grp], s_hq[grp], s_hd[grp], s_hn[grp], P.penalty_us, lambda, P.p_z,
+                 a.time44 != 0, P.hazard_online ? P.online_sessions : 0u};
+  load_hazard(a, P, simc, K, lane, G);
   __syncthreads();
   if (!live) return;
-  const KeyCtx K{s_hf[grp], s_hq[grp], P.penalty_us, lambda, P.p_z, a.time44 != 0};
   switch (sim_policy(a, P)) {
     case kSpear:
       if (P.score_mode) regs_run<G, EPL, kSpear, 1>(a, sim, lane, P, K);
@@ -1265,6 +1337,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
       a.t_len[tb + i] = T.len[i];
     }
   }
+  store_hazard(a, sim, K, tid, BLOCK);
   if (tid == 0) {
     finish_costs(S, P, C);
     store_scalars(a.state[sim], S, next_event);
@@ -1276,15 +1349,17 @@ template <int BLOCK, bool IN_LDS>
 __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   __shared__ float s_hf[52];
   __shared__ uint32_t s_hq[52];
+  __shared__ uint32_t s_hd[52];
+  __shared__ uint32_t s_hn[52];
   __shared__ Cand s_red[2 * (BLOCK / 64)];
   extern __shared__ uint64_t s_tab[];
   const uint32_t sim = blockIdx.x;
   const unison_sim_params P = a.params[sim];
   const uint32_t lambda = (1u << P.b_h) - 1u;
-  load_lut(a.lut_d + (size_t)P.lut * kLut, a.lut_n + (size_t)P.lut * kLut, lambda, s_hf, s_hq,
-           threadIdx.x, BLOCK);
+  const KeyCtx K{s_hf, s_hq, s_hd, s_hn, P.penalty_us, lambda, P.p_z, a.time44 != 0,
+                 P.hazard_online ? P.online_sessions : 0u};
+  load_hazard(a, P, sim, K, threadIdx.x, BLOCK);
   __syncthreads();
-  const KeyCtx K{s_hf, s_hq, P.penalty_us, lambda, P.p_z, a.time44 != 0};
   switch (sim_policy(a, P)) {
     case kSpear:
       if (P.score_mode) block_run<BLOCK, kSpear, 1, IN_LDS>(a, sim, P, K, s_red, s_tab);

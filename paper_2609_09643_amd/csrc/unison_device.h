@@ -169,6 +169,7 @@ struct SimArgs {
   uint64_t* t_last;
   uint64_t* t_next;
   unison_record* log;
+  uint32_t* hcount;        // [n_sims][2][51] hazard counts d, n at the end of a launch
   uint64_t max_events;
   uint32_t n_sims;
   uint32_t max_sessions;

@@ -1,4 +1,5 @@
-"""The fixed-point format sweep (Sec. IV-C) and its two hard gates.
+"""The fixed-point format sweep (Sec. IV-C) with its two hard gates, and the
+online convergence of the hazard table (eq. (attainment)).
 
 For every (b_h, b_g, tau) point of the pre-registered grid (exact divider,
 b_s = 64, P_Z = P / tau) this measures, on the GPU:
@@ -122,3 +123,44 @@ def sweep(traces=None, rs=None, formats=None, penalty_us=5e8):
                      "mean_tau_b": mtau, "pooled_tau_b": ptau, "top1": top1,
                      "passes": bool(worst <= HR_GATE_PP and top1 >= TOP1_GATE)})
     return rows, len(cells)
+
+
+def attainment(counters, meta):
+    """eq. (attainment) per trace: A(n) = (H_on(n) - H_LRU) / (H_off - H_LRU),
+    the share of the offline table's hit-rate surplus over LRU realised after
+    n observed sessions, for a table rebuilt online from the first n
+    completions ("online") and for a fixed table fitted on them ("prefix").
+    Returns {trace: {"online" | "prefix": [(n, A(n), H(n))]}} and {trace:
+    (H_LRU, H_off)}."""
+    hr = hit_rate(counters)
+    ref, curves = {}, {}
+    for i, m in enumerate(meta):
+        t = int(m["trace"])
+        lru, off = ref.get(t, (None, None))
+        if int(m["kind"]) == synth.ATTAIN_LRU:
+            lru = hr[i]
+        elif int(m["kind"]) == synth.ATTAIN_OFFLINE:
+            off = hr[i]
+        ref[t] = (lru, off)
+    names = {synth.ATTAIN_ONLINE: "online", synth.ATTAIN_PREFIX: "prefix"}
+    for i, m in enumerate(meta):
+        kind = int(m["kind"])
+        if kind not in names:
+            continue
+        t = int(m["trace"])
+        lru, off = ref[t]
+        a = (hr[i] - lru) / (off - lru) if off != lru else float("nan")
+        curves.setdefault(t, {}).setdefault(names[kind], []).append((int(m["n"]), float(a), float(hr[i])))
+    for t in curves:
+        for k in curves[t]:
+            curves[t][k].sort()
+    return curves, ref
+
+
+def run_attainment(traces=None, envelope=synth.FIDELITY_ENVELOPES[0], points=None):
+    """Runs the attainment batch on the GPU (one launch)."""
+    w, meta = synth.attainment_workload(traces, envelope, points)
+    sim = U.Simulator(w)
+    sim.run()
+    c = sim.counters()
+    return attainment(c, meta) + (c, w)

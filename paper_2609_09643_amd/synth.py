@@ -38,8 +38,8 @@ NS = 1_000_000_000
 # own argument layout.
 SIM_PARAMS_DTYPE = np.dtype([
     ("policy", np.uint32), ("tide", np.uint32), ("score_mode", np.uint32),
-    ("lut", np.uint32), ("trace", np.uint32),
-    ("cap_sram_B", np.uint64), ("cap_hbm_B", np.uint64), ("n_slots", np.uint64),
+    ("lut", np.uint32), ("trace", np.uint32), ("hazard_online", np.uint32),
+    ("online_sessions", np.uint32), ("cap_sram_B", np.uint64), ("cap_hbm_B", np.uint64), ("n_slots", np.uint64),
     ("dma_B_per_us", np.uint64), ("ttl_ns", np.uint64),
     ("t_s_ns_per_B", np.float64), ("t_h_ns_per_B", np.float64),
     ("t_p_ns_per_tok", np.float64), ("penalty_us", np.float32),
@@ -218,6 +218,7 @@ def default_params(n):
     p["t_p_ns_per_tok"] = 5e4
     p["penalty_us"] = np.float32(5e8)
     p["b_h"], p["b_g"], p["tau_ns"], p["p_z"] = 12, 32, 1000, 500_000_000
+    p["online_sessions"] = 0xFFFFFFFF
     return p
 
 
@@ -481,3 +482,46 @@ def fidelity_snapshots(n_snap=7265, n_per=64, seed=6) -> RankingSet:
     C5 session pool drawn into 7,265 snapshots of 64 live sessions (the
     paper's traces keep at most 64 live)."""
     return c5_ranking(n_snap=n_snap, n_per=n_per, seed=seed)
+
+
+ATTAIN_META_DTYPE = np.dtype([("trace", np.uint32), ("kind", np.uint32), ("n", np.uint32)])
+ATTAIN_LRU, ATTAIN_OFFLINE, ATTAIN_ONLINE, ATTAIN_PREFIX = 0, 1, 2, 3
+
+
+def completion_order(tr):
+    """Session ids in the order their DONE events occur."""
+    return tr.sid[tr.kind == KIND_DONE]
+
+
+def attainment_workload(traces=None, envelope=FIDELITY_ENVELOPES[0], points=None):
+    """Per trace: LRU; SPEAR+TIDE with the table fitted on the whole trace;
+    and, for n in `points` (default 0, 1, 2, 4, ... and the trace's session
+    count), SPEAR+TIDE whose table starts empty and counts the first n
+    completions as they happen (ATTAIN_ONLINE), and SPEAR+TIDE with a fixed
+    table fitted on the turn counts of the first n sessions to complete
+    (ATTAIN_PREFIX)."""
+    traces = fidelity_traces() if traces is None else traces
+    rows, pops = [], [tr.turns for tr in traces]
+    for ti, tr in enumerate(traces):
+        N = tr.n_sessions
+        pts = points if points is not None else sorted({0, N} | {1 << k for k in range(20) if (1 << k) < N})
+        order = completion_order(tr)
+        rows.append((ti, ATTAIN_LRU, 0, ti))
+        rows.append((ti, ATTAIN_OFFLINE, N, ti))
+        for n in pts:
+            rows.append((ti, ATTAIN_ONLINE, int(n), ti))
+            pops.append(tr.turns[order[:int(n)]])
+            rows.append((ti, ATTAIN_PREFIX, int(n), len(pops) - 1))
+    p = default_params(len(rows))
+    meta = np.zeros(len(rows), ATTAIN_META_DTYPE)
+    for r, (ti, kind, n, lut) in enumerate(rows):
+        set_policy(p[r:r + 1], POLICY_LRU if kind == ATTAIN_LRU else POLICY_SPEAR)
+        p[r]["trace"] = ti
+        p[r]["lut"] = lut
+        p[r]["cap_sram_B"] = envelope[0] * 128 * KIB
+        p[r]["cap_hbm_B"] = envelope[1] * 128 * KIB
+        if kind == ATTAIN_ONLINE:
+            p[r]["hazard_online"] = 1
+            p[r]["online_sessions"] = n
+        meta[r] = (ti, kind, n)
+    return Workload("attainment", list(traces), pops, p), meta

@@ -35,12 +35,13 @@ class Dims(C.Structure):
 class SimParams(C.Structure):
     _fields_ = [
         ("policy", C.c_uint32), ("tide", C.c_uint32), ("score_mode", C.c_uint32),
-        ("lut", C.c_uint32), ("trace", C.c_uint32), ("pad0", C.c_uint32),
+        ("lut", C.c_uint32), ("trace", C.c_uint32), ("hazard_online", C.c_uint32),
         ("cap_sram_B", C.c_uint64), ("cap_hbm_B", C.c_uint64), ("n_slots", C.c_uint64),
         ("dma_B_per_us", C.c_uint64), ("ttl_ns", C.c_uint64),
         ("t_s_ns_per_B", C.c_double), ("t_h_ns_per_B", C.c_double),
         ("t_p_ns_per_tok", C.c_double), ("penalty_us", C.c_float), ("b_h", C.c_uint32),
-        ("b_g", C.c_uint32), ("pad1", C.c_uint32), ("tau_ns", C.c_uint64), ("p_z", C.c_uint64),
+        ("b_g", C.c_uint32), ("online_sessions", C.c_uint32), ("tau_ns", C.c_uint64),
+        ("p_z", C.c_uint64),
     ]
 
 
@@ -83,6 +84,7 @@ def lib():
             "unison_read_counters": [vp, vp, u32, u32],
             "unison_counters_device": [vp, C.POINTER(vp)],
             "unison_read_log": [vp, u32, vp, u32, C.POINTER(C.c_uint64)],
+            "unison_read_hazard": [vp, u32, vp, vp],
             "unison_ema_replay": [vp, u32, u32, vp, vp, u32, u64, vp, vp],
             "unison_score_fp32": [vp, u32, vp, vp, vp, vp, vp, C.c_float, vp],
             "unison_score_fixed": [vp, u32, vp, vp, vp, vp, vp, u32, u64, vp],
@@ -252,6 +254,15 @@ class Simulator:
         if int(n.value) > self.log_cap:
             raise RuntimeError("decision log overflow: %d > %d" % (n.value, self.log_cap))
         return out[:kept]
+
+    def hazard(self, sim):
+        """The hazard counts (d, n) [51] of simulation `sim`'s table after the
+        latest run."""
+        d = np.zeros(LUT_LEN, np.uint32)
+        n = np.zeros(LUT_LEN, np.uint32)
+        _check(lib().unison_read_hazard(self.ctx, sim, d.ctypes.data_as(C.c_void_p),
+                                        n.ctypes.data_as(C.c_void_p)), self.ctx)
+        return d, n
 
     def close(self):
         if self.ctx:

@@ -49,6 +49,11 @@ def test_host_side_validation(lib):
     # a context over a fake (never dereferenced) address: no HIP call happens
     assert lib.unison_create(C.byref(ctx), C.byref(d), None, C.c_void_p(0x100000), size) == 0
     assert lib.unison_run(ctx, 0xFF, 0, 1) == U.E_NOT_READY
+    hd = (C.c_uint32 * 51)()
+    hn = (C.c_uint32 * 51)()
+    assert lib.unison_read_hazard(ctx, 0, hd, hn) == U.E_NOT_READY
+    assert lib.unison_read_hazard(ctx, 4, hd, hn) == U.E_INVALID
+    assert lib.unison_read_hazard(ctx, 0, None, hn) == U.E_INVALID
     p = (U.SimParams * 4)()
     assert lib.unison_set_params(ctx, p) == U.E_NOT_READY
     assert b"traces" in lib.unison_last_error(ctx)
