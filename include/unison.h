@@ -92,6 +92,15 @@ extern "C" {
 
 typedef struct unison_ctx unison_ctx;
 
+/* Register-file organisation (Sec. III-D, eq. (rf), eq. (stale)): the unified
+ * file, or two private copies -- the eviction engine's and TIDE's -- that are
+ * overwritten with the live file after every request and gap onset, after every
+ * 8th request, or at gap onsets only. */
+#define UNISON_DUAL_NONE 0u
+#define UNISON_DUAL_EVERY 1u
+#define UNISON_DUAL_EIGHT 2u
+#define UNISON_DUAL_GAP 3u
+
 /* Sizes that fix the workspace. */
 typedef struct {
   uint32_t n_sims;       /* simulations in the batch, >= 1 */
@@ -99,6 +108,8 @@ typedef struct {
   uint32_t max_sessions; /* largest session count of any trace, 1..UNISON_MAX_SESSIONS */
   uint32_t n_luts;       /* hazard tables, >= 1 */
   uint32_t log_cap;      /* decision records kept per simulation (0: no log) */
+  uint32_t views;        /* 1: reserve the two register-file copies of the dual design
+                            (64 B per session slot), needed by any row with dual_sync != 0 */
 } unison_dims;
 
 /* One simulation's parameters (eq. (cap), eq. (esp), eq. (budget),
@@ -128,6 +139,10 @@ typedef struct {
   uint32_t online_sessions; /* completions an online table counts (hazard_online = 1) */
   uint64_t tau_ns;         /* gap time divisor tau, >= 1 */
   uint64_t p_z;            /* integer penalty P_Z = P / tau */
+  uint32_t dual_sync;      /* UNISON_DUAL_*: one live register file (0), or the dual design of
+                              eq. (stale) whose eviction and TIDE engines decide from private
+                              copies refreshed at the given points */
+  uint32_t pad0;
 } unison_sim_params;
 
 /* Per-simulation results. */
@@ -148,6 +163,12 @@ typedef struct {
                                  0xFFFFFFFF when nothing is evictable) */
   uint64_t events;            /* events processed so far */
   uint64_t error;             /* 0, or 1 + index of the event that broke the format */
+  uint64_t prefetch_hits;     /* SRAM hits on sessions TIDE moved into SRAM since their previous
+                                 request (prefetch accuracy = prefetch_hits / (promote + swap)) */
+  uint64_t vict_diff;         /* dual-view runs: evictions whose victim the live table would not
+                                 have picked (eq. (stale)) */
+  uint64_t prom_diff;         /* dual-view runs: TIDE moves whose promoted session the live
+                                 table would not have picked */
   double amat_sum_ns;         /* sum of per-request access costs, eq. (hr-amat) */
   double ttft_sum_ns;         /* sum of per-request first-token cost proxies */
 } unison_counters;
@@ -201,14 +222,17 @@ int unison_set_hazard(unison_ctx* ctx, uint32_t lut, const uint32_t* d, const ui
 
 /* Copies n_sims parameter rows (HOST) into the workspace.  Errors:
  * UNISON_E_INVALID for an out-of-range field (policy, lut, trace, b_h, b_g,
- * tau, n_slots, dma bandwidth, negative or NaN penalty). */
+ * tau, n_slots, dma bandwidth, negative or NaN penalty, hazard_online,
+ * dual_sync, or a dual row when dims.views is 0). */
 int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
 
 /* Runs every simulation over at most `max_events` further events of its
  * trace (UINT64_MAX: to the end).  Without UNISON_RUN_CONTINUE each
  * simulation starts from an empty pool.  policy_override is a
  * UNISON_POLICY_* value applied to all simulations, or UNISON_POLICY_PARAMS.
- * Asynchronous.  Errors: UNISON_E_NOT_READY, UNISON_E_INVALID. */
+ * A batch with a dual-design row runs on a streamed-table kernel.
+ * Asynchronous.  Errors: UNISON_E_NOT_READY, UNISON_E_INVALID (also: a
+ * register-table variant forced on a batch with a dual-design row). */
 int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64_t max_events);
 
 /* Copies counters of simulations [first, first+n) to HOST `dst`; synchronises

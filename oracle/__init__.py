@@ -48,6 +48,7 @@ class Params(C.Structure):
         ("t_p_ns_per_tok", C.c_double), ("penalty_us", C.c_float), ("b_h", C.c_uint32),
         ("b_g", C.c_uint32), ("hazard_online", C.c_uint32), ("online_sessions", C.c_uint32),
         ("pad0", C.c_uint32), ("tau_ns", C.c_uint64), ("p_z", C.c_uint64),
+        ("dual_sync", C.c_uint32), ("pad1", C.c_uint32),
     ]
 
 
@@ -55,6 +56,7 @@ COUNTER_NAMES = (
     "requests", "hit_sram", "hit_hbm", "miss", "bypass", "evict", "expire", "promote", "swap",
     "dma_bytes", "tide_passes", "tokens_total", "tokens_computed", "extra_prefill_tok",
     "score_evals", "resident_evals", "digest", "victim_digest", "events", "error",
+    "prefetch_hits", "vict_diff", "prom_diff",
 )
 
 
@@ -208,7 +210,7 @@ def tau_b(counts):
 def params_struct(row):
     p = Params()
     for name, _ in Params._fields_:
-        if name == "pad0":
+        if name.startswith("pad"):
             continue
         v = row[name]
         setattr(p, name, float(v) if name.startswith("t_") or name == "penalty_us" else int(v))

@@ -74,6 +74,22 @@
  *            first online_sessions completions.  The update follows the DONE's
  *            register write, so that event's scan already uses the new table;
  *            every score is then re-evaluated against it.
+ *  prefetch  A promotion or swap moves its session into SRAM ahead of its
+ *            return; the session's next request is a prefetch hit when it
+ *            finds the session in SRAM (prefetch accuracy = prefetch hits /
+ *            (promotions + swaps), the ablation of scoring and tiering).
+ *  dual      The dual design of eq. (rf) / eq. (stale): the eviction engine and
+ *            the TIDE engine each read keys from a private copy of the
+ *            register file (every field of every session), overwritten with
+ *            the live file after every ARRIVE and GAP_START ("after every
+ *            request and gap"), after every 8th ARRIVE, or after every
+ *            GAP_START.  Which sessions are resident, in which tier, and
+ *            which are pinned stays live (it is the pool's physical state).
+ *            The per-event scan and the victims use the eviction copy; TIDE's
+ *            p, d and key(p) < key(d) use the TIDE copy.  At each eviction and
+ *            at each TIDE move the live file's choice over the same candidates
+ *            is computed too: vict_diff / prom_diff count the decisions that
+ *            differ.  The copies start as the empty register file.
  *  timeout   Before an event is written, every resident that has been idle
  *            longer than the TTL expires (its timer fired since the last event).
  *  account   eq. (hr-amat), eq. (prered): SRAM hit amat += len*kvb*t_s,
@@ -128,12 +144,15 @@ typedef struct {
   uint32_t pad0;
   uint64_t tau_ns;      /* gap time divisor */
   uint64_t p_z;         /* integer penalty P_Z */
+  uint32_t dual_sync;   /* 0 unified; 1, 2, 3: dual copies (see "dual" above) */
+  uint32_t pad1;
 } orc_params;
 
 typedef struct {
   uint64_t requests, hit_sram, hit_hbm, miss, bypass, evict, expire, promote, swap;
   uint64_t dma_bytes, tide_passes, tokens_total, tokens_computed, extra_prefill_tok;
   uint64_t score_evals, resident_evals, digest, victim_digest, events, error;
+  uint64_t prefetch_hits, vict_diff, prom_diff;
   double amat_sum_ns, ttft_sum_ns;
 } orc_counters;
 
@@ -326,6 +345,7 @@ void orc_kendall(uint32_t n_snap, uint32_t n_per, const float* x, const uint64_t
 
 typedef struct {
   uint32_t phase, tier, turn, len;
+  uint32_t prefetched; /* TIDE moved it into SRAM since its last request */
   float g;
   uint64_t gq, last_ns, next_ns;
 } sess_t;
@@ -333,6 +353,8 @@ typedef struct {
 typedef struct {
   const orc_params* p;
   sess_t* s;
+  sess_t* view[2];  /* dual design: the eviction engine's and TIDE's copies */
+  int keysrc;       /* where keys are read: -1 the live file, 0 or 1 a copy */
   const uint32_t* kvb;
   uint32_t n_sess;
   float hf[LUT_LEN];
@@ -364,7 +386,7 @@ static uint64_t size_of(const sim_t* m, uint32_t i) {
 
 /* "larger = evict first" key of one table entry */
 static uint64_t key_of(const sim_t* m, uint32_t i) {
-  const sess_t* e = &m->s[i];
+  const sess_t* e = m->keysrc < 0 ? &m->s[i] : &m->view[m->keysrc][i];
   switch (m->p->policy) {
     case P_SPEAR:
       if (m->p->score_mode == 1)
@@ -446,6 +468,12 @@ static void place(sim_t* m, uint32_t sid, uint32_t pref) {
     if (fits(m, pref, size)) { put(m, sid, pref); emit(m, OP_PLACE, sid, pref); return; }
     if (fits(m, other, size)) { put(m, sid, other); emit(m, OP_PLACE, sid, other); return; }
     uint32_t v = argmax_key(m, T_NONE);
+    if (m->view[0] && v != NONE_ID) {
+      int src = m->keysrc;
+      m->keysrc = -1;
+      if (argmax_key(m, T_NONE) != v) m->c->vict_diff++; /* eq. (stale) */
+      m->keysrc = src;
+    }
     if (v == NONE_ID) {
       emit(m, OP_BYPASS, sid, NONE_ID);
       m->c->bypass++;
@@ -470,9 +498,17 @@ static void tide(sim_t* m, uint32_t sid, uint64_t now, orc_state* st) {
   uint64_t inf = done_key(m);
   int has_inf = p->policy == P_SPEAR || p->policy == P_BELADY;
   m->c->tide_passes++;
+  int src = m->keysrc;
+  m->keysrc = m->view[1] ? 1 : -1;
+  uint32_t live_p = NONE_ID;
   for (;;) {
     uint32_t pid = argmin_key(m, T_HBM);
     if (pid == NONE_ID) break;
+    if (m->view[1]) {
+      m->keysrc = -1;
+      live_p = argmin_key(m, T_HBM);
+      m->keysrc = 1;
+    }
     uint64_t kp = key_of(m, pid);
     if (has_inf && kp == inf) break;
     uint64_t sp = size_of(m, pid);
@@ -480,10 +516,12 @@ static void tide(sim_t* m, uint32_t sid, uint64_t now, orc_state* st) {
       m->used[T_HBM] -= sp;
       m->used[T_SRAM] += sp;
       m->s[pid].tier = T_SRAM;
+      m->s[pid].prefetched = 1;
       left -= sp;
       moved += sp;
       emit(m, OP_PROMOTE, pid, NONE_ID);
       m->c->promote++;
+      if (m->view[1] && live_p != pid) m->c->prom_diff++;
       continue;
     }
     uint32_t did = argmax_key(m, T_SRAM);
@@ -497,12 +535,15 @@ static void tide(sim_t* m, uint32_t sid, uint64_t now, orc_state* st) {
     m->used[T_SRAM] = m->used[T_SRAM] - sd + sp;
     m->used[T_HBM] = m->used[T_HBM] - sp + sd;
     m->s[pid].tier = T_SRAM;
+    m->s[pid].prefetched = 1;
     m->s[did].tier = T_HBM;
     left -= sp + sd;
     moved += sp + sd;
     emit(m, OP_SWAP, pid, did);
     m->c->swap++;
+    if (m->view[1] && live_p != pid) m->c->prom_diff++;
   }
+  m->keysrc = src;
   if (moved) {
     unsigned __int128 ns = ((unsigned __int128)moved * 1000 + p->dma_B_per_us - 1) / p->dma_B_per_us;
     m->dma_free_at = sat_u64((unsigned __int128)now + ns);
@@ -530,7 +571,7 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
             orc_counters* out, orc_rec* log, uint32_t log_cap, uint32_t* log_len,
             orc_state* states, uint32_t* counts_out, uint64_t* elapsed_ns) {
   if (!p || !out || p->policy > P_BELADY || p->dma_B_per_us == 0 || p->n_slots == 0 ||
-      p->tau_ns == 0 || p->b_h < 1 || p->b_h > 32 || p->b_g < 1 || p->b_g > 64 ||
+      p->tau_ns == 0 || p->b_h < 1 || p->b_h > 32 || p->b_g < 1 || p->b_g > 64 || p->dual_sync > 3 ||
       !(p->penalty_us >= 0.0f))
     return ORC_E_INVALID;
   memset(out, 0, sizeof *out);
@@ -544,6 +585,15 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
   m.log_cap = log_cap;
   m.s = (sess_t*)calloc(n_sess ? n_sess : 1, sizeof(sess_t));
   if (!m.s) return ORC_E_INVALID;
+  for (uint32_t i = 0; i < n_sess; i++) m.s[i].next_ns = UINT64_MAX; /* no next arrival yet */
+  m.keysrc = -1;
+  if (p->dual_sync) {
+    for (int k = 0; k < 2; k++) {
+      m.view[k] = (sess_t*)calloc(n_sess ? n_sess : 1, sizeof(sess_t));
+      if (!m.view[k]) { free(m.s); free(m.view[0]); return ORC_E_INVALID; }
+      memcpy(m.view[k], m.s, (size_t)n_sess * sizeof(sess_t)); /* the empty register file */
+    }
+  }
   for (int t = 0; t < LUT_LEN; t++) {
     m.hd[t] = p->hazard_online ? 0 : lut_d[t];
     m.hn[t] = p->hazard_online ? 0 : lut_n[t];
@@ -626,6 +676,7 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
      * is scored; its result is this event's victim index */
     out->score_evals += m.n_table;
     out->resident_evals += m.n_res;
+    m.keysrc = m.view[0] ? 0 : -1;
     uint32_t v0 = argmax_key(&m, T_NONE);
     /* odd weight per event: a different victim at any one event changes the sum */
     out->victim_digest += ((uint64_t)v0 + 1) * ((2 * (uint64_t)m.ev + 1) * 0x9e3779b97f4a7c15ULL);
@@ -641,6 +692,7 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
       if (tier0 == T_SRAM || tier0 == T_HBM) {
         double t_mem = tier0 == T_SRAM ? p->t_s_ns_per_B : p->t_h_ns_per_B;
         if (tier0 == T_SRAM) out->hit_sram++; else out->hit_hbm++;
+        if (tier0 == T_SRAM && x->prefetched) out->prefetch_hits++;
         double a = (double)(len * kb) * t_mem;
         double b = (double)(len_prev * kb) * t_mem;
         double c = (double)dlen * p->t_p_ns_per_tok;
@@ -656,6 +708,7 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
         out->tokens_computed += len;
         out->extra_prefill_tok += len_prev;
       }
+      x->prefetched = 0;
       x->len = (uint32_t)len;
       place(&m, sid, tier0 == T_HBM ? T_HBM : T_SRAM);
     } else if (kind == K_GAP_START) {
@@ -664,6 +717,13 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
       if (x->tier == T_NONE) m.n_table--;
     }
 
+    if (m.view[0]) {
+      int sync = (p->dual_sync == 1 && kind != K_DONE) ||
+                 (p->dual_sync == 2 && kind == K_ARRIVE && out->requests % 8 == 0) ||
+                 (p->dual_sync == 3 && kind == K_GAP_START);
+      if (sync)
+        for (int k = 0; k < 2; k++) memcpy(m.view[k], m.s, (size_t)n_sess * sizeof(sess_t));
+    }
     if (st) {
       st->used_sram = m.used[T_SRAM];
       st->used_hbm = m.used[T_HBM];
@@ -683,6 +743,8 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
       counts_out[LUT_LEN + t] = m.hn[t];
     }
   free(m.s);
+  free(m.view[0]);
+  free(m.view[1]);
   return rc;
 }
 

@@ -49,7 +49,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // Workspace layout; offsets in bytes from the workspace base.
 struct Layout {
   size_t params, ev_off, sess_off, lut_d, lut_n, state, counters, hcount, mg, gq, len, last, next,
-      log, scratch, total;
+      views, log, scratch, total;
 };
 
 bool make_layout(const unison_dims& d, Layout& L) {
@@ -73,6 +73,7 @@ bool make_layout(const unison_dims& d, Layout& L) {
   L.len = take(sizeof(uint32_t) * entries);
   L.last = take(sizeof(uint64_t) * entries);
   L.next = take(sizeof(uint64_t) * entries);
+  L.views = take(d.views ? sizeof(uint64_t) * 8 * entries : 0);
   L.log = take(sizeof(unison_record) * (size_t)d.log_cap * d.n_sims);
   L.scratch = take(256);
   L.total = off;
@@ -81,7 +82,7 @@ bool make_layout(const unison_dims& d, Layout& L) {
 
 bool dims_ok(const unison_dims* d) {
   return d && d->n_sims >= 1 && d->n_traces >= 1 && d->n_luts >= 1 && d->max_sessions >= 1 &&
-         d->max_sessions <= UNISON_MAX_SESSIONS;
+         d->max_sessions <= UNISON_MAX_SESSIONS && d->views <= 1;
 }
 
 }  // namespace
@@ -98,6 +99,7 @@ struct unison_ctx {
   std::vector<uint8_t> lut_set;
   bool traces_loaded = false, params_set = false, ran = false;
   bool time44 = false;  // every trace time is below 2^44 - 1 ns
+  bool dual = false;    // some row uses the dual register-file design
   uint32_t max_sess_batch = 0;
   int force_variant = -1;
   char err[512];
@@ -247,6 +249,9 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
   uint32_t max_sess = 0;
   for (uint32_t i = 0; i < ctx->dims.n_sims; ++i) {
     const unison_sim_params& p = params[i];
+    if (p.dual_sync > UNISON_DUAL_GAP || (p.dual_sync && !ctx->dims.views))
+      return ctx->fail(UNISON_E_INVALID, "parameter row %u: dual_sync %u (dims.views = %u)", i,
+                       p.dual_sync, ctx->dims.views);
     if (p.policy > UNISON_POLICY_BELADY || p.tide > 1 || p.score_mode > 1 || p.hazard_online > 1 ||
         p.lut >= ctx->dims.n_luts || p.trace >= ctx->dims.n_traces || p.b_h < 1 || p.b_h > 16 ||
         p.b_g < 1 || p.b_g > 64 || p.tau_ns < 1 || p.n_slots < 1 || p.dma_B_per_us < 1 ||
@@ -257,6 +262,8 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
     max_sess = std::max<uint32_t>(max_sess, (uint32_t)ns);
   }
   ctx->h_params.assign(params, params + ctx->dims.n_sims);
+  ctx->dual = false;
+  for (uint32_t i = 0; i < ctx->dims.n_sims; ++i) ctx->dual = ctx->dual || params[i].dual_sync != 0;
   int rc = ctx->hip(hipMemcpyAsync(ctx->at<unison_sim_params>(ctx->L.params), ctx->h_params.data(),
                                    sizeof(unison_sim_params) * ctx->dims.n_sims,
                                    hipMemcpyHostToDevice, ctx->stream),
@@ -303,6 +310,7 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   a.t_next = ctx->at<uint64_t>(ctx->L.next);
   a.log = ctx->dims.log_cap ? ctx->at<unison_record>(ctx->L.log) : nullptr;
   a.hcount = ctx->at<uint32_t>(ctx->L.hcount);
+  a.views = ctx->dims.views ? ctx->at<uint64_t>(ctx->L.views) : nullptr;
   a.max_events = max_events;
   a.n_sims = ctx->dims.n_sims;
   a.max_sessions = ctx->dims.max_sessions;
@@ -311,6 +319,12 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   a.policy_override = policy_override;
   a.time44 = ctx->time44 ? 1u : 0u;
   int v = ctx->force_variant;
+  // the dual design's copies live in the workspace: a streamed-table kernel runs it
+  if (ctx->dual) {
+    if (v < 0) v = 10;
+    if (v != 3 && v != 10)
+      return ctx->fail(UNISON_E_INVALID, "dual register files run on the streamed-table variants (3, 10), not %d", v);
+  }
   if (v >= 0 && (sim_variant_capacity(v) == 0 || sim_variant_capacity(v) < ctx->max_sess_batch))
     return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds %u sessions < %u", v,
                      sim_variant_capacity(v), ctx->max_sess_batch);

@@ -233,6 +233,7 @@ struct Entry {
 template <int G, int EPL, uint32_t POL, uint32_t SMODE>
 struct RegTable {
   using PT = Pol<POL, SMODE>;
+  static constexpr bool kViews = false;  // no dual-design copies
   uint32_t lane;
   uint32_t meta[EPL];
   float g[EPL];
@@ -451,12 +452,21 @@ struct MemTable {
   using PT = Pol<POL, SMODE>;
   static constexpr int NW = BLOCK / 64;
   static constexpr int UNROLL = 4;
+  static constexpr bool kViews = true;
   uint64_t* mg;
   uint64_t* gq;
   uint32_t* len;
   uint64_t* last;
   uint64_t* next;
   const uint32_t* kvb;
+  // The dual design (eq. (rf), eq. (stale)): the eviction engine's (0) and
+  // TIDE's (1) copies of the key fields; keys come from copy `src`, or from
+  // the live table when src < 0.  Eligibility and tiers are always live.
+  uint64_t* vmg[2];
+  uint64_t* vgq[2];
+  uint64_t* vlast[2];
+  uint64_t* vnext[2];
+  int src;
   uint32_t tid;
   uint32_t hi;        // entries [0, hi) can be in the table
   uint32_t parity;
@@ -540,10 +550,34 @@ struct MemTable {
   }
 
   __device__ __forceinline__ uint64_t key_at(const KeyCtx& K, uint32_t i, uint64_t x) const {
+    const uint64_t* q = gq;
+    const uint64_t* l = last;
+    const uint64_t* n = next;
+    if (src >= 0) {
+      x = vmg[src][i];
+      q = vgq[src];
+      l = vlast[src];
+      n = vnext[src];
+    }
     const uint32_t m = (uint32_t)x;
     const float gv = __uint_as_float((uint32_t)(x >> 32));
-    return key_of<POL, SMODE>(K, m, hazard_of<POL, SMODE>(K, m), gv, PT::fixed ? gq[i] : 0ull,
-                              PT::recency ? last[i] : 0ull, PT::belady ? next[i] : 0ull);
+    return key_of<POL, SMODE>(K, m, hazard_of<POL, SMODE>(K, m), gv, PT::fixed ? q[i] : 0ull,
+                              PT::recency ? l[i] : 0ull, PT::belady ? n[i] : 0ull);
+  }
+
+  // Overwrites both copies with the live key fields of every entry.
+  __device__ __forceinline__ void sync_views() {
+    for (uint32_t i = tid; i < hi; i += BLOCK) {
+      const uint64_t m = mg[i], q = gq[i], l = last[i], n = next[i];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        vmg[c][i] = m;
+        vgq[c][i] = q;
+        vlast[c][i] = l;
+        vnext[c][i] = n;
+      }
+    }
+    __syncthreads();
   }
 
   // Streams the window and reduces the keys of evictable entries in `tier`.
@@ -640,7 +674,7 @@ struct Scalars {
 // Counters as kept during a run: event-bounded counts in 32 bits.
 struct Cnt {
   uint32_t requests, hit_sram, hit_hbm, miss, bypass, evict, expire, promote, swap, tide_passes,
-      events;
+      events, prefetch_hits, vict_diff, prom_diff;
   uint64_t dma_bytes, tokens_total, tokens_computed, extra_prefill, score_evals, resident_evals,
       digest, victim_digest, error;
   double amat, ttft;
@@ -659,6 +693,9 @@ __device__ __forceinline__ Cnt cnt_from(const unison_counters& c) {
   k.swap = (uint32_t)c.swap;
   k.tide_passes = (uint32_t)c.tide_passes;
   k.events = (uint32_t)c.events;
+  k.prefetch_hits = (uint32_t)c.prefetch_hits;
+  k.vict_diff = (uint32_t)c.vict_diff;
+  k.prom_diff = (uint32_t)c.prom_diff;
   k.dma_bytes = c.dma_bytes;
   k.tokens_total = c.tokens_total;
   k.tokens_computed = c.tokens_computed;
@@ -695,6 +732,9 @@ __device__ __forceinline__ unison_counters cnt_to(const Cnt& k) {
   c.victim_digest = k.victim_digest;
   c.events = k.events;
   c.error = k.error;
+  c.prefetch_hits = k.prefetch_hits;
+  c.vict_diff = k.vict_diff;
+  c.prom_diff = k.prom_diff;
   c.amat_sum_ns = k.amat;
   c.ttft_sum_ns = k.ttft;
   return c;
@@ -739,6 +779,9 @@ __device__ __forceinline__ void pin_vgpr(Cnt& k) {
   k.swap = in_vgpr(k.swap);
   k.tide_passes = in_vgpr(k.tide_passes);
   k.events = in_vgpr(k.events);
+  k.prefetch_hits = in_vgpr(k.prefetch_hits);
+  k.vict_diff = in_vgpr(k.vict_diff);
+  k.prom_diff = in_vgpr(k.prom_diff);
   k.dma_bytes = in_vgpr(k.dma_bytes);
   k.tokens_total = in_vgpr(k.tokens_total);
   k.tokens_computed = in_vgpr(k.tokens_computed);
@@ -861,10 +904,12 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     // Alg. 1: write e into R; on gap_end update the EMA
     Entry x;
     uint32_t ph, tier0, len_prev = 0;
+    bool prefetched = false;
     if (kind == kArrive) {
       x = T.read(sid);
       ph = meta_phase(x.meta);
       tier0 = meta_tier(x.meta);
+      prefetched = (x.meta & kPrefetched) != 0;
       len_prev = x.len;
       bool bad;
       if (turn == 0) {
@@ -911,6 +956,11 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     C.score_evals += S.n_table;
     C.resident_evals += S.n_res;
     T.scan(K);
+    bool dual = false;
+    if constexpr (Tab::kViews) {
+      dual = P.dual_sync != 0;
+      T.src = dual ? 0 : -1;  // the eviction engine scans its own copy
+    }
     const Cand v0 = T.argmax_first(K);
     // odd weight per event: a different victim at any one event changes the sum
     C.victim_digest += ((uint64_t)v0.sid + 1u) * vw;
@@ -932,6 +982,7 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         const uint64_t old = (uint64_t)len_prev * kb;
         if (tier0 == kTierSram) {
           C.hit_sram++;
+          C.prefetch_hits += prefetched ? 1u : 0u;
           S.hit_s_bytes += now_b;
           S.prev_s_bytes += old;
           S.used_s -= old;
@@ -986,6 +1037,14 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
             v = T.template select<true>(0, K);
           }
           first = false;
+          if constexpr (Tab::kViews) {
+            if (dual && v.sid != kNone) {  // eq. (stale): would the live table agree?
+              T.src = -1;
+              const Cand vl = T.template select<true>(0, K);
+              T.src = 0;
+              C.vict_diff += vl.sid != v.sid ? 1u : 0u;
+            }
+          }
           if (v.sid == kNone) {
             emit(C, S, L, ev, kOpBypass, sid, kNone);
             C.bypass++;
@@ -1009,10 +1068,19 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
         const uint64_t budget = sat_mul(delta_us, P.dma_B_per_us);
         uint64_t left = budget, moved = 0;
         C.tide_passes++;
+        if constexpr (Tab::kViews) T.src = dual ? 1 : -1;  // TIDE decides from its own copy
         for (;;) {
           Cand p, d;
           T.select_pd(K, p, d);  // eq. (promote), eq. (demote)
           if (p.sid == kNone) break;
+          uint32_t live_p = p.sid;
+          if constexpr (Tab::kViews) {
+            if (dual) {
+              T.src = -1;
+              live_p = T.template select<false>(kTierHbm, K).sid;
+              T.src = 1;
+            }
+          }
           if (PT::has_inf && p.key == PT::inf_key) break;
           uint64_t sp;
           uint32_t mp;
@@ -1020,11 +1088,12 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
           if (S.used_s + sp <= P.cap_sram_B && sp <= left) {
             S.used_h -= sp;
             S.used_s += sp;
-            T.set_meta(p.sid, with_tier(mp, kTierSram));
+            T.set_meta(p.sid, with_tier(mp, kTierSram) | kPrefetched);
             left -= sp;
             moved += sp;
             emit(C, S, L, ev, kOpPromote, p.sid, kNone);
             C.promote++;
+            C.prom_diff += live_p != p.sid ? 1u : 0u;
             continue;
           }
           if (d.sid == kNone) break;
@@ -1036,12 +1105,13 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
           if (!legal) break;
           S.used_s = S.used_s - sd + sp;
           S.used_h = S.used_h - sp + sd;
-          T.set_meta(p.sid, with_tier(mp, kTierSram));
+          T.set_meta(p.sid, with_tier(mp, kTierSram) | kPrefetched);
           T.set_meta(d.sid, with_tier(md, kTierHbm));
           left -= sp + sd;
           moved += sp + sd;
           emit(C, S, L, ev, kOpSwap, p.sid, d.sid);
           C.swap++;
+          C.prom_diff += live_p != p.sid ? 1u : 0u;
         }
         if (moved) {
           // DMA busy for ceil(moved * 1000 / B) ns
@@ -1054,6 +1124,16 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
       }
     } else {
       if (tier0 == kTierNone) S.n_table--;
+    }
+    if constexpr (Tab::kViews) {
+      // the copies are refreshed after every request and gap onset, every 8th
+      // request, or every gap onset
+      if (dual) {
+        const bool sync = (P.dual_sync == UNISON_DUAL_EVERY && kind != kDone) ||
+                          (P.dual_sync == UNISON_DUAL_EIGHT && kind == kArrive && C.requests % 8u == 0) ||
+                          (P.dual_sync == UNISON_DUAL_GAP && kind == kGapStart);
+        if (uni32(sync ? 1u : 0u)) T.sync_views();
+      }
     }
     C.events++;
     cur = nxt;
@@ -1189,8 +1269,8 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
   const LogSink L{log_on, log_on ? a.log + (size_t)sim * a.log_cap : nullptr, a.log_cap, lane == 0,
                   log_on && (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
   if (C.error == 0) {
-    if (n_sess > (uint32_t)(G * EPL)) {
-      C.error = ~0ull;  // the launcher picks a variant that holds the trace
+    if (n_sess > (uint32_t)(G * EPL) || P.dual_sync) {
+      C.error = ~0ull;  // the launcher picks a variant that holds the trace (and its copies)
     } else {
       run_events<POL, SMODE, false>(T, P, K, tr, S, C, L, next_event, a.max_events);
     }
@@ -1302,6 +1382,28 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
       }
     }
   }
+  // the dual design's copies, [2][4 fields][max_sessions] per simulation; a
+  // fresh run starts them as the empty register file
+  T.src = -1;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    uint64_t* vb = a.views ? a.views + ((size_t)sim * 8 + 4 * c) * a.max_sessions : nullptr;
+    T.vmg[c] = vb;
+    T.vgq[c] = vb ? vb + a.max_sessions : nullptr;
+    T.vlast[c] = vb ? vb + 2 * (size_t)a.max_sessions : nullptr;
+    T.vnext[c] = vb ? vb + 3 * (size_t)a.max_sessions : nullptr;
+  }
+  if (P.dual_sync && a.views && !cont) {
+    for (uint32_t i = tid; i < n_sess; i += BLOCK) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        T.vmg[c][i] = 0;
+        T.vgq[c][i] = 0;
+        T.vlast[c][i] = 0;
+        T.vnext[c][i] = ~0ull;
+      }
+    }
+  }
   __syncthreads();
 
   Scalars S;
@@ -1317,6 +1419,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   }
   if (S.hi > n_sess) S.hi = n_sess;  // never scan past the trace's sessions
   T.hi = S.hi;
+  if (P.dual_sync && !a.views) C.error = ~0ull;  // the launcher reserves the copies
   pin_vgpr(S);
   pin_vgpr(C);
   const bool log_on = (a.flags & UNISON_RUN_LOG) && a.log_cap;

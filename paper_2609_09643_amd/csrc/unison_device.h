@@ -2,7 +2,7 @@
 //
 // The session register file of one simulation is a struct-of-arrays table
 // indexed by session id.  Each entry holds:
-//   mg    u64  low 32 bits: meta = phase | tier << 2 | turn << 4
+//   mg    u64  low 32 bits: meta = phase | tier << 2 | prefetched << 4 | turn << 5
 //              high 32 bits: the fp32 gap EMA g in microseconds (eq. (ema))
 //   gq    u64  the integer gap EMA g_q (eq. (gapq), eq. (ema-int))
 //   len   u32  resident KV length of the latest turn, tokens
@@ -32,9 +32,11 @@ enum : uint32_t { kOpEvict = 1, kOpExpire = 2, kOpBypass = 3, kOpPromote = 4, kO
 
 __host__ __device__ __forceinline__ uint32_t meta_phase(uint32_t m) { return m & 3u; }
 __host__ __device__ __forceinline__ uint32_t meta_tier(uint32_t m) { return (m >> 2) & 3u; }
-__host__ __device__ __forceinline__ uint32_t meta_turn(uint32_t m) { return m >> 4; }
+// Set when TIDE moves the session into SRAM; cleared by its next request.
+constexpr uint32_t kPrefetched = 1u << 4;
+__host__ __device__ __forceinline__ uint32_t meta_turn(uint32_t m) { return m >> 5; }
 __host__ __device__ __forceinline__ uint32_t make_meta(uint32_t ph, uint32_t tier, uint32_t turn) {
-  return ph | (tier << 2) | (turn << 4);
+  return ph | (tier << 2) | (turn << 5);
 }
 __host__ __device__ __forceinline__ uint32_t with_tier(uint32_t m, uint32_t tier) {
   return (m & ~0xCu) | (tier << 2);
@@ -170,6 +172,7 @@ struct SimArgs {
   uint64_t* t_next;
   unison_record* log;
   uint32_t* hcount;        // [n_sims][2][51] hazard counts d, n at the end of a launch
+  uint64_t* views;         // dual design: [n_sims][2 copies][4 fields][max_sessions], or null
   uint64_t max_events;
   uint32_t n_sims;
   uint32_t max_sessions;

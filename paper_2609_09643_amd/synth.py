@@ -44,7 +44,9 @@ SIM_PARAMS_DTYPE = np.dtype([
     ("t_s_ns_per_B", np.float64), ("t_h_ns_per_B", np.float64),
     ("t_p_ns_per_tok", np.float64), ("penalty_us", np.float32),
     ("b_h", np.uint32), ("b_g", np.uint32), ("tau_ns", np.uint64), ("p_z", np.uint64),
+    ("dual_sync", np.uint32),
 ])
+DUAL_NONE, DUAL_EVERY, DUAL_EIGHT, DUAL_GAP = 0, 1, 2, 3
 
 
 @dataclass

@@ -29,7 +29,7 @@ class UnisonError(RuntimeError):
 
 class Dims(C.Structure):
     _fields_ = [("n_sims", C.c_uint32), ("n_traces", C.c_uint32), ("max_sessions", C.c_uint32),
-                ("n_luts", C.c_uint32), ("log_cap", C.c_uint32)]
+                ("n_luts", C.c_uint32), ("log_cap", C.c_uint32), ("views", C.c_uint32)]
 
 
 class SimParams(C.Structure):
@@ -41,7 +41,7 @@ class SimParams(C.Structure):
         ("t_s_ns_per_B", C.c_double), ("t_h_ns_per_B", C.c_double),
         ("t_p_ns_per_tok", C.c_double), ("penalty_us", C.c_float), ("b_h", C.c_uint32),
         ("b_g", C.c_uint32), ("online_sessions", C.c_uint32), ("tau_ns", C.c_uint64),
-        ("p_z", C.c_uint64),
+        ("p_z", C.c_uint64), ("dual_sync", C.c_uint32), ("pad0", C.c_uint32),
     ]
 
 
@@ -49,6 +49,7 @@ COUNTER_FIELDS = (
     "requests", "hit_sram", "hit_hbm", "miss", "bypass", "evict", "expire", "promote", "swap",
     "dma_bytes", "tide_passes", "tokens_total", "tokens_computed", "extra_prefill_tok",
     "score_evals", "resident_evals", "digest", "victim_digest", "events", "error",
+    "prefetch_hits", "vict_diff", "prom_diff",
 )
 COUNTERS_DTYPE = np.dtype([(n, np.uint64) for n in COUNTER_FIELDS] +
                           [("amat_sum_ns", np.float64), ("ttft_sum_ns", np.float64)])
@@ -175,7 +176,9 @@ class Simulator:
         self.n_sims = workload.n_sims
         self.log_cap = int(log_cap)
         max_sess = max(t.n_sessions for t in traces)
-        self.dims = Dims(self.n_sims, len(traces), max_sess, len(workload.lut_pops), self.log_cap)
+        views = int(np.any(workload.params["dual_sync"] != 0))
+        self.dims = Dims(self.n_sims, len(traces), max_sess, len(workload.lut_pops), self.log_cap,
+                         views)
         nbytes = C.c_size_t()
         _check(L.unison_workspace_size(C.byref(self.dims), C.byref(nbytes)))
         self.ws_bytes = int(nbytes.value)

@@ -69,7 +69,7 @@ def test_host_side_validation(lib):
 
 def test_struct_layouts_match_header():
     from paper_2609_09643_amd import unison as U
-    assert C.sizeof(U.SimParams) == 120
-    assert U.COUNTERS_DTYPE.itemsize == 22 * 8
+    assert C.sizeof(U.SimParams) == 128
+    assert U.COUNTERS_DTYPE.itemsize == 25 * 8
     assert U.RECORD_DTYPE.itemsize == 16
     assert C.sizeof(U.TraceBatch) == 8 + 8 * 8
