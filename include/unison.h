@@ -230,7 +230,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
  * trace (UINT64_MAX: to the end).  Without UNISON_RUN_CONTINUE each
  * simulation starts from an empty pool.  policy_override is a
  * UNISON_POLICY_* value applied to all simulations, or UNISON_POLICY_PARAMS.
- * A batch with a dual-design row runs on a streamed-table kernel.
+ * A batch with a dual-design row runs on the copies' kernel (variant 11).
  * Asynchronous.  Errors: UNISON_E_NOT_READY, UNISON_E_INVALID (also: a
  * register-table variant forced on a batch with a dual-design row). */
 int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64_t max_events);
@@ -296,7 +296,9 @@ int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t*
  * trace; register tables of lanes x sessions per lane 0: 16 x 1, 1: 64 x 1,
  * 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 6: 64 x 24, 7: 16 x 4, 8: 32 x 8; one
  * workgroup per simulation with the table 3: streamed from the workspace by
- * 256 threads, 10: by 512 threads, 9: held in LDS).  A variant too small for the traces, or an unknown id,
+ * 256 threads, 10: by 512 threads, 9: held in LDS, 11: streamed by 512
+ * threads with the dual design's copies -- the only variant for a batch with
+ * a dual-design row).  A variant too small for the traces, or an unknown id,
  * makes unison_run return UNISON_E_CAPACITY. */
 int unison_debug_force_variant(unison_ctx* ctx, int variant);
 

@@ -319,11 +319,11 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   a.policy_override = policy_override;
   a.time44 = ctx->time44 ? 1u : 0u;
   int v = ctx->force_variant;
-  // the dual design's copies live in the workspace: a streamed-table kernel runs it
+  // the dual design's copies live in the workspace: its streamed-table kernel runs it
   if (ctx->dual) {
-    if (v < 0) v = 10;
-    if (v != 3 && v != 10)
-      return ctx->fail(UNISON_E_INVALID, "dual register files run on the streamed-table variants (3, 10), not %d", v);
+    if (v < 0) v = 11;
+    if (v != 11)
+      return ctx->fail(UNISON_E_INVALID, "dual register files run on variant 11, not %d", v);
   }
   if (v >= 0 && (sim_variant_capacity(v) == 0 || sim_variant_capacity(v) < ctx->max_sess_batch))
     return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds %u sessions < %u", v,

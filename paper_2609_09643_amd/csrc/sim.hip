@@ -447,12 +447,12 @@ struct RegTable {
 // Table in the workspace, one workgroup per simulation.  Uniform values read
 // from memory or LDS go through readfirstlane so the engine's scalars live in
 // SGPRs.
-template <int BLOCK, uint32_t POL, uint32_t SMODE>
+template <int BLOCK, uint32_t POL, uint32_t SMODE, bool VIEWS>
 struct MemTable {
   using PT = Pol<POL, SMODE>;
   static constexpr int NW = BLOCK / 64;
   static constexpr int UNROLL = 4;
-  static constexpr bool kViews = true;
+  static constexpr bool kViews = VIEWS;  // instantiated with the dual design's copies
   uint64_t* mg;
   uint64_t* gq;
   uint32_t* len;
@@ -553,7 +553,7 @@ struct MemTable {
     const uint64_t* q = gq;
     const uint64_t* l = last;
     const uint64_t* n = next;
-    if (src >= 0) {
+    if (VIEWS && src >= 0) {
       x = vmg[src][i];
       q = vgq[src];
       l = vlast[src];
@@ -1331,7 +1331,7 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
 // One workgroup per simulation.  IN_LDS keeps the table in LDS for the whole
 // run (copied from and back to the workspace); otherwise it is streamed from
 // the workspace in place.
-template <int BLOCK, uint32_t POL, uint32_t SMODE, bool IN_LDS>
+template <int BLOCK, uint32_t POL, uint32_t SMODE, bool IN_LDS, bool VIEWS>
 __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const unison_sim_params& P,
                                           const KeyCtx& K, Cand* s_red, uint64_t* s_tab) {
   const uint32_t tid = threadIdx.x;
@@ -1343,7 +1343,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   const size_t tb = (size_t)sim * a.max_sessions;
   const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
 
-  MemTable<BLOCK, POL, SMODE> T;
+  MemTable<BLOCK, POL, SMODE, VIEWS> T;
   T.tid = tid;
   T.parity = 0;
   T.red = s_red;
@@ -1393,7 +1393,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
     T.vlast[c] = vb ? vb + 2 * (size_t)a.max_sessions : nullptr;
     T.vnext[c] = vb ? vb + 3 * (size_t)a.max_sessions : nullptr;
   }
-  if (P.dual_sync && a.views && !cont) {
+  if (VIEWS && P.dual_sync && a.views && !cont) {
     for (uint32_t i = tid; i < n_sess; i += BLOCK) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
@@ -1419,7 +1419,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   }
   if (S.hi > n_sess) S.hi = n_sess;  // never scan past the trace's sessions
   T.hi = S.hi;
-  if (P.dual_sync && !a.views) C.error = ~0ull;  // the launcher reserves the copies
+  if (P.dual_sync && !(VIEWS && a.views)) C.error = ~0ull;  // the launcher picks the copies' kernel
   pin_vgpr(S);
   pin_vgpr(C);
   const bool log_on = (a.flags & UNISON_RUN_LOG) && a.log_cap;
@@ -1448,7 +1448,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   }
 }
 
-template <int BLOCK, bool IN_LDS>
+template <int BLOCK, bool IN_LDS, bool VIEWS>
 __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   __shared__ float s_hf[52];
   __shared__ uint32_t s_hq[52];
@@ -1465,12 +1465,12 @@ __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   __syncthreads();
   switch (sim_policy(a, P)) {
     case kSpear:
-      if (P.score_mode) block_run<BLOCK, kSpear, 1, IN_LDS>(a, sim, P, K, s_red, s_tab);
-      else block_run<BLOCK, kSpear, 0, IN_LDS>(a, sim, P, K, s_red, s_tab);
+      if (P.score_mode) block_run<BLOCK, kSpear, 1, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab);
+      else block_run<BLOCK, kSpear, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab);
       break;
-    case kLru: block_run<BLOCK, kLru, 0, IN_LDS>(a, sim, P, K, s_red, s_tab); break;
-    case kTimeout: block_run<BLOCK, kTimeout, 0, IN_LDS>(a, sim, P, K, s_red, s_tab); break;
-    default: block_run<BLOCK, kBelady, 0, IN_LDS>(a, sim, P, K, s_red, s_tab); break;
+    case kLru: block_run<BLOCK, kLru, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
+    case kTimeout: block_run<BLOCK, kTimeout, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
+    default: block_run<BLOCK, kBelady, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
   }
 }
 
@@ -1503,12 +1503,14 @@ struct Variant {
 };
 
 // Register-table shapes (lanes per simulation x sessions per lane); ids 3
-// and 10 stream the table with 256 and 512 threads, id 9 keeps it in LDS.
+// and 10 stream the table with 256 and 512 threads, id 9 keeps it in LDS,
+// id 11 streams it with 512 threads and also keeps the dual design's copies.
 constexpr Variant kVariants[] = {{16, 1}, {64, 1}, {64, 4}, {0, 0}, {4, 4},
-                                 {8, 2},  {64, 24}, {16, 4}, {32, 8}, {0, 1}, {0, 0}};
+                                 {8, 2},  {64, 24}, {16, 4}, {32, 8}, {0, 1}, {0, 0}, {0, 0}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kBlock = 256;
 constexpr int kLdsVariant = 9;
+constexpr int kDualVariant = 11;  // streamed, 512 threads, with the dual design's copies
 constexpr uint32_t kLdsBytesPerSession = 4 * 8 + 2 * 4;  // mg, last, gq, next; len, kvb
 
 // Largest dynamic LDS one workgroup may take on the current device.
@@ -1560,14 +1562,17 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
     case 8: launch_regs<32, 8>(a, stream); break;
     case kLdsVariant: {
       const size_t lds = (size_t)(max_sess_in_batch ? max_sess_in_batch : 1) * kLdsBytesPerSession;
-      hipLaunchKernelGGL((sim_block_kernel<kBlock, true>), dim3(a.n_sims), dim3(kBlock), lds, stream, a);
+      hipLaunchKernelGGL((sim_block_kernel<kBlock, true, false>), dim3(a.n_sims), dim3(kBlock), lds, stream, a);
       break;
     }
     case 10:
-      hipLaunchKernelGGL((sim_block_kernel<512, false>), dim3(a.n_sims), dim3(512), 0, stream, a);
+      hipLaunchKernelGGL((sim_block_kernel<512, false, false>), dim3(a.n_sims), dim3(512), 0, stream, a);
+      break;
+    case kDualVariant:
+      hipLaunchKernelGGL((sim_block_kernel<512, false, true>), dim3(a.n_sims), dim3(512), 0, stream, a);
       break;
     default:
-      hipLaunchKernelGGL((sim_block_kernel<kBlock, false>), dim3(a.n_sims), dim3(kBlock), 0, stream, a);
+      hipLaunchKernelGGL((sim_block_kernel<kBlock, false, false>), dim3(a.n_sims), dim3(kBlock), 0, stream, a);
       break;
   }
   return hipGetLastError();

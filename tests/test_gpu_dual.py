@@ -55,7 +55,7 @@ def paper_shaped_rows(n_traces=1):
     return np.array(rows, dtype=synth.SIM_PARAMS_DTYPE)
 
 
-@pytest.mark.parametrize("variant", [None, 3])
+@pytest.mark.parametrize("variant", [None, 11])
 def test_paper_shaped_trace_with_tide(variant):
     trs = synth.fidelity_traces()[:2]
     w = synth.Workload("dual_fid", trs, [t.turns for t in trs], paper_shaped_rows(2))

@@ -13,7 +13,7 @@ from tracekit import trace_from_events
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = (0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10)
+VARIANTS = (0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11)
 
 
 def say(*a):
