@@ -227,12 +227,47 @@ def section_online(torch):
             "s": dt, "events_per_s": float(c["events"].sum()) / dt, "traces": out}
 
 
+def section_studies(torch):
+    """The dual register-file ablation (Table V), the scoring x tiering
+    ablation with prefetch accuracy, and ASE over the session capacity
+    (eq. (ase)), on the six stand-in traces; one launch each."""
+    from paper_2609_09643_amd import studies
+    out = {}
+    for name, build in (("dual", synth_mod().dual_ablation), ("components", synth_mod().component_ablation),
+                        ("ase", synth_mod().slot_sweep)):
+        w, meta = build()
+        t0 = time.perf_counter()
+        c = studies.run(w)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        if name == "dual":
+            rows = studies.dual_table(c, meta)
+            res = {str(k): {key: round(float(sum(r[key] for r in rows if r["sync"] == k) /
+                                            max(1, sum(1 for r in rows if r["sync"] == k))), 3)
+                            for key in ("vict_ne_pct", "prom_ne_pct", "d_hr_pp", "d_sram_pp",
+                                        "d_pre_pp", "d_amat_pct")}
+                   for k in (1, 2, 3)}
+            res["per_trace"] = [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in r.items()}
+                                for r in rows]
+        elif name == "components":
+            res = studies.component_table(c, meta)
+        else:
+            res = studies.ase(c, meta)
+        out[name] = {"simulations": int(w.n_sims), "s": dt, "result": res}
+    return out
+
+
+def synth_mod():
+    from paper_2609_09643_amd import synth
+    return synth
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--sections", default="c2,c5", help="comma list of c2,c4,c5,fmt,online or 'none'")
+    ap.add_argument("--sections", default="c2,c5", help="comma list of c2,c4,c5,fmt,online,studies or 'none'")
     ap.add_argument("--c4-events", type=int, default=200_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", type=int, default=None)
@@ -312,6 +347,9 @@ def main():
     if "online" in secs:
         log("section online")
         extra["online"] = section_online(torch)
+    if "studies" in secs:
+        log("section studies")
+        extra["studies"] = section_studies(torch)
     if "fmt" in secs:
         log("section fmt")
         extra["fmt"] = section_fmt(torch)

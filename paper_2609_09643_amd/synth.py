@@ -527,3 +527,59 @@ def attainment_workload(traces=None, envelope=FIDELITY_ENVELOPES[0], points=None
             p[r]["online_sessions"] = n
         meta[r] = (ti, kind, n)
     return Workload("attainment", list(traces), pops, p), meta
+
+
+# ---------------------------------------------- ablations and capacity sweep
+
+# Six SRAM/HBM envelopes (tokens at 128 KiB) along the axes of Table VI.
+ABLATION_ENVELOPES = ((10_000, 30_000), (10_000, 50_000), (10_000, 100_000), (10_000, 200_000),
+                      (20_000, 50_000), (40_000, 50_000))
+# scoring x tiering: (policy, tide)
+COMPONENTS = (("lru", POLICY_LRU, 0), ("lru+tide", POLICY_LRU, 1), ("spear", POLICY_SPEAR, 0),
+              ("spear+tide", POLICY_SPEAR, 1))
+ASE_SLOTS = (4, 8, 16, 32, 64, 128, 256)
+STUDY_META_DTYPE = np.dtype([("trace", np.uint32), ("envelope", np.uint32), ("arm", np.uint32)])
+
+
+def _study_rows(traces, cells):
+    """cells: list of (trace, envelope (sram_tok, hbm_tok), arm, dict of
+    parameter overrides)."""
+    p = default_params(len(cells))
+    meta = np.zeros(len(cells), STUDY_META_DTYPE)
+    for r, (ti, env, ei, arm, over) in enumerate(cells):
+        p[r]["trace"], p[r]["lut"] = ti, ti
+        p[r]["cap_sram_B"] = env[0] * 128 * KIB
+        p[r]["cap_hbm_B"] = env[1] * 128 * KIB
+        for k, v in over.items():
+            p[r][k] = v
+        meta[r] = (ti, ei, arm)
+    return Workload("study", list(traces), [tr.turns for tr in traces], p), meta
+
+
+def dual_ablation(traces=None, envelope=FIDELITY_ENVELOPES[0]):
+    """Sec. III-D / Table V: SPEAR+TIDE with the unified register file (arm 0)
+    and with dual copies refreshed after every request and gap (1), every 8
+    requests (2) or at gap onsets (3), per trace."""
+    traces = fidelity_traces() if traces is None else traces
+    cells = [(ti, envelope, 0, sync, {"policy": POLICY_SPEAR, "tide": 1, "dual_sync": sync})
+             for ti in range(len(traces)) for sync in (DUAL_NONE, DUAL_EVERY, DUAL_EIGHT, DUAL_GAP)]
+    return _study_rows(traces, cells)
+
+
+def component_ablation(traces=None, envelopes=ABLATION_ENVELOPES):
+    """Scoring x tiering (the ablation beside Table IV): LRU, LRU+TIDE, SPEAR,
+    SPEAR+TIDE (arm = index in COMPONENTS) per trace and envelope."""
+    traces = fidelity_traces() if traces is None else traces
+    cells = [(ti, env, ei, a, {"policy": pol, "tide": tide})
+             for ti in range(len(traces)) for ei, env in enumerate(envelopes)
+             for a, (_, pol, tide) in enumerate(COMPONENTS)]
+    return _study_rows(traces, cells)
+
+
+def slot_sweep(traces=None, envelope=FIDELITY_ENVELOPES[0], slots=ASE_SLOTS):
+    """eq. (ase): SPEAR+TIDE with N session slots (arm = index in slots) per
+    trace."""
+    traces = fidelity_traces() if traces is None else traces
+    cells = [(ti, envelope, 0, a, {"policy": POLICY_SPEAR, "tide": 1, "n_slots": n})
+             for ti in range(len(traces)) for a, n in enumerate(slots)]
+    return _study_rows(traces, cells)
