@@ -281,7 +281,9 @@ int unison_score_fixed(void* hip_stream, uint32_t n, const uint8_t* turn, const 
  * Snapshot s holds x[idx[s][j]], y[idx[s][j]] for j < n_per (idx NULL: rows
  * s*n_per .. s*n_per+n_per-1, which must lie below n_x).  An index >= n_x
  * is not read: the snapshot's top1 is then 255 and its counts are void.
- * 2 <= n_per <= 4096. */
+ * x holds scores, never NaN (a NaN has no rank; its snapshot's counts are
+ * unspecified).  2 <= n_per <= 4096; from 256 entries on the counts come
+ * from sorting the snapshot in LDS (O(n log^2 n)), below it pair by pair. */
 int unison_kendall(void* hip_stream, uint32_t n_snap, uint32_t n_per, uint64_t n_x, const float* x,
                    const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1);
 

@@ -2,11 +2,12 @@
 // Kendall tau-b statistics of the ranking-fidelity study (Sec. IV-C, Sec. VI-F).
 //
 // The scorers are elementwise and HBM-bound (one thread per session, coalesced
-// loads, the hazard table in LDS).  The Kendall kernel gives each snapshot one
-// workgroup: the snapshot's (x, y) pairs are gathered into LDS once, each
-// thread owns rows i and walks j > i with all lanes of a wave reading the same
-// LDS word (a broadcast), so the O(n^2) pair classification runs from LDS at
-// VALU rate.
+// loads, the hazard table in LDS).  The Kendall kernels give each snapshot one
+// workgroup and gather its (x, y) pairs into LDS once.  Small snapshots are
+// classified pair by pair (each thread owns rows i and walks j > i with all
+// lanes of a wave reading the same LDS word, a broadcast); from 256 entries
+// on, a bitonic sort and a counting merge sort find the same counts in
+// O(n log^2 n).
 #include <hip/hip_runtime.h>
 
 #include "unison_device.h"
@@ -64,7 +65,8 @@ __global__ __launch_bounds__(256) void score_fixed_kernel(uint32_t n, const uint
 }
 
 constexpr int kKendallBlock = 256;
-constexpr uint32_t kKendallMax = 4096;  // 12 B of LDS per entry: 48 KiB per snapshot
+constexpr uint32_t kKendallMax = 4096;  // sort-based path: 20 B of LDS per entry, 80 KiB
+constexpr uint32_t kKendallSortFrom = 256;  // snapshots this large or larger are sorted
 
 __device__ __forceinline__ bool fbetter(float a, uint32_t ia, float b, uint32_t ib) {
   return a > b || (a == b && ia < ib);
@@ -184,6 +186,208 @@ __global__ __launch_bounds__(kKendallBlock) void kendall_kernel(uint32_t n_per, 
   }
 }
 
+// ---------------------------------------------- Kendall tau-b, sort-based
+
+// The same five pair counts in O(n log^2 n) per snapshot (Knight's method):
+// sort the pairs by (x, y); pairs tied in x, and in both, are counted from the
+// sorted runs; the discordant pairs are the inversions of the y sequence in
+// that order, counted while it is merge-sorted; pairs tied in y are counted
+// from the finally sorted y.  Concordant = all pairs minus the rest.
+constexpr int kSortBlock = 512;
+
+// Order-preserving u32 image of a float, -0 and +0 taken as equal (scores
+// are never NaN; a NaN has no place in the order).
+__device__ __forceinline__ uint32_t float_key(uint32_t b) {
+  if ((b & 0x7FFFFFFFu) == 0) b = 0;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ bool pair_less(uint32_t xa, uint64_t ya, uint32_t xb, uint64_t yb) {
+  return xa < xb || (xa == xb && ya < yb);
+}
+
+// Number of entries of the sorted run a[lo, lo + n) below v (lower bound), or
+// at most v (upper bound).
+__device__ __forceinline__ uint32_t count_below(const uint64_t* a, uint32_t lo, uint32_t n, uint64_t v) {
+  uint32_t l = 0, h = n;
+  while (l < h) {
+    const uint32_t m = (l + h) >> 1;
+    if (a[lo + m] < v) l = m + 1; else h = m;
+  }
+  return l;
+}
+__device__ __forceinline__ uint32_t count_upto(const uint64_t* a, uint32_t lo, uint32_t n, uint64_t v) {
+  uint32_t l = 0, h = n;
+  while (l < h) {
+    const uint32_t m = (l + h) >> 1;
+    if (a[lo + m] <= v) l = m + 1; else h = m;
+  }
+  return l;
+}
+
+__global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
+                                                                  uint64_t n_x, const float* x,
+                                                                  const uint64_t* y,
+                                                                  const uint32_t* idx,
+                                                                  uint64_t* counts, uint8_t* top1) {
+  extern __shared__ uint64_t s_dyn[];
+  uint64_t* s_ky = s_dyn;                                        // [P] y, then merge buffer A
+  uint64_t* s_yb = s_dyn + P;                                    // [P] merge buffer B
+  uint32_t* s_kx = reinterpret_cast<uint32_t*>(s_dyn + 2 * (size_t)P);  // [P] x keys
+  __shared__ uint64_t s_sum[4][kSortBlock / 64];
+  __shared__ float s_bx[kSortBlock / 64];
+  __shared__ uint32_t s_bxi[kSortBlock / 64], s_byi[kSortBlock / 64];
+  __shared__ uint64_t s_by[kSortBlock / 64];
+  __shared__ uint32_t s_bad;
+  const uint32_t snap = blockIdx.x;
+  const uint32_t tid = threadIdx.x;
+  const size_t base = (size_t)snap * n_per;
+  const uint32_t n = n_per;
+
+  // gather, both argmaxes (ties to the earlier position), padding that sorts last
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  float bx = 0.0f;
+  uint32_t bxi = kNone, byi = kNone;
+  uint64_t by = 0;
+  for (uint32_t i = tid; i < P; i += kSortBlock) {
+    if (i < n) {
+      size_t e = idx ? (size_t)idx[base + i] : base + i;
+      if (e >= n_x) {
+        s_bad = 1;
+        e = 0;
+      }
+      const float xv = x[e];
+      const uint64_t yv = y[e];
+      s_kx[i] = __float_as_uint(xv);
+      s_ky[i] = yv;
+      if (bxi == kNone || fbetter(xv, i, bx, bxi)) { bx = xv; bxi = i; }
+      if (byi == kNone || ubetter(yv, i, by, byi)) { by = yv; byi = i; }
+    } else {
+      s_kx[i] = 0xFFFFFFFFu;
+      s_ky[i] = ~0ull;
+    }
+  }
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    const float ox = __shfl_xor(bx, m);
+    const uint32_t oxi = __shfl_xor(bxi, m);
+    const uint64_t oy = __shfl_xor(by, m);
+    const uint32_t oyi = __shfl_xor(byi, m);
+    if (oxi != kNone && (bxi == kNone || fbetter(ox, oxi, bx, bxi))) { bx = ox; bxi = oxi; }
+    if (oyi != kNone && (byi == kNone || ubetter(oy, oyi, by, byi))) { by = oy; byi = oyi; }
+  }
+  if ((tid & 63u) == 0) {
+    s_bx[tid >> 6] = bx;
+    s_bxi[tid >> 6] = bxi;
+    s_by[tid >> 6] = by;
+    s_byi[tid >> 6] = byi;
+  }
+  __syncthreads();
+
+  uint64_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
+  {
+    for (uint32_t i = tid; i < n; i += kSortBlock) s_kx[i] = float_key(s_kx[i]);
+    __syncthreads();
+    // bitonic sort of the P pairs by (x, y)
+    for (uint32_t k = 2; k <= P; k <<= 1) {
+      for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+        for (uint32_t t = tid; t < (P >> 1); t += kSortBlock) {
+          const uint32_t i = ((t & ~(j - 1)) << 1) | (t & (j - 1));
+          const uint32_t l = i + j;
+          const uint32_t xa = s_kx[i], xb = s_kx[l];
+          const uint64_t ya = s_ky[i], yb = s_ky[l];
+          const bool up = (i & k) == 0;
+          if (up ? pair_less(xb, yb, xa, ya) : pair_less(xa, ya, xb, yb)) {
+            s_kx[i] = xb;
+            s_kx[l] = xa;
+            s_ky[i] = yb;
+            s_ky[l] = ya;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    // pairs tied in x, and in x and y: each entry counts the earlier entries of its run
+    for (uint32_t i = tid; i < n; i += kSortBlock) {
+      const uint32_t xv = s_kx[i];
+      const uint64_t yv = s_ky[i];
+      uint32_t l = 0, h = i;
+      while (l < h) {
+        const uint32_t m = (l + h) >> 1;
+        if (s_kx[m] < xv) l = m + 1; else h = m;
+      }
+      t_x += i - l;
+      h = i;
+      while (l < h) {
+        const uint32_t m = (l + h) >> 1;
+        if (s_ky[m] < yv) l = m + 1; else h = m;
+      }
+      t_xy += i - l;
+    }
+    // merge sort of y in that order; a right-run entry is discordant with every
+    // larger entry of its left run
+    uint64_t* src = s_ky;
+    uint64_t* dst = s_yb;
+    for (uint32_t w = 1; w < P; w <<= 1) {
+      for (uint32_t p = tid; p < P; p += kSortBlock) {
+        const uint32_t b0 = p & ~(2 * w - 1);
+        const uint32_t off = p - b0;
+        const uint64_t v = src[p];
+        if (off < w) {
+          dst[b0 + off + count_below(src, b0 + w, w, v)] = v;
+        } else {
+          const uint32_t u = count_upto(src, b0, w, v);
+          dst[b0 + (off - w) + u] = v;
+          inv += w - u;
+        }
+      }
+      __syncthreads();
+      uint64_t* tmp = src;
+      src = dst;
+      dst = tmp;
+    }
+    // pairs tied in y
+    for (uint32_t i = tid; i < n; i += kSortBlock) t_y += i - count_below(src, 0, i, src[i]);
+  }
+
+  uint64_t v[4] = {inv, t_x, t_y, t_xy};
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) v[c] += __shfl_xor(v[c], m);
+    if ((tid & 63u) == 0) s_sum[c][tid >> 6] = v[c];
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t tot[4] = {0, 0, 0, 0};
+    for (int w = 0; w < kSortBlock / 64; ++w)
+      for (int c = 0; c < 4; ++c) tot[c] += s_sum[c][w];
+    const uint64_t pairs = (uint64_t)n * (n - 1) / 2;
+    const uint64_t d = tot[0], both = tot[3];
+    const uint64_t only_x = tot[1] - both, only_y = tot[2] - both;
+    counts[(size_t)snap * 5 + 0] = pairs - d - only_x - only_y - both;
+    counts[(size_t)snap * 5 + 1] = d;
+    counts[(size_t)snap * 5 + 2] = only_x;
+    counts[(size_t)snap * 5 + 3] = only_y;
+    counts[(size_t)snap * 5 + 4] = both;
+    float fx = s_bx[0];
+    uint32_t fxi = s_bxi[0], fyi = s_byi[0];
+    uint64_t fy = s_by[0];
+    for (int w = 1; w < kSortBlock / 64; ++w) {
+      if (s_bxi[w] != kNone && (fxi == kNone || fbetter(s_bx[w], s_bxi[w], fx, fxi))) {
+        fx = s_bx[w];
+        fxi = s_bxi[w];
+      }
+      if (s_byi[w] != kNone && (fyi == kNone || ubetter(s_by[w], s_byi[w], fy, fyi))) {
+        fy = s_by[w];
+        fyi = s_byi[w];
+      }
+    }
+    top1[snap] = s_bad ? (uint8_t)255 : (uint8_t)(fxi == fyi);
+  }
+}
+
 hipError_t launch_ema_replay(uint32_t n, uint32_t max_hist, const uint64_t* gaps,
                              const uint8_t* n_hist, uint32_t b_g, uint64_t tau, float* g,
                              uint64_t* gq, hipStream_t s) {
@@ -215,9 +419,17 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
                           const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1,
                           hipStream_t s) {
   if (n_snap == 0) return hipSuccess;
-  const size_t lds = (size_t)(n_per ? n_per : 1) * (sizeof(uint64_t) + sizeof(float));
-  hipLaunchKernelGGL(kendall_kernel, dim3(n_snap), dim3(kKendallBlock), lds, s, n_per, n_x, x, y,
-                     idx, counts, top1);
+  if (n_per < kKendallSortFrom) {
+    const size_t lds = (size_t)(n_per ? n_per : 1) * (sizeof(uint64_t) + sizeof(float));
+    hipLaunchKernelGGL(kendall_kernel, dim3(n_snap), dim3(kKendallBlock), lds, s, n_per, n_x, x, y,
+                       idx, counts, top1);
+  } else {
+    uint32_t P = 2;
+    while (P < n_per) P <<= 1;
+    const size_t lds = (size_t)P * (2 * sizeof(uint64_t) + sizeof(uint32_t));
+    hipLaunchKernelGGL(kendall_sort_kernel, dim3(n_snap), dim3(kSortBlock), lds, s, n_per, P, n_x,
+                       x, y, idx, counts, top1);
+  }
   return hipGetLastError();
 }
 

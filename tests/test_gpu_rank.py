@@ -102,6 +102,27 @@ def test_kendall_ranking_snapshots(U, rs):
     assert np.array_equal(t[sample], ot)
 
 
+@pytest.mark.parametrize("n_per", [256, 257, 1000, 2048, 4095, 4096])
+def test_kendall_sorted_path_heavy_ties(U, n_per):
+    """From 256 entries the counts come from sorting: few distinct values, the
+    extremes of both scores, -0 beside +0, and padding to a power of two."""
+    rng = np.random.default_rng(1000 + n_per)
+    n_snap = 5
+    x = rng.integers(0, 6, (n_snap, n_per)).astype(np.float32)
+    y = rng.integers(0, 5, (n_snap, n_per)).astype(np.uint64)
+    x[0, ::7] = np.inf
+    x[1, ::5] = -0.0
+    x[1, 1::5] = 0.0
+    y[2, ::3] = 2 ** 64 - 1
+    x[3] = rng.standard_normal(n_per).astype(np.float32)       # all distinct, both signs
+    y[3] = rng.integers(0, 2 ** 63, n_per).astype(np.uint64)
+    x[4] = 1.0                                                  # one x value
+    c, t = U.kendall(dev(U, x.ravel()), dev(U, y.ravel(), np.uint64), None, n_snap, n_per)
+    oc, ot = oracle.kendall(x, y)
+    assert np.array_equal(U._host(c, np.uint64), oc)
+    assert np.array_equal(t.cpu().numpy(), ot)
+
+
 def test_kendall_rejects_out_of_range_index(U):
     x = np.arange(10, dtype=np.float32)
     y = np.arange(10, dtype=np.uint64)
