@@ -205,9 +205,14 @@ typedef struct {
   const uint32_t* sess_kvb;    /* DEVICE */
 } unison_trace_batch;
 
-/* Registers the traces (the arrays stay borrowed).  Errors: UNISON_E_INVALID
- * (count differs from the dims, offsets not monotone), UNISON_E_CAPACITY (a
- * trace has more sessions than dims.max_sessions). */
+/* Registers the traces (the arrays stay borrowed) and checks the event format
+ * of each once, on a host copy of its events (session id in range, kind <=
+ * DONE, times non-decreasing, every session's turns in order, prefixes
+ * non-decreasing): a simulation then stops at its trace's first malformed
+ * event and reports it through counters.error.  Synchronises the stream.
+ * Errors: UNISON_E_INVALID (count differs from the dims, offsets not
+ * monotone), UNISON_E_CAPACITY (a trace has more sessions than
+ * dims.max_sessions), UNISON_E_HIP. */
 int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb);
 
 /* eq. (hazard): counts d(t) = #{T = t+1} and n(t) = #{T > t}, t = 0..50, over

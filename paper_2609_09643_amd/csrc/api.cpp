@@ -48,7 +48,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Workspace layout; offsets in bytes from the workspace base.
 struct Layout {
-  size_t params, ev_off, sess_off, lut_d, lut_n, state, counters, hcount, mg, gq, len, last, next,
+  size_t params, ev_off, first_bad, sess_off, lut_d, lut_n, state, counters, hcount, mg, gq, len, last, next,
       views, log, scratch, total;
 };
 
@@ -62,6 +62,7 @@ bool make_layout(const unison_dims& d, Layout& L) {
   };
   L.params = take(sizeof(unison_sim_params) * d.n_sims);
   L.ev_off = take(sizeof(uint64_t) * (d.n_traces + 1));
+  L.first_bad = take(sizeof(uint64_t) * d.n_traces);
   L.sess_off = take(sizeof(uint64_t) * (d.n_traces + 1));
   L.lut_d = take(sizeof(uint32_t) * kLut * d.n_luts);
   L.lut_n = take(sizeof(uint32_t) * kLut * d.n_luts);
@@ -80,6 +81,37 @@ bool make_layout(const unison_dims& d, Layout& L) {
   return true;
 }
 
+// Index of the first event of a trace that breaks the event format, or ~0:
+// a session id past the trace's sessions, a kind above DONE, a time before
+// the previous event's; an ARRIVE of turn 0 for a session already seen, of
+// turn k >= 1 that does not follow the GAP_START of turn k - 1 or shortens the
+// prefix; a GAP_START or DONE of a session that is not being served.  These
+// depend on the trace alone, so they are checked once per load.
+uint64_t first_bad_event(const uint64_t* t, const uint32_t* sid, const uint32_t* info,
+                         const uint32_t* len, uint64_t n, uint32_t n_sess) {
+  struct Sess {
+    uint32_t phase, turn, len;  // phase: 0 unseen, 1 served, 2 in a gap, 3 completed
+  };
+  std::vector<Sess> st(n_sess, Sess{0, 0, 0});
+  uint64_t prev = 0;
+  for (uint64_t e = 0; e < n; ++e) {
+    const uint32_t s = sid[e], kind = info[e] >> 24, turn = info[e] & 0xFFFFFFu;
+    if (s >= n_sess || kind > 2 || t[e] < prev) return e;
+    prev = t[e];
+    Sess& x = st[s];
+    if (kind == 0) {
+      if (turn == 0 ? x.phase != 0 : (x.phase != 2 || turn != x.turn + 1 || len[e] < x.len)) return e;
+      x.phase = 1;
+      x.turn = turn;
+      x.len = len[e];
+    } else {
+      if (x.phase != 1) return e;
+      x.phase = kind == 1 ? 2 : 3;
+    }
+  }
+  return ~0ull;
+}
+
 bool dims_ok(const unison_dims* d) {
   return d && d->n_sims >= 1 && d->n_traces >= 1 && d->n_luts >= 1 && d->max_sessions >= 1 &&
          d->max_sessions <= UNISON_MAX_SESSIONS && d->views <= 1;
@@ -94,7 +126,7 @@ struct unison_ctx {
   size_t ws_bytes;
   Layout L;
   unison_trace_batch tb;
-  std::vector<uint64_t> h_ev_off, h_sess_off;
+  std::vector<uint64_t> h_ev_off, h_sess_off, h_first_bad;
   std::vector<unison_sim_params> h_params;
   std::vector<uint8_t> lut_set;
   bool traces_loaded = false, params_set = false, ran = false;
@@ -217,6 +249,39 @@ int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
   rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise after offsets");
   if (rc) return rc;
   ctx->time44 = h_max < (1ull << 44) - 1;
+  // the event format, checked once per trace on a host copy of its events
+  ctx->h_first_bad.assign(nt, ~0ull);
+  std::vector<uint64_t> ht;
+  std::vector<uint32_t> hs, hi, hl;
+  for (uint32_t i = 0; i < nt; ++i) {
+    const uint64_t b = tb->ev_offset[i], n = tb->ev_offset[i + 1] - b;
+    if (n == 0) continue;
+    ht.resize(n);
+    hs.resize(n);
+    hi.resize(n);
+    hl.resize(n);
+    rc = ctx->hip(hipMemcpyAsync(ht.data(), tb->ev_t_ns + b, n * sizeof(uint64_t), hipMemcpyDeviceToHost,
+                                 ctx->stream), "copy trace times");
+    if (rc == UNISON_OK)
+      rc = ctx->hip(hipMemcpyAsync(hs.data(), tb->ev_sid + b, n * sizeof(uint32_t), hipMemcpyDeviceToHost,
+                                   ctx->stream), "copy trace sessions");
+    if (rc == UNISON_OK)
+      rc = ctx->hip(hipMemcpyAsync(hi.data(), tb->ev_info + b, n * sizeof(uint32_t), hipMemcpyDeviceToHost,
+                                   ctx->stream), "copy trace kinds");
+    if (rc == UNISON_OK)
+      rc = ctx->hip(hipMemcpyAsync(hl.data(), tb->ev_len + b, n * sizeof(uint32_t), hipMemcpyDeviceToHost,
+                                   ctx->stream), "copy trace lengths");
+    if (rc == UNISON_OK) rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise trace copy");
+    if (rc) return rc;
+    ctx->h_first_bad[i] = first_bad_event(ht.data(), hs.data(), hi.data(), hl.data(), n,
+                                          (uint32_t)(tb->sess_offset[i + 1] - tb->sess_offset[i]));
+  }
+  rc = ctx->hip(hipMemcpyAsync(ctx->at<uint64_t>(ctx->L.first_bad), ctx->h_first_bad.data(),
+                               sizeof(uint64_t) * nt, hipMemcpyHostToDevice, ctx->stream),
+                "copy format checks");
+  if (rc) return rc;
+  rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise format checks");
+  if (rc) return rc;
   ctx->traces_loaded = true;
   return UNISON_OK;
 }
@@ -292,6 +357,7 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   std::memset(&a, 0, sizeof a);
   a.params = ctx->at<unison_sim_params>(ctx->L.params);
   a.ev_off = ctx->at<uint64_t>(ctx->L.ev_off);
+  a.first_bad = ctx->at<uint64_t>(ctx->L.first_bad);
   a.sess_off = ctx->at<uint64_t>(ctx->L.sess_off);
   a.ev_t = ctx->tb.ev_t_ns;
   a.ev_sid = ctx->tb.ev_sid;

@@ -857,18 +857,12 @@ __device__ __forceinline__ void release(Tab& T, Scalars& S, uint32_t sid) {
   T.set_meta(sid, with_tier(m, kTierNone));
 }
 
-// Algorithm 1 over the simulation's events [next_event, next_event + max_events).
-// UNI: every lane replays the same trace from the same event (one simulation
-// per workgroup), so the event record is read as uniform values that live in
-// SGPRs: scalar decode and scalar branches on the event kind.
+// Events [e_io, end) of one simulation; e_io ends at end.
 template <uint32_t POL, uint32_t SMODE, bool UNI, class Tab>
-__device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
-                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& next_event,
-                           uint64_t max_events) {
+__device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
+                          Scalars& S, Cnt& C, const LogSink& L, uint64_t& e_io, uint64_t end) {
   using PT = Pol<POL, SMODE>;
-  uint64_t e = next_event;
-  const uint64_t end = (e >= tr.n_ev || tr.n_ev - e < max_events) ? tr.n_ev : e + max_events;
-  if (e >= end) return;
+  uint64_t e = e_io;
   Ev cur = load_ev<PT::belady>(tr, e);
   // victim-digest weight of event e, (2e + 1) * 0x9e3779b97f4a7c15, stepped per event
   constexpr uint64_t kGolden = 0x9e3779b97f4a7c15ull;
@@ -884,11 +878,6 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     const uint32_t cur_len = UNI ? uni32(cur.len) : cur.len;
     const uint64_t cur_next = (UNI && PT::belady) ? uni64(cur.next) : cur.next;
     const uint32_t ev = (uint32_t)e;
-    if (sid >= tr.n_sess || now < S.prev_t || kind > kDone) {
-      C.error = e + 1;
-      break;
-    }
-    S.prev_t = now;
 
     // timeout policy: TTL timers that fired since the previous event
     if constexpr (PT::timeout) {
@@ -903,30 +892,22 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
 
     // Alg. 1: write e into R; on gap_end update the EMA
     Entry x;
-    uint32_t ph, tier0, len_prev = 0;
+    uint32_t tier0, len_prev = 0;
     bool prefetched = false;
     if (kind == kArrive) {
       x = T.read(sid);
-      ph = meta_phase(x.meta);
       tier0 = meta_tier(x.meta);
       prefetched = (x.meta & kPrefetched) != 0;
       len_prev = x.len;
-      bool bad;
       if (turn == 0) {
-        bad = ph != kUnseen;
         x.g = 0.0f;
         x.gq = 0;
         x.len = 0;
         len_prev = 0;
       } else {
-        bad = ph != kGap || turn != meta_turn(x.meta) + 1 || cur_len < x.len;
         const uint64_t gap = now - x.last;  // eq. (gap)
         x.g = ema_f32(x.g, gap);
         if constexpr (PT::fixed) x.gq = ema_int(x.gq, gap, P.b_g, P.tau_ns);
-      }
-      if (bad) {
-        C.error = e + 1;
-        break;
       }
       x.meta = make_meta(kServing, tier0, turn);
       x.last = now;
@@ -939,12 +920,7 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
       T.set_turn(sid, x.meta, K);
     } else {
       T.read_end(sid, x);
-      ph = meta_phase(x.meta);
       tier0 = meta_tier(x.meta);
-      if (ph != kServing) {
-        C.error = e + 1;
-        break;
-      }
       x.meta = make_meta(kind == kGapStart ? kGap : kDoneP, tier0, meta_turn(x.meta));
       T.write_end(sid, x.meta, now, kind == kGapStart ? cur_next : ~0ull);
       // an online hazard table counts the completed session before the scan
@@ -1138,7 +1114,27 @@ __device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, 
     C.events++;
     cur = nxt;
   }
+  e_io = e;
+}
+
+// Algorithm 1 over the simulation's events [next_event, next_event + max_events).
+// UNI: every lane replays the same trace from the same event (one simulation
+// per workgroup), so the event record is read as uniform values that live in
+// SGPRs: scalar decode and scalar branches on the event kind.
+// bad_at is the index of the trace's first event that breaks the event format
+// (found once when the traces are loaded, ~0 if none): the run stops there and
+// reports it, so the loop itself checks nothing.
+template <uint32_t POL, uint32_t SMODE, bool UNI, class Tab>
+__device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
+                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& next_event,
+                           uint64_t max_events, uint64_t bad_at) {
+  uint64_t e = next_event;
+  uint64_t end = (e >= tr.n_ev || tr.n_ev - e < max_events) ? tr.n_ev : e + max_events;
+  const bool stops = bad_at < end;
+  if (stops) end = bad_at;
+  if (e < end) run_range<POL, SMODE, UNI>(T, P, K, tr, S, C, L, e, end);
   next_event = e;
+  if (stops) C.error = bad_at + 1;
 }
 
 // The simulation's hazard table into LDS: the counts of its fixed table, or
@@ -1272,7 +1268,8 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
     if (n_sess > (uint32_t)(G * EPL) || P.dual_sync) {
       C.error = ~0ull;  // the launcher picks a variant that holds the trace (and its copies)
     } else {
-      run_events<POL, SMODE, false>(T, P, K, tr, S, C, L, next_event, a.max_events);
+      run_events<POL, SMODE, false>(T, P, K, tr, S, C, L, next_event, a.max_events,
+                                    a.first_bad[P.trace]);
     }
   }
 
@@ -1428,7 +1425,8 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   if (C.error == 0) {
     unison_sim_params Pv = P;
     pin_vgpr(Pv);
-    run_events<POL, SMODE, true>(T, Pv, K, tr, S, C, L, next_event, a.max_events);
+    run_events<POL, SMODE, true>(T, Pv, K, tr, S, C, L, next_event, a.max_events,
+                                 a.first_bad[P.trace]);
   }
   __syncthreads();
   if constexpr (IN_LDS) {

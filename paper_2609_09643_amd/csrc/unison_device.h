@@ -154,6 +154,7 @@ struct SimState {
 struct SimArgs {
   const unison_sim_params* params;
   const uint64_t* ev_off;
+  const uint64_t* first_bad;  // [n_traces] first malformed event of each trace, ~0 if none
   const uint64_t* sess_off;
   const uint64_t* ev_t;
   const uint32_t* ev_sid;

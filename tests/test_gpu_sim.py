@@ -207,6 +207,48 @@ def test_bad_trace_is_reported():
     assert int(got[0]["error"]) == 5
 
 
+BAD_TRACES = {
+    # name: events (t, sid, kind, turn, len) with one violation at index 4
+    "turn_skipped": [(10, 0, 0, 0, 3), (20, 0, 1, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                     (50, 0, 0, 2, 5), (60, 0, 1, 2, 0)],
+    "time_goes_back": [(10, 0, 0, 0, 3), (20, 0, 1, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                       (35, 0, 0, 1, 5), (60, 0, 2, 1, 0)],
+    "sid_out_of_range": [(10, 0, 0, 0, 3), (20, 0, 1, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                         (50, 7, 0, 0, 5), (60, 0, 2, 1, 0)],
+    "unknown_kind": [(10, 0, 0, 0, 3), (20, 0, 1, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                     (50, 0, 3, 0, 0), (60, 0, 2, 1, 0)],
+    "gap_while_in_gap": [(10, 0, 0, 0, 3), (20, 0, 1, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                         (50, 0, 1, 0, 0), (60, 0, 2, 1, 0)],
+    "prefix_shrinks": [(10, 0, 0, 0, 3), (20, 0, 1, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                       (50, 0, 0, 1, 2), (60, 0, 2, 1, 0)],
+    "arrive_after_done": [(10, 0, 0, 0, 3), (20, 0, 2, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                          (50, 0, 0, 1, 5), (60, 0, 2, 1, 0)],
+    "first_arrival_twice": [(10, 0, 0, 0, 3), (20, 0, 1, 0, 0), (30, 1, 0, 0, 4), (40, 1, 1, 0, 0),
+                            (50, 0, 0, 0, 5), (60, 0, 2, 0, 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(BAD_TRACES))
+def test_each_format_violation_stops_at_its_event(name):
+    from paper_2609_09643_amd.unison import E_BAD_TRACE, UnisonError
+    tr = trace_from_events(BAD_TRACES[name], 2)
+    p = synth.default_params(2)
+    p["policy"] = [POLICY_SPEAR, POLICY_LRU]
+    p["cap_sram_B"], p["cap_hbm_B"] = 1 << 20, 1 << 30
+    w = synth.Workload("bad", [tr], [tr.turns], p)
+    for v in (None, 9, 11):
+        s = Sim(w, variant=v)
+        s.run(max_events=3)
+        assert int(s.counters()["error"][0]) == 0          # not reached yet
+        s.run(flags=1)
+        with pytest.raises(UnisonError) as e:
+            s.counters()
+        assert e.value.code == E_BAD_TRACE
+        got = s.counters(check=False)
+        compare_counters(got, oracle_counters_allow_error(w), label="%s variant %s" % (name, v))
+        assert int(got[1]["error"]) == 5
+
+
 def oracle_counters_allow_error(w):
     D, N = oracle.luts_for(w)
     out = []
