@@ -447,12 +447,17 @@ int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t*
   if (!ctx || !d_out || !n_out) return UNISON_E_INVALID;
   if (sim >= ctx->dims.n_sims) return ctx->fail(UNISON_E_INVALID, "sim %u", sim);
   if (!ctx->ran) return ctx->fail(UNISON_E_NOT_READY, "no run on this context yet");
-  const uint32_t* src = ctx->at<uint32_t>(ctx->L.hcount) + (size_t)sim * 2 * kLut;
-  int rc = ctx->hip(hipMemcpyAsync(d_out, src, sizeof(uint32_t) * kLut, hipMemcpyDeviceToHost,
+  // an online table's counts are in the workspace; a fixed table's are its own
+  const unison_sim_params& p = ctx->h_params[sim];
+  const uint32_t* src_d = p.hazard_online ? ctx->at<uint32_t>(ctx->L.hcount) + (size_t)sim * 2 * kLut
+                                          : ctx->at<uint32_t>(ctx->L.lut_d) + (size_t)p.lut * kLut;
+  const uint32_t* src_n = p.hazard_online ? src_d + kLut
+                                          : ctx->at<uint32_t>(ctx->L.lut_n) + (size_t)p.lut * kLut;
+  int rc = ctx->hip(hipMemcpyAsync(d_out, src_d, sizeof(uint32_t) * kLut, hipMemcpyDeviceToHost,
                                    ctx->stream),
                     "copy hazard counts d");
   if (rc) return rc;
-  rc = ctx->hip(hipMemcpyAsync(n_out, src + kLut, sizeof(uint32_t) * kLut, hipMemcpyDeviceToHost,
+  rc = ctx->hip(hipMemcpyAsync(n_out, src_n, sizeof(uint32_t) * kLut, hipMemcpyDeviceToHost,
                                ctx->stream),
                 "copy hazard counts n");
   if (rc) return rc;

@@ -1156,10 +1156,12 @@ __device__ __forceinline__ void load_hazard(const SimArgs& a, const unison_sim_p
   }
 }
 
-// The table's counts at the end of the launch, for a later CONTINUE and for
-// unison_read_hazard.
-__device__ __forceinline__ void store_hazard(const SimArgs& a, uint32_t sim, const KeyCtx& K,
-                                             uint32_t lane, uint32_t width) {
+// An online table's counts at the end of the launch, for a later CONTINUE
+// and for unison_read_hazard (a fixed table never changes: nothing to store).
+__device__ __forceinline__ void store_hazard(const SimArgs& a, const unison_sim_params& P,
+                                             uint32_t sim, const KeyCtx& K, uint32_t lane,
+                                             uint32_t width) {
+  if (!P.hazard_online) return;
   uint32_t* out = a.hcount + (size_t)sim * 2 * kLut;
   for (uint32_t t = lane; t < kLut; t += width) {
     out[t] = K.hd[t];
@@ -1284,7 +1286,7 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
       if constexpr (PT::belady) a.t_next[tb + s] = T.next[j];
     }
   }
-  store_hazard(a, sim, K, lane, G);
+  store_hazard(a, P, sim, K, lane, G);
   if (lane == 0) {
     finish_costs(S, P, C);
     store_scalars(a.state[sim], S, next_event);
@@ -1438,7 +1440,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
       a.t_len[tb + i] = T.len[i];
     }
   }
-  store_hazard(a, sim, K, tid, BLOCK);
+  store_hazard(a, P, sim, K, tid, BLOCK);
   if (tid == 0) {
     finish_costs(S, P, C);
     store_scalars(a.state[sim], S, next_event);
