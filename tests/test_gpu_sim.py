@@ -125,6 +125,18 @@ def test_c4_large_live_set_prefix():
     assert int(got[0]["evict"]) > 0 and int(got[0]["score_evals"]) > 10_000_000
 
 
+def test_c4_longer_prefix_in_the_timed_configuration():
+    """The 65,536-session table deep into its trace (40,000 events, tables of
+    ~10,000 entries), on the variant the bench times, across a CONTINUE."""
+    w = synth.c4_large(n_traces=1)
+    ww = subset(w, [0])
+    say("c4: 1 sim, 40,000 events in two launches (the oracle needs ~20 s)")
+    s = Sim(ww)
+    s.run(max_events=25_000)
+    s.run(flags=1, max_events=15_000)
+    compare_counters(s.counters(), oracle_counters(ww, max_events=40_000), label="c4 40k")
+
+
 def edge_workload(traces, rows):
     luts = [np.array([1, 2, 2, 3, 30, 51, 60], np.uint32), None]
     return synth.Workload("edge", traces, luts, rows, flat_luts=[(1, 3, 7)])
