@@ -120,10 +120,19 @@ def section_c2(torch, U, synth, steps):
     per, _ = time_launches(torch, sim.run, steps, 1)
     c = sim.counters()
     ms = float(np.median(per))
-    ev = float(c["events"].sum())
-    ev_s = float(c["score_evals"].sum())
+    sec = ms / 1e3
     return {"workload": "c2 paper-scale: 1,415 sessions, 33,596 turns, 4 policies",
-            "ms_per_run": ms, "events_per_s": ev / (ms / 1e3), "evals_per_s": ev_s / (ms / 1e3)}
+            "ms_per_run": ms, **_domain_rates(c, sec)}
+
+
+def _domain_rates(c, sec):
+    """Rates of a workgroup-kernel run.  Those kernels visit resident
+    entries only (no other entry can be a victim or a migrant), so the table-
+    domain evals of the scan counter are the paper's scan work, not key
+    computations; the resident-domain rate is what the kernel evaluates."""
+    return {"events_per_s": float(c["events"].sum()) / sec,
+            "table_evals_per_s": float(c["score_evals"].sum()) / sec,
+            "resident_evals_per_s": float(c["resident_evals"].sum()) / sec}
 
 
 def section_c4(torch, U, synth, max_events):
@@ -134,13 +143,12 @@ def section_c4(torch, U, synth, max_events):
     per, _ = time_launches(torch, lambda: sim.run(max_events=max_events), 1, 1)
     c = sim.counters()
     ms = float(per[0])
-    ab = algorithmic_bytes(w.params, c)
+    sec = ms / 1e3
+    ev = float(c["events"].sum())
     return {"workload": "c4 large live set: 64 sims x 65,536 sessions, first %d events each"
                         % max_events,
-            "ms_per_run": ms, "events_per_s": float(c["events"].sum()) / (ms / 1e3),
-            "evals_per_s": float(c["score_evals"].sum()) / (ms / 1e3),
-            "algorithmic_GBps": ab / (ms / 1e3) / 1e9,
-            "hbm_frac_algorithmic": ab / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}
+            "ms_per_run": ms, **_domain_rates(c, sec),
+            "us_per_event_per_sim": sec * 1e6 / (ev / w.n_sims)}
 
 
 def section_c5(torch, U, synth, steps):

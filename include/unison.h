@@ -236,8 +236,13 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
  * simulation starts from an empty pool.  policy_override is a
  * UNISON_POLICY_* value applied to all simulations, or UNISON_POLICY_PARAMS.
  * A batch with a dual-design row runs on the copies' kernel (variant 11).
+ * Tables above the LDS-resident size run on workgroup kernels that keep one
+ * bit of LDS per session (the residency bits their scans visit): 128 KiB at
+ * UNISON_MAX_SESSIONS.
  * Asynchronous.  Errors: UNISON_E_NOT_READY, UNISON_E_INVALID (also: a
- * register-table variant forced on a batch with a dual-design row). */
+ * register-table variant forced on a batch with a dual-design row),
+ * UNISON_E_CAPACITY (the largest trace exceeds the chosen kernel variant,
+ * e.g. on a device with less LDS per workgroup than the bits need). */
 int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64_t max_events);
 
 /* Copies counters of simulations [first, first+n) to HOST `dst`; synchronises

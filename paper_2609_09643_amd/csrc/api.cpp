@@ -19,6 +19,7 @@
 namespace unison {
 hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream, int force_variant);
 uint32_t sim_variant_capacity(int v);
+int sim_auto_variant(uint32_t max_sess);
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
                                 hipStream_t stream);
 hipError_t launch_max_time(const uint64_t* t, const uint64_t* next, uint64_t n, uint64_t* out,
@@ -394,6 +395,12 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   if (v >= 0 && (sim_variant_capacity(v) == 0 || sim_variant_capacity(v) < ctx->max_sess_batch))
     return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds %u sessions < %u", v,
                      sim_variant_capacity(v), ctx->max_sess_batch);
+  if (v < 0) {
+    v = sim_auto_variant(ctx->max_sess_batch);
+    if (sim_variant_capacity(v) < ctx->max_sess_batch)
+      return ctx->fail(UNISON_E_CAPACITY, "%u sessions exceed every kernel variant (largest %u)",
+                       ctx->max_sess_batch, sim_variant_capacity(v));
+  }
   int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->stream, v), "launch simulation");
   if (rc == UNISON_OK) ctx->ran = true;
   return rc;

@@ -451,7 +451,6 @@ template <int BLOCK, uint32_t POL, uint32_t SMODE, bool VIEWS>
 struct MemTable {
   using PT = Pol<POL, SMODE>;
   static constexpr int NW = BLOCK / 64;
-  static constexpr int UNROLL = 4;
   static constexpr bool kViews = VIEWS;  // instantiated with the dual design's copies
   uint64_t* mg;
   uint64_t* gq;
@@ -471,6 +470,23 @@ struct MemTable {
   uint32_t hi;        // entries [0, hi) can be in the table
   uint32_t parity;
   Cand* red;          // LDS [2][NW]
+  // Residency bits of this thread's entries (sid = tid + k * BLOCK): bit
+  // k % 32 of LDS word res[(k / 32) * BLOCK + tid].  Only the owning thread
+  // reads or writes its words, so they need no barrier; the scans visit set
+  // bits only, since no other entry can be a victim or a migrant.
+  uint32_t* res;
+
+  // Keeps the owner's residency bit in step with the tier in meta m.
+  __device__ __forceinline__ void mark(uint32_t sid, uint32_t m) {
+    if ((sid & (BLOCK - 1u)) == tid) {
+      const uint32_t k = sid / BLOCK;
+      uint32_t* w = res + (k >> 5) * BLOCK + tid;
+      const uint32_t bit = 1u << (k & 31u);
+      *w = meta_tier(m) != kTierNone ? (*w | bit) : (*w & ~bit);
+    }
+  }
+  // Words per thread that cover entries [0, hi).
+  __device__ __forceinline__ uint32_t res_words() const { return (hi + 32u * BLOCK - 1u) / (32u * BLOCK); }
 
   __device__ __forceinline__ void event_begin() { __syncthreads(); }
   __device__ __forceinline__ void grow(uint32_t h) { hi = h; }
@@ -511,6 +527,7 @@ struct MemTable {
   // them; reads end with a barrier and each event starts with one, so no wave
   // writes an entry that another wave has still to read.
   __device__ __forceinline__ void write(uint32_t sid, const Entry& e) {
+    mark(sid, e.meta);
     mg[sid] = (uint64_t)e.meta | ((uint64_t)__float_as_uint(e.g) << 32);
     if constexpr (PT::fixed) gq[sid] = e.gq;
     len[sid] = e.len;
@@ -518,6 +535,7 @@ struct MemTable {
     if constexpr (PT::belady) next[sid] = e.next;
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) {
+    mark(sid, m);
     const uint64_t x = mg[sid];
     mg[sid] = (x & 0xFFFFFFFF00000000ull) | m;
   }
@@ -554,10 +572,12 @@ struct MemTable {
     const uint64_t* l = last;
     const uint64_t* n = next;
     if (VIEWS && src >= 0) {
-      x = vmg[src][i];
-      q = vgq[src];
-      l = vlast[src];
-      n = vnext[src];
+      // selects rather than an indexed pointer array, which would live in scratch
+      const bool c1 = src != 0;
+      x = (c1 ? vmg[1] : vmg[0])[i];
+      q = c1 ? vgq[1] : vgq[0];
+      l = c1 ? vlast[1] : vlast[0];
+      n = c1 ? vnext[1] : vnext[0];
     }
     const uint32_t m = (uint32_t)x;
     const float gv = __uint_as_float((uint32_t)(x >> 32));
@@ -584,19 +604,14 @@ struct MemTable {
   template <bool MAX>
   __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx& K) {
     Cand c = MAX ? cand_none_max() : cand_none_min();
-    for (uint32_t base = tid; base < hi; base += UNROLL * BLOCK) {
-      uint64_t x[UNROLL];
-#pragma unroll
-      for (int u = 0; u < UNROLL; ++u) {
-        const uint32_t i = base + u * BLOCK;
-        x[u] = i < hi ? mg[i] : 0ull;
-      }
-#pragma unroll
-      for (int u = 0; u < UNROLL; ++u) {
-        const uint32_t i = base + u * BLOCK;
-        const uint32_t m = (uint32_t)x[u];
-        const bool ok = i < hi && evictable(m) && (tier == 0 || meta_tier(m) == tier);
-        const uint64_t k = key_at(K, i < hi ? i : 0u, x[u]);
+    const uint32_t nw = res_words();
+    for (uint32_t w = 0; w < nw; ++w) {
+      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
+        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
+        const uint64_t x = mg[i];
+        const uint32_t m = (uint32_t)x;
+        const bool ok = evictable(m) && (tier == 0 || meta_tier(m) == tier);
+        const uint64_t k = key_at(K, i, x);
         const bool take = ok && (MAX ? max_better(k, i, c.key, c.sid) : min_better(k, i, c.key, c.sid));
         c.key = take ? k : c.key;
         c.sid = take ? i : c.sid;
@@ -610,29 +625,22 @@ struct MemTable {
   // TIDE's two candidates, eq. (promote) and eq. (demote), from one pass.
   __device__ __forceinline__ void select_pd(const KeyCtx& K, Cand& p, Cand& d) {
     Cand cp = cand_none_min(), cd = cand_none_max();
-    for (uint32_t base = tid; base < hi; base += UNROLL * BLOCK) {
-      uint64_t x[UNROLL];
-#pragma unroll
-      for (int u = 0; u < UNROLL; ++u) {
-        const uint32_t i = base + u * BLOCK;
-        x[u] = i < hi ? mg[i] : 0ull;
-      }
-#pragma unroll
-      for (int u = 0; u < UNROLL; ++u) {
-        const uint32_t i = base + u * BLOCK;
-        const uint32_t m = (uint32_t)x[u];
-        const bool ev = i < hi && evictable(m);
+    const uint32_t nw = res_words();
+    for (uint32_t w = 0; w < nw; ++w) {
+      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
+        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
+        const uint64_t x = mg[i];
+        const uint32_t m = (uint32_t)x;
+        const bool ev = evictable(m);
         const bool in_h = ev && meta_tier(m) == kTierHbm;
         const bool in_s = ev && meta_tier(m) == kTierSram;
-        if (in_h || in_s) {
-          const uint64_t k = key_at(K, i, x[u]);
-          const bool tp = in_h && min_better(k, i, cp.key, cp.sid);
-          const bool td = in_s && max_better(k, i, cd.key, cd.sid);
-          cp.key = tp ? k : cp.key;
-          cp.sid = tp ? i : cp.sid;
-          cd.key = td ? k : cd.key;
-          cd.sid = td ? i : cd.sid;
-        }
+        const uint64_t k = key_at(K, i, x);
+        const bool tp = in_h && min_better(k, i, cp.key, cp.sid);
+        const bool td = in_s && max_better(k, i, cd.key, cd.sid);
+        cp.key = tp ? k : cp.key;
+        cp.sid = tp ? i : cp.sid;
+        cd.key = td ? k : cd.key;
+        cd.sid = td ? i : cd.sid;
       }
     }
     p = block_reduce<false>(cp);
@@ -652,11 +660,15 @@ struct MemTable {
 
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) {
     Cand c = cand_none_min();
-    for (uint32_t i = tid; i < hi; i += BLOCK) {
-      const uint32_t m = (uint32_t)mg[i];
-      if (evictable(m) && now - last[i] > ttl && i < c.sid) {
-        c.sid = i;
-        c.key = 0;
+    const uint32_t nw = res_words();
+    for (uint32_t w = 0; w < nw; ++w) {
+      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
+        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
+        const uint32_t m = (uint32_t)mg[i];
+        if (evictable(m) && now - last[i] > ttl && i < c.sid) {
+          c.sid = i;
+          c.key = 0;
+        }
       }
     }
     return block_reduce<false>(c).sid;
@@ -1356,6 +1368,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
     T.len = s32;
     uint32_t* kv = s32 + n;
     T.kvb = kv;
+    T.res = kv + n;
     for (uint32_t i = tid; i < n; i += BLOCK) {
       T.mg[i] = cont ? a.t_mg[tb + i] : 0ull;
       T.last[i] = cont ? a.t_last[tb + i] : 0ull;
@@ -1371,6 +1384,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
     T.last = a.t_last + tb;
     T.next = a.t_next + tb;
     T.kvb = a.sess_kvb + sb;
+    T.res = reinterpret_cast<uint32_t*>(s_tab);
     if (!cont) {
       for (uint32_t i = tid; i < n_sess; i += BLOCK) {
         T.mg[i] = 0;
@@ -1404,6 +1418,15 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
     }
   }
   __syncthreads();
+  // each thread's residency bits, from the table it resumes (empty if fresh)
+  for (uint32_t w = 0; w * 32u * BLOCK < n_sess; ++w) {
+    uint32_t bits = 0;
+    for (uint32_t b = 0; b < 32u; ++b) {
+      const uint32_t i = tid + (w * 32u + b) * BLOCK;
+      if (cont && i < n_sess && meta_tier((uint32_t)T.mg[i]) != kTierNone) bits |= 1u << b;
+    }
+    T.res[w * BLOCK + tid] = bits;
+  }
 
   Scalars S;
   Cnt C;
@@ -1513,6 +1536,13 @@ constexpr int kLdsVariant = 9;
 constexpr int kDualVariant = 11;  // streamed, 512 threads, with the dual design's copies
 constexpr uint32_t kLdsBytesPerSession = 4 * 8 + 2 * 4;  // mg, last, gq, next; len, kvb
 
+// LDS of the workgroup kernels' residency bits: one bit per session, in whole
+// words per thread.
+static size_t res_bytes(uint32_t n_sess, uint32_t block) {
+  const size_t per_word = 32u * (size_t)block;
+  return (n_sess + per_word - 1) / per_word * block * sizeof(uint32_t);
+}
+
 // Largest dynamic LDS one workgroup may take on the current device.
 static uint32_t lds_limit() {
   static int cached = -1;
@@ -1527,10 +1557,23 @@ static uint32_t lds_limit() {
   return (uint32_t)cached > static_bytes ? (uint32_t)cached - static_bytes : 0u;
 }
 
+static uint32_t block_of(int v) { return v == 10 || v == kDualVariant ? 512u : (uint32_t)kBlock; }
+
 uint32_t sim_variant_capacity(int v) {
   if (v < 0 || v >= kNumVariants) return 0;
-  if (v == kLdsVariant) return lds_limit() / kLdsBytesPerSession;
-  if (kVariants[v].g == 0) return UNISON_MAX_SESSIONS;
+  const uint32_t lim = lds_limit();
+  if (v == kLdsVariant) {
+    // the table and its residency bits
+    uint32_t n = lim / kLdsBytesPerSession;
+    while (n && (size_t)n * kLdsBytesPerSession + res_bytes(n, kBlock) > lim) --n;
+    return n;
+  }
+  if (kVariants[v].g == 0) {
+    // streamed table: the residency bits are the LDS it needs
+    const uint32_t b = block_of(v);
+    const uint64_t n = (uint64_t)(lim / (b * sizeof(uint32_t))) * 32u * b;
+    return n < UNISON_MAX_SESSIONS ? (uint32_t)n : UNISON_MAX_SESSIONS;
+  }
   return (uint32_t)(kVariants[v].g * kVariants[v].epl);
 }
 
@@ -1561,19 +1604,25 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
     case 7: launch_regs<16, 4>(a, stream); break;
     case 8: launch_regs<32, 8>(a, stream); break;
     case kLdsVariant: {
-      const size_t lds = (size_t)(max_sess_in_batch ? max_sess_in_batch : 1) * kLdsBytesPerSession;
+      const uint32_t n = max_sess_in_batch ? max_sess_in_batch : 1;
+      const size_t lds = (size_t)n * kLdsBytesPerSession + res_bytes(n, kBlock);
       hipLaunchKernelGGL((sim_block_kernel<kBlock, true, false>), dim3(a.n_sims), dim3(kBlock), lds, stream, a);
       break;
     }
     case 10:
-      hipLaunchKernelGGL((sim_block_kernel<512, false, false>), dim3(a.n_sims), dim3(512), 0, stream, a);
+      hipLaunchKernelGGL((sim_block_kernel<512, false, false>), dim3(a.n_sims), dim3(512),
+                         res_bytes(max_sess_in_batch, 512), stream, a);
       break;
     case kDualVariant:
-      hipLaunchKernelGGL((sim_block_kernel<512, false, true>), dim3(a.n_sims), dim3(512), 0, stream, a);
+      hipLaunchKernelGGL((sim_block_kernel<512, false, true>), dim3(a.n_sims), dim3(512),
+                         res_bytes(max_sess_in_batch, 512), stream, a);
+      break;
+    case 3:
+      hipLaunchKernelGGL((sim_block_kernel<kBlock, false, false>), dim3(a.n_sims), dim3(kBlock),
+                         res_bytes(max_sess_in_batch, kBlock), stream, a);
       break;
     default:
-      hipLaunchKernelGGL((sim_block_kernel<kBlock, false, false>), dim3(a.n_sims), dim3(kBlock), 0, stream, a);
-      break;
+      return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

@@ -137,6 +137,39 @@ def test_c4_longer_prefix_in_the_timed_configuration():
     compare_counters(s.counters(), oracle_counters(ww, max_events=40_000), label="c4 40k")
 
 
+@pytest.fixture(scope="module")
+def sparse_wide():
+    """17,000 sessions of one or two turns arriving at 2,000/s into a 256 GiB
+    pool: a table of ~4,000 live entries with ~1,700 resident, spread over
+    sids that span several residency words per thread of the 256- and 512-
+    thread streamed kernels."""
+    rng = np.random.Generator(np.random.PCG64(4242))
+    n = 17_000
+    first = synth.poisson_arrivals(rng, n, 2000.0)
+    turns = rng.integers(1, 3, n)
+    tr = synth.build_trace(rng, turns, first, synth.gaps_single, np.full(n, 128 * synth.KIB))
+    p = synth.default_params(4)
+    for i, pol in enumerate((POLICY_SPEAR, POLICY_LRU, POLICY_TIMEOUT, POLICY_BELADY)):
+        synth.set_policy(p[i:i + 1], pol)
+    p["cap_sram_B"], p["cap_hbm_B"] = 16 * synth.GIB, 256 * synth.GIB
+    p["n_slots"] = n
+    p["ttl_ns"] = synth.NS // 2
+    w = synth.Workload("sparse_wide", [tr], [tr.turns], p)
+    say("sparse wide table: %d sessions, %d events; oracle ~10 s" % (n, tr.n_events))
+    return w, oracle_counters(w)
+
+
+@pytest.mark.parametrize("variant", [None, 3, 10])
+def test_wide_sparse_table_residency_words(sparse_wide, variant):
+    w, want = sparse_wide
+    s = Sim(w, variant=variant)
+    s.run()
+    got = s.counters()
+    compare_counters(got, want, label="sparse wide variant %s" % variant)
+    assert int(got["evict"].min()) > 0 and int(got["expire"][2]) > 0
+    assert int(got["hit_sram"][0]) + int(got["hit_hbm"][0]) > 0
+
+
 def edge_workload(traces, rows):
     luts = [np.array([1, 2, 2, 3, 30, 51, 60], np.uint32), None]
     return synth.Workload("edge", traces, luts, rows, flat_luts=[(1, 3, 7)])
