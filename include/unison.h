@@ -233,7 +233,9 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
 
 /* Runs every simulation over at most `max_events` further events of its
  * trace (UINT64_MAX: to the end).  Without UNISON_RUN_CONTINUE each
- * simulation starts from an empty pool.  policy_override is a
+ * simulation starts from an empty pool; with it, each simulation resumes
+ * under the parameter row and policy it ran with (state a policy never
+ * reads, such as the gap EMA of LRU or timeout without TIDE, is not kept).  policy_override is a
  * UNISON_POLICY_* value applied to all simulations, or UNISON_POLICY_PARAMS.
  * A batch with a dual-design row runs on the copies' kernel (variant 11).
  * Tables above the LDS-resident size run on workgroup kernels that keep one

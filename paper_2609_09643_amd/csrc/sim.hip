@@ -218,6 +218,12 @@ __device__ __forceinline__ uint64_t key_of(const KeyCtx& K, uint32_t meta, uint3
   }
 }
 
+// A session's timer has fired (now - last > ttl) exactly when last lies below
+// this threshold: last never exceeds now, and nothing fires while now <= ttl.
+__device__ __forceinline__ uint64_t idle_threshold(uint64_t now, uint64_t ttl) {
+  return now > ttl ? now - ttl : 0ull;
+}
+
 struct Entry {
   uint32_t meta;
   float g;
@@ -242,7 +248,11 @@ struct RegTable {
   uint32_t kvb[EPL];
   uint64_t last[EPL];
   uint64_t next[EPL];
-  uint64_t key[EPL];
+  // Each entry's key in the form its reductions compare (packed_key).  A key
+  // reads only its own entry's fields and the hazard table, so it is
+  // recomputed for the event's entry at each scan, and for all entries when
+  // the hazard table changes.
+  uint64_t pk[EPL];
   uint32_t hz[EPL];   // hazard value at the entry's turn (hazard_of), set when the turn changes
 
   __device__ __forceinline__ uint32_t sid_of(int j) const { return (uint32_t)j * G + lane; }
@@ -338,12 +348,46 @@ struct RegTable {
     }
   }
 
-  // The per-event scan: every entry's key, kept for this event's reductions.
-  __device__ __forceinline__ void scan(const KeyCtx& K) {
+  // An entry's key as its reductions take it: an fp32 score in the upper
+  // word (select32); a recency or next-arrival time as k44 << 20 when times
+  // pack (select44); otherwise the key itself.
+  __device__ __forceinline__ static uint64_t packed_key(const KeyCtx& K, uint32_t m, uint32_t h,
+                                                        float gv, uint64_t gqv, uint64_t lastv,
+                                                        uint64_t nextv) {
+    if constexpr (PT::spear) {
+      const uint64_t k = key_of<POL, SMODE>(K, m, h, gv, gqv, 0ull, 0ull);
+      return PT::fixed ? k : k << 32;
+    } else {
+      constexpr uint64_t kCap = (1ull << 44) - 1;
+      if (K.pack44) {
+        uint64_t k44;
+        if constexpr (PT::belady) k44 = nextv < kCap ? nextv : kCap;
+        else k44 = kCap - lastv;
+        return k44 << 20;
+      }
+      return key_of<POL, SMODE>(K, m, h, gv, gqv, lastv, nextv);
+    }
+  }
+  __device__ __forceinline__ uint64_t packed_key_at(const KeyCtx& K, int j) const {
+    return packed_key(K, meta[j], hz[j], g[j], PT::fixed ? gq[j] : 0ull, PT::recency ? last[j] : 0ull,
+                      PT::belady ? next[j] : 0ull);
+  }
+  __device__ __forceinline__ void rescore_all(const KeyCtx& K) {
 #pragma unroll
-    for (int j = 0; j < EPL; ++j)
-      key[j] = key_of<POL, SMODE>(K, meta[j], hz[j], g[j], PT::fixed ? gq[j] : 0ull, last[j],
-                                  PT::belady ? next[j] : 0ull);
+    for (int j = 0; j < EPL; ++j) pk[j] = packed_key_at(K, j);
+  }
+
+  // The per-event scan.  Only the event's session changed a field a key
+  // reads, so its key is the one to recompute; every other entry keeps its
+  // key from its own latest event.
+  __device__ __forceinline__ void scan(const KeyCtx& K, uint32_t sid) {
+    const uint32_t js = sid / G;
+    const bool mine = lane == sid % G;
+    const uint64_t k = packed_key(K, pick(meta, js), pick(hz, js), pick(g, js),
+                                  PT::fixed ? pick(gq, js) : 0ull, PT::recency ? pick(last, js) : 0ull,
+                                  PT::belady ? pick(next, js) : 0ull);
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) pk[j] = (mine && js == (uint32_t)j) ? k : pk[j];
   }
 
   // argmax / argmin of the keys over evictable entries in `tier` (0 = any).
@@ -358,8 +402,8 @@ struct RegTable {
       const bool ok = evictable(meta[j]) && (tier == 0 || meta_tier(meta[j]) == tier);
       const uint32_t s = sid_of(j);
       const bool take =
-          ok && (MAX ? max_better(key[j], s, c.key, c.sid) : min_better(key[j], s, c.key, c.sid));
-      c.key = take ? key[j] : c.key;
+          ok && (MAX ? max_better(pk[j], s, c.key, c.sid) : min_better(pk[j], s, c.key, c.sid));
+      c.key = take ? pk[j] : c.key;
       c.sid = take ? s : c.sid;
     }
     return reduce_group<G, MAX>(c);
@@ -376,7 +420,7 @@ struct RegTable {
     for (int j = 0; j < EPL; ++j) {
       const bool ok = evictable(meta[j]) && (tier == 0 || meta_tier(meta[j]) == tier);
       const uint32_t s = sid_of(j);
-      const uint64_t p = (key[j] << 32) | (MAX ? (0xFFFFFFFFu - s) : s);
+      const uint64_t p = pk[j] | (MAX ? (0xFFFFFFFFu - s) : s);
       c = ok && (MAX ? p > c : p < c) ? p : c;
     }
     c = reduce_packed<G, 1, MAX>(c);
@@ -399,10 +443,7 @@ struct RegTable {
     for (int j = 0; j < EPL; ++j) {
       const bool ok = evictable(meta[j]) && (tier == 0 || meta_tier(meta[j]) == tier);
       const uint32_t s = sid_of(j);
-      uint64_t k44;
-      if constexpr (PT::belady) k44 = next[j] < kCap ? next[j] : kCap;
-      else k44 = kCap - last[j];
-      const uint64_t p = (k44 << 20) | (MAX ? (0xFFFFFu - s) : s);
+      const uint64_t p = pk[j] | (MAX ? (0xFFFFFu - s) : s);
       c = ok && (MAX ? p > c : p < c) ? p : c;
     }
     c = reduce_packed<G, 1, MAX>(c);
@@ -428,18 +469,22 @@ struct RegTable {
     hazard_add_counts(K, Tn, lane, G);
 #pragma unroll
     for (int j = 0; j < EPL; ++j) hz[j] = hazard_of<POL, SMODE>(K, meta[j]);
+    rescore_all(K);
   }
 
   // Smallest evictable session idle for longer than ttl (timeout policy);
   // kNone if there is none.
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) const {
+    const uint64_t thr = idle_threshold(now, ttl);
     uint32_t c = kNone;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
-      const bool ok = evictable(meta[j]) && now - last[j] > ttl;
+      const bool ok = evictable(meta[j]) && last[j] < thr;
       const uint32_t s = sid_of(j);
       c = ok && s < c ? s : c;
     }
+    // no timer fired anywhere in the wavefront: nothing to reduce
+    if (__builtin_amdgcn_ballot_w64(c != kNone) == 0) return kNone;
     return reduce_min32<G, 1>(c);
   }
 };
@@ -545,7 +590,7 @@ struct MemTable {
   }
   __device__ __forceinline__ void set_turn(uint32_t, uint32_t, const KeyCtx&) {}
 
-  __device__ __forceinline__ void scan(const KeyCtx&) {}
+  __device__ __forceinline__ void scan(const KeyCtx&, uint32_t) {}
 
   template <bool MAX>
   __device__ __forceinline__ Cand block_reduce(Cand c) {
@@ -659,13 +704,14 @@ struct MemTable {
   }
 
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) {
+    const uint64_t thr = idle_threshold(now, ttl);
     Cand c = cand_none_min();
     const uint32_t nw = res_words();
     for (uint32_t w = 0; w < nw; ++w) {
       for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
         const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
         const uint32_t m = (uint32_t)mg[i];
-        if (evictable(m) && now - last[i] > ttl && i < c.sid) {
+        if (evictable(m) && last[i] < thr && i < c.sid) {
           c.sid = i;
           c.key = 0;
         }
@@ -918,7 +964,8 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
         len_prev = 0;
       } else {
         const uint64_t gap = now - x.last;  // eq. (gap)
-        x.g = ema_f32(x.g, gap);
+        // only SPEAR keys and TIDE budgets read the gap EMA
+        if (PT::spear || PT::belady || P.tide) x.g = ema_f32(x.g, gap);
         if constexpr (PT::fixed) x.gq = ema_int(x.gq, gap, P.b_g, P.tau_ns);
       }
       x.meta = make_meta(kServing, tier0, turn);
@@ -943,7 +990,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
     // evictable residents is this event's victim index
     C.score_evals += S.n_table;
     C.resident_evals += S.n_res;
-    T.scan(K);
+    T.scan(K, sid);
     bool dual = false;
     if constexpr (Tab::kViews) {
       dual = P.dual_sync != 0;
@@ -1260,9 +1307,9 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
     T.len[j] = ld ? a.t_len[tb + s] : 0u;
     T.last[j] = ld ? a.t_last[tb + s] : 0ull;
     if constexpr (PT::belady) T.next[j] = ld ? a.t_next[tb + s] : ~0ull;
-    T.key[j] = 0;
     T.hz[j] = hazard_of<POL, SMODE>(K, T.meta[j]);
   }
+  T.rescore_all(K);  // a resumed table's keys; a fresh table's are never read before its writes
 
   Scalars S;
   Cnt C;
