@@ -71,15 +71,36 @@ __device__ __forceinline__ uint64_t sat_mul(uint64_t a, uint64_t b) {
   return __umul64hi(a, b) ? ~0ull : a * b;
 }
 
+// s / 10 rounded to nearest even, as the IEEE division gives it.  Between
+// 2^-64 and 2^64 the quotient comes from one product and one residual step:
+// q0 = s * 0.1f, r = s - 10 * q0 (exact in one fma), q = q0 + r * 0.1f (one
+// fma).  An exhaustive comparison over every finite float shows this equal to
+// the division from 2^-125 upwards; outside the window (zero, for one) the
+// division itself runs.  Gap EMAs stay below 2^36 us.
+__device__ __forceinline__ float div10(float s) {
+  if (s >= 0x1p-64f && s <= 0x1p64f) {
+    const float q0 = s * 0.1f;
+    const float r = __builtin_fmaf(-q0, 10.0f, s);
+    return __builtin_fmaf(r, 0.1f, q0);
+  }
+  return s / 10.0f;
+}
+
 // eq. (ema) on the fp32 register.  The sample is the gap in whole
 // microseconds (the tau = 10^3 resolution of eq. (lock)), clipped to 32 bits;
-// every operation is rounded to fp32.
+// every operation is rounded to fp32.  Gaps below 2^32 ns divide in 32 bits.
 __device__ __forceinline__ float ema_f32(float g, uint64_t gap_ns) {
-  const uint64_t us = gap_ns / 1000u;
-  const float x = (float)(us > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)us);
+  uint32_t us;
+  if (gap_ns < (1ull << 32)) {
+    us = (uint32_t)gap_ns / 1000u;
+  } else {
+    const uint64_t u = gap_ns / 1000u;
+    us = u > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)u;
+  }
+  const float x = (float)us;
   const float a = 3.0f * x;
   const float b = 7.0f * g;
-  return (a + b) / 10.0f;
+  return div10(a + b);
 }
 
 // eq. (gapq) then eq. (ema-int) on the integer register.
