@@ -592,9 +592,35 @@ struct MemTable {
 
   __device__ __forceinline__ void scan(const KeyCtx&, uint32_t) {}
 
+  // The wavefront's best candidate as uniform values.  The scans visit
+  // resident entries only, so most lanes usually hold none: up to 16
+  // candidates are compared one lane at a time in scalar registers, more
+  // go through the DPP butterfly.
+  template <bool MAX>
+  __device__ __forceinline__ Cand wave_best(Cand c) {
+    uint64_t lanes = __builtin_amdgcn_ballot_w64(c.sid != kNone);
+    if (__builtin_popcountll(lanes) > 16) {
+      c = reduce_group<64, MAX>(c);
+      return Cand{uni64(c.key), uni32(c.sid)};
+    }
+    Cand b = MAX ? cand_none_max() : cand_none_min();
+    while (lanes) {
+      const int l = __builtin_ctzll(lanes);
+      lanes &= lanes - 1u;
+      const uint32_t khi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(c.key >> 32), l);
+      const uint32_t klo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)c.key, l);
+      const uint32_t s = (uint32_t)__builtin_amdgcn_readlane((int)c.sid, l);
+      const uint64_t k = ((uint64_t)khi << 32) | klo;
+      const bool take = MAX ? max_better(k, s, b.key, b.sid) : min_better(k, s, b.key, b.sid);
+      b.key = take ? k : b.key;
+      b.sid = take ? s : b.sid;
+    }
+    return b;
+  }
+
   template <bool MAX>
   __device__ __forceinline__ Cand block_reduce(Cand c) {
-    c = reduce_group<64, MAX>(c);
+    c = wave_best<MAX>(c);
     Cand* buf = red + parity * NW;
     parity ^= 1u;
     if ((tid & 63u) == 0) buf[tid >> 6] = c;
