@@ -137,6 +137,30 @@ def test_c4_longer_prefix_in_the_timed_configuration():
     compare_counters(s.counters(), oracle_counters(ww, max_events=40_000), label="c4 40k")
 
 
+def test_c4_full_trace_properties():
+    """The whole C4 trace (about 4 million events per simulation), past what
+    the oracle can replay: one launch equals two launches split by CONTINUE,
+    and the counts the trace fixes by itself hold."""
+    w = synth.c4_large(n_traces=1)
+    tr = w.traces[0]
+    ww = subset(w, list(range(8)))
+    say("c4 full: 8 sims x %d events, twice (~25 s each)" % tr.n_events)
+    s = Sim(ww)
+    s.run()
+    one = s.counters().copy()
+    s.run(max_events=tr.n_events // 2)
+    s.run(flags=1)
+    two = s.counters()
+    assert np.array_equal(one.view(np.uint64), two.view(np.uint64))
+    arrive = tr.kind == synth.KIND_ARRIVE
+    assert (one["error"] == 0).all() and (one["events"] == tr.n_events).all()
+    assert (one["requests"] == int(arrive.sum())).all()
+    assert (one["tokens_total"] == int(tr.length[arrive].astype(np.uint64).sum())).all()
+    assert (one["hit_sram"] + one["hit_hbm"] + one["miss"] == one["requests"]).all()
+    assert (one["resident_evals"] <= one["score_evals"]).all()
+    assert (one["evict"] > 0).all() and (one["promote"] + one["swap"] > 0).any()
+
+
 @pytest.fixture(scope="module")
 def sparse_wide():
     """17,000 sessions of one or two turns arriving at 2,000/s into a 256 GiB
