@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void score_fixed_kernel(uint32_t n, const uint
 }
 
 constexpr int kKendallBlock = 256;
-constexpr uint32_t kKendallMax = 4096;  // sort-based path: 20 B of LDS per entry, 80 KiB
+constexpr uint32_t kKendallMax = 4096;  // sort-based path: 16 B of LDS per entry, 64 KiB
 constexpr uint32_t kKendallSortFrom = 256;  // snapshots this large or larger are sorted
 
 __device__ __forceinline__ bool fbetter(float a, uint32_t ia, float b, uint32_t ib) {
@@ -206,34 +206,24 @@ __device__ __forceinline__ bool pair_less(uint32_t xa, uint64_t ya, uint32_t xb,
   return xa < xb || (xa == xb && ya < yb);
 }
 
-// Number of entries of the sorted run a[lo, lo + n) below v (lower bound), or
-// at most v (upper bound).
-__device__ __forceinline__ uint32_t count_below(const uint64_t* a, uint32_t lo, uint32_t n, uint64_t v) {
-  uint32_t l = 0, h = n;
-  while (l < h) {
-    const uint32_t m = (l + h) >> 1;
-    if (a[lo + m] < v) l = m + 1; else h = m;
-  }
-  return l;
-}
-__device__ __forceinline__ uint32_t count_upto(const uint64_t* a, uint32_t lo, uint32_t n, uint64_t v) {
-  uint32_t l = 0, h = n;
-  while (l < h) {
-    const uint32_t m = (l + h) >> 1;
-    if (a[lo + m] <= v) l = m + 1; else h = m;
-  }
-  return l;
-}
+// Entries per thread, compare-exchanges per thread and pass, and binary-search
+// steps at the largest snapshot.  Each thread runs its searches (and its
+// compare-exchanges) in lockstep, so their LDS loads are in flight together.
+constexpr uint32_t kSortE = kKendallMax / kSortBlock;
+constexpr uint32_t kSortQ = kSortE / 2;
+constexpr uint32_t kSortSteps = 13;  // log2(4096) + 1
 
 __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
                                                                   uint64_t n_x, const float* x,
                                                                   const uint64_t* y,
                                                                   const uint32_t* idx,
                                                                   uint64_t* counts, uint8_t* top1) {
+  // [P] y, then merge buffer A; [P] merge buffer B, which holds the x keys
+  // until the merge sort starts (16 B of LDS per entry: 64 KiB at 4,096)
   extern __shared__ uint64_t s_dyn[];
-  uint64_t* s_ky = s_dyn;                                        // [P] y, then merge buffer A
-  uint64_t* s_yb = s_dyn + P;                                    // [P] merge buffer B
-  uint32_t* s_kx = reinterpret_cast<uint32_t*>(s_dyn + 2 * (size_t)P);  // [P] x keys
+  uint64_t* s_ky = s_dyn;
+  uint64_t* s_yb = s_dyn + P;
+  uint32_t* s_kx = reinterpret_cast<uint32_t*>(s_yb);
   __shared__ uint64_t s_sum[4][kSortBlock / 64];
   __shared__ float s_bx[kSortBlock / 64];
   __shared__ uint32_t s_bxi[kSortBlock / 64], s_byi[kSortBlock / 64];
@@ -259,7 +249,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
       }
       const float xv = x[e];
       const uint64_t yv = y[e];
-      s_kx[i] = __float_as_uint(xv);
+      s_kx[i] = float_key(__float_as_uint(xv));
       s_ky[i] = yv;
       if (bxi == kNone || fbetter(xv, i, bx, bxi)) { bx = xv; bxi = i; }
       if (byi == kNone || ubetter(yv, i, by, byi)) { by = yv; byi = i; }
@@ -286,69 +276,164 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
   __syncthreads();
 
   uint64_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
-  {
-    for (uint32_t i = tid; i < n; i += kSortBlock) s_kx[i] = float_key(s_kx[i]);
-    __syncthreads();
-    // bitonic sort of the P pairs by (x, y)
-    for (uint32_t k = 2; k <= P; k <<= 1) {
-      for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-        for (uint32_t t = tid; t < (P >> 1); t += kSortBlock) {
-          const uint32_t i = ((t & ~(j - 1)) << 1) | (t & (j - 1));
-          const uint32_t l = i + j;
-          const uint32_t xa = s_kx[i], xb = s_kx[l];
-          const uint64_t ya = s_ky[i], yb = s_ky[l];
+  // bitonic sort of the P pairs by (x, y); a pass's compare-exchanges touch
+  // disjoint pairs, so each thread loads all of its pairs before storing any
+  for (uint32_t k = 2; k <= P; k <<= 1) {
+    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+      uint32_t ia[kSortQ], xa[kSortQ], xb[kSortQ];
+      uint64_t ya[kSortQ], yb[kSortQ];
+#pragma unroll
+      for (uint32_t q = 0; q < kSortQ; ++q) {
+        const uint32_t t = tid + q * kSortBlock;
+        const uint32_t i = t < (P >> 1) ? ((t & ~(j - 1)) << 1) | (t & (j - 1)) : 0u;
+        ia[q] = t < (P >> 1) ? i : ~0u;
+        xa[q] = s_kx[i];
+        xb[q] = s_kx[i + j];
+        ya[q] = s_ky[i];
+        yb[q] = s_ky[i + j];
+      }
+#pragma unroll
+      for (uint32_t q = 0; q < kSortQ; ++q) {
+        const uint32_t i = ia[q];
+        if (i != ~0u) {
           const bool up = (i & k) == 0;
-          if (up ? pair_less(xb, yb, xa, ya) : pair_less(xa, ya, xb, yb)) {
-            s_kx[i] = xb;
-            s_kx[l] = xa;
-            s_ky[i] = yb;
-            s_ky[l] = ya;
+          if (up ? pair_less(xb[q], yb[q], xa[q], ya[q]) : pair_less(xa[q], ya[q], xb[q], yb[q])) {
+            s_kx[i] = xb[q];
+            s_kx[i + j] = xa[q];
+            s_ky[i] = yb[q];
+            s_ky[i + j] = ya[q];
           }
-        }
-        __syncthreads();
-      }
-    }
-    // pairs tied in x, and in x and y: each entry counts the earlier entries of its run
-    for (uint32_t i = tid; i < n; i += kSortBlock) {
-      const uint32_t xv = s_kx[i];
-      const uint64_t yv = s_ky[i];
-      uint32_t l = 0, h = i;
-      while (l < h) {
-        const uint32_t m = (l + h) >> 1;
-        if (s_kx[m] < xv) l = m + 1; else h = m;
-      }
-      t_x += i - l;
-      h = i;
-      while (l < h) {
-        const uint32_t m = (l + h) >> 1;
-        if (s_ky[m] < yv) l = m + 1; else h = m;
-      }
-      t_xy += i - l;
-    }
-    // merge sort of y in that order; a right-run entry is discordant with every
-    // larger entry of its left run
-    uint64_t* src = s_ky;
-    uint64_t* dst = s_yb;
-    for (uint32_t w = 1; w < P; w <<= 1) {
-      for (uint32_t p = tid; p < P; p += kSortBlock) {
-        const uint32_t b0 = p & ~(2 * w - 1);
-        const uint32_t off = p - b0;
-        const uint64_t v = src[p];
-        if (off < w) {
-          dst[b0 + off + count_below(src, b0 + w, w, v)] = v;
-        } else {
-          const uint32_t u = count_upto(src, b0, w, v);
-          dst[b0 + (off - w) + u] = v;
-          inv += w - u;
         }
       }
       __syncthreads();
-      uint64_t* tmp = src;
-      src = dst;
-      dst = tmp;
     }
-    // pairs tied in y
-    for (uint32_t i = tid; i < n; i += kSortBlock) t_y += i - count_below(src, 0, i, src[i]);
+  }
+  // pairs tied in x, and in x and y: each entry counts the earlier entries of
+  // its run, found by two lower-bound searches over [0, i)
+  {
+    uint32_t lo[kSortE], hi[kSortE], xv[kSortE];
+    uint64_t yv[kSortE];
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = tid + e * kSortBlock;
+      const bool ok = i < n;
+      xv[e] = ok ? s_kx[i] : 0u;
+      yv[e] = ok ? s_ky[i] : 0ull;
+      lo[e] = 0;
+      hi[e] = ok ? i : 0u;
+    }
+    for (uint32_t step = 0; step < kSortSteps; ++step) {
+#pragma unroll
+      for (uint32_t e = 0; e < kSortE; ++e) {
+        const uint32_t m = (lo[e] + hi[e]) >> 1;  // below i < P while the search is open
+        const bool open = lo[e] < hi[e];
+        const bool below = s_kx[open ? m : 0u] < xv[e];
+        lo[e] = open && below ? m + 1 : lo[e];
+        hi[e] = open && !below ? m : hi[e];
+      }
+    }
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = tid + e * kSortBlock;
+      if (i < n) t_x += i - lo[e];
+      hi[e] = i < n ? i : lo[e];
+    }
+    for (uint32_t step = 0; step < kSortSteps; ++step) {
+#pragma unroll
+      for (uint32_t e = 0; e < kSortE; ++e) {
+        const uint32_t m = (lo[e] + hi[e]) >> 1;
+        const bool open = lo[e] < hi[e];
+        const bool below = s_ky[open ? m : 0u] < yv[e];
+        lo[e] = open && below ? m + 1 : lo[e];
+        hi[e] = open && !below ? m : hi[e];
+      }
+    }
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = tid + e * kSortBlock;
+      if (i < n) t_xy += i - lo[e];
+    }
+  }
+  __syncthreads();  // the x keys are read for the last time; buffer B is free
+  // merge sort of y in that order; a right-run entry is discordant with every
+  // larger entry of its left run.  A left-run entry lands after the entries
+  // of the right run below it, a right-run entry after those of the left run
+  // at or below it.
+  uint64_t* src = s_ky;
+  uint64_t* dst = s_yb;
+  uint32_t steps = 1;  // log2(w) + 1 binary-search steps over a run of w
+  for (uint32_t w = 1; w < P; w <<= 1, ++steps) {
+    uint32_t lo[kSortE], hi[kSortE], rb[kSortE];
+    uint64_t v[kSortE];
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t p = tid + e * kSortBlock;
+      const bool ok = p < P;
+      const uint32_t b0 = p & ~(2 * w - 1);
+      const bool left = (p - b0) < w;
+      v[e] = ok ? src[p] : 0ull;
+      rb[e] = left ? b0 + w : b0;  // the other run
+      lo[e] = 0;
+      hi[e] = ok ? w : 0u;
+    }
+    for (uint32_t step = 0; step < steps; ++step) {
+#pragma unroll
+      for (uint32_t e = 0; e < kSortE; ++e) {
+        const uint32_t p = tid + e * kSortBlock;
+        const bool left = (p & (2 * w - 1)) < w;
+        const uint32_t m = (lo[e] + hi[e]) >> 1;
+        const bool open = lo[e] < hi[e];
+        const uint64_t a = src[open ? rb[e] + m : 0u];
+        const bool goes_right = left ? a < v[e] : a <= v[e];
+        lo[e] = open && goes_right ? m + 1 : lo[e];
+        hi[e] = open && !goes_right ? m : hi[e];
+      }
+    }
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t p = tid + e * kSortBlock;
+      if (p < P) {
+        const uint32_t b0 = p & ~(2 * w - 1);
+        const uint32_t off = p - b0;
+        if (off < w) {
+          dst[b0 + off + lo[e]] = v[e];
+        } else {
+          dst[b0 + (off - w) + lo[e]] = v[e];
+          inv += w - lo[e];
+        }
+      }
+    }
+    __syncthreads();
+    uint64_t* tmp = src;
+    src = dst;
+    dst = tmp;
+  }
+  // pairs tied in y: each entry counts the earlier equal entries of the sorted y
+  {
+    uint32_t lo[kSortE], hi[kSortE];
+    uint64_t yv[kSortE];
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = tid + e * kSortBlock;
+      yv[e] = i < n ? src[i] : 0ull;
+      lo[e] = 0;
+      hi[e] = i < n ? i : 0u;
+    }
+    for (uint32_t step = 0; step < kSortSteps; ++step) {
+#pragma unroll
+      for (uint32_t e = 0; e < kSortE; ++e) {
+        const uint32_t m = (lo[e] + hi[e]) >> 1;
+        const bool open = lo[e] < hi[e];
+        const bool below = src[open ? m : 0u] < yv[e];
+        lo[e] = open && below ? m + 1 : lo[e];
+        hi[e] = open && !below ? m : hi[e];
+      }
+    }
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = tid + e * kSortBlock;
+      if (i < n) t_y += i - lo[e];
+    }
   }
 
   uint64_t v[4] = {inv, t_x, t_y, t_xy};
@@ -426,7 +511,7 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
   } else {
     uint32_t P = 2;
     while (P < n_per) P <<= 1;
-    const size_t lds = (size_t)P * (2 * sizeof(uint64_t) + sizeof(uint32_t));
+    const size_t lds = (size_t)P * 2 * sizeof(uint64_t);
     hipLaunchKernelGGL(kendall_sort_kernel, dim3(n_snap), dim3(kSortBlock), lds, s, n_per, P, n_x,
                        x, y, idx, counts, top1);
   }
