@@ -503,14 +503,27 @@ struct MemTable {
   uint64_t* last;
   uint64_t* next;
   const uint32_t* kvb;
-  // The dual design (eq. (rf), eq. (stale)): the eviction engine's (0) and
-  // TIDE's (1) copies of the key fields; keys come from copy `src`, or from
-  // the live table when src < 0.  Eligibility and tiers are always live.
-  uint64_t* vmg[2];
-  uint64_t* vgq[2];
-  uint64_t* vlast[2];
-  uint64_t* vnext[2];
-  int src;
+  // The dual design (eq. (rf), eq. (stale)): the eviction engine's (copy 0)
+  // and TIDE's (copy 1) copies of the key fields, [4 fields][max_sessions]
+  // each.  Keys come from the copy set_src chose, or from the live table.
+  // Eligibility and tiers are always live.
+  uint64_t* view0;
+  uint64_t* view1;
+  uint32_t view_stride;  // max_sessions
+  const uint64_t* kmg;   // the key fields the scans read
+  const uint64_t* kgq;
+  const uint64_t* klast;
+  const uint64_t* knext;
+
+  // Keys from copy c (0 or 1), or from the live table for c < 0.
+  __device__ __forceinline__ void set_src(int c) {
+    const uint64_t* v = c == 0 ? view0 : view1;
+    const bool live = c < 0;
+    kmg = live ? mg : v;
+    kgq = live ? gq : v + view_stride;
+    klast = live ? last : v + 2 * (size_t)view_stride;
+    knext = live ? next : v + 3 * (size_t)view_stride;
+  }
   uint32_t tid;
   uint32_t hi;        // entries [0, hi) can be in the table
   uint32_t parity;
@@ -642,13 +655,11 @@ struct MemTable {
     const uint64_t* q = gq;
     const uint64_t* l = last;
     const uint64_t* n = next;
-    if (VIEWS && src >= 0) {
-      // selects rather than an indexed pointer array, which would live in scratch
-      const bool c1 = src != 0;
-      x = (c1 ? vmg[1] : vmg[0])[i];
-      q = c1 ? vgq[1] : vgq[0];
-      l = c1 ? vlast[1] : vlast[0];
-      n = c1 ? vnext[1] : vnext[0];
+    if constexpr (VIEWS) {
+      x = kmg[i];
+      q = kgq;
+      l = klast;
+      n = knext;
     }
     const uint32_t m = (uint32_t)x;
     const float gv = __uint_as_float((uint32_t)(x >> 32));
@@ -658,15 +669,17 @@ struct MemTable {
 
   // Overwrites both copies with the live key fields of every entry.
   __device__ __forceinline__ void sync_views() {
+    const size_t st = view_stride;
     for (uint32_t i = tid; i < hi; i += BLOCK) {
       const uint64_t m = mg[i], q = gq[i], l = last[i], n = next[i];
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        vmg[c][i] = m;
-        vgq[c][i] = q;
-        vlast[c][i] = l;
-        vnext[c][i] = n;
-      }
+      view0[i] = m;
+      view0[st + i] = q;
+      view0[2 * st + i] = l;
+      view0[3 * st + i] = n;
+      view1[i] = m;
+      view1[st + i] = q;
+      view1[2 * st + i] = l;
+      view1[3 * st + i] = n;
     }
     __syncthreads();
   }
@@ -1020,7 +1033,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
     bool dual = false;
     if constexpr (Tab::kViews) {
       dual = P.dual_sync != 0;
-      T.src = dual ? 0 : -1;  // the eviction engine scans its own copy
+      T.set_src(dual ? 0 : -1);  // the eviction engine scans its own copy
     }
     const Cand v0 = T.argmax_first(K);
     // odd weight per event: a different victim at any one event changes the sum
@@ -1100,9 +1113,9 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
           first = false;
           if constexpr (Tab::kViews) {
             if (dual && v.sid != kNone) {  // eq. (stale): would the live table agree?
-              T.src = -1;
+              T.set_src(-1);
               const Cand vl = T.template select<true>(0, K);
-              T.src = 0;
+              T.set_src(0);
               C.vict_diff += vl.sid != v.sid ? 1u : 0u;
             }
           }
@@ -1129,7 +1142,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
         const uint64_t budget = sat_mul(delta_us, P.dma_B_per_us);
         uint64_t left = budget, moved = 0;
         C.tide_passes++;
-        if constexpr (Tab::kViews) T.src = dual ? 1 : -1;  // TIDE decides from its own copy
+        if constexpr (Tab::kViews) T.set_src(dual ? 1 : -1);  // TIDE decides from its own copy
         for (;;) {
           Cand p, d;
           T.select_pd(K, p, d);  // eq. (promote), eq. (demote)
@@ -1137,9 +1150,9 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
           uint32_t live_p = p.sid;
           if constexpr (Tab::kViews) {
             if (dual) {
-              T.src = -1;
+              T.set_src(-1);
               live_p = T.template select<false>(kTierHbm, K).sid;
-              T.src = 1;
+              T.set_src(1);
             }
           }
           if (PT::has_inf && p.key == PT::inf_key) break;
@@ -1470,24 +1483,21 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   }
   // the dual design's copies, [2][4 fields][max_sessions] per simulation; a
   // fresh run starts them as the empty register file
-  T.src = -1;
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    uint64_t* vb = a.views ? a.views + ((size_t)sim * 8 + 4 * c) * a.max_sessions : nullptr;
-    T.vmg[c] = vb;
-    T.vgq[c] = vb ? vb + a.max_sessions : nullptr;
-    T.vlast[c] = vb ? vb + 2 * (size_t)a.max_sessions : nullptr;
-    T.vnext[c] = vb ? vb + 3 * (size_t)a.max_sessions : nullptr;
-  }
+  const size_t st = a.max_sessions;
+  T.view_stride = a.max_sessions;
+  T.view0 = a.views ? a.views + (size_t)sim * 8 * st : nullptr;
+  T.view1 = a.views ? T.view0 + 4 * st : nullptr;
+  T.set_src(-1);
   if (VIEWS && P.dual_sync && a.views && !cont) {
     for (uint32_t i = tid; i < n_sess; i += BLOCK) {
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        T.vmg[c][i] = 0;
-        T.vgq[c][i] = 0;
-        T.vlast[c][i] = 0;
-        T.vnext[c][i] = ~0ull;
-      }
+      T.view0[i] = 0;
+      T.view0[st + i] = 0;
+      T.view0[2 * st + i] = 0;
+      T.view0[3 * st + i] = ~0ull;
+      T.view1[i] = 0;
+      T.view1[st + i] = 0;
+      T.view1[2 * st + i] = 0;
+      T.view1[3 * st + i] = ~0ull;
     }
   }
   __syncthreads();
