@@ -161,6 +161,54 @@ def test_c4_full_trace_properties():
     assert (one["evict"] > 0).all() and (one["promote"] + one["swap"] > 0).any()
 
 
+MAX_PREFIX = 1500
+
+
+@pytest.fixture(scope="module")
+def max_sessions():
+    """One trace of UNISON_MAX_SESSIONS = 2^20 sessions (one or two turns,
+    2.6 million events) whose arrival order is independent of the session
+    id, so the first events already set residency bits in every word."""
+    rng = np.random.Generator(np.random.PCG64(2020))
+    n = 1 << 20
+    first = rng.uniform(0.0, 5000.0, n)
+    turns = 1 + (rng.random(n) < 0.5).astype(np.int64)
+    tr = synth.build_trace(rng, turns, first, synth.gaps_single, np.full(n, 128 * synth.KIB))
+    p = synth.default_params(2)
+    synth.set_policy(p[0:1], POLICY_SPEAR)
+    synth.set_policy(p[1:2], POLICY_BELADY)
+    p["cap_sram_B"], p["cap_hbm_B"] = synth.GIB, 8 * synth.GIB
+    p["n_slots"] = n
+    w = synth.Workload("max_sessions", [tr], [tr.turns], p)
+    say("2^20 sessions, %d events; oracle on the first %d (~15 s)" % (tr.n_events, MAX_PREFIX))
+    return w, oracle_counters(w, max_events=MAX_PREFIX), {}
+
+
+@pytest.mark.parametrize("variant", [None, 3])
+def test_maximum_session_count(max_sessions, variant):
+    """The largest table the ABI admits, on the 512- and 256-thread streamed
+    kernels (128 KiB of residency bits each): the oracle's counters on a
+    prefix, then 300,000 more events by size-independent properties, with
+    the same digests on both kernels."""
+    w, want, seen = max_sessions
+    tr = w.traces[0]
+    s = Sim(w, variant=variant)
+    s.run(max_events=MAX_PREFIX)
+    got = s.counters()
+    compare_counters(got, want, label="2^20 sessions, variant %s" % variant)
+    assert int(got["evict"].min()) > 0
+    end = MAX_PREFIX + 300_000
+    s.run(flags=1, max_events=end - MAX_PREFIX)
+    got = s.counters()
+    arrive = tr.kind[:end] == synth.KIND_ARRIVE
+    assert (got["error"] == 0).all() and (got["events"] == end).all()
+    assert (got["requests"] == int(arrive.sum())).all()
+    assert (got["hit_sram"] + got["hit_hbm"] + got["miss"] == got["requests"]).all()
+    for k in ("digest", "victim_digest", "score_evals", "resident_evals"):
+        seen.setdefault(k, got[k].copy())
+        assert np.array_equal(seen[k], got[k]), "%s differs between kernel variants" % k
+
+
 @pytest.fixture(scope="module")
 def sparse_wide():
     """17,000 sessions of one or two turns arriving at 2,000/s into a 256 GiB
