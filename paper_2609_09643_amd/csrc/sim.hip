@@ -1660,9 +1660,13 @@ uint32_t sim_variant_capacity(int v) {
   return (uint32_t)(kVariants[v].g * kVariants[v].epl);
 }
 
+// Measured on 4,096-simulation batches: register tables win up to 256
+// sessions (32 x 8 takes half the LDS table's time there), the LDS table up
+// to its capacity, then the 512-thread streamed table.
 int sim_auto_variant(uint32_t max_sess) {
   if (max_sess <= 16) return 5;
   if (max_sess <= 64) return 7;
+  if (max_sess <= 256) return 8;
   if (max_sess <= sim_variant_capacity(kLdsVariant)) return kLdsVariant;
   return 10;
 }
