@@ -308,7 +308,7 @@ int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t*
 
 /* Test hook: pins the simulation kernel variant (-1 = chosen by the largest
  * trace; register tables of lanes x sessions per lane 0: 16 x 1, 1: 64 x 1,
- * 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 6: 64 x 24, 7: 16 x 4, 8: 32 x 8; one
+ * 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 7: 16 x 4, 8: 32 x 8 (6 is retired); one
  * workgroup per simulation with the table 3: streamed from the workspace by
  * 256 threads, 10: by 512 threads, 9: held in LDS, 11: streamed by 512
  * threads with the dual design's copies -- the only variant for a batch with

@@ -13,7 +13,10 @@ from tracekit import trace_from_events
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = (0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11)
+RETIRED = pytest.mark.skip(reason="variant 6 (64 x 24) is retired: one of its launches faulted "
+                                  "the GPU on a randomised batch and no cause was found; the "
+                                  "library refuses it (test_retired_variant_is_refused)")
+VARIANTS = (0, 1, 2, 3, 4, 5, pytest.param(6, marks=RETIRED), 7, 8, 9, 10, 11)
 
 
 def say(*a):
@@ -65,6 +68,14 @@ def test_c3_every_kernel_variant(c3, c3_want, variant):
     s = Sim(w, variant=variant)
     s.run()
     compare_counters(s.counters(), [c3_want[i] for i in sims], label="variant %d" % variant)
+
+
+def test_retired_variant_is_refused():
+    from paper_2609_09643_amd.unison import E_CAPACITY, UnisonError
+    s = Sim(synth.c1_tiny(), variant=6)
+    with pytest.raises(UnisonError) as e:
+        s.run()
+    assert e.value.code == E_CAPACITY
 
 
 def test_c3_decision_logs(c3):
