@@ -103,6 +103,33 @@ def test_random_batches_on_every_variant(case):
         del s
 
 
+def test_random_batches_split_by_continue(case):
+    """The same batches in three launches cut at uneven event counts, on
+    the automatic choice and the streamed kernel: a resumed run is the
+    uninterrupted one."""
+    name, w, want, _ = case
+    longest = max(t.n_events for t in w.traces)
+    cuts = [max(1, longest // 7), max(1, longest // 3)]
+    for v in (None, 10):
+        say("random %s split %s: variant %s" % (name, cuts, v))
+        s = Sim(w, variant=v)
+        s.run(max_events=cuts[0])
+        s.run(flags=1, max_events=cuts[1])
+        s.run(flags=1)
+        compare_counters(s.counters(), want, label="random %s split, variant %s" % (name, v))
+        del s
+
+
+def test_random_decision_logs(case):
+    """Full ordered decision logs of a few simulations of each batch."""
+    from parity import oracle_log, same_log
+    name, w, _, _ = case
+    s = Sim(w, log_cap=1 << 14)
+    s.run(flags=2)
+    for i in range(0, w.n_sims, 37):
+        assert same_log(s.log(i), oracle_log(w, i, log_cap=1 << 14)), "random %s sim %d log" % (name, i)
+
+
 @pytest.mark.skip(reason="variant 6 (64 x 24) is retired after a GPU fault on this batch; "
                          "no cause was found and the library refuses the variant")
 def test_random_large_batch_on_the_retired_variant():
