@@ -153,7 +153,8 @@ typedef struct {
   uint64_t tokens_total;      /* sum of request lengths, eq. (prered) denominator */
   uint64_t tokens_computed;   /* tokens prefilled, eq. (prered) numerator */
   uint64_t extra_prefill_tok; /* prefix tokens re-prefilled after a loss */
-  uint64_t score_evals;       /* table entries scored: sum over events of |table| */
+  uint64_t score_evals;       /* the register-file scan's domain: sum over events of |table|
+                                 (every entry the paper's scan covers) */
   uint64_t resident_evals;    /* sum over events of the resident count */
   uint64_t digest;            /* sum mod 2^64 of hashes of every decision record:
                                  mix(w0 ^ w1 * 0x9e3779b97f4a7c15), w0 = ev << 8 | op,
@@ -235,16 +236,16 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
  * trace (UINT64_MAX: to the end).  Without UNISON_RUN_CONTINUE each
  * simulation starts from an empty pool; with it, each simulation resumes
  * under the parameter row and policy it ran with (state a policy never
- * reads, such as the gap EMA of LRU or timeout without TIDE, is not kept).  policy_override is a
- * UNISON_POLICY_* value applied to all simulations, or UNISON_POLICY_PARAMS.
- * A batch with a dual-design row runs on the copies' kernel (variant 11).
- * Tables above the LDS-resident size run on workgroup kernels that keep one
- * bit of LDS per session (the residency bits their scans visit): 128 KiB at
- * UNISON_MAX_SESSIONS.
- * Asynchronous.  Errors: UNISON_E_NOT_READY, UNISON_E_INVALID (also: a
- * register-table variant forced on a batch with a dual-design row),
- * UNISON_E_CAPACITY (the largest trace exceeds the chosen kernel variant,
- * e.g. on a device with less LDS per workgroup than the bits need). */
+ * reads, such as the gap EMA of LRU or timeout without TIDE, is not kept).
+ * policy_override is a UNISON_POLICY_* value applied to all simulations, or
+ * UNISON_POLICY_PARAMS.  A batch with a dual-design row runs on the copies'
+ * kernel (variant 11).  Tables above the LDS-resident size run on workgroup
+ * kernels that keep one bit of LDS per session (the residency bits their
+ * scans visit): 128 KiB at UNISON_MAX_SESSIONS.  Asynchronous.
+ * Errors: UNISON_E_NOT_READY, UNISON_E_INVALID (also: a register-table
+ * variant forced on a batch with a dual-design row), UNISON_E_CAPACITY (the
+ * largest trace exceeds the chosen kernel variant, e.g. on a device with
+ * less LDS per workgroup than the bits need). */
 int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64_t max_events);
 
 /* Copies counters of simulations [first, first+n) to HOST `dst`; synchronises
