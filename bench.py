@@ -91,6 +91,19 @@ def time_launches(torch, fn, steps, warmup):
     return per, wall
 
 
+def host_cpu():
+    """The host's CPU model and visible CPU count."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"model": model, "cpus_visible": os.cpu_count()}
+
+
 def cpu_baseline(workload, budget_s=20.0):
     """The oracle, single-threaded, on the same simulations: whole sweeps are
     repeated until about budget_s of event-loop time has accumulated."""
@@ -109,7 +122,7 @@ def cpu_baseline(workload, budget_s=20.0):
             break
     sec = loop_ns / 1e9
     return {"value": evals / sec, "unit": "score evals/s", "cores": 1, "kind": "oracle",
-            "events_per_s": events / sec,
+            "events_per_s": events / sec, "host": host_cpu(),
             "sample": "the full %d-simulation sweep, %d repetition(s), %.1f s of event-loop "
                       "time on one host core" % (workload.n_sims, reps, sec)}
 
@@ -349,6 +362,11 @@ def main():
         "kernel_ms_mean": ms, "kernel_ms_median": float(np.median(per)),
         "wall_s": wall,
     }
+    if traffic is not None:
+        # the same launch against measured DRAM bytes (rocprofv3 FETCH/WRITE)
+        dram = traffic / (ms / 1e3) / 1e9
+        result["dram_roofline"] = {"achieved": dram, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                   "frac": dram / HBM_PEAK_GBS}
     secs = [s for s in args.sections.split(",") if s and s != "none"]
     extra = {}
     if "c2" in secs:
