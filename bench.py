@@ -127,6 +127,17 @@ def cpu_baseline(workload, budget_s=20.0):
                       "time on one host core" % (workload.n_sims, reps, sec)}
 
 
+def section_c1(torch, U, synth, steps):
+    w = synth.c1_tiny()
+    sim = U.Simulator(w)
+    per, _ = time_launches(torch, sim.run, steps, 2)
+    c = sim.counters()
+    ms = float(np.median(per))
+    return {"workload": "c1 tiny: 16 sessions x 12 turns, SPEAR+TIDE and Belady",
+            "ms_per_run": ms, "events_per_s": float(c["events"].sum()) / (ms / 1e3),
+            "evals_per_s": float(c["score_evals"].sum()) / (ms / 1e3)}
+
+
 def section_c2(torch, U, synth, steps):
     w = synth.c2_paper_scale()
     sim = U.Simulator(w)
@@ -296,7 +307,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--sections", default="c2,c5", help="comma list of c2,c4,c5,fmt,online,studies or 'none'")
+    ap.add_argument("--sections", default="c1,c2,c5",
+                    help="comma list of c1,c2,c4,c5,fmt,online,studies or 'none'")
     ap.add_argument("--c4-events", type=int, default=200_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", type=int, default=None)
@@ -369,6 +381,9 @@ def main():
                                    "frac": dram / HBM_PEAK_GBS}
     secs = [s for s in args.sections.split(",") if s and s != "none"]
     extra = {}
+    if "c1" in secs:
+        log("section c1")
+        extra["c1"] = section_c1(torch, U, synth, 20)
     if "c2" in secs:
         log("section c2")
         extra["c2"] = section_c2(torch, U, synth, 5)
