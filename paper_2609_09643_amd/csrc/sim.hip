@@ -240,6 +240,9 @@ template <int G, int EPL, uint32_t POL, uint32_t SMODE>
 struct RegTable {
   using PT = Pol<POL, SMODE>;
   static constexpr bool kViews = false;  // no dual-design copies
+  // Gap onsets reduce their scan victim and TIDE's candidates separately:
+  // fusing the three reductions made this kernel slower (0.518 vs 0.498 ms).
+  static constexpr bool kFuseGap = false;
   uint32_t lane;
   uint32_t meta[EPL];
   float g[EPL];
@@ -497,6 +500,9 @@ struct MemTable {
   using PT = Pol<POL, SMODE>;
   static constexpr int NW = BLOCK / 64;
   static constexpr bool kViews = VIEWS;  // instantiated with the dual design's copies
+  // A gap onset's scan and TIDE's first candidates share one pass and one
+  // barrier (the dual design scans different copies for the two engines).
+  static constexpr bool kFuseGap = !VIEWS;
   uint64_t* mg;
   uint64_t* gq;
   uint32_t* len;
@@ -527,7 +533,7 @@ struct MemTable {
   uint32_t tid;
   uint32_t hi;        // entries [0, hi) can be in the table
   uint32_t parity;
-  Cand* red;          // LDS [2][NW]
+  Cand* red;          // LDS [2][3][NW]: two alternating sets of up to three reductions
   // Residency bits of this thread's entries (sid = tid + k * BLOCK): bit
   // k % 32 of LDS word res[(k / 32) * BLOCK + tid].  Only the owning thread
   // reads or writes its words, so they need no barrier; the scans visit set
@@ -631,13 +637,9 @@ struct MemTable {
     return b;
   }
 
+  // The wavefronts' results, read back from LDS after the barrier.
   template <bool MAX>
-  __device__ __forceinline__ Cand block_reduce(Cand c) {
-    c = wave_best<MAX>(c);
-    Cand* buf = red + parity * NW;
-    parity ^= 1u;
-    if ((tid & 63u) == 0) buf[tid >> 6] = c;
-    __syncthreads();
+  __device__ __forceinline__ Cand combine(const Cand* buf) const {
     uint64_t rk = buf[0].key;
     uint32_t rs = buf[0].sid;
 #pragma unroll
@@ -649,6 +651,34 @@ struct MemTable {
       rs = take ? os : rs;
     }
     return Cand{uni64(rk), uni32(rs)};
+  }
+
+  template <bool MAX>
+  __device__ __forceinline__ Cand block_reduce(Cand c) {
+    c = wave_best<MAX>(c);
+    Cand* buf = red + parity * 3 * NW;
+    parity ^= 1u;
+    if ((tid & 63u) == 0) buf[tid >> 6] = c;
+    __syncthreads();
+    return combine<MAX>(buf);
+  }
+
+  // Three reductions (max, min, max) behind one barrier.
+  __device__ __forceinline__ void block_reduce3(Cand& v, Cand& p, Cand& d) {
+    v = wave_best<true>(v);
+    p = wave_best<false>(p);
+    d = wave_best<true>(d);
+    Cand* buf = red + parity * 3 * NW;
+    parity ^= 1u;
+    if ((tid & 63u) == 0) {
+      buf[tid >> 6] = v;
+      buf[NW + (tid >> 6)] = p;
+      buf[2 * NW + (tid >> 6)] = d;
+    }
+    __syncthreads();
+    v = combine<true>(buf);
+    p = combine<false>(buf + NW);
+    d = combine<true>(buf + 2 * NW);
   }
 
   __device__ __forceinline__ uint64_t key_at(const KeyCtx& K, uint32_t i, uint64_t x) const {
@@ -729,6 +759,34 @@ struct MemTable {
     }
     p = block_reduce<false>(cp);
     d = block_reduce<true>(cd);
+  }
+  // A gap onset's scan victim and TIDE's first candidates from one pass over
+  // the residents and one barrier.
+  __device__ __forceinline__ void scan3(const KeyCtx& K, Cand& v, Cand& p, Cand& d) {
+    Cand cv = cand_none_max(), cp = cand_none_min(), cd = cand_none_max();
+    const uint32_t nw = res_words();
+    for (uint32_t w = 0; w < nw; ++w) {
+      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
+        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
+        const uint64_t x = mg[i];
+        const uint32_t m = (uint32_t)x;
+        const bool ev = evictable(m);
+        const uint64_t k = key_at(K, i, x);
+        const bool tv = ev && max_better(k, i, cv.key, cv.sid);
+        const bool tp = ev && meta_tier(m) == kTierHbm && min_better(k, i, cp.key, cp.sid);
+        const bool td = ev && meta_tier(m) == kTierSram && max_better(k, i, cd.key, cd.sid);
+        cv.key = tv ? k : cv.key;
+        cv.sid = tv ? i : cv.sid;
+        cp.key = tp ? k : cp.key;
+        cp.sid = tp ? i : cp.sid;
+        cd.key = td ? k : cd.key;
+        cd.sid = td ? i : cd.sid;
+      }
+    }
+    block_reduce3(cv, cp, cd);
+    v = cv;
+    p = cp;
+    d = cd;
   }
 
   // Online hazard table: both calls are made by the whole workgroup.
@@ -1035,7 +1093,20 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       dual = P.dual_sync != 0;
       T.set_src(dual ? 0 : -1);  // the eviction engine scans its own copy
     }
-    const Cand v0 = T.argmax_first(K);
+    // At a gap onset of a TIDE simulation the same pass can also yield TIDE's
+    // first candidates: nothing changes the table before the TIDE pass.
+    Cand v0, p0, d0;
+    bool have_pd = false;
+    if constexpr (Tab::kFuseGap) {
+      if (kind == kGapStart && P.tide) {
+        T.scan3(K, v0, p0, d0);
+        have_pd = true;
+      } else {
+        v0 = T.argmax_first(K);
+      }
+    } else {
+      v0 = T.argmax_first(K);
+    }
     // odd weight per event: a different victim at any one event changes the sum
     C.victim_digest += ((uint64_t)v0.sid + 1u) * vw;
     vw += 2ull * kGolden;
@@ -1145,7 +1216,13 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
         if constexpr (Tab::kViews) T.set_src(dual ? 1 : -1);  // TIDE decides from its own copy
         for (;;) {
           Cand p, d;
-          T.select_pd(K, p, d);  // eq. (promote), eq. (demote)
+          if (have_pd) {
+            p = p0;
+            d = d0;
+            have_pd = false;
+          } else {
+            T.select_pd(K, p, d);  // eq. (promote), eq. (demote)
+          }
           if (p.sid == kNone) break;
           uint32_t live_p = p.sid;
           if constexpr (Tab::kViews) {
@@ -1560,7 +1637,7 @@ __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   __shared__ uint32_t s_hq[52];
   __shared__ uint32_t s_hd[52];
   __shared__ uint32_t s_hn[52];
-  __shared__ Cand s_red[2 * (BLOCK / 64)];
+  __shared__ Cand s_red[2 * 3 * (BLOCK / 64)];
   extern __shared__ uint64_t s_tab[];
   const uint32_t sim = blockIdx.x;
   const unison_sim_params P = a.params[sim];
