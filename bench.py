@@ -33,6 +33,11 @@ METRIC = "simulated session-events/s and score evals/s (1 GPU); % HBM roofline"
 EVAL_BYTES = {0: 12, 1: 20, 2: 20, 3: 20}   # SPEAR, LRU, timeout, Belady
 EVENT_BYTES = 32
 PMC_FILE = os.path.join(ROOT, "profiles", "sim_c3_pmc.txt")
+UTIL_FILE = os.path.join(ROOT, "profiles", "kernel_util_counters.txt")
+HEADLINE_KERNEL = "sim_regs_kernel<8, 2>"
+# VALU issue limit: 256 CUs x 4 SIMDs at 2.4 GHz, one wave64 VALU instruction
+# per SIMD every 4 cycles (16 lanes wide): 614.4e9 instructions/s.
+VALU_PEAK_GINST = 256 * 4 * 2.4 / 4
 SIM_SOURCES = [os.path.join(ROOT, "paper_2609_09643_amd", "csrc", f)
                for f in ("sim.hip", "unison_device.h")]
 
@@ -64,6 +69,25 @@ def measured_traffic():
         return int(float(kv["hbm_bytes_per_launch"]))
     except (KeyError, ValueError):
         return None
+
+
+def measured_valu():
+    """wave64 VALU instructions per launch of the headline kernel from the
+    committed rocprofv3 utilisation summary, if it was taken on the current
+    kernel source."""
+    if not os.path.exists(UTIL_FILE):
+        return None
+    ok = False
+    for line in open(UTIL_FILE):
+        if line.startswith("source_hash:"):
+            ok = line.split(":", 1)[1].strip() == source_hash()
+        elif ok and line.startswith(HEADLINE_KERNEL + " |"):
+            cols = [c.strip() for c in line.split("|")]
+            try:
+                return float(cols[9])
+            except (IndexError, ValueError):
+                return None
+    return None
 
 
 def algorithmic_bytes(params, counters):
@@ -348,7 +372,10 @@ def main():
     evals = float(c["score_evals"].sum())
     ab = algorithmic_bytes(w.params, c)
     achieved = ab / (ms / 1e3) / 1e9
-    traffic = measured_traffic()
+    # the counter summaries describe the automatic kernel on the full sweep
+    profiled = args.variant is None and args.policies == "0,1,2,3"
+    traffic = measured_traffic() if profiled else None
+    valu = measured_valu() if profiled else None
     result = {
         "metric": METRIC,
         "value": evals / (ms / 1e3),
@@ -379,6 +406,12 @@ def main():
         dram = traffic / (ms / 1e3) / 1e9
         result["dram_roofline"] = {"achieved": dram, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                    "frac": dram / HBM_PEAK_GBS}
+    if valu is not None:
+        # the same launch against the VALU issue limit (rocprofv3 SQ_INSTS_VALU)
+        g = valu / (ms / 1e3) / 1e9
+        result["alu_roofline"] = {"bound": "alu", "achieved": g, "peak": VALU_PEAK_GINST,
+                                  "unit": "G wave64 VALU instructions/s",
+                                  "frac": g / VALU_PEAK_GINST, "valu_per_launch": valu}
     secs = [s for s in args.sections.split(",") if s and s != "none"]
     extra = {}
     if "c1" in secs:
