@@ -317,6 +317,13 @@ int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t*
  * makes unison_run return UNISON_E_CAPACITY. */
 int unison_debug_force_variant(unison_ctx* ctx, int variant);
 
+/* Test hook: at most `slots` resident-cache slots per thread for the streamed
+ * table kernels (variants 3 and 10), so tests can drive threads past their
+ * slots; -1 restores the automatic count (up to 8, as the LDS left by the
+ * residency bits allows).  The results never depend on it.  Errors:
+ * UNISON_E_INVALID (null context, slots < -1). */
+int unison_debug_cache_slots(unison_ctx* ctx, int slots);
+
 uint32_t unison_version(void);
 
 #ifdef __cplusplus

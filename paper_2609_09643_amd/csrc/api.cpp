@@ -17,7 +17,8 @@
 #include "unison_device.h"
 
 namespace unison {
-hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream, int force_variant);
+hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream, int force_variant,
+                      int force_cache_slots);
 uint32_t sim_variant_capacity(int v);
 int sim_auto_variant(uint32_t max_sess);
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
@@ -135,6 +136,7 @@ struct unison_ctx {
   bool dual = false;    // some row uses the dual register-file design
   uint32_t max_sess_batch = 0;
   int force_variant = -1;
+  int force_cache_slots = -1;  // test hook: resident-cache slots of the streamed tables
   char err[512];
 
   template <class T>
@@ -401,7 +403,7 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
       return ctx->fail(UNISON_E_CAPACITY, "%u sessions exceed every kernel variant (largest %u)",
                        ctx->max_sess_batch, sim_variant_capacity(v));
   }
-  int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->stream, v), "launch simulation");
+  int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->stream, v, ctx->force_cache_slots), "launch simulation");
   if (rc == UNISON_OK) ctx->ran = true;
   return rc;
 }
@@ -475,6 +477,13 @@ int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t*
 int unison_debug_force_variant(unison_ctx* ctx, int variant) {
   if (!ctx) return UNISON_E_INVALID;
   ctx->force_variant = variant;
+  return UNISON_OK;
+}
+
+// Test hook: cap the streamed tables' resident-cache slots (-1 = automatic).
+int unison_debug_cache_slots(unison_ctx* ctx, int slots) {
+  if (!ctx || slots < -1) return UNISON_E_INVALID;
+  ctx->force_cache_slots = slots;
   return UNISON_OK;
 }
 

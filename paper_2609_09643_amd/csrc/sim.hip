@@ -298,7 +298,10 @@ struct RegTable {
     e.g = bcast(g, sid);
     e.gq = PT::fixed ? bcast(gq, sid) : 0ull;
   }
-  __device__ __forceinline__ void write_end(uint32_t sid, uint32_t m, uint64_t t, uint64_t nx) {
+  // A gap onset or completion: the new meta x.meta (its EMAs x.g, x.gq are
+  // unchanged), the event time t and, at a gap onset, the next arrival nx.
+  __device__ __forceinline__ void write_end(uint32_t sid, const Entry& x, uint64_t t, uint64_t nx) {
+    const uint32_t m = x.meta;
     const uint32_t js = sid / G;
     const bool mine = lane == sid % G;
 #pragma unroll
@@ -495,7 +498,7 @@ struct RegTable {
 // Table in the workspace, one workgroup per simulation.  Uniform values read
 // from memory or LDS go through readfirstlane so the engine's scalars live in
 // SGPRs.
-template <int BLOCK, uint32_t POL, uint32_t SMODE, bool VIEWS>
+template <int BLOCK, uint32_t POL, uint32_t SMODE, bool VIEWS, bool CACHE>
 struct MemTable {
   using PT = Pol<POL, SMODE>;
   static constexpr int NW = BLOCK / 64;
@@ -539,15 +542,122 @@ struct MemTable {
   // reads or writes its words, so they need no barrier; the scans visit set
   // bits only, since no other entry can be a victim or a migrant.
   uint32_t* res;
+  // Resident cache (CACHE: a table streamed from the workspace).  The meta /
+  // gap word, the aux field (aux_table) and the key of this thread's
+  // resident entries, in LDS slots o = s * BLOCK + tid, s < rc_cap, which
+  // only the owning thread reads or writes.  While the thread has at most rc_cap
+  // residents the slots hold all of them and its scans read no table memory;
+  // with more, it reads them from the table, and it refills the slots once
+  // it is back within them.
+  uint64_t* rc_mg;
+  uint64_t* rc_aux;
+  uint64_t* rc_key;   // the entry's key, kept current with its fields and the hazard table
+  uint32_t* rc_k;     // k of the entry in slot s (sid = tid + k * BLOCK)
+  KeyCtx kc;          // the simulation's key context
+  uint32_t rc_cap;
+  uint32_t rc_used;   // bit s: slot s is taken
+  uint32_t n_mine;    // residents of this thread
+  uint32_t w_sid;     // the entry of the latest write(), its meta / gap word and aux field
+  uint64_t w_x;
+  uint64_t w_aux;
 
-  // Keeps the owner's residency bit in step with the tier in meta m.
-  __device__ __forceinline__ void mark(uint32_t sid, uint32_t m) {
-    if ((sid & (BLOCK - 1u)) == tid) {
-      const uint32_t k = sid / BLOCK;
-      uint32_t* w = res + (k >> 5) * BLOCK + tid;
-      const uint32_t bit = 1u << (k & 31u);
-      *w = meta_tier(m) != kTierNone ? (*w | bit) : (*w & ~bit);
+  // The one field besides meta and the gap EMA that an entry's key reads:
+  // the integer gap EMA (fixed-point score), the next arrival (Belady) or
+  // the last event time (LRU, timeout).
+  __device__ __forceinline__ static uint64_t aux_pick(uint64_t q, uint64_t l, uint64_t n) {
+    return PT::fixed ? q : PT::belady ? n : PT::recency ? l : 0ull;
+  }
+  __device__ __forceinline__ uint64_t aux_table(uint32_t i) const {
+    if constexpr (PT::fixed) return gq[i];
+    else if constexpr (PT::belady) return next[i];
+    else if constexpr (PT::recency) return last[i];
+    else return 0ull;
+  }
+  // The key of an entry with meta / gap word x and aux field aux.
+  __device__ __forceinline__ uint64_t key_from(uint64_t x, uint64_t aux) const {
+    const uint32_t m = (uint32_t)x;
+    return key_of<POL, SMODE>(kc, m, hazard_of<POL, SMODE>(kc, m),
+                              __uint_as_float((uint32_t)(x >> 32)), aux, aux, aux);
+  }
+
+  // Refills the slots from the table with every resident of this thread
+  // (at most rc_cap of them).
+  __device__ __forceinline__ void rc_refill() {
+    uint32_t n = 0;
+    const uint32_t nw = res_words();
+    for (uint32_t w = 0; w < nw; ++w) {
+      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
+        const uint32_t k = w * 32u + (uint32_t)__builtin_ctz(bits);
+        const uint32_t i = tid + k * BLOCK;
+        const uint32_t o = n * BLOCK + tid;
+        const uint64_t x = mg[i], aux = aux_table(i);
+        rc_k[o] = k;
+        rc_mg[o] = x;
+        rc_aux[o] = aux;
+        rc_key[o] = key_from(x, aux);
+        ++n;
+      }
     }
+    rc_used = n ? (0xFFFFFFFFu >> (32u - n)) : 0u;
+  }
+
+  // Keeps the owner's residency bit, and its resident cache, in step with
+  // an entry's new meta m: its whole new meta / gap word is x when has_x,
+  // else m over the old gap EMA; its aux field changes to aux when has_aux.
+  __device__ __forceinline__ void note(uint32_t sid, uint32_t m, uint64_t x, bool has_x,
+                                       uint64_t aux, bool has_aux) {
+    if ((sid & (BLOCK - 1u)) != tid) return;
+    const uint32_t k = sid / BLOCK;
+    uint32_t* w = res + (k >> 5) * BLOCK + tid;
+    const uint32_t bit = 1u << (k & 31u);
+    const bool was = (*w & bit) != 0;
+    const bool now = meta_tier(m) != kTierNone;
+    *w = now ? (*w | bit) : (*w & ~bit);
+    if constexpr (CACHE) {
+      constexpr uint64_t kGapHalf = 0xFFFFFFFF00000000ull;
+      uint32_t slot = kNone;
+      if (was && n_mine <= rc_cap) {
+        for (uint32_t u = rc_used; u; u &= u - 1u) {
+          const uint32_t t = (uint32_t)__builtin_ctz(u);
+          if (rc_k[t * BLOCK + tid] == k) slot = t;
+        }
+      }
+      if (now && !was) {
+        ++n_mine;
+        if (n_mine <= rc_cap) {
+          // a placement follows the arriving session's write(); otherwise
+          // the entry's other fields come from the table
+          const bool latest = sid == w_sid;
+          if (!has_x) x = ((latest ? w_x : mg[sid]) & kGapHalf) | m;
+          if (!has_aux) aux = latest ? w_aux : aux_table(sid);
+          slot = (uint32_t)__builtin_ctz(~rc_used);
+          rc_used |= 1u << slot;
+          const uint32_t o = slot * BLOCK + tid;
+          rc_k[o] = k;
+          rc_mg[o] = x;
+          rc_aux[o] = aux;
+          rc_key[o] = key_from(x, aux);
+        } else {
+          rc_used = 0;  // more residents than slots: the scans read the table
+        }
+      } else if (!now && was) {
+        --n_mine;
+        if (slot != kNone) rc_used &= ~(1u << slot);
+        else if (n_mine == rc_cap) rc_refill();
+      } else if (slot != kNone) {
+        // a meta word alone changes the tier or the prefetch flag, which no
+        // key reads; new EMAs or times change the key
+        const uint32_t o = slot * BLOCK + tid;
+        x = has_x ? x : (rc_mg[o] & kGapHalf) | m;
+        rc_mg[o] = x;
+        if (has_aux) rc_aux[o] = aux;
+        if (has_x || has_aux) rc_key[o] = key_from(x, has_aux ? aux : rc_aux[o]);
+      }
+    }
+  }
+  // An entry's meta word alone: the low half of its meta / gap word.
+  __device__ __forceinline__ void store_meta(uint32_t sid, uint32_t m) {
+    reinterpret_cast<uint32_t*>(mg + sid)[0] = m;
   }
   // Words per thread that cover entries [0, hi).
   __device__ __forceinline__ uint32_t res_words() const { return (hi + 32u * BLOCK - 1u) / (32u * BLOCK); }
@@ -582,8 +692,13 @@ struct MemTable {
     e.gq = PT::fixed ? uni64(gq[sid]) : 0ull;
     __syncthreads();
   }
-  __device__ __forceinline__ void write_end(uint32_t sid, uint32_t m, uint64_t t, uint64_t nx) {
-    set_meta(sid, m);
+  __device__ __forceinline__ void write_end(uint32_t sid, const Entry& e, uint64_t t, uint64_t nx) {
+    const uint32_t m = e.meta;
+    const uint64_t x = (uint64_t)m | ((uint64_t)__float_as_uint(e.g) << 32);
+    // the event moves the key's time field (LRU / timeout: last; Belady: next)
+    note(sid, m, x, true, aux_pick(e.gq, t, nx), true);
+    w_sid = kNone;
+    store_meta(sid, m);
     last[sid] = t;
     if constexpr (PT::belady) next[sid] = nx;
   }
@@ -591,17 +706,20 @@ struct MemTable {
   // them; reads end with a barrier and each event starts with one, so no wave
   // writes an entry that another wave has still to read.
   __device__ __forceinline__ void write(uint32_t sid, const Entry& e) {
-    mark(sid, e.meta);
-    mg[sid] = (uint64_t)e.meta | ((uint64_t)__float_as_uint(e.g) << 32);
+    const uint64_t x = (uint64_t)e.meta | ((uint64_t)__float_as_uint(e.g) << 32);
+    w_sid = sid;
+    w_x = x;
+    w_aux = aux_pick(e.gq, e.last, e.next);
+    note(sid, e.meta, x, true, w_aux, true);
+    mg[sid] = x;
     if constexpr (PT::fixed) gq[sid] = e.gq;
     len[sid] = e.len;
     last[sid] = e.last;
     if constexpr (PT::belady) next[sid] = e.next;
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) {
-    mark(sid, m);
-    const uint64_t x = mg[sid];
-    mg[sid] = (x & 0xFFFFFFFF00000000ull) | m;
+    note(sid, m, 0ull, false, 0ull, false);
+    store_meta(sid, m);
   }
   __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
     set_meta(sid, m);
@@ -697,6 +815,39 @@ struct MemTable {
                               PT::recency ? l[i] : 0ull, PT::belady ? n[i] : 0ull);
   }
 
+  // f(i, x, aux, k) for each resident entry i of this thread: x its live
+  // meta / gap word, aux its live aux field and k its key (from the copies
+  // set_src chose, for the dual design), from the resident cache or the
+  // table.
+  template <class F>
+  __device__ __forceinline__ void each_resident(const KeyCtx& K, F&& f) const {
+    if constexpr (CACHE) {
+      if (n_mine <= rc_cap) {
+        for (uint32_t u = rc_used; u; u &= u - 1u) {
+          const uint32_t o = (uint32_t)__builtin_ctz(u) * BLOCK + tid;
+          f(tid + rc_k[o] * BLOCK, rc_mg[o], rc_aux[o], rc_key[o]);
+        }
+        return;
+      }
+    }
+    const uint32_t nw = res_words();
+    for (uint32_t w = 0; w < nw; ++w) {
+      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
+        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
+        const uint64_t x = mg[i], aux = aux_table(i);
+        uint64_t k;
+        if constexpr (VIEWS) {
+          k = key_at(K, i, x);
+        } else {
+          const uint32_t m = (uint32_t)x;
+          k = key_of<POL, SMODE>(K, m, hazard_of<POL, SMODE>(K, m),
+                                 __uint_as_float((uint32_t)(x >> 32)), aux, aux, aux);
+        }
+        f(i, x, aux, k);
+      }
+    }
+  }
+
   // Overwrites both copies with the live key fields of every entry.
   __device__ __forceinline__ void sync_views() {
     const size_t st = view_stride;
@@ -718,19 +869,13 @@ struct MemTable {
   template <bool MAX>
   __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx& K) {
     Cand c = MAX ? cand_none_max() : cand_none_min();
-    const uint32_t nw = res_words();
-    for (uint32_t w = 0; w < nw; ++w) {
-      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
-        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
-        const uint64_t x = mg[i];
-        const uint32_t m = (uint32_t)x;
-        const bool ok = evictable(m) && (tier == 0 || meta_tier(m) == tier);
-        const uint64_t k = key_at(K, i, x);
-        const bool take = ok && (MAX ? max_better(k, i, c.key, c.sid) : min_better(k, i, c.key, c.sid));
-        c.key = take ? k : c.key;
-        c.sid = take ? i : c.sid;
-      }
-    }
+    each_resident(K, [&](uint32_t i, uint64_t x, uint64_t, uint64_t k) {
+      const uint32_t m = (uint32_t)x;
+      const bool ok = evictable(m) && (tier == 0 || meta_tier(m) == tier);
+      const bool take = ok && (MAX ? max_better(k, i, c.key, c.sid) : min_better(k, i, c.key, c.sid));
+      c.key = take ? k : c.key;
+      c.sid = take ? i : c.sid;
+    });
     return block_reduce<MAX>(c);
   }
   // The first reduction of an event is the full-table scan.
@@ -739,24 +884,18 @@ struct MemTable {
   // TIDE's two candidates, eq. (promote) and eq. (demote), from one pass.
   __device__ __forceinline__ void select_pd(const KeyCtx& K, Cand& p, Cand& d) {
     Cand cp = cand_none_min(), cd = cand_none_max();
-    const uint32_t nw = res_words();
-    for (uint32_t w = 0; w < nw; ++w) {
-      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
-        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
-        const uint64_t x = mg[i];
-        const uint32_t m = (uint32_t)x;
-        const bool ev = evictable(m);
-        const bool in_h = ev && meta_tier(m) == kTierHbm;
-        const bool in_s = ev && meta_tier(m) == kTierSram;
-        const uint64_t k = key_at(K, i, x);
-        const bool tp = in_h && min_better(k, i, cp.key, cp.sid);
-        const bool td = in_s && max_better(k, i, cd.key, cd.sid);
-        cp.key = tp ? k : cp.key;
-        cp.sid = tp ? i : cp.sid;
-        cd.key = td ? k : cd.key;
-        cd.sid = td ? i : cd.sid;
-      }
-    }
+    each_resident(K, [&](uint32_t i, uint64_t x, uint64_t, uint64_t k) {
+      const uint32_t m = (uint32_t)x;
+      const bool ev = evictable(m);
+      const bool in_h = ev && meta_tier(m) == kTierHbm;
+      const bool in_s = ev && meta_tier(m) == kTierSram;
+      const bool tp = in_h && min_better(k, i, cp.key, cp.sid);
+      const bool td = in_s && max_better(k, i, cd.key, cd.sid);
+      cp.key = tp ? k : cp.key;
+      cp.sid = tp ? i : cp.sid;
+      cd.key = td ? k : cd.key;
+      cd.sid = td ? i : cd.sid;
+    });
     p = block_reduce<false>(cp);
     d = block_reduce<true>(cd);
   }
@@ -764,25 +903,19 @@ struct MemTable {
   // the residents and one barrier.
   __device__ __forceinline__ void scan3(const KeyCtx& K, Cand& v, Cand& p, Cand& d) {
     Cand cv = cand_none_max(), cp = cand_none_min(), cd = cand_none_max();
-    const uint32_t nw = res_words();
-    for (uint32_t w = 0; w < nw; ++w) {
-      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
-        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
-        const uint64_t x = mg[i];
-        const uint32_t m = (uint32_t)x;
-        const bool ev = evictable(m);
-        const uint64_t k = key_at(K, i, x);
-        const bool tv = ev && max_better(k, i, cv.key, cv.sid);
-        const bool tp = ev && meta_tier(m) == kTierHbm && min_better(k, i, cp.key, cp.sid);
-        const bool td = ev && meta_tier(m) == kTierSram && max_better(k, i, cd.key, cd.sid);
-        cv.key = tv ? k : cv.key;
-        cv.sid = tv ? i : cv.sid;
-        cp.key = tp ? k : cp.key;
-        cp.sid = tp ? i : cp.sid;
-        cd.key = td ? k : cd.key;
-        cd.sid = td ? i : cd.sid;
-      }
-    }
+    each_resident(K, [&](uint32_t i, uint64_t x, uint64_t, uint64_t k) {
+      const uint32_t m = (uint32_t)x;
+      const bool ev = evictable(m);
+      const bool tv = ev && max_better(k, i, cv.key, cv.sid);
+      const bool tp = ev && meta_tier(m) == kTierHbm && min_better(k, i, cp.key, cp.sid);
+      const bool td = ev && meta_tier(m) == kTierSram && max_better(k, i, cd.key, cd.sid);
+      cv.key = tv ? k : cv.key;
+      cv.sid = tv ? i : cv.sid;
+      cp.key = tp ? k : cp.key;
+      cp.sid = tp ? i : cp.sid;
+      cd.key = td ? k : cd.key;
+      cd.sid = td ? i : cd.sid;
+    });
     block_reduce3(cv, cp, cd);
     v = cv;
     p = cp;
@@ -798,22 +931,27 @@ struct MemTable {
   __device__ __forceinline__ void hazard_add(const KeyCtx& K, uint32_t Tn) {
     hazard_add_counts(K, Tn, tid, BLOCK);
     __syncthreads();
+    if constexpr (CACHE) {
+      // every cached key reads the table that just changed
+      if (n_mine <= rc_cap) {
+        for (uint32_t u = rc_used; u; u &= u - 1u) {
+          const uint32_t o = (uint32_t)__builtin_ctz(u) * BLOCK + tid;
+          rc_key[o] = key_from(rc_mg[o], rc_aux[o]);
+        }
+      }
+    }
   }
 
   __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) {
     const uint64_t thr = idle_threshold(now, ttl);
     Cand c = cand_none_min();
-    const uint32_t nw = res_words();
-    for (uint32_t w = 0; w < nw; ++w) {
-      for (uint32_t bits = res[w * BLOCK + tid]; bits; bits &= bits - 1u) {
-        const uint32_t i = tid + (w * 32u + (uint32_t)__builtin_ctz(bits)) * BLOCK;
-        const uint32_t m = (uint32_t)mg[i];
-        if (evictable(m) && last[i] < thr && i < c.sid) {
-          c.sid = i;
-          c.key = 0;
-        }
+    // the timeout policy's aux field is the last event time
+    each_resident(kc, [&](uint32_t i, uint64_t x, uint64_t last_t, uint64_t) {
+      if (evictable((uint32_t)x) && last_t < thr && i < c.sid) {
+        c.sid = i;
+        c.key = 0;
       }
-    }
+    });
     return block_reduce<false>(c).sid;
   }
 };
@@ -1078,7 +1216,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       T.read_end(sid, x);
       tier0 = meta_tier(x.meta);
       x.meta = make_meta(kind == kGapStart ? kGap : kDoneP, tier0, meta_turn(x.meta));
-      T.write_end(sid, x.meta, now, kind == kGapStart ? cur_next : ~0ull);
+      T.write_end(sid, x, now, kind == kGapStart ? cur_next : ~0ull);
       // an online hazard table counts the completed session before the scan
       if (kind == kDone && K.online_cap && T.hazard_open(K)) T.hazard_add(K, meta_turn(x.meta) + 1u);
     }
@@ -1517,10 +1655,18 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   const size_t tb = (size_t)sim * a.max_sessions;
   const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
 
-  MemTable<BLOCK, POL, SMODE, VIEWS> T;
+  constexpr bool kCache = !IN_LDS && !VIEWS;
+  MemTable<BLOCK, POL, SMODE, VIEWS, kCache> T;
   T.tid = tid;
   T.parity = 0;
   T.red = s_red;
+  T.rc_cap = 0;
+  T.rc_used = 0;
+  T.kc = K;
+  T.n_mine = 0;
+  T.w_sid = kNone;
+  T.w_x = 0;
+  T.w_aux = 0;
   if constexpr (IN_LDS) {
     const uint32_t n = n_sess;
     T.mg = s_tab;
@@ -1548,6 +1694,15 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
     T.next = a.t_next + tb;
     T.kvb = a.sess_kvb + sb;
     T.res = reinterpret_cast<uint32_t*>(s_tab);
+    if constexpr (kCache) {
+      // the resident cache's slots follow the residency bits
+      const uint32_t cap = a.rc_slots;
+      T.rc_cap = cap;
+      T.rc_mg = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(s_tab) + a.rc_off);
+      T.rc_aux = T.rc_mg + (size_t)cap * BLOCK;
+      T.rc_key = T.rc_aux + (size_t)cap * BLOCK;
+      T.rc_k = reinterpret_cast<uint32_t*>(T.rc_key + (size_t)cap * BLOCK);
+    }
     if (!cont) {
       for (uint32_t i = tid; i < n_sess; i += BLOCK) {
         T.mg[i] = 0;
@@ -1586,6 +1741,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
       if (cont && i < n_sess && meta_tier((uint32_t)T.mg[i]) != kTierNone) bits |= 1u << b;
     }
     T.res[w * BLOCK + tid] = bits;
+    T.n_mine += (uint32_t)__builtin_popcount(bits);
   }
 
   Scalars S;
@@ -1601,6 +1757,9 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   }
   if (S.hi > n_sess) S.hi = n_sess;  // never scan past the trace's sessions
   T.hi = S.hi;
+  if constexpr (kCache) {
+    if (T.n_mine && T.n_mine <= T.rc_cap) T.rc_refill();  // a resumed table's residents
+  }
   if (P.dual_sync && !(VIEWS && a.views)) C.error = ~0ull;  // the launcher picks the copies' kernel
   pin_vgpr(S);
   pin_vgpr(C);
@@ -1752,6 +1911,25 @@ int sim_auto_variant(uint32_t max_sess) {
   return 10;
 }
 
+// The streamed-table kernels' resident cache: slots per thread of 8 + 8 + 8
+// + 4 bytes each, after the residency bits; as many as the LDS left by the bits
+// allows, up to kCacheSlots, or fewer when a test pins the count.
+constexpr uint32_t kCacheSlots = 8;
+static size_t cache_bytes(uint32_t slots, uint32_t block) {
+  return (size_t)slots * block * (3 * sizeof(uint64_t) + sizeof(uint32_t));
+}
+static SimArgs with_cache(const SimArgs& a, uint32_t n_sess, uint32_t block, int force_slots) {
+  SimArgs b = a;
+  const size_t bits = res_bytes(n_sess ? n_sess : 1, block);
+  const size_t lim = lds_limit();
+  uint32_t slots = 0;
+  while (slots < kCacheSlots && bits + cache_bytes(slots + 1, block) <= lim) ++slots;
+  if (force_slots >= 0 && (uint32_t)force_slots < slots) slots = (uint32_t)force_slots;
+  b.rc_off = (uint32_t)bits;
+  b.rc_slots = slots;
+  return b;
+}
+
 template <int G, int EPL>
 static void launch_regs(const SimArgs& a, hipStream_t stream) {
   const uint32_t groups_per_block = 256 / G;
@@ -1760,7 +1938,7 @@ static void launch_regs(const SimArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream,
-                      int force_variant) {
+                      int force_variant, int force_cache_slots) {
   const int v = force_variant >= 0 ? force_variant : sim_auto_variant(max_sess_in_batch);
   switch (v) {
     case 0: launch_regs<16, 1>(a, stream); break;
@@ -1776,18 +1954,22 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
       hipLaunchKernelGGL((sim_block_kernel<kBlock, true, false>), dim3(a.n_sims), dim3(kBlock), lds, stream, a);
       break;
     }
-    case 10:
+    case 10: {
+      SimArgs b = with_cache(a, max_sess_in_batch, 512, force_cache_slots);
       hipLaunchKernelGGL((sim_block_kernel<512, false, false>), dim3(a.n_sims), dim3(512),
-                         res_bytes(max_sess_in_batch, 512), stream, a);
+                         b.rc_off + cache_bytes(b.rc_slots, 512), stream, b);
       break;
+    }
     case kDualVariant:
       hipLaunchKernelGGL((sim_block_kernel<512, false, true>), dim3(a.n_sims), dim3(512),
                          res_bytes(max_sess_in_batch, 512), stream, a);
       break;
-    case 3:
+    case 3: {
+      SimArgs b = with_cache(a, max_sess_in_batch, kBlock, force_cache_slots);
       hipLaunchKernelGGL((sim_block_kernel<kBlock, false, false>), dim3(a.n_sims), dim3(kBlock),
-                         res_bytes(max_sess_in_batch, kBlock), stream, a);
+                         b.rc_off + cache_bytes(b.rc_slots, kBlock), stream, b);
       break;
+    }
     default:
       return hipErrorInvalidValue;
   }

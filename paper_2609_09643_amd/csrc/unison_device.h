@@ -202,6 +202,8 @@ struct SimArgs {
   uint32_t flags;
   uint32_t policy_override;
   uint32_t time44;         // every trace time is below 2^44 - 1 ns
+  uint32_t rc_off;         // streamed tables: byte offset of the resident cache in dynamic LDS
+  uint32_t rc_slots;       // and its slots per thread (set by the launcher)
 };
 
 }  // namespace unison

@@ -91,6 +91,7 @@ def lib():
             "unison_score_fixed": [vp, u32, vp, vp, vp, vp, vp, u32, u64, vp],
             "unison_kendall": [vp, u32, u32, u64, vp, vp, vp, vp, vp],
             "unison_debug_force_variant": [vp, i32],
+            "unison_debug_cache_slots": [vp, i32],
             "unison_set_stream": [vp, vp],
         }
         for name, args in sig.items():
@@ -154,7 +155,7 @@ class Simulator:
     """A batch of simulations on the GPU: traces, hazard tables and parameter
     rows of a workload (see paper_2609_09643_amd.synth.Workload)."""
 
-    def __init__(self, workload, log_cap=0, variant=None):
+    def __init__(self, workload, log_cap=0, variant=None, cache_slots=None):
         torch = _torch()
         L = lib()
         self.workload = workload
@@ -190,6 +191,8 @@ class Simulator:
                                C.c_void_p(aligned), C.c_size_t(self.ws_bytes)))
         if variant is not None:
             _check(L.unison_debug_force_variant(self.ctx, int(variant)), self.ctx)
+        if cache_slots is not None:
+            _check(L.unison_debug_cache_slots(self.ctx, int(cache_slots)), self.ctx)
         tb = TraceBatch()
         tb.n_traces = len(traces)
         self._ev_off_c = (C.c_uint64 * len(ev_off))(*[int(x) for x in ev_off])

@@ -120,6 +120,22 @@ def test_random_batches_split_by_continue(case):
         del s
 
 
+def test_random_batches_with_few_cache_slots(case):
+    """The streamed kernels with zero and one resident-cache slot per
+    thread, across a CONTINUE: every thread with residents reads the table
+    or refills its slot."""
+    name, w, want, _ = case
+    longest = max(t.n_events for t in w.traces)
+    for v in (3, 10):
+        for slots in (0, 1):
+            say("random %s: variant %s, %d cache slots" % (name, v, slots))
+            s = Sim(w, variant=v, cache_slots=slots)
+            s.run(max_events=max(1, longest // 3))
+            s.run(flags=1)
+            compare_counters(s.counters(), want, label="random %s variant %s, %d slots" % (name, v, slots))
+            del s
+
+
 def test_random_decision_logs(case):
     """Full ordered decision logs of a few simulations of each batch."""
     from parity import oracle_log, same_log

@@ -253,6 +253,19 @@ def test_wide_sparse_table_residency_words(sparse_wide, variant):
     assert int(got["hit_sram"][0]) + int(got["hit_hbm"][0]) > 0
 
 
+@pytest.mark.parametrize("variant,slots", [(3, 0), (3, 1), (3, 3), (10, 1), (10, 2)])
+def test_wide_sparse_table_few_cache_slots(sparse_wide, variant, slots):
+    """The streamed kernels keep each thread's residents in a few LDS slots.
+    With fewer slots than most threads have residents (~6.6 per thread of
+    256, ~3.3 of 512), threads keep crossing their slot count both ways as
+    sessions come and go: they read the table, then refill their slots.
+    The counters are the oracle's whatever the count."""
+    w, want = sparse_wide
+    s = Sim(w, variant=variant, cache_slots=slots)
+    s.run()
+    compare_counters(s.counters(), want, label="sparse wide variant %s, %d slots" % (variant, slots))
+
+
 def edge_workload(traces, rows):
     luts = [np.array([1, 2, 2, 3, 30, 51, 60], np.uint32), None]
     return synth.Workload("edge", traces, luts, rows, flat_luts=[(1, 3, 7)])
