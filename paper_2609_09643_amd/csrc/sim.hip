@@ -236,6 +236,9 @@ struct Entry {
 
 // ------------------------------------------------------------ tables
 
+// Most resident-cache slots per thread of the streamed-table kernels.
+constexpr uint32_t kCacheSlotsMax = 8;
+
 template <int G, int EPL, uint32_t POL, uint32_t SMODE>
 struct RegTable {
   using PT = Pol<POL, SMODE>;
@@ -755,20 +758,39 @@ struct MemTable {
     return b;
   }
 
-  // The wavefronts' results, read back from LDS after the barrier.
-  template <bool MAX>
-  __device__ __forceinline__ Cand combine(const Cand* buf) const {
-    uint64_t rk = buf[0].key;
-    uint32_t rs = buf[0].sid;
+
+  // Lane l of every wavefront takes buf[l]: NW per reduction, up to three
+  // reductions side by side (lanes [r NW, (r + 1) NW) for reduction r, an
+  // argmax where is_max, else an argmin); a butterfly within each group of
+  // NW lanes leaves its winner in all of them.
+  __device__ __forceinline__ Cand gather_best(const Cand* buf, uint32_t n_red, uint32_t max_mask) const {
+    const uint32_t l = tid & 63u;
+    const uint32_t r = l / NW;
+    const bool is_max = (max_mask >> (r < 3u ? r : 0u)) & 1u;
+    Cand c = is_max ? cand_none_max() : cand_none_min();
+    if (r < n_red) c = buf[l];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) {
-      const uint64_t ok = buf[w].key;
-      const uint32_t os = buf[w].sid;
-      const bool take = MAX ? max_better(ok, os, rk, rs) : min_better(ok, os, rk, rs);
-      rk = take ? ok : rk;
-      rs = take ? os : rs;
+    for (uint32_t m = 1; m < (uint32_t)NW; m <<= 1) {
+      uint32_t klo, khi, s;
+      if (m == 1) {
+        klo = xchg<1>((uint32_t)c.key); khi = xchg<1>((uint32_t)(c.key >> 32)); s = xchg<1>(c.sid);
+      } else if (m == 2) {
+        klo = xchg<2>((uint32_t)c.key); khi = xchg<2>((uint32_t)(c.key >> 32)); s = xchg<2>(c.sid);
+      } else {
+        klo = xchg<4>((uint32_t)c.key); khi = xchg<4>((uint32_t)(c.key >> 32)); s = xchg<4>(c.sid);
+      }
+      const uint64_t k = ((uint64_t)khi << 32) | klo;
+      const bool take = is_max ? max_better(k, s, c.key, c.sid) : min_better(k, s, c.key, c.sid);
+      c.key = take ? k : c.key;
+      c.sid = take ? s : c.sid;
     }
-    return Cand{uni64(rk), uni32(rs)};
+    return c;
+  }
+  __device__ __forceinline__ static Cand lane_cand(const Cand& c, int lane) {
+    const uint32_t khi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(c.key >> 32), lane);
+    const uint32_t klo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)c.key, lane);
+    const uint32_t s = (uint32_t)__builtin_amdgcn_readlane((int)c.sid, lane);
+    return Cand{((uint64_t)khi << 32) | klo, s};
   }
 
   template <bool MAX>
@@ -778,7 +800,7 @@ struct MemTable {
     parity ^= 1u;
     if ((tid & 63u) == 0) buf[tid >> 6] = c;
     __syncthreads();
-    return combine<MAX>(buf);
+    return lane_cand(gather_best(buf, 1, MAX ? 1u : 0u), 0);
   }
 
   // Three reductions (max, min, max) behind one barrier.
@@ -794,9 +816,10 @@ struct MemTable {
       buf[2 * NW + (tid >> 6)] = d;
     }
     __syncthreads();
-    v = combine<true>(buf);
-    p = combine<false>(buf + NW);
-    d = combine<true>(buf + 2 * NW);
+    const Cand g = gather_best(buf, 3, 0x5u);
+    v = lane_cand(g, 0);
+    p = lane_cand(g, NW);
+    d = lane_cand(g, 2 * NW);
   }
 
   __device__ __forceinline__ uint64_t key_at(const KeyCtx& K, uint32_t i, uint64_t x) const {
@@ -823,9 +846,25 @@ struct MemTable {
   __device__ __forceinline__ void each_resident(const KeyCtx& K, F&& f) const {
     if constexpr (CACHE) {
       if (n_mine <= rc_cap) {
-        for (uint32_t u = rc_used; u; u &= u - 1u) {
-          const uint32_t o = (uint32_t)__builtin_ctz(u) * BLOCK + tid;
-          f(tid + rc_k[o] * BLOCK, rc_mg[o], rc_aux[o], rc_key[o]);
+        // the next slot's loads issue before the current slot is used
+        uint32_t u = rc_used;
+        if (u) {
+          uint32_t o = (uint32_t)__builtin_ctz(u) * BLOCK + tid;
+          uint32_t ck = rc_k[o];
+          uint64_t cx = rc_mg[o], ca = rc_aux[o], cv = rc_key[o];
+          for (;;) {
+            u &= u - 1u;
+            const bool more = u != 0;
+            o = more ? (uint32_t)__builtin_ctz(u) * BLOCK + tid : o;
+            const uint32_t nk = rc_k[o];
+            const uint64_t nx = rc_mg[o], na = rc_aux[o], nv = rc_key[o];
+            f(tid + ck * BLOCK, cx, ca, cv);
+            if (!more) break;
+            ck = nk;
+            cx = nx;
+            ca = na;
+            cv = nv;
+          }
         }
         return;
       }
@@ -1914,7 +1953,7 @@ int sim_auto_variant(uint32_t max_sess) {
 // The streamed-table kernels' resident cache: slots per thread of 8 + 8 + 8
 // + 4 bytes each, after the residency bits; as many as the LDS left by the bits
 // allows, up to kCacheSlots, or fewer when a test pins the count.
-constexpr uint32_t kCacheSlots = 8;
+constexpr uint32_t kCacheSlots = kCacheSlotsMax;
 static size_t cache_bytes(uint32_t slots, uint32_t block) {
   return (size_t)slots * block * (3 * sizeof(uint64_t) + sizeof(uint32_t));
 }
