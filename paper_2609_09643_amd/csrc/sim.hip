@@ -803,6 +803,22 @@ struct MemTable {
     return lane_cand(gather_best(buf, 1, MAX ? 1u : 0u), 0);
   }
 
+  // Two reductions (min, max) behind one barrier.
+  __device__ __forceinline__ void block_reduce2(Cand& p, Cand& d) {
+    p = wave_best<false>(p);
+    d = wave_best<true>(d);
+    Cand* buf = red + parity * 3 * NW;
+    parity ^= 1u;
+    if ((tid & 63u) == 0) {
+      buf[tid >> 6] = p;
+      buf[NW + (tid >> 6)] = d;
+    }
+    __syncthreads();
+    const Cand g = gather_best(buf, 2, 0x2u);
+    p = lane_cand(g, 0);
+    d = lane_cand(g, NW);
+  }
+
   // Three reductions (max, min, max) behind one barrier.
   __device__ __forceinline__ void block_reduce3(Cand& v, Cand& p, Cand& d) {
     v = wave_best<true>(v);
@@ -935,8 +951,9 @@ struct MemTable {
       cd.key = td ? k : cd.key;
       cd.sid = td ? i : cd.sid;
     });
-    p = block_reduce<false>(cp);
-    d = block_reduce<true>(cd);
+    block_reduce2(cp, cd);
+    p = cp;
+    d = cd;
   }
   // A gap onset's scan victim and TIDE's first candidates from one pass over
   // the residents and one barrier.
