@@ -266,6 +266,30 @@ def test_wide_sparse_table_few_cache_slots(sparse_wide, variant, slots):
     compare_counters(s.counters(), want, label="sparse wide variant %s, %d slots" % (variant, slots))
 
 
+def test_wide_sparse_table_logs_with_one_cache_slot(sparse_wide):
+    """Full decision logs, each event's scan victim included, of all four
+    policies on the 256-thread streamed kernel with one resident-cache slot
+    per thread: every eviction, expiry, placement and TIDE move, in order,
+    and every event's victim are the oracle's while threads keep leaving and
+    refilling their slot."""
+    w, _ = sparse_wide
+    tr = w.traces[0]
+    cap = 1 << 18
+    s = Sim(w, log_cap=cap, variant=3, cache_slots=1)
+    s.run(flags=2 | 4)
+    D, N = oracle.luts_for(w)
+    for i in range(w.n_sims):
+        g = s.log(i)
+        row = w.params[i]
+        _, _, olog, st, _ = oracle.run(tr, row, D[int(row["lut"])], N[int(row["lut"])],
+                                       log_cap=cap, states=True)
+        gv = g[g["op"] == 6]["a"]
+        assert len(gv) == tr.n_events
+        bad = np.nonzero(gv != st["victim"])[0]
+        assert len(bad) == 0, "sparse wide sim %d: scan victim differs at events %s" % (i, bad[:5].tolist())
+        assert len(olog) > 0 and same_log(g[g["op"] != 6], olog), "sparse wide sim %d decision log" % i
+
+
 def edge_workload(traces, rows):
     luts = [np.array([1, 2, 2, 3, 30, 51, 60], np.uint32), None]
     return synth.Workload("edge", traces, luts, rows, flat_luts=[(1, 3, 7)])
