@@ -21,6 +21,7 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
                       int force_cache_slots);
 uint32_t sim_variant_capacity(int v);
 int sim_auto_variant(uint32_t max_sess);
+uint32_t sim_variant_lanes(int v);
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
                                 hipStream_t stream);
 hipError_t launch_max_time(const uint64_t* t, const uint64_t* next, uint64_t n, uint64_t* out,
@@ -51,7 +52,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // Workspace layout; offsets in bytes from the workspace base.
 struct Layout {
   size_t params, ev_off, first_bad, sess_off, lut_d, lut_n, state, counters, hcount, mg, gq, len, last, next,
-      views, log, scratch, total;
+      views, log, slots, scratch, total;
 };
 
 bool make_layout(const unison_dims& d, Layout& L) {
@@ -78,6 +79,9 @@ bool make_layout(const unison_dims& d, Layout& L) {
   L.next = take(sizeof(uint64_t) * entries);
   L.views = take(d.views ? sizeof(uint64_t) * 8 * entries : 0);
   L.log = take(sizeof(unison_record) * (size_t)d.log_cap * d.n_sims);
+  // register-table lane groups -> simulations: at most one partly filled
+  // wavefront per simulation, of up to kMaxGroupsPerWave groups
+  L.slots = take(sizeof(uint32_t) * (size_t)kMaxGroupsPerWave * d.n_sims);
   L.scratch = take(256);
   L.total = off;
   return true;
@@ -137,6 +141,12 @@ struct unison_ctx {
   uint32_t max_sess_batch = 0;
   int force_variant = -1;
   int force_cache_slots = -1;  // test hook: resident-cache slots of the streamed tables
+  // the register-table kernels' lane-group -> simulation map (slot_map)
+  std::vector<uint32_t> h_slots;
+  uint64_t params_gen = 0;         // bumped by every unison_set_params
+  uint64_t slots_for = ~0ull;      // (params_gen, policy override, lanes) the map was built for
+  bool slots_identity = true;
+  uint32_t n_slots = 0;
   char err[512];
 
   template <class T>
@@ -341,6 +351,58 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
   if (rc) return rc;
   ctx->max_sess_batch = max_sess;
   ctx->params_set = true;
+  ctx->params_gen++;
+  return UNISON_OK;
+}
+
+// Register-table kernels run a group of `lanes` lanes per simulation, 64 /
+// lanes groups to a wavefront, and a wavefront executes every path any of
+// its simulations takes.  The map puts simulations that share policy, score
+// form and trace side by side and starts a new wavefront where they change
+// (the groups left over stay empty), so a wavefront never serialises two
+// policies or two traces' event kinds.  A batch already in that order keeps
+// the identity map (no map at all).
+static int slot_map(unison_ctx* ctx, uint32_t policy_override, uint32_t lanes) {
+  const uint64_t key = (ctx->params_gen << 16) ^ ((uint64_t)policy_override << 8) ^ lanes;
+  if (ctx->slots_for == key) return UNISON_OK;
+  const uint32_t n = ctx->dims.n_sims;
+  const uint32_t gpw = 64u / lanes;
+  if (gpw == 1) {  // one simulation per wavefront: nothing to group
+    ctx->slots_identity = true;
+    ctx->n_slots = n;
+    ctx->slots_for = key;
+    return UNISON_OK;
+  }
+  auto sort_key = [&](uint32_t i) {
+    const unison_sim_params& p = ctx->h_params[i];
+    const uint32_t pol = policy_override == UNISON_POLICY_PARAMS ? p.policy : policy_override;
+    const uint32_t mode = pol == UNISON_POLICY_SPEAR ? p.score_mode : 0u;
+    return ((uint64_t)pol << 40) | ((uint64_t)mode << 32) | p.trace;
+  };
+  std::vector<uint32_t> order(n);
+  for (uint32_t i = 0; i < n; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](uint32_t a, uint32_t b) { return sort_key(a) < sort_key(b); });
+  ctx->h_slots.clear();
+  for (uint32_t j = 0; j < n; ++j) {
+    if (j && sort_key(order[j]) != sort_key(order[j - 1]))
+      while (ctx->h_slots.size() % gpw) ctx->h_slots.push_back(0xFFFFFFFFu);
+    ctx->h_slots.push_back(order[j]);
+  }
+  bool identity = ctx->h_slots.size() == n;
+  for (uint32_t j = 0; identity && j < n; ++j) identity = ctx->h_slots[j] == j;
+  ctx->slots_identity = identity;
+  ctx->n_slots = identity ? n : (uint32_t)ctx->h_slots.size();
+  if (!identity) {
+    int rc = ctx->hip(hipMemcpyAsync(ctx->at<uint32_t>(ctx->L.slots), ctx->h_slots.data(),
+                                     sizeof(uint32_t) * ctx->h_slots.size(), hipMemcpyHostToDevice,
+                                     ctx->stream),
+                      "copy lane-group map");
+    if (rc) return rc;
+    rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise after lane-group map");
+    if (rc) return rc;
+  }
+  ctx->slots_for = key;
   return UNISON_OK;
 }
 
@@ -402,6 +464,16 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
     if (sim_variant_capacity(v) < ctx->max_sess_batch)
       return ctx->fail(UNISON_E_CAPACITY, "%u sessions exceed every kernel variant (largest %u)",
                        ctx->max_sess_batch, sim_variant_capacity(v));
+  }
+  a.slot_sim = nullptr;
+  a.n_slots = a.n_sims;
+  if (const uint32_t lanes = sim_variant_lanes(v)) {
+    const int mrc = slot_map(ctx, policy_override, lanes);
+    if (mrc) return mrc;
+    if (!ctx->slots_identity) {
+      a.slot_sim = ctx->at<uint32_t>(ctx->L.slots);
+      a.n_slots = ctx->n_slots;
+    }
   }
   int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->stream, v, ctx->force_cache_slots), "launch simulation");
   if (rc == UNISON_OK) ctx->ran = true;

@@ -1671,7 +1671,8 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
   __shared__ uint32_t s_hd[GROUPS][52];
   __shared__ uint32_t s_hn[GROUPS][52];
   const uint32_t gtid = blockIdx.x * 256u + threadIdx.x;
-  const uint32_t sim = gtid / G;
+  const uint32_t slot = gtid / G;
+  const uint32_t sim = a.slot_sim ? (slot < a.n_slots ? a.slot_sim[slot] : kNone) : slot;
   const uint32_t lane = gtid % G;
   const uint32_t grp = threadIdx.x / G;
   const bool live = sim < a.n_sims;
@@ -1956,6 +1957,12 @@ uint32_t sim_variant_capacity(int v) {
   return (uint32_t)(kVariants[v].g * kVariants[v].epl);
 }
 
+// Lanes per simulation of a register-table variant; 0 for the workgroup kernels.
+uint32_t sim_variant_lanes(int v) {
+  if (v < 0 || v >= kNumVariants || kVariants[v].g <= 0) return 0;
+  return (uint32_t)kVariants[v].g;
+}
+
 // Measured on 4,096-simulation batches: register tables win up to 256
 // sessions (32 x 8 takes half the LDS table's time there), the LDS table up
 // to its capacity, then the 512-thread streamed table.
@@ -1989,7 +1996,7 @@ static SimArgs with_cache(const SimArgs& a, uint32_t n_sess, uint32_t block, int
 template <int G, int EPL>
 static void launch_regs(const SimArgs& a, hipStream_t stream) {
   const uint32_t groups_per_block = 256 / G;
-  const uint32_t blocks = (a.n_sims + groups_per_block - 1) / groups_per_block;
+  const uint32_t blocks = (a.n_slots + groups_per_block - 1) / groups_per_block;
   hipLaunchKernelGGL((sim_regs_kernel<G, EPL>), dim3(blocks), dim3(256), 0, stream, a);
 }
 

@@ -204,6 +204,12 @@ struct SimArgs {
   uint32_t time44;         // every trace time is below 2^44 - 1 ns
   uint32_t rc_off;         // streamed tables: byte offset of the resident cache in dynamic LDS
   uint32_t rc_slots;       // and its slots per thread (set by the launcher)
+  const uint32_t* slot_sim;  // register tables: lane group -> simulation (0xFFFFFFFF: empty), or
+                             // null for group g = simulation g
+  uint32_t n_slots;        // lane groups the register-table grid covers
 };
+
+// Most lane groups of a wavefront (the 4-lane register table's 16).
+constexpr uint32_t kMaxGroupsPerWave = 16;
 
 }  // namespace unison

@@ -136,6 +136,24 @@ def test_random_batches_with_few_cache_slots(case):
             del s
 
 
+def test_random_batches_under_a_policy_override(case):
+    """One policy for every row (unison_run's override), then the rows' own
+    policies again on the same context: the register-table kernels regroup
+    their simulations by policy, score form and trace for each."""
+    import copy
+    name, w, want, _ = case
+    s = Sim(w)
+    for pol in (synth.POLICY_LRU, synth.POLICY_BELADY, synth.POLICY_SPEAR):
+        say("random %s: override %d" % (name, pol))
+        w2 = copy.copy(w)
+        w2.params = w.params.copy()
+        w2.params["policy"] = pol
+        s.run(policy=pol)
+        compare_counters(s.counters(), oracle_counters(w2), label="random %s override %d" % (name, pol))
+    s.run()
+    compare_counters(s.counters(), want, label="random %s after overrides" % name)
+
+
 def test_random_decision_logs(case):
     """Full ordered decision logs of a few simulations of each batch."""
     from parity import oracle_log, same_log
