@@ -241,7 +241,8 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
  * UNISON_POLICY_PARAMS.  A batch with a dual-design row runs on the copies'
  * kernel (variant 11).  Tables above the LDS-resident size run on workgroup
  * kernels that keep one bit of LDS per session (the residency bits their
- * scans visit): 128 KiB at UNISON_MAX_SESSIONS.  Asynchronous.
+ * scans visit): 128 KiB at UNISON_MAX_SESSIONS; the LDS left holds up to 8
+ * resident-cache slots of 28 B per thread.  Asynchronous.
  * Errors: UNISON_E_NOT_READY, UNISON_E_INVALID (also: a register-table
  * variant forced on a batch with a dual-design row), UNISON_E_CAPACITY (the
  * largest trace exceeds the chosen kernel variant, e.g. on a device with
