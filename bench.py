@@ -38,8 +38,10 @@ HEADLINE_KERNEL = "sim_regs_kernel<8, 2>"
 # VALU issue limit: 256 CUs x 4 SIMDs at 2.4 GHz, one wave64 VALU instruction
 # per SIMD every 4 cycles (16 lanes wide): 614.4e9 instructions/s.
 VALU_PEAK_GINST = 256 * 4 * 2.4 / 4
+# what the simulation kernel is built from: its sources and the build flags
 SIM_SOURCES = [os.path.join(ROOT, "paper_2609_09643_amd", "csrc", f)
-               for f in ("sim.hip", "unison_device.h")]
+               for f in ("sim.hip", "unison_device.h")] + \
+              [os.path.join(ROOT, "paper_2609_09643_amd", "build.py")]
 
 
 def log(*a):
