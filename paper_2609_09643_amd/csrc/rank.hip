@@ -6,8 +6,8 @@
 // workgroup and gather its (x, y) pairs into LDS once.  Small snapshots are
 // classified pair by pair (each thread owns rows i and walks j > i with all
 // lanes of a wave reading the same LDS word, a broadcast); from 256 entries
-// on, a bitonic sort and a counting merge sort find the same counts in
-// O(n log^2 n).
+// on, a bitonic sort and a counting merge sort (merge path from runs of 8)
+// find the same counts in O(n log^2 n).
 #include <hip/hip_runtime.h>
 
 #include "unison_device.h"
@@ -212,6 +212,11 @@ __device__ __forceinline__ bool pair_less(uint32_t xa, uint64_t ya, uint32_t xb,
 constexpr uint32_t kSortE = kKendallMax / kSortBlock;
 constexpr uint32_t kSortQ = kSortE / 2;
 constexpr uint32_t kSortSteps = 13;  // log2(4096) + 1
+// From runs of this width on, the merge levels use merge path (each thread
+// merges its own 8 outputs); narrower runs place each entry by a short
+// binary search.
+constexpr uint32_t kMergeRun = 8;
+static_assert(kSortE == 8 && kSortE * kSortBlock == kKendallMax, "8 outputs per thread");
 
 __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
                                                                   uint64_t n_x, const float* x,
@@ -363,6 +368,46 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
   uint64_t* dst = s_yb;
   uint32_t steps = 1;  // log2(w) + 1 binary-search steps over a run of w
   for (uint32_t w = 1; w < P; w <<= 1, ++steps) {
+    if (w >= kMergeRun) {
+      // merge path: thread t writes outputs [8t, 8t + 8) of its pair of
+      // runs A (left) and B (right).  A binary search on its diagonal finds
+      // how many of them come from A; then it merges sequentially, A first
+      // on equal values, and each B entry taken adds the A entries still
+      // waiting, all of them larger.
+      const uint32_t o0 = tid * kSortE;
+      if (o0 < P) {
+        const uint32_t b0 = o0 & ~(2 * w - 1);
+        const uint32_t d = o0 - b0;
+        const uint64_t* A = src + b0;
+        const uint64_t* B = A + w;
+        uint32_t lo = d > w ? d - w : 0u, hi = d < w ? d : w;
+        while (lo < hi) {
+          const uint32_t mid = (lo + hi) >> 1;
+          if (A[mid] <= B[d - 1 - mid]) lo = mid + 1;
+          else hi = mid;
+        }
+        uint32_t i = lo, j = d - lo;
+        uint64_t a = i < w ? A[i] : 0ull, b = j < w ? B[j] : 0ull;
+#pragma unroll
+        for (uint32_t e = 0; e < kSortE; ++e) {
+          const bool take_a = i < w && (j >= w || a <= b);
+          dst[o0 + e] = take_a ? a : b;
+          if (take_a) {
+            ++i;
+            a = i < w ? A[i] : 0ull;
+          } else {
+            inv += w - i;
+            ++j;
+            b = j < w ? B[j] : 0ull;
+          }
+        }
+      }
+      __syncthreads();
+      uint64_t* tmp = src;
+      src = dst;
+      dst = tmp;
+      continue;
+    }
     uint32_t lo[kSortE], hi[kSortE], rb[kSortE];
     uint64_t v[kSortE];
 #pragma unroll
