@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void score_fixed_kernel(uint32_t n, const uint
 }
 
 constexpr int kKendallBlock = 256;
-constexpr uint32_t kKendallMax = 4096;  // sort-based path: 16 B of LDS per entry, 64 KiB
+constexpr uint32_t kKendallMax = 4096;  // sort-based path: 18 B of LDS per entry, 72 KiB
 constexpr uint32_t kKendallSortFrom = 256;  // snapshots this large or larger are sorted
 
 __device__ __forceinline__ bool fbetter(float a, uint32_t ia, float b, uint32_t ib) {
@@ -216,6 +216,12 @@ constexpr uint32_t kSortSteps = 13;  // log2(4096) + 1
 // merges its own 8 outputs); narrower runs place each entry by a short
 // binary search.
 constexpr uint32_t kMergeRun = 8;
+// Merge-path levels store entry i at i + i / 8: a thread's 8 consecutive
+// outputs then start 72 B after its neighbour's, not 64 B, which spreads a
+// wavefront's stores over the LDS banks.
+__device__ __forceinline__ uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
+// Entries of each sort buffer, the padding included.
+__host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
 static_assert(kSortE == 8 && kSortE * kSortBlock == kKendallMax, "8 outputs per thread");
 
 __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
@@ -224,10 +230,11 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
                                                                   const uint32_t* idx,
                                                                   uint64_t* counts, uint8_t* top1) {
   // [P] y, then merge buffer A; [P] merge buffer B, which holds the x keys
-  // until the merge sort starts (16 B of LDS per entry: 64 KiB at 4,096)
+  // until the merge sort starts (two buffers of P + P/8 entries, 18 B of LDS
+  // per entry: 72 KiB at 4,096, so two snapshots share a CU)
   extern __shared__ uint64_t s_dyn[];
   uint64_t* s_ky = s_dyn;
-  uint64_t* s_yb = s_dyn + P;
+  uint64_t* s_yb = s_dyn + sort_buf(P);
   uint32_t* s_kx = reinterpret_cast<uint32_t*>(s_yb);
   __shared__ uint64_t s_sum[4][kSortBlock / 64];
   __shared__ float s_bx[kSortBlock / 64];
@@ -378,27 +385,29 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
       if (o0 < P) {
         const uint32_t b0 = o0 & ~(2 * w - 1);
         const uint32_t d = o0 - b0;
-        const uint64_t* A = src + b0;
-        const uint64_t* B = A + w;
+        // the first merge-path level reads the plain layout
+        const bool padded = w > kMergeRun;
+        auto at = [&](uint32_t k) { return src[padded ? mp_pad(k) : k]; };
+        const uint32_t bb = b0 + w;
         uint32_t lo = d > w ? d - w : 0u, hi = d < w ? d : w;
         while (lo < hi) {
           const uint32_t mid = (lo + hi) >> 1;
-          if (A[mid] <= B[d - 1 - mid]) lo = mid + 1;
+          if (at(b0 + mid) <= at(bb + d - 1 - mid)) lo = mid + 1;
           else hi = mid;
         }
         uint32_t i = lo, j = d - lo;
-        uint64_t a = i < w ? A[i] : 0ull, b = j < w ? B[j] : 0ull;
+        uint64_t a = i < w ? at(b0 + i) : 0ull, b = j < w ? at(bb + j) : 0ull;
 #pragma unroll
         for (uint32_t e = 0; e < kSortE; ++e) {
           const bool take_a = i < w && (j >= w || a <= b);
-          dst[o0 + e] = take_a ? a : b;
+          dst[mp_pad(o0 + e)] = take_a ? a : b;
           if (take_a) {
             ++i;
-            a = i < w ? A[i] : 0ull;
+            a = i < w ? at(b0 + i) : 0ull;
           } else {
             inv += w - i;
             ++j;
-            b = j < w ? B[j] : 0ull;
+            b = j < w ? at(bb + j) : 0ull;
           }
         }
       }
@@ -460,7 +469,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
 #pragma unroll
     for (uint32_t e = 0; e < kSortE; ++e) {
       const uint32_t i = tid + e * kSortBlock;
-      yv[e] = i < n ? src[i] : 0ull;
+      yv[e] = i < n ? src[mp_pad(i)] : 0ull;
       lo[e] = 0;
       hi[e] = i < n ? i : 0u;
     }
@@ -469,7 +478,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
       for (uint32_t e = 0; e < kSortE; ++e) {
         const uint32_t m = (lo[e] + hi[e]) >> 1;
         const bool open = lo[e] < hi[e];
-        const bool below = src[open ? m : 0u] < yv[e];
+        const bool below = src[mp_pad(open ? m : 0u)] < yv[e];
         lo[e] = open && below ? m + 1 : lo[e];
         hi[e] = open && !below ? m : hi[e];
       }
@@ -556,7 +565,7 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
   } else {
     uint32_t P = 2;
     while (P < n_per) P <<= 1;
-    const size_t lds = (size_t)P * 2 * sizeof(uint64_t);
+    const size_t lds = (size_t)sort_buf(P) * 2 * sizeof(uint64_t);
     hipLaunchKernelGGL(kendall_sort_kernel, dim3(n_snap), dim3(kSortBlock), lds, s, n_per, P, n_x,
                        x, y, idx, counts, top1);
   }
