@@ -206,12 +206,11 @@ __device__ __forceinline__ bool pair_less(uint32_t xa, uint64_t ya, uint32_t xb,
   return xa < xb || (xa == xb && ya < yb);
 }
 
-// Entries per thread, compare-exchanges per thread and pass, and binary-search
-// steps at the largest snapshot.  Each thread runs its searches (and its
-// compare-exchanges) in lockstep, so their LDS loads are in flight together.
+// Entries per thread and compare-exchanges per thread and pass at the largest
+// snapshot.  Each thread runs its compare-exchanges (and its searches) in
+// lockstep, so their LDS loads are in flight together.
 constexpr uint32_t kSortE = kKendallMax / kSortBlock;
 constexpr uint32_t kSortQ = kSortE / 2;
-constexpr uint32_t kSortSteps = 13;  // log2(4096) + 1
 // From runs of this width on, the merge levels use merge path (each thread
 // merges its own 8 outputs); narrower runs place each entry by a short
 // binary search.
@@ -222,6 +221,30 @@ constexpr uint32_t kMergeRun = 8;
 __device__ __forceinline__ uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
 // Entries of each sort buffer, the padding included.
 __host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
+
+// Inclusive max-scan over the workgroup of v[e] at position tid * 8 + e
+// (each thread's 8 positions in order): v[e] becomes the largest value at or
+// before its position.  s_part: LDS [kSortBlock / 64], free again on return.
+__device__ __forceinline__ void block_max_scan(uint32_t (&v)[kSortE], uint32_t* s_part,
+                                               uint32_t tid) {
+#pragma unroll
+  for (uint32_t e = 1; e < kSortE; ++e) v[e] = v[e] > v[e - 1] ? v[e] : v[e - 1];
+  const uint32_t lane = tid & 63u;
+  uint32_t w = v[kSortE - 1];
+#pragma unroll
+  for (uint32_t d = 1; d < 64; d <<= 1) {
+    const uint32_t o = (uint32_t)__shfl_up((int)w, d);
+    if (lane >= d && o > w) w = o;
+  }
+  uint32_t pre = (uint32_t)__shfl_up((int)w, 1);
+  if (lane == 0) pre = 0;
+  if (lane == 63) s_part[tid >> 6] = w;
+  __syncthreads();
+  for (uint32_t k = 0; k < (tid >> 6); ++k) pre = s_part[k] > pre ? s_part[k] : pre;
+#pragma unroll
+  for (uint32_t e = 0; e < kSortE; ++e) v[e] = v[e] > pre ? v[e] : pre;
+  __syncthreads();
+}
 static_assert(kSortE == 8 && kSortE * kSortBlock == kKendallMax, "8 outputs per thread");
 
 __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
@@ -241,6 +264,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
   __shared__ uint32_t s_bxi[kSortBlock / 64], s_byi[kSortBlock / 64];
   __shared__ uint64_t s_by[kSortBlock / 64];
   __shared__ uint32_t s_bad;
+  __shared__ uint32_t s_part[kSortBlock / 64];
   const uint32_t snap = blockIdx.x;
   const uint32_t tid = threadIdx.x;
   const size_t base = (size_t)snap * n_per;
@@ -321,49 +345,38 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
     }
   }
   // pairs tied in x, and in x and y: each entry counts the earlier entries of
-  // its run, found by two lower-bound searches over [0, i)
+  // its run; a run starts where the key differs from the one before, and a
+  // max-scan of those starts gives every entry the start of its run
   {
-    uint32_t lo[kSortE], hi[kSortE], xv[kSortE];
-    uint64_t yv[kSortE];
+    const uint32_t b = tid * kSortE;
+    uint32_t sx[kSortE], sxy[kSortE];
+    uint32_t px = 0;
+    uint64_t py = 0;
+    if (b > 0 && b < P) {
+      px = s_kx[b - 1];
+      py = s_ky[b - 1];
+    }
 #pragma unroll
     for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = tid + e * kSortBlock;
-      const bool ok = i < n;
-      xv[e] = ok ? s_kx[i] : 0u;
-      yv[e] = ok ? s_ky[i] : 0ull;
-      lo[e] = 0;
-      hi[e] = ok ? i : 0u;
+      const uint32_t i = b + e;
+      const bool ok = i < P;
+      const uint32_t xk = ok ? s_kx[i] : 0u;
+      const uint64_t yk = ok ? s_ky[i] : 0ull;
+      const bool new_x = i == 0 || xk != px;
+      sx[e] = ok && new_x ? i : 0u;
+      sxy[e] = ok && (new_x || yk != py) ? i : 0u;
+      px = xk;
+      py = yk;
     }
-    for (uint32_t step = 0; step < kSortSteps; ++step) {
+    block_max_scan(sx, s_part, tid);
+    block_max_scan(sxy, s_part, tid);
 #pragma unroll
-      for (uint32_t e = 0; e < kSortE; ++e) {
-        const uint32_t m = (lo[e] + hi[e]) >> 1;  // below i < P while the search is open
-        const bool open = lo[e] < hi[e];
-        const bool below = s_kx[open ? m : 0u] < xv[e];
-        lo[e] = open && below ? m + 1 : lo[e];
-        hi[e] = open && !below ? m : hi[e];
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = b + e;
+      if (i < n) {
+        t_x += i - sx[e];
+        t_xy += i - sxy[e];
       }
-    }
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = tid + e * kSortBlock;
-      if (i < n) t_x += i - lo[e];
-      hi[e] = i < n ? i : lo[e];
-    }
-    for (uint32_t step = 0; step < kSortSteps; ++step) {
-#pragma unroll
-      for (uint32_t e = 0; e < kSortE; ++e) {
-        const uint32_t m = (lo[e] + hi[e]) >> 1;
-        const bool open = lo[e] < hi[e];
-        const bool below = s_ky[open ? m : 0u] < yv[e];
-        lo[e] = open && below ? m + 1 : lo[e];
-        hi[e] = open && !below ? m : hi[e];
-      }
-    }
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = tid + e * kSortBlock;
-      if (i < n) t_xy += i - lo[e];
     }
   }
   __syncthreads();  // the x keys are read for the last time; buffer B is free
@@ -462,31 +475,25 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
     src = dst;
     dst = tmp;
   }
-  // pairs tied in y: each entry counts the earlier equal entries of the sorted y
+  // pairs tied in y: each entry counts the earlier equal entries of the
+  // sorted y (real entries hold positions [0, n): the padding sorts last)
   {
-    uint32_t lo[kSortE], hi[kSortE];
-    uint64_t yv[kSortE];
+    const uint32_t b = tid * kSortE;
+    uint32_t sy[kSortE];
+    uint64_t py = b > 0 && b < P ? src[mp_pad(b - 1)] : 0ull;
 #pragma unroll
     for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = tid + e * kSortBlock;
-      yv[e] = i < n ? src[mp_pad(i)] : 0ull;
-      lo[e] = 0;
-      hi[e] = i < n ? i : 0u;
+      const uint32_t i = b + e;
+      const bool ok = i < P;
+      const uint64_t yk = ok ? src[mp_pad(i)] : 0ull;
+      sy[e] = ok && (i == 0 || yk != py) ? i : 0u;
+      py = yk;
     }
-    for (uint32_t step = 0; step < kSortSteps; ++step) {
-#pragma unroll
-      for (uint32_t e = 0; e < kSortE; ++e) {
-        const uint32_t m = (lo[e] + hi[e]) >> 1;
-        const bool open = lo[e] < hi[e];
-        const bool below = src[mp_pad(open ? m : 0u)] < yv[e];
-        lo[e] = open && below ? m + 1 : lo[e];
-        hi[e] = open && !below ? m : hi[e];
-      }
-    }
+    block_max_scan(sy, s_part, tid);
 #pragma unroll
     for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = tid + e * kSortBlock;
-      if (i < n) t_y += i - lo[e];
+      const uint32_t i = b + e;
+      if (i < n) t_y += i - sy[e];
     }
   }
 
