@@ -202,6 +202,7 @@ __device__ __forceinline__ uint32_t float_key(uint32_t b) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+
 __device__ __forceinline__ bool pair_less(uint32_t xa, uint64_t ya, uint32_t xb, uint64_t yb) {
   return xa < xb || (xa == xb && ya < yb);
 }
@@ -221,6 +222,27 @@ constexpr uint32_t kMergeRun = 8;
 __device__ __forceinline__ uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
 // Entries of each sort buffer, the padding included.
 __host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
+
+// Orders a wavefront's LDS accesses before and after this point (its lanes
+// then see each other's stores); no other wavefront waits.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Between merge level w and level 2w.  Levels of runs below 4 keep each
+// entry p = tid + e * 512 inside its aligned group of 8, which one wavefront
+// owns; merge-path levels keep a thread's outputs and the runs it reads
+// inside one wavefront's 512 consecutive entries while the pair of runs of
+// the next level spans at most 512.  Elsewhere entries cross wavefronts, and
+// the last level is followed by the scan of the sorted y.
+__device__ __forceinline__ void level_sync(uint32_t w, uint32_t P) {
+  const bool within = w < kMergeRun / 2 ||
+                      (w >= kMergeRun && 4 * w <= (uint32_t)kSortBlock && 2 * w < P);
+  if (within) wave_lds_sync();
+  else __syncthreads();
+}
 
 // Inclusive max-scan over the workgroup of v[e] at position tid * 8 + e
 // (each thread's 8 positions in order): v[e] becomes the largest value at or
@@ -341,7 +363,14 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
           }
         }
       }
-      __syncthreads();
+      // With strides up to 64 every compare-exchange stays inside the 128
+      // entries that one wavefront owns for each q (t = tid + q * 512), so
+      // two such passes in a row need only the wavefront's own in-order LDS
+      // accesses between them; passes of longer strides exchange entries
+      // across wavefronts and take a workgroup barrier on both sides.
+      const bool cross = j >= 128 || (j == 1 && k >= 128);
+      if (cross) __syncthreads();
+      else wave_lds_sync();
     }
   }
   // pairs tied in x, and in x and y: each entry counts the earlier entries of
@@ -424,7 +453,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
           }
         }
       }
-      __syncthreads();
+      level_sync(w, P);
       uint64_t* tmp = src;
       src = dst;
       dst = tmp;
@@ -470,7 +499,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
         }
       }
     }
-    __syncthreads();
+    level_sync(w, P);
     uint64_t* tmp = src;
     src = dst;
     dst = tmp;
