@@ -312,8 +312,9 @@ int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t*
  * trace; register tables of lanes x sessions per lane 0: 16 x 1, 1: 64 x 1,
  * 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 7: 16 x 4, 8: 32 x 8 (6 is retired); one
  * workgroup per simulation with the table 3: streamed from the workspace by
- * 256 threads, 10: by 512 threads, 9: held in LDS, 11: streamed by 512
- * threads with the dual design's copies -- the only variant for a batch with
+ * 256 threads, 10: by 512 threads, 9: held in LDS (256 threads), 12: held in
+ * LDS by one wavefront, 11: streamed by 512 threads with the dual design's
+ * copies -- the only variant for a batch with
  * a dual-design row).  A variant too small for the traces, or an unknown id,
  * makes unison_run return UNISON_E_CAPACITY. */
 int unison_debug_force_variant(unison_ctx* ctx, int variant);

@@ -1908,10 +1908,12 @@ struct Variant {
 // 2 KB per lane, lost to the LDS table on its sizes, and one of its launches
 // faulted the GPU on a randomised batch without a cause found.
 constexpr Variant kVariants[] = {{16, 1}, {64, 1}, {64, 4}, {0, 0}, {4, 4},
-                                 {8, 2},  {-1, 0}, {16, 4}, {32, 8}, {0, 1}, {0, 0}, {0, 0}};
+                                 {8, 2},  {-1, 0}, {16, 4}, {32, 8}, {0, 1}, {0, 0}, {0, 0},
+                                 {0, 1}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kBlock = 256;
 constexpr int kLdsVariant = 9;
+constexpr int kLdsWaveVariant = 12;  // the table in LDS, one wavefront per simulation
 constexpr int kDualVariant = 11;  // streamed, 512 threads, with the dual design's copies
 constexpr uint32_t kLdsBytesPerSession = 4 * 8 + 2 * 4;  // mg, last, gq, next; len, kvb
 
@@ -1941,10 +1943,11 @@ static uint32_t block_of(int v) { return v == 10 || v == kDualVariant ? 512u : (
 uint32_t sim_variant_capacity(int v) {
   if (v < 0 || v >= kNumVariants) return 0;
   const uint32_t lim = lds_limit();
-  if (v == kLdsVariant) {
+  if (v == kLdsVariant || v == kLdsWaveVariant) {
     // the table and its residency bits
     uint32_t n = lim / kLdsBytesPerSession;
-    while (n && (size_t)n * kLdsBytesPerSession + res_bytes(n, kBlock) > lim) --n;
+    const uint32_t b = v == kLdsVariant ? (uint32_t)kBlock : 64u;
+    while (n && (size_t)n * kLdsBytesPerSession + res_bytes(n, b) > lim) --n;
     return n;
   }
   if (kVariants[v].g < 0) return 0;  // retired
@@ -1965,12 +1968,14 @@ uint32_t sim_variant_lanes(int v) {
 
 // Measured on 4,096-simulation batches: register tables win up to 256
 // sessions (32 x 8 takes half the LDS table's time there), the LDS table up
-// to its capacity, then the 512-thread streamed table.
+// to its capacity (one wavefront per simulation, which needs no workgroup
+// barriers: C2 163 vs 169 ms with 256 threads), then the 512-thread streamed
+// table.
 int sim_auto_variant(uint32_t max_sess) {
   if (max_sess <= 16) return 5;
   if (max_sess <= 64) return 7;
   if (max_sess <= 256) return 8;
-  if (max_sess <= sim_variant_capacity(kLdsVariant)) return kLdsVariant;
+  if (max_sess <= sim_variant_capacity(kLdsWaveVariant)) return kLdsWaveVariant;
   return 10;
 }
 
@@ -2015,6 +2020,12 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t 
       const uint32_t n = max_sess_in_batch ? max_sess_in_batch : 1;
       const size_t lds = (size_t)n * kLdsBytesPerSession + res_bytes(n, kBlock);
       hipLaunchKernelGGL((sim_block_kernel<kBlock, true, false>), dim3(a.n_sims), dim3(kBlock), lds, stream, a);
+      break;
+    }
+    case kLdsWaveVariant: {
+      const uint32_t n = max_sess_in_batch ? max_sess_in_batch : 1;
+      const size_t lds = (size_t)n * kLdsBytesPerSession + res_bytes(n, 64);
+      hipLaunchKernelGGL((sim_block_kernel<64, true, false>), dim3(a.n_sims), dim3(64), lds, stream, a);
       break;
     }
     case 10: {

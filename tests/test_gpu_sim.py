@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 RETIRED = pytest.mark.skip(reason="variant 6 (64 x 24) is retired: one of its launches faulted "
                                   "the GPU on a randomised batch and no cause was found; the "
                                   "library refuses it (test_retired_variant_is_refused)")
-VARIANTS = (0, 1, 2, 3, 4, 5, pytest.param(6, marks=RETIRED), 7, 8, 9, 10, 11)
+VARIANTS = (0, 1, 2, 3, 4, 5, pytest.param(6, marks=RETIRED), 7, 8, 9, 10, 11, 12)
 
 
 def say(*a):
@@ -88,7 +88,7 @@ def test_c3_decision_logs(c3):
         assert same_log(s.log(k), oracle_log(c3, i)), "c3 sim %d log" % i
 
 
-@pytest.mark.parametrize("variant", [None, 3, 9, 10])
+@pytest.mark.parametrize("variant", [None, 3, 9, 12, 10])
 def test_continue_matches_single_run(c3, c3_want, variant):
     sims = list(range(5, c3.n_sims, 61))
     w = subset(c3, sims)
