@@ -84,24 +84,50 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
             build()
-        L = C.CDLL(_LIB)
-        u32p, u64p, f32p, u8p = (C.POINTER(C.c_uint32), C.POINTER(C.c_uint64),
-                                 C.POINTER(C.c_float), C.POINTER(C.c_uint8))
-        L.orc_run.restype = C.c_int
-        L.orc_run.argtypes = [C.POINTER(Params), C.c_uint64, u64p, u32p, u32p, u32p, u64p,
-                              C.c_uint32, u32p, u32p, u32p, C.c_uint64, C.POINTER(Counters),
-                              C.c_void_p, C.c_uint32, u32p, C.c_void_p, C.c_void_p, u64p]
-        L.orc_hazard_counts.argtypes = [u32p, C.c_uint32, u32p, u32p]
-        L.orc_lut_f32.argtypes = [u32p, u32p, f32p]
-        L.orc_lut_q.argtypes = [u32p, u32p, C.c_uint32, u64p]
-        L.orc_score_f32.argtypes = [C.c_uint32, u8p, f32p, u8p, f32p, C.c_float, f32p]
-        L.orc_score_fixed.argtypes = [C.c_uint32, u8p, u64p, u8p, u64p, C.c_uint32,
-                                      C.c_uint64, u64p]
-        L.orc_ema_replay.argtypes = [C.c_uint32, C.c_uint32, u64p, u8p, C.c_uint32,
-                                     C.c_uint64, f32p, u64p]
-        L.orc_kendall.argtypes = [C.c_uint32, C.c_uint32, f32p, u64p, u32p, u64p, u8p]
-        _lib = L
+        _lib = load_library(_LIB)
     return _lib
+
+
+def compile_source(src_text, out_path):
+    """Compiles oracle C source text (the oracle's own, or a test's altered
+    copy of it) into a shared library at out_path, with the oracle's flags."""
+    c_path = out_path + ".c"
+    with open(c_path, "w") as f:
+        f.write(src_text)
+    subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math",
+                           "-shared", "-fPIC", c_path, "-o", out_path, "-lm"])
+    return out_path
+
+
+def source_text():
+    with open(_SRC) as f:
+        return f.read()
+
+
+def load_library(path):
+    """Loads a library built from the oracle source and declares its entry
+    points."""
+    L = C.CDLL(path)
+    u32p, u64p, f32p, u8p = (C.POINTER(C.c_uint32), C.POINTER(C.c_uint64),
+                             C.POINTER(C.c_float), C.POINTER(C.c_uint8))
+    L.orc_run.restype = C.c_int
+    L.orc_run.argtypes = [C.POINTER(Params), C.c_uint64, u64p, u32p, u32p, u32p, u64p,
+                          C.c_uint32, u32p, u32p, u32p, C.c_uint64, C.POINTER(Counters),
+                          C.c_void_p, C.c_uint32, u32p, C.c_void_p, C.c_void_p, u64p]
+    L.orc_hazard_counts.argtypes = [u32p, C.c_uint32, u32p, u32p]
+    L.orc_lut_f32.argtypes = [u32p, u32p, f32p]
+    L.orc_lut_q.argtypes = [u32p, u32p, C.c_uint32, u64p]
+    L.orc_score_f32.argtypes = [C.c_uint32, u8p, f32p, u8p, f32p, C.c_float, f32p]
+    L.orc_score_fixed.argtypes = [C.c_uint32, u8p, u64p, u8p, u64p, C.c_uint32,
+                                  C.c_uint64, u64p]
+    L.orc_ema_replay.argtypes = [C.c_uint32, C.c_uint32, u64p, u8p, C.c_uint32,
+                                 C.c_uint64, f32p, u64p]
+    L.orc_kendall.argtypes = [C.c_uint32, C.c_uint32, f32p, u64p, u32p, u64p, u8p]
+    L.orc_run_batch.restype = C.c_int
+    L.orc_run_batch.argtypes = [C.c_void_p, C.c_uint32, u32p, u32p, u64p, u64p, u64p, u32p,
+                                u32p, u32p, u64p, u32p, u32p, u32p, C.c_uint64, C.c_void_p,
+                                u64p]
+    return L
 
 
 def _c(a, dtype):
@@ -217,11 +243,13 @@ def params_struct(row):
     return p
 
 
-def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False, counts=None):
+def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False, counts=None,
+        library=None):
     """Runs one simulation. Returns (rc, counters dict, log or None, states or None,
     elapsed_ns of the event loop).  counts: optional uint32 array [2, 51] that
-    receives the hazard counts d, n of the table at the end."""
-    L = lib()
+    receives the hazard counts d, n of the table at the end.  library: a
+    library from load_library() to run instead of the oracle's own build."""
+    L = lib() if library is None else library
     p = params_struct(row)
     t_ns, sid = _c(trace.t_ns, np.uint64), _c(trace.sid, np.uint32)
     info, length = _c(trace.info, np.uint32), _c(trace.length, np.uint32)
@@ -251,19 +279,59 @@ def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False, coun
     return rc, cnt.as_dict(), log, st, int(el[0])
 
 
-def run_workload(workload, sims=None, max_events=None):
+class Batch:
+    """A workload's traces, hazard counts and parameter rows marshalled once
+    for orc_run_batch."""
+
+    def __init__(self, workload):
+        trs = workload.traces
+        self.ev_off = np.zeros(len(trs) + 1, np.uint64)
+        self.ss_off = np.zeros(len(trs) + 1, np.uint64)
+        self.ev_off[1:] = np.cumsum([t.n_events for t in trs])
+        self.ss_off[1:] = np.cumsum([t.n_sessions for t in trs])
+        cat = lambda name, dt: np.ascontiguousarray(
+            np.concatenate([getattr(t, name) for t in trs] + [np.zeros(1, dt)]), dtype=dt)
+        self.t, self.sid = cat("t_ns", np.uint64), cat("sid", np.uint32)
+        self.info, self.len = cat("info", np.uint32), cat("length", np.uint32)
+        self.next, self.kvb = cat("next_ns", np.uint64), cat("kvb", np.uint32)
+        D, N = luts_for(workload)
+        self.D, self.N = np.ascontiguousarray(D), np.ascontiguousarray(N)
+        self.params = workload.params
+
+    def prepare(self, sims):
+        """The parameter rows of `sims` in the oracle's layout, to run more
+        than once."""
+        sims = list(sims)
+        rows = (Params * max(len(sims), 1))()
+        for k, i in enumerate(sims):
+            rows[k] = params_struct(self.params[i])
+        tr_idx = np.ascontiguousarray(self.params["trace"][sims], dtype=np.uint32)
+        lut_idx = np.ascontiguousarray(self.params["lut"][sims], dtype=np.uint32)
+        return sims, rows, tr_idx, lut_idx
+
+    def run(self, sims, max_events=None):
+        """Runs `sims` (a list, or what prepare() returned); returns (rc,
+        counter dicts, summed event-loop ns)."""
+        sims, rows, tr_idx, lut_idx = sims if isinstance(sims, tuple) else self.prepare(sims)
+        n = len(sims)
+        cnt = (Counters * max(n, 1))()
+        el = np.zeros(1, np.uint64)
+        me = 0xFFFFFFFFFFFFFFFF if max_events is None else int(max_events)
+        rc = lib().orc_run_batch(
+            C.cast(rows, C.c_void_p), n, _p(tr_idx, C.c_uint32), _p(lut_idx, C.c_uint32),
+            _p(self.ev_off, C.c_uint64), _p(self.ss_off, C.c_uint64), _p(self.t, C.c_uint64),
+            _p(self.sid, C.c_uint32), _p(self.info, C.c_uint32), _p(self.len, C.c_uint32),
+            _p(self.next, C.c_uint64), _p(self.kvb, C.c_uint32), _p(self.D, C.c_uint32),
+            _p(self.N, C.c_uint32), me, C.cast(cnt, C.c_void_p), _p(el, C.c_uint64))
+        return rc, [cnt[k].as_dict() for k in range(n)], int(el[0])
+
+
+def run_workload(workload, sims=None, max_events=None, batch=None):
     """Runs the listed simulations (default: all) of a workload.  Returns a
     list of counter dicts and the summed event-loop time in ns."""
-    D, N = luts_for(workload)
     sims = range(workload.n_sims) if sims is None else sims
-    out, total_ns = [], 0
-    for i in sims:
-        row = workload.params[i]
-        tr = workload.traces[int(row["trace"])]
-        rc, cnt, _, _, el = run(tr, row, D[int(row["lut"])], N[int(row["lut"])],
-                                max_events=max_events)
-        if rc != 0:
-            raise RuntimeError("oracle returned %d for simulation %d" % (rc, i))
-        out.append(cnt)
-        total_ns += el
+    b = Batch(workload) if batch is None else batch
+    rc, out, total_ns = b.run(sims, max_events=max_events)
+    if rc != 0:
+        raise RuntimeError("oracle returned %d" % rc)
     return out, total_ns

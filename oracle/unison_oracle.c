@@ -748,5 +748,38 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
   return rc;
 }
 
+/*
+ * Runs n_rows simulations one after another, each exactly as orc_run does
+ * (no decision log, no per-event states): a driver over orc_run for batches.
+ * The traces are concatenated: trace k holds events [ev_off[k], ev_off[k+1])
+ * of the ev_* arrays and sessions [ss_off[k], ss_off[k+1]) of kvb.  Row i
+ * replays trace row_trace[i] with the hazard counts lut_d/lut_n + 51 *
+ * row_lut[i] and writes out[i]; elapsed_ns (optional) receives the summed
+ * event-loop time.  Every row runs; the first non-zero orc_run code is
+ * returned.
+ */
+int orc_run_batch(const orc_params* rows, uint32_t n_rows, const uint32_t* row_trace,
+                  const uint32_t* row_lut, const uint64_t* ev_off, const uint64_t* ss_off,
+                  const uint64_t* ev_t, const uint32_t* ev_sid, const uint32_t* ev_info,
+                  const uint32_t* ev_len, const uint64_t* ev_next, const uint32_t* kvb,
+                  const uint32_t* lut_d, const uint32_t* lut_n, uint64_t max_events,
+                  orc_counters* out, uint64_t* elapsed_ns) {
+  int rc_all = ORC_OK;
+  uint64_t total = 0;
+  for (uint32_t i = 0; i < n_rows; i++) {
+    uint32_t k = row_trace[i];
+    uint64_t e0 = ev_off[k], n_ev = ev_off[k + 1] - e0, s0 = ss_off[k];
+    uint64_t ns = 0;
+    int rc = orc_run(&rows[i], n_ev, ev_t + e0, ev_sid + e0, ev_info + e0, ev_len + e0,
+                     ev_next + e0, (uint32_t)(ss_off[k + 1] - s0), kvb + s0,
+                     lut_d + (uint64_t)LUT_LEN * row_lut[i], lut_n + (uint64_t)LUT_LEN * row_lut[i],
+                     max_events, &out[i], NULL, 0, NULL, NULL, NULL, &ns);
+    total += ns;
+    if (rc != ORC_OK && rc_all == ORC_OK) rc_all = rc;
+  }
+  if (elapsed_ns) *elapsed_ns = total;
+  return rc_all;
+}
+
 /* Layout version of the structs above. */
 uint32_t orc_version(void) { return 1; }

@@ -39,6 +39,7 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
                           const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1,
                           hipStream_t s);
 uint32_t kendall_max_per();
+int kendall_barrier_after(uint32_t P, uint32_t step, uint32_t a, uint32_t b);
 }  // namespace unison
 
 using namespace unison;
@@ -557,6 +558,12 @@ int unison_debug_cache_slots(unison_ctx* ctx, int slots) {
   if (!ctx || slots < -1) return UNISON_E_INVALID;
   ctx->force_cache_slots = slots;
   return UNISON_OK;
+}
+
+// Test hook: the Kendall sort kernel's barrier plan (host only).
+int unison_debug_kendall_barrier(uint32_t n_pad, uint32_t step, uint32_t a, uint32_t b) {
+  const int r = kendall_barrier_after(n_pad, step, a, b);
+  return r < 0 ? UNISON_E_INVALID : r;
 }
 
 int unison_ema_replay(void* hip_stream, uint32_t n, uint32_t max_hist, const uint64_t* gaps_ns,

@@ -231,17 +231,36 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Between merge level w and level 2w.  Levels of runs below 4 keep each
-// entry p = tid + e * 512 inside its aligned group of 8, which one wavefront
-// owns; merge-path levels keep a thread's outputs and the runs it reads
-// inside one wavefront's 512 consecutive entries while the pair of runs of
-// the next level spans at most 512.  Elsewhere entries cross wavefronts, and
-// the last level is followed by the scan of the sorted y.
+// Whether bitonic pass (k, j) is followed by a workgroup barrier.  With
+// strides up to 64 every compare-exchange stays inside the 128 entries that
+// one wavefront owns for each q (t = tid + q * 512), so two such passes in a
+// row need only the wavefront's own in-order LDS accesses between them;
+// passes of longer strides exchange entries across wavefronts and take a
+// workgroup barrier on both sides (the last pass of a stage precedes the
+// first, longest-stride pass of the next).
+__host__ __device__ constexpr bool bitonic_barrier_after(uint32_t k, uint32_t j) {
+  return j >= 128 || (j == 1 && k >= 128);
+}
+
+// Whether merge level w (runs of w merged into runs of 2w) is followed by a
+// workgroup barrier.  Levels of runs below 4 keep each entry p = tid + e * 512
+// inside its aligned group of 8, which one wavefront owns.  Merge-path levels
+// after the first keep a thread's outputs and the runs it reads inside one
+// wavefront's 512 consecutive entries (576 padded) while the pair of runs of
+// the next level spans at most 512.  The first merge-path level (w = 8) reads
+// the plain layout that the search levels wrote, and the next level stores
+// padded positions into that same buffer: a wavefront's padded stores there
+// reach past its own 512 plain entries into those its neighbour reads at
+// w = 8, so that step takes the barrier.  Elsewhere entries cross wavefronts,
+// and the last level is followed by the scan of the sorted y.
+__host__ __device__ constexpr bool merge_barrier_after(uint32_t w, uint32_t P) {
+  return !(w < kMergeRun / 2 ||
+           (w > kMergeRun && 4 * w <= (uint32_t)kSortBlock && 2 * w < P));
+}
+
 __device__ __forceinline__ void level_sync(uint32_t w, uint32_t P) {
-  const bool within = w < kMergeRun / 2 ||
-                      (w >= kMergeRun && 4 * w <= (uint32_t)kSortBlock && 2 * w < P);
-  if (within) wave_lds_sync();
-  else __syncthreads();
+  if (merge_barrier_after(w, P)) __syncthreads();
+  else wave_lds_sync();
 }
 
 // Inclusive max-scan over the workgroup of v[e] at position tid * 8 + e
@@ -363,13 +382,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
           }
         }
       }
-      // With strides up to 64 every compare-exchange stays inside the 128
-      // entries that one wavefront owns for each q (t = tid + q * 512), so
-      // two such passes in a row need only the wavefront's own in-order LDS
-      // accesses between them; passes of longer strides exchange entries
-      // across wavefronts and take a workgroup barrier on both sides.
-      const bool cross = j >= 128 || (j == 1 && k >= 128);
-      if (cross) __syncthreads();
+      if (bitonic_barrier_after(k, j)) __syncthreads();
       else wave_lds_sync();
     }
   }
@@ -609,5 +622,20 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
 }
 
 uint32_t kendall_max_per() { return kKendallMax; }
+
+// The sort kernel's barrier plan, for host-side checks: 1 when the step is
+// followed by a workgroup barrier, 0 when by the wavefront-local fence.
+int kendall_barrier_after(uint32_t P, uint32_t step, uint32_t a, uint32_t b) {
+  if (P < kKendallSortFrom || P > kKendallMax || (P & (P - 1))) return -1;
+  if (step == 0) {  // bitonic pass (k = a, j = b)
+    if (a < 2 || a > P || (a & (a - 1)) || b == 0 || b >= a || (b & (b - 1))) return -1;
+    return bitonic_barrier_after(a, b) ? 1 : 0;
+  }
+  if (step == 1) {  // merge level w = a
+    if (a == 0 || a >= P || (a & (a - 1))) return -1;
+    return merge_barrier_after(a, P) ? 1 : 0;
+  }
+  return -1;
+}
 
 }  // namespace unison

@@ -93,6 +93,7 @@ def lib():
             "unison_debug_force_variant": [vp, i32],
             "unison_debug_cache_slots": [vp, i32],
             "unison_set_stream": [vp, vp],
+            "unison_debug_kendall_barrier": [u32, u32, u32, u32],
         }
         for name, args in sig.items():
             f = getattr(L, name)

@@ -129,3 +129,34 @@ def test_kendall_rejects_out_of_range_index(U):
     idx = np.array([[0, 1, 2], [3, 4, 99]], np.uint32)
     c, t = U.kendall(dev(U, x), dev(U, y, np.uint64), dev(U, idx))
     assert t.cpu().numpy().tolist() == [1, 255]
+
+
+def test_every_c5_snapshot_in_the_bench_pipeline(U):
+    """The whole ranking-fidelity pass as bench.py times it (hazard counts,
+    both EMA replays, both scorers, the sorted Kendall kernel) on all 10,000
+    snapshots of 4,096 sessions, at b_h = 16 and 12: every snapshot's five
+    pair counts and top-1 flag equal the oracle's, through the digests that
+    tests/golden/make_c5_golden.py wrote with the oracle."""
+    import os
+    import sys as _sys
+    here = os.path.dirname(os.path.abspath(__file__))
+    _sys.path.insert(0, os.path.join(here, "golden"))
+    import make_c5_golden as G
+    gold = np.load(os.path.join(here, "golden", "c5_kendall.npz"))
+    full = synth.c5_ranking()
+    assert tuple(int(v) for v in gold["shape"]) == (full.n_snap, full.n_per)
+    say("kendall: all %d snapshots x %d, two formats" % (full.n_snap, full.n_per))
+    pop = dev(U, full.lut_pop, np.uint32)
+    d, n = U.hazard_counts(pop)
+    g, gq = U.ema_replay(dev(U, full.gaps_ns, np.uint64), dev(U, full.n_hist))
+    x = U.score_fp32(dev(U, full.turn), g, dev(U, full.done), d, n, G.P_US)
+    idx = dev(U, full.idx, np.uint32)
+    for bh in G.FORMATS:
+        y = U.score_fixed(dev(U, full.turn), gq, dev(U, full.done), d, n, bh, G.P_Z)
+        c, t = U.kendall(x, y, idx)
+        c = U._host(c, np.uint64)
+        t = t.cpu().numpy()
+        assert np.array_equal(c.sum(axis=0, dtype=np.uint64), gold["sum_bh%d" % bh])
+        assert int(t.astype(np.uint64).sum()) == int(gold["top1_bh%d" % bh][0])
+        bad = np.nonzero(G.snapshot_digests(c, t) != gold["digest_bh%d" % bh])[0]
+        assert len(bad) == 0, "b_h %d: snapshots %s differ from the oracle" % (bh, bad[:8].tolist())

@@ -148,6 +148,31 @@ def test_c4_longer_prefix_in_the_timed_configuration():
     compare_counters(s.counters(), oracle_counters(ww, max_events=40_000), label="c4 40k")
 
 
+def test_c4_golden_prefix_in_the_timed_configuration():
+    """The 65,536-session trace on the kernel the bench times, resumed by
+    CONTINUE to 100,000, 200,000, 300,000 and 400,000 events, against the
+    oracle's counters and both decision digests at each point
+    (tests/golden/make_c4_golden.py).  By the last point the register file
+    holds about 57,000 of its 65,536 entries."""
+    import json
+    import os
+    here = os.path.dirname(os.path.abspath(__file__))
+    sys.path.insert(0, os.path.join(here, "golden"))
+    import make_c4_golden as G
+    gold = json.load(open(os.path.join(here, "golden", "c4_prefix.json")))
+    w = G.workload()
+    assert G.trace_sha(w.traces[0]) == gold["trace_sha256"], "the C4 generator changed"
+    ww = subset(w, gold["sims"])
+    s = Sim(ww)
+    done = 0
+    for n in gold["checkpoints"]:
+        say("c4 golden: %d sims to event %d" % (len(gold["sims"]), n))
+        s.run(flags=1 if done else 0, max_events=n - done)
+        done = n
+        compare_counters(s.counters(), gold["counters"][str(n)], label="c4 golden %d" % n)
+    assert max(gold["table_entries"][str(done)]) > 50_000
+
+
 def test_c4_full_trace_properties():
     """The whole C4 trace (about 4 million events per simulation), past what
     the oracle can replay: one launch equals two launches split by CONTINUE,
