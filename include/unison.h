@@ -187,6 +187,31 @@ int unison_workspace_size(const unison_dims* d, size_t* bytes);
  * for the context's lifetime. */
 int unison_create(unison_ctx** out, const unison_dims* d, void* hip_stream, void* workspace,
                   size_t workspace_bytes);
+/* Bytes of the library's static workspace (unison_create_static). */
+#define UNISON_STATIC_WORKSPACE_BYTES (32u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): creates a
+ * context like unison_create whose workspace is the library's own static
+ * device array of UNISON_STATIC_WORKSPACE_BYTES (32 MiB), one per GPU,
+ * reserved when the library is loaded and held until the process ends.  No
+ * device memory is allocated (the context itself is host memory, as for
+ * unison_create).  The array's address on the current device is taken once,
+ * at the first call on that device.  Every other entry point works on such
+ * a context as on any other.
+ * All contexts made this way on one GPU share its array, which keeps the
+ * contents the latest call left: each new context takes the array over, and
+ * calls on an older context of the same device then fail with
+ * UNISON_E_INVALID ("superseded").  Work of two such contexts that overlaps
+ * on one GPU races; a fresh unison_run (without UNISON_RUN_CONTINUE) starts
+ * every simulation from an empty pool whatever the array held.
+ * Errors: UNISON_E_INVALID (null out, invalid dims), UNISON_E_CAPACITY
+ * (unison_workspace_size(d) exceeds UNISON_STATIC_WORKSPACE_BYTES; nothing
+ * is created), UNISON_E_HIP (no current device, or the array's address could
+ * not be taken).  unison_last_error(NULL) gives the message of this thread's
+ * latest failed create call. */
+int unison_create_static(unison_ctx** out, const unison_dims* d, void* hip_stream);
+
 void unison_destroy(unison_ctx* ctx);
 const char* unison_last_error(const unison_ctx* ctx);
 const char* unison_strerror(int code);

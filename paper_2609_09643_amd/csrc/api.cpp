@@ -7,10 +7,12 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -119,6 +121,34 @@ uint64_t first_bad_event(const uint64_t* t, const uint32_t* sid, const uint32_t*
   return ~0ull;
 }
 
+// The workspace of contexts made by unison_create_static: a file-scope
+// device array, one copy per GPU the library runs on, held until the
+// process ends.  Host code never passes the array's name to a kernel or a
+// copy (on the host it is only a stand-in for the symbol): it takes each
+// device's address once, with hipGetSymbolAddress on that device, and uses
+// that address wherever the workspace is needed.
+constexpr int kStaticMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[UNISON_STATIC_WORKSPACE_BYTES];
+
+struct StaticWorkspace {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+  std::atomic<uint64_t> gen{0};  // bumped by every unison_create_static on the device
+};
+StaticWorkspace g_static[kStaticMaxDevices];
+
+// Message of the latest failed create call on this thread (no context yet).
+thread_local char g_create_err[256] = "";
+
+int create_fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_create_err, sizeof g_create_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
 bool dims_ok(const unison_dims* d) {
   return d && d->n_sims >= 1 && d->n_traces >= 1 && d->n_luts >= 1 && d->max_sessions >= 1 &&
          d->max_sessions <= UNISON_MAX_SESSIONS && d->views <= 1;
@@ -148,6 +178,8 @@ struct unison_ctx {
   uint64_t slots_for = ~0ull;      // (params_gen, policy override, lanes) the map was built for
   bool slots_identity = true;
   uint32_t n_slots = 0;
+  int static_dev = -1;       // unison_create_static: the device whose array is the workspace
+  uint64_t static_gen = 0;   // and the array's generation this context was made for
   char err[512];
 
   template <class T>
@@ -164,7 +196,22 @@ struct unison_ctx {
     if (e == hipSuccess) return UNISON_OK;
     return fail(UNISON_E_HIP, "%s: %s", what, hipGetErrorString(e));
   }
+  // A context on the device's static array is superseded once a newer one
+  // takes the array over.
+  bool superseded() const {
+    return static_dev >= 0 && g_static[static_dev].gen.load() != static_gen;
+  }
+  int refuse_superseded() {
+    return fail(UNISON_E_INVALID,
+                "context superseded: a later unison_create_static on device %d took over its "
+                "workspace", static_dev);
+  }
 };
+
+#define UNISON_LIVE(ctx)                                   \
+  do {                                                     \
+    if ((ctx)->superseded()) return (ctx)->refuse_superseded(); \
+  } while (0)
 
 extern "C" {
 
@@ -182,7 +229,10 @@ const char* unison_strerror(int code) {
   }
 }
 
-const char* unison_last_error(const unison_ctx* ctx) { return ctx ? ctx->err : "null context"; }
+const char* unison_last_error(const unison_ctx* ctx) {
+  if (ctx) return ctx->err;
+  return g_create_err[0] ? g_create_err : "null context";
+}
 
 int unison_workspace_size(const unison_dims* d, size_t* bytes) {
   if (!dims_ok(d) || !bytes) return UNISON_E_INVALID;
@@ -214,6 +264,41 @@ int unison_create(unison_ctx** out, const unison_dims* d, void* hip_stream, void
   return UNISON_OK;
 }
 
+int unison_create_static(unison_ctx** out, const unison_dims* d, void* hip_stream) {
+  if (!out || !dims_ok(d)) return create_fail(UNISON_E_INVALID, "null output or invalid dims");
+  *out = nullptr;
+  Layout L;
+  make_layout(*d, L);
+  if (L.total > (size_t)UNISON_STATIC_WORKSPACE_BYTES)
+    return create_fail(UNISON_E_CAPACITY,
+                       "these dims need a workspace of %zu bytes; the static workspace holds %zu",
+                       L.total, (size_t)UNISON_STATIC_WORKSPACE_BYTES);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kStaticMaxDevices)
+    return create_fail(UNISON_E_HIP, "no current HIP device (or device id above %d)",
+                       kStaticMaxDevices - 1);
+  StaticWorkspace& sw = g_static[dev];
+  std::call_once(sw.once, [&] { sw.err = hipGetSymbolAddress(&sw.ptr, HIP_SYMBOL(scratch)); });
+  if (sw.err != hipSuccess || !sw.ptr)
+    return create_fail(UNISON_E_HIP, "address of the static workspace on device %d: %s", dev,
+                       hipGetErrorString(sw.err));
+  unison_ctx* c = new (std::nothrow) unison_ctx();
+  if (!c) return create_fail(UNISON_E_INVALID, "out of host memory for the context");
+  c->dims = *d;
+  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  c->ws = reinterpret_cast<char*>(sw.ptr);
+  c->ws_bytes = UNISON_STATIC_WORKSPACE_BYTES;
+  c->L = L;
+  c->lut_set.assign(d->n_luts, 0);
+  c->err[0] = 0;
+  std::memset(&c->tb, 0, sizeof c->tb);
+  c->static_dev = dev;
+  c->static_gen = sw.gen.fetch_add(1) + 1;
+  g_create_err[0] = 0;
+  *out = c;
+  return UNISON_OK;
+}
+
 void unison_destroy(unison_ctx* ctx) { delete ctx; }
 
 int unison_set_stream(unison_ctx* ctx, void* hip_stream) {
@@ -224,6 +309,7 @@ int unison_set_stream(unison_ctx* ctx, void* hip_stream) {
 
 int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
   if (!ctx || !tb) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   const uint32_t nt = tb->n_traces;
   if (nt != ctx->dims.n_traces)
     return ctx->fail(UNISON_E_INVALID, "n_traces %u differs from dims %u", nt, ctx->dims.n_traces);
@@ -309,6 +395,7 @@ int unison_hazard_counts(void* hip_stream, const uint32_t* turns, uint32_t n, ui
 
 int unison_set_hazard(unison_ctx* ctx, uint32_t lut, const uint32_t* d, const uint32_t* n) {
   if (!ctx || !d || !n) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   if (lut >= ctx->dims.n_luts) return ctx->fail(UNISON_E_INVALID, "lut %u >= n_luts", lut);
   int rc = ctx->hip(hipMemcpyAsync(ctx->at<uint32_t>(ctx->L.lut_d) + (size_t)lut * kLut, d,
                                    sizeof(uint32_t) * kLut, hipMemcpyDeviceToDevice, ctx->stream),
@@ -324,6 +411,7 @@ int unison_set_hazard(unison_ctx* ctx, uint32_t lut, const uint32_t* d, const ui
 
 int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
   if (!ctx || !params) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   if (!ctx->traces_loaded) return ctx->fail(UNISON_E_NOT_READY, "load traces before parameters");
   uint32_t max_sess = 0;
   for (uint32_t i = 0; i < ctx->dims.n_sims; ++i) {
@@ -409,6 +497,7 @@ static int slot_map(unison_ctx* ctx, uint32_t policy_override, uint32_t lanes) {
 
 int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64_t max_events) {
   if (!ctx) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   if (!ctx->traces_loaded || !ctx->params_set)
     return ctx->fail(UNISON_E_NOT_READY, "traces and parameters must be set before a run");
   for (const auto& p : ctx->h_params)
@@ -483,6 +572,7 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
 
 int unison_read_counters(unison_ctx* ctx, unison_counters* dst, uint32_t first, uint32_t n) {
   if (!ctx || (!dst && n)) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   if ((uint64_t)first + n > ctx->dims.n_sims) return ctx->fail(UNISON_E_INVALID, "range");
   int rc = ctx->hip(hipMemcpyAsync(dst, ctx->at<unison_counters>(ctx->L.counters) + first,
                                    sizeof(unison_counters) * n, hipMemcpyDeviceToHost, ctx->stream),
@@ -498,12 +588,14 @@ int unison_read_counters(unison_ctx* ctx, unison_counters* dst, uint32_t first, 
 
 int unison_counters_device(unison_ctx* ctx, const unison_counters** out) {
   if (!ctx || !out) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   *out = ctx->at<unison_counters>(ctx->L.counters);
   return UNISON_OK;
 }
 
 int unison_read_log(unison_ctx* ctx, uint32_t sim, unison_record* dst, uint32_t cap, uint64_t* n_total) {
   if (!ctx || !n_total || (!dst && cap)) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   if (sim >= ctx->dims.n_sims) return ctx->fail(UNISON_E_INVALID, "sim %u", sim);
   SimState st;
   int rc = ctx->hip(hipMemcpyAsync(&st, ctx->at<SimState>(ctx->L.state) + sim, sizeof st,
@@ -527,6 +619,7 @@ int unison_read_log(unison_ctx* ctx, uint32_t sim, unison_record* dst, uint32_t 
 
 int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t* n_out) {
   if (!ctx || !d_out || !n_out) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
   if (sim >= ctx->dims.n_sims) return ctx->fail(UNISON_E_INVALID, "sim %u", sim);
   if (!ctx->ran) return ctx->fail(UNISON_E_NOT_READY, "no run on this context yet");
   // an online table's counts are in the workspace; a fixed table's are its own

@@ -77,6 +77,7 @@ def lib():
         sig = {
             "unison_workspace_size": [C.POINTER(Dims), C.POINTER(C.c_size_t)],
             "unison_create": [C.POINTER(vp), C.POINTER(Dims), vp, vp, C.c_size_t],
+            "unison_create_static": [C.POINTER(vp), C.POINTER(Dims), vp],
             "unison_load_traces": [vp, C.POINTER(TraceBatch)],
             "unison_hazard_counts": [vp, vp, u32, vp, vp],
             "unison_set_hazard": [vp, u32, vp, vp],
@@ -156,7 +157,7 @@ class Simulator:
     """A batch of simulations on the GPU: traces, hazard tables and parameter
     rows of a workload (see paper_2609_09643_amd.synth.Workload)."""
 
-    def __init__(self, workload, log_cap=0, variant=None, cache_slots=None):
+    def __init__(self, workload, log_cap=0, variant=None, cache_slots=None, static=False):
         torch = _torch()
         L = lib()
         self.workload = workload
@@ -184,12 +185,19 @@ class Simulator:
         nbytes = C.c_size_t()
         _check(L.unison_workspace_size(C.byref(self.dims), C.byref(nbytes)))
         self.ws_bytes = int(nbytes.value)
-        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device="cuda")
-        base = self.ws.data_ptr()
-        aligned = (base + 255) // 256 * 256
         self.ctx = C.c_void_p()
-        _check(L.unison_create(C.byref(self.ctx), C.byref(self.dims), _stream(),
-                               C.c_void_p(aligned), C.c_size_t(self.ws_bytes)))
+        if static:
+            # the library's own static workspace: no device allocation
+            self.ws = None
+            rc = L.unison_create_static(C.byref(self.ctx), C.byref(self.dims), _stream())
+            if rc != UNISON_OK:
+                raise UnisonError(rc, L.unison_last_error(None).decode())
+        else:
+            self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device="cuda")
+            base = self.ws.data_ptr()
+            aligned = (base + 255) // 256 * 256
+            _check(L.unison_create(C.byref(self.ctx), C.byref(self.dims), _stream(),
+                                   C.c_void_p(aligned), C.c_size_t(self.ws_bytes)))
         if variant is not None:
             _check(L.unison_debug_force_variant(self.ctx, int(variant)), self.ctx)
         if cache_slots is not None:
