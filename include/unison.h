@@ -38,6 +38,9 @@
  *                      (non-decreasing per session, eq. (reuse)); else 0
  *   ev_next_ns uint64  GAP_START: time of the session's next ARRIVE (read
  *                      only by the Belady policy); else UINT64_MAX
+ *   ev_tool    uint32  GAP_START: tool class of the gap that starts, below
+ *                      UNISON_ETA_CLASSES (read only by the ETA policy); else
+ *                      ignored.  Optional: without it every gap is class 0
  *   sess_kvb   uint32  per session: KV bytes per token (eq. (cap) in bytes)
  * A session's events must run ARRIVE(0), GAP_START(0), ARRIVE(1), ...,
  * ARRIVE(T-1), DONE(T-1).  A simulation that meets an event breaking this
@@ -70,6 +73,8 @@ extern "C" {
 #define UNISON_POLICY_LRU 1u     /* recency: evict the longest-idle session */
 #define UNISON_POLICY_TIMEOUT 2u /* recency plus expiry after an idle TTL */
 #define UNISON_POLICY_BELADY 3u  /* offline oracle: evict the farthest next request */
+#define UNISON_POLICY_ETA 4u     /* tool-type arrival table: evict the farthest predicted
+                                    return, gap onset + the expected wait of its tool class */
 #define UNISON_POLICY_PARAMS 0xFFu /* unison_run: use each simulation's own policy */
 
 #define UNISON_RUN_CONTINUE 1u   /* resume every simulation where the last run stopped */
@@ -80,6 +85,7 @@ extern "C" {
 
 #define UNISON_LUT_LEN 51u       /* hazard table entries, t = 0..50 (eq. (hazard)) */
 #define UNISON_MAX_SESSIONS (1u << 20) /* largest session count of one trace */
+#define UNISON_ETA_CLASSES 16u   /* tool classes of an ETA table */
 
 /* Decision record operations; `b` holds the second session or the tier. */
 #define UNISON_OP_EVICT 1u    /* a = victim (Alg. 1, capacity branch) */
@@ -115,7 +121,7 @@ typedef struct {
 /* One simulation's parameters (eq. (cap), eq. (esp), eq. (budget),
  * eq. (hr-amat), eq. (lock)); host array of n_sims rows. */
 typedef struct {
-  uint32_t policy;         /* UNISON_POLICY_SPEAR .. UNISON_POLICY_BELADY */
+  uint32_t policy;         /* UNISON_POLICY_SPEAR .. UNISON_POLICY_ETA */
   uint32_t tide;           /* 1: TIDE pass on gap onsets while the DMA is free */
   uint32_t score_mode;     /* 0: fp32 score; 1: fixed-point score_q (SPEAR only) */
   uint32_t lut;            /* hazard table index, < n_luts */
@@ -229,13 +235,15 @@ typedef struct {
   const uint32_t* ev_len;      /* DEVICE */
   const uint64_t* ev_next_ns;  /* DEVICE */
   const uint32_t* sess_kvb;    /* DEVICE */
+  const uint32_t* ev_tool;     /* DEVICE, or NULL: every gap is tool class 0 */
 } unison_trace_batch;
 
 /* Registers the traces (the arrays stay borrowed) and checks the event format
  * of each once, on a host copy of its events (session id in range, kind <=
  * DONE, times non-decreasing, every session's turns in order, prefixes
- * non-decreasing): a simulation then stops at its trace's first malformed
- * event and reports it through counters.error.  Synchronises the stream.
+ * non-decreasing, gap onsets' tool classes below UNISON_ETA_CLASSES): a
+ * simulation then stops at its trace's first malformed event and reports it
+ * through counters.error.  Synchronises the stream.
  * Errors: UNISON_E_INVALID (count differs from the dims, offsets not
  * monotone), UNISON_E_CAPACITY (a trace has more sessions than
  * dims.max_sessions), UNISON_E_HIP. */
@@ -250,6 +258,23 @@ int unison_hazard_counts(void* hip_stream, const uint32_t* turns, uint32_t n, ui
 /* Installs hazard table `lut` from its counts: h(t) = d(t)/n(t) (0 where
  * n(t) = 0).  d, n: DEVICE [51], copied on the context's stream. */
 int unison_set_hazard(unison_ctx* ctx, uint32_t lut, const uint32_t* d, const uint32_t* n);
+
+/* The ETA baseline's table fitted on a trace: for each tool class c, the
+ * mean (floor, integer ns) of next ARRIVE time - GAP_START time over the
+ * trace's gap onsets of class c that have a next arrival; 0 for a class
+ * without any.  Events: DEVICE arrays of n_events entries (ev_tool may be
+ * NULL: all class 0); mean_out: DEVICE [UNISON_ETA_CLASSES].  Classes at or
+ * above UNISON_ETA_CLASSES are skipped.  Asynchronous on `hip_stream`. */
+int unison_eta_fit(void* hip_stream, uint64_t n_events, const uint64_t* ev_t_ns,
+                   const uint32_t* ev_info, const uint32_t* ev_tool, const uint64_t* ev_next_ns,
+                   uint64_t* mean_out);
+
+/* Installs the ETA table of trace `trace`: the expected wait (ns) of each of
+ * the UNISON_ETA_CLASSES tool classes.  A simulation of that trace under
+ * UNISON_POLICY_ETA keys a session at its gap onset by the predicted return
+ * onset + mean[class] (saturating); a completed session never returns.
+ * mean: DEVICE, copied on the context's stream.  Errors: UNISON_E_INVALID. */
+int unison_set_eta(unison_ctx* ctx, uint32_t trace, const uint64_t* mean);
 
 /* Copies n_sims parameter rows (HOST) into the workspace.  Errors:
  * UNISON_E_INVALID for an out-of-range field (policy, lut, trace, b_h, b_g,
@@ -268,7 +293,8 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
  * kernels that keep one bit of LDS per session (the residency bits their
  * scans visit): 128 KiB at UNISON_MAX_SESSIONS; the LDS left holds up to 8
  * resident-cache slots of 28 B per thread.  Asynchronous.
- * Errors: UNISON_E_NOT_READY, UNISON_E_INVALID (also: a register-table
+ * Errors: UNISON_E_NOT_READY (also: an ETA simulation whose trace has no ETA
+ * table), UNISON_E_INVALID (also: a register-table
  * variant forced on a batch with a dual-design row), UNISON_E_CAPACITY (the
  * largest trace exceeds the chosen kernel variant, e.g. on a device with
  * less LDS per workgroup than the bits need). */

@@ -7,8 +7,9 @@ the product path never does, and this module imports nothing from the
 product package.
 
 Inputs are duck-typed: a trace is any object with ``t_ns, sid, info, length,
-next_ns, kvb`` numpy arrays; a parameter row is any numpy structured row with
-the field names used below.
+next_ns, kvb`` numpy arrays (and optionally ``tool``, the tool class of each
+gap onset); a parameter row is any numpy structured row with the field names
+used below.
 """
 from __future__ import annotations
 
@@ -24,6 +25,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 LUT_LEN = 51
+ETA_CLASSES = 16
 NONE_ID = 0xFFFFFFFF
 OP_EVICT, OP_EXPIRE, OP_BYPASS, OP_PROMOTE, OP_SWAP, OP_VICTIM, OP_PLACE = 1, 2, 3, 4, 5, 6, 7
 TIER_NONE, TIER_SRAM, TIER_HBM = 0, 1, 2
@@ -113,7 +115,9 @@ def load_library(path):
     L.orc_run.restype = C.c_int
     L.orc_run.argtypes = [C.POINTER(Params), C.c_uint64, u64p, u32p, u32p, u32p, u64p,
                           C.c_uint32, u32p, u32p, u32p, C.c_uint64, C.POINTER(Counters),
-                          C.c_void_p, C.c_uint32, u32p, C.c_void_p, C.c_void_p, u64p]
+                          C.c_void_p, C.c_uint32, u32p, C.c_void_p, C.c_void_p, u64p,
+                          u32p, u64p]
+    L.orc_eta_fit.argtypes = [C.c_uint64, u64p, u32p, u32p, u64p, u64p]
     L.orc_hazard_counts.argtypes = [u32p, C.c_uint32, u32p, u32p]
     L.orc_lut_f32.argtypes = [u32p, u32p, f32p]
     L.orc_lut_q.argtypes = [u32p, u32p, C.c_uint32, u64p]
@@ -126,7 +130,7 @@ def load_library(path):
     L.orc_run_batch.restype = C.c_int
     L.orc_run_batch.argtypes = [C.c_void_p, C.c_uint32, u32p, u32p, u64p, u64p, u64p, u32p,
                                 u32p, u32p, u64p, u32p, u32p, u32p, C.c_uint64, C.c_void_p,
-                                u64p]
+                                u64p, u32p, u64p]
     return L
 
 
@@ -233,6 +237,21 @@ def tau_b(counts):
 
 # -------------------------------------------------------------- simulation
 
+def _tool(trace):
+    t = getattr(trace, "tool", None)
+    return _c(t if t is not None else np.zeros(trace.t_ns.shape[0], np.uint32), np.uint32)
+
+
+def eta_table(trace):
+    """The ETA table fitted on a trace: mean wait (ns) per tool class."""
+    t, info = _c(trace.t_ns, np.uint64), _c(trace.info, np.uint32)
+    nxt, tool = _c(trace.next_ns, np.uint64), _tool(trace)
+    out = np.zeros(ETA_CLASSES, np.uint64)
+    lib().orc_eta_fit(t.shape[0], _p(t, C.c_uint64), _p(info, C.c_uint32), _p(tool, C.c_uint32),
+                      _p(nxt, C.c_uint64), _p(out, C.c_uint64))
+    return out
+
+
 def params_struct(row):
     p = Params()
     for name, _ in Params._fields_:
@@ -244,12 +263,15 @@ def params_struct(row):
 
 
 def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False, counts=None,
-        library=None):
+        library=None, eta=None):
     """Runs one simulation. Returns (rc, counters dict, log or None, states or None,
     elapsed_ns of the event loop).  counts: optional uint32 array [2, 51] that
     receives the hazard counts d, n of the table at the end.  library: a
-    library from load_library() to run instead of the oracle's own build."""
+    library from load_library() to run instead of the oracle's own build.
+    eta: the ETA table (default: fitted on the trace)."""
     L = lib() if library is None else library
+    tool = _tool(trace)
+    eta = _c(eta_table(trace) if eta is None else eta, np.uint64)
     p = params_struct(row)
     t_ns, sid = _c(trace.t_ns, np.uint64), _c(trace.sid, np.uint32)
     info, length = _c(trace.info, np.uint32), _c(trace.length, np.uint32)
@@ -271,7 +293,7 @@ def run(trace, row, lut_d, lut_n, max_events=None, log_cap=0, states=False, coun
                    _p(log_len, C.c_uint32),
                    st.ctypes.data_as(C.c_void_p) if st is not None else None,
                    counts.ctypes.data_as(C.c_void_p) if counts is not None else None,
-                   _p(el, C.c_uint64))
+                   _p(el, C.c_uint64), _p(tool, C.c_uint32), _p(eta, C.c_uint64))
     if log is not None:
         log = log[:min(int(log_len[0]), log_cap)]
         if int(log_len[0]) > log_cap:
@@ -294,6 +316,9 @@ class Batch:
         self.t, self.sid = cat("t_ns", np.uint64), cat("sid", np.uint32)
         self.info, self.len = cat("info", np.uint32), cat("length", np.uint32)
         self.next, self.kvb = cat("next_ns", np.uint64), cat("kvb", np.uint32)
+        self.tool = np.ascontiguousarray(np.concatenate([_tool(t) for t in trs] +
+                                                        [np.zeros(1, np.uint32)]))
+        self.eta = np.ascontiguousarray(np.stack([eta_table(t) for t in trs]), dtype=np.uint64)
         D, N = luts_for(workload)
         self.D, self.N = np.ascontiguousarray(D), np.ascontiguousarray(N)
         self.params = workload.params
@@ -322,7 +347,8 @@ class Batch:
             _p(self.ev_off, C.c_uint64), _p(self.ss_off, C.c_uint64), _p(self.t, C.c_uint64),
             _p(self.sid, C.c_uint32), _p(self.info, C.c_uint32), _p(self.len, C.c_uint32),
             _p(self.next, C.c_uint64), _p(self.kvb, C.c_uint32), _p(self.D, C.c_uint32),
-            _p(self.N, C.c_uint32), me, C.cast(cnt, C.c_void_p), _p(el, C.c_uint64))
+            _p(self.N, C.c_uint32), me, C.cast(cnt, C.c_void_p), _p(el, C.c_uint64),
+            _p(self.tool, C.c_uint32), _p(self.eta, C.c_uint64))
         return rc, [cnt[k].as_dict() for k in range(n)], int(el[0])
 
 

@@ -92,6 +92,17 @@
  *            differ.  The copies start as the empty register file.
  *  timeout   Before an event is written, every resident that has been idle
  *            longer than the TTL expires (its timer fired since the last event).
+ *  ETA       The tool-type arrival-table baseline (the expected-completion
+ *            estimator among the related methods): each gap onset names the
+ *            tool class of the gap it opens, and a table holds one expected
+ *            wait per class -- the same wait for every session that calls
+ *            the tool.  By default the table is fitted on the whole trace, as
+ *            the hazard table is: the mean (floor, integer ns) of the gaps of
+ *            that class, a gap being the next ARRIVE's time minus the
+ *            GAP_START's.  The key is the predicted return, gap start + the
+ *            class's wait (saturating), larger = evict first; a completed
+ *            session never returns (2^64 - 1).  Tool classes are 0..15; a
+ *            gap onset naming a larger one breaks the trace format.
  *  account   eq. (hr-amat), eq. (prered): SRAM hit amat += len*kvb*t_s,
  *            ttft += len_prev*kvb*t_s + dlen*t_p, computed += dlen; HBM hit
  *            likewise with t_h; miss amat += len*t_p, ttft += len*t_p,
@@ -113,9 +124,10 @@
 
 #define NONE_ID 0xFFFFFFFFu
 #define LUT_LEN 51 /* t = 0..50, eq. (hazard) */
+#define ETA_CLASSES 16 /* tool classes of the ETA table */
 
 enum { K_ARRIVE = 0, K_GAP_START = 1, K_DONE = 2 };
-enum { P_SPEAR = 0, P_LRU = 1, P_TIMEOUT = 2, P_BELADY = 3 };
+enum { P_SPEAR = 0, P_LRU = 1, P_TIMEOUT = 2, P_BELADY = 3, P_ETA = 4 };
 enum { T_NONE = 0, T_SRAM = 1, T_HBM = 2 };
 enum { PH_UNSEEN = 0, PH_SERVING = 1, PH_GAP = 2, PH_DONE = 3 };
 enum { OP_EVICT = 1, OP_EXPIRE = 2, OP_BYPASS = 3, OP_PROMOTE = 4, OP_SWAP = 5, OP_VICTIM = 6,
@@ -124,7 +136,7 @@ enum { OP_EVICT = 1, OP_EXPIRE = 2, OP_BYPASS = 3, OP_PROMOTE = 4, OP_SWAP = 5, 
 enum { ORC_OK = 0, ORC_E_INVALID = -1, ORC_E_BAD_TRACE = -2 };
 
 typedef struct {
-  uint32_t policy;      /* P_SPEAR .. P_BELADY */
+  uint32_t policy;      /* P_SPEAR .. P_ETA */
   uint32_t tide;        /* 1: run the TIDE pass on GAP_START */
   uint32_t score_mode;  /* 0: fp32 score, 1: fixed-point score (SPEAR only) */
   uint32_t lut;         /* index of the hazard count table */
@@ -302,6 +314,27 @@ void orc_ema_replay(uint32_t n, uint32_t max_hist, const uint64_t* gaps_ns,
   }
 }
 
+/* ------------------------------------------------------- the ETA table */
+
+/* Mean wait per tool class over a trace's gaps (see "ETA" above): for every
+ * GAP_START with a next arrival, gap = next - t joins its class's sum; mean =
+ * floor(sum / count), 0 for a class without gaps. */
+void orc_eta_fit(uint64_t n_events, const uint64_t* ev_t, const uint32_t* ev_info,
+                 const uint32_t* ev_tool, const uint64_t* ev_next, uint64_t* mean_out) {
+  unsigned __int128 sum[ETA_CLASSES];
+  uint64_t cnt[ETA_CLASSES];
+  for (int c = 0; c < ETA_CLASSES; c++) { sum[c] = 0; cnt[c] = 0; }
+  for (uint64_t e = 0; e < n_events; e++) {
+    if ((ev_info[e] >> 24) != K_GAP_START || ev_next[e] == UINT64_MAX) continue;
+    uint32_t c = ev_tool ? ev_tool[e] : 0;
+    if (c >= ETA_CLASSES || ev_next[e] < ev_t[e]) continue;
+    sum[c] += ev_next[e] - ev_t[e];
+    cnt[c]++;
+  }
+  for (int c = 0; c < ETA_CLASSES; c++)
+    mean_out[c] = cnt[c] ? sat_u64(sum[c] / cnt[c]) : 0;
+}
+
 /* --------------------------------------------- Kendall tau-b pair counts */
 
 /* counts = {concordant, discordant, tied in x only, tied in y only, tied in
@@ -352,6 +385,7 @@ typedef struct {
 
 typedef struct {
   const orc_params* p;
+  const uint64_t* eta;  /* the ETA table, ETA_CLASSES waits in ns */
   sess_t* s;
   sess_t* view[2];  /* dual design: the eviction engine's and TIDE's copies */
   int keysrc;       /* where keys are read: -1 the live file, 0 or 1 a copy */
@@ -400,14 +434,14 @@ static uint64_t key_of(const sim_t* m, uint32_t i) {
     case P_LRU:
     case P_TIMEOUT:
       return UINT64_MAX - e->last_ns;
-    default:
+    default: /* Belady: the next arrival; ETA: the predicted one */
       return e->next_ns;
   }
 }
 
 static uint64_t done_key(const sim_t* m) {
   if (m->p->policy == P_SPEAR) return m->p->score_mode == 1 ? UINT64_MAX : 0x7F800000u;
-  if (m->p->policy == P_BELADY) return UINT64_MAX;
+  if (m->p->policy == P_BELADY || m->p->policy == P_ETA) return UINT64_MAX;
   return 0; /* recency keys have no completion value */
 }
 
@@ -496,7 +530,7 @@ static void tide(sim_t* m, uint32_t sid, uint64_t now, orc_state* st) {
   uint64_t budget = sat_u64((unsigned __int128)delta_us * p->dma_B_per_us);
   uint64_t left = budget, moved = 0;
   uint64_t inf = done_key(m);
-  int has_inf = p->policy == P_SPEAR || p->policy == P_BELADY;
+  int has_inf = p->policy == P_SPEAR || p->policy == P_BELADY || p->policy == P_ETA;
   m->c->tide_passes++;
   int src = m->keysrc;
   m->keysrc = m->view[1] ? 1 : -1;
@@ -562,6 +596,8 @@ static void tide(sim_t* m, uint32_t sid, uint64_t now, orc_state* st) {
  *   log/states optional outputs (NULL to skip); states has one entry per event
  *   counts_out optional: the table's counts at the end, d[51] then n[51]
  *   elapsed_ns wall time of the event loop alone (optional)
+ *   ev_tool    tool class of each event (read at gap onsets; NULL: all 0)
+ *   eta_mean   the ETA table (ETA_CLASSES waits, ns); needed by the ETA policy
  * Returns ORC_OK, ORC_E_INVALID or ORC_E_BAD_TRACE (counters.error = event+1).
  */
 int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
@@ -569,8 +605,10 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
             const uint64_t* ev_next, uint32_t n_sess, const uint32_t* kvb,
             const uint32_t* lut_d, const uint32_t* lut_n, uint64_t max_events,
             orc_counters* out, orc_rec* log, uint32_t log_cap, uint32_t* log_len,
-            orc_state* states, uint32_t* counts_out, uint64_t* elapsed_ns) {
-  if (!p || !out || p->policy > P_BELADY || p->dma_B_per_us == 0 || p->n_slots == 0 ||
+            orc_state* states, uint32_t* counts_out, uint64_t* elapsed_ns,
+            const uint32_t* ev_tool, const uint64_t* eta_mean) {
+  if (!p || !out || p->policy > P_ETA || (p->policy == P_ETA && !eta_mean) ||
+      p->dma_B_per_us == 0 || p->n_slots == 0 ||
       p->tau_ns == 0 || p->b_h < 1 || p->b_h > 32 || p->b_g < 1 || p->b_g > 64 || p->dual_sync > 3 ||
       !(p->penalty_us >= 0.0f))
     return ORC_E_INVALID;
@@ -578,6 +616,7 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
   sim_t m;
   memset(&m, 0, sizeof m);
   m.p = p;
+  m.eta = eta_mean;
   m.kvb = kvb;
   m.n_sess = n_sess;
   m.c = out;
@@ -614,7 +653,10 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
     uint32_t turn = ev_info[e] & 0xFFFFFFu;
     orc_state* st = states ? &states[e] : NULL;
     if (st) memset(st, 0, sizeof *st);
-    if (sid >= n_sess || now < prev_t || kind > K_DONE) { rc = ORC_E_BAD_TRACE; out->error = e + 1; break; }
+    uint32_t tool = ev_tool ? ev_tool[e] : 0;
+    if (sid >= n_sess || now < prev_t || kind > K_DONE || (kind == K_GAP_START && tool >= ETA_CLASSES)) {
+      rc = ORC_E_BAD_TRACE; out->error = e + 1; break;
+    }
     prev_t = now;
     sess_t* x = &m.s[sid];
 
@@ -656,7 +698,8 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
       x->last_ns = now;
       if (kind == K_GAP_START) {
         x->phase = PH_GAP;
-        x->next_ns = ev_next[e];
+        /* Belady reads the true next arrival; ETA predicts it from the tool */
+        x->next_ns = p->policy == P_ETA ? sat_u64((unsigned __int128)now + m.eta[tool]) : ev_next[e];
       } else {
         x->phase = PH_DONE;
         x->next_ns = UINT64_MAX;
@@ -755,15 +798,17 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
  * of the ev_* arrays and sessions [ss_off[k], ss_off[k+1]) of kvb.  Row i
  * replays trace row_trace[i] with the hazard counts lut_d/lut_n + 51 *
  * row_lut[i] and writes out[i]; elapsed_ns (optional) receives the summed
- * event-loop time.  Every row runs; the first non-zero orc_run code is
- * returned.
+ * event-loop time.  ev_tool is concatenated like the events; eta holds the
+ * ETA table of each trace (ETA_CLASSES waits per trace).  Every row runs;
+ * the first non-zero orc_run code is returned.
  */
 int orc_run_batch(const orc_params* rows, uint32_t n_rows, const uint32_t* row_trace,
                   const uint32_t* row_lut, const uint64_t* ev_off, const uint64_t* ss_off,
                   const uint64_t* ev_t, const uint32_t* ev_sid, const uint32_t* ev_info,
                   const uint32_t* ev_len, const uint64_t* ev_next, const uint32_t* kvb,
                   const uint32_t* lut_d, const uint32_t* lut_n, uint64_t max_events,
-                  orc_counters* out, uint64_t* elapsed_ns) {
+                  orc_counters* out, uint64_t* elapsed_ns, const uint32_t* ev_tool,
+                  const uint64_t* eta) {
   int rc_all = ORC_OK;
   uint64_t total = 0;
   for (uint32_t i = 0; i < n_rows; i++) {
@@ -773,7 +818,8 @@ int orc_run_batch(const orc_params* rows, uint32_t n_rows, const uint32_t* row_t
     int rc = orc_run(&rows[i], n_ev, ev_t + e0, ev_sid + e0, ev_info + e0, ev_len + e0,
                      ev_next + e0, (uint32_t)(ss_off[k + 1] - s0), kvb + s0,
                      lut_d + (uint64_t)LUT_LEN * row_lut[i], lut_n + (uint64_t)LUT_LEN * row_lut[i],
-                     max_events, &out[i], NULL, 0, NULL, NULL, NULL, &ns);
+                     max_events, &out[i], NULL, 0, NULL, NULL, NULL, &ns, ev_tool + e0,
+                     eta + (uint64_t)ETA_CLASSES * k);
     total += ns;
     if (rc != ORC_OK && rc_all == ORC_OK) rc_all = rc;
   }

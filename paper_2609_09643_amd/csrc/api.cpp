@@ -26,6 +26,8 @@ int sim_auto_variant(uint32_t max_sess);
 uint32_t sim_variant_lanes(int v);
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
                                 hipStream_t stream);
+hipError_t launch_eta_fit(uint64_t n, const uint64_t* t, const uint32_t* info, const uint32_t* tool,
+                          const uint64_t* next, uint64_t* mean, hipStream_t stream);
 hipError_t launch_max_time(const uint64_t* t, const uint64_t* next, uint64_t n, uint64_t* out,
                            hipStream_t stream);
 hipError_t launch_ema_replay(uint32_t n, uint32_t max_hist, const uint64_t* gaps,
@@ -54,8 +56,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Workspace layout; offsets in bytes from the workspace base.
 struct Layout {
-  size_t params, ev_off, first_bad, sess_off, lut_d, lut_n, state, counters, hcount, mg, gq, len, last, next,
-      views, log, slots, scratch, total;
+  size_t params, ev_off, first_bad, sess_off, lut_d, lut_n, eta, state, counters, hcount, mg, gq, len,
+      last, next, views, log, slots, scratch, total;
 };
 
 bool make_layout(const unison_dims& d, Layout& L) {
@@ -72,6 +74,7 @@ bool make_layout(const unison_dims& d, Layout& L) {
   L.sess_off = take(sizeof(uint64_t) * (d.n_traces + 1));
   L.lut_d = take(sizeof(uint32_t) * kLut * d.n_luts);
   L.lut_n = take(sizeof(uint32_t) * kLut * d.n_luts);
+  L.eta = take(sizeof(uint64_t) * UNISON_ETA_CLASSES * d.n_traces);
   L.state = take(sizeof(SimState) * d.n_sims);
   L.counters = take(sizeof(unison_counters) * d.n_sims);
   L.hcount = take(sizeof(uint32_t) * 2 * kLut * d.n_sims);
@@ -94,10 +97,11 @@ bool make_layout(const unison_dims& d, Layout& L) {
 // a session id past the trace's sessions, a kind above DONE, a time before
 // the previous event's; an ARRIVE of turn 0 for a session already seen, of
 // turn k >= 1 that does not follow the GAP_START of turn k - 1 or shortens the
-// prefix; a GAP_START or DONE of a session that is not being served.  These
-// depend on the trace alone, so they are checked once per load.
+// prefix; a GAP_START or DONE of a session that is not being served; a
+// GAP_START whose tool class is UNISON_ETA_CLASSES or more.  These depend on
+// the trace alone, so they are checked once per load.
 uint64_t first_bad_event(const uint64_t* t, const uint32_t* sid, const uint32_t* info,
-                         const uint32_t* len, uint64_t n, uint32_t n_sess) {
+                         const uint32_t* len, const uint32_t* tool, uint64_t n, uint32_t n_sess) {
   struct Sess {
     uint32_t phase, turn, len;  // phase: 0 unseen, 1 served, 2 in a gap, 3 completed
   };
@@ -115,6 +119,7 @@ uint64_t first_bad_event(const uint64_t* t, const uint32_t* sid, const uint32_t*
       x.len = len[e];
     } else {
       if (x.phase != 1) return e;
+      if (kind == 1 && tool && tool[e] >= UNISON_ETA_CLASSES) return e;
       x.phase = kind == 1 ? 2 : 3;
     }
   }
@@ -166,6 +171,7 @@ struct unison_ctx {
   std::vector<uint64_t> h_ev_off, h_sess_off, h_first_bad;
   std::vector<unison_sim_params> h_params;
   std::vector<uint8_t> lut_set;
+  std::vector<uint8_t> eta_set;  // per trace: an ETA table was installed
   bool traces_loaded = false, params_set = false, ran = false;
   bool time44 = false;  // every trace time is below 2^44 - 1 ns
   bool dual = false;    // some row uses the dual register-file design
@@ -327,6 +333,7 @@ int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
                        (unsigned long long)ns, ctx->dims.max_sessions);
   }
   ctx->tb = *tb;
+  ctx->eta_set.assign(nt, 0);
   ctx->h_ev_off.assign(tb->ev_offset, tb->ev_offset + nt + 1);
   ctx->h_sess_off.assign(tb->sess_offset, tb->sess_offset + nt + 1);
   int rc = ctx->hip(hipMemcpyAsync(ctx->at<uint64_t>(ctx->L.ev_off), ctx->h_ev_off.data(),
@@ -352,7 +359,7 @@ int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
   // the event format, checked once per trace on a host copy of its events
   ctx->h_first_bad.assign(nt, ~0ull);
   std::vector<uint64_t> ht;
-  std::vector<uint32_t> hs, hi, hl;
+  std::vector<uint32_t> hs, hi, hl, hk;
   for (uint32_t i = 0; i < nt; ++i) {
     const uint64_t b = tb->ev_offset[i], n = tb->ev_offset[i + 1] - b;
     if (n == 0) continue;
@@ -360,6 +367,7 @@ int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
     hs.resize(n);
     hi.resize(n);
     hl.resize(n);
+    hk.resize(tb->ev_tool ? n : 0);
     rc = ctx->hip(hipMemcpyAsync(ht.data(), tb->ev_t_ns + b, n * sizeof(uint64_t), hipMemcpyDeviceToHost,
                                  ctx->stream), "copy trace times");
     if (rc == UNISON_OK)
@@ -371,9 +379,13 @@ int unison_load_traces(unison_ctx* ctx, const unison_trace_batch* tb) {
     if (rc == UNISON_OK)
       rc = ctx->hip(hipMemcpyAsync(hl.data(), tb->ev_len + b, n * sizeof(uint32_t), hipMemcpyDeviceToHost,
                                    ctx->stream), "copy trace lengths");
+    if (rc == UNISON_OK && tb->ev_tool)
+      rc = ctx->hip(hipMemcpyAsync(hk.data(), tb->ev_tool + b, n * sizeof(uint32_t), hipMemcpyDeviceToHost,
+                                   ctx->stream), "copy trace tool classes");
     if (rc == UNISON_OK) rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise trace copy");
     if (rc) return rc;
-    ctx->h_first_bad[i] = first_bad_event(ht.data(), hs.data(), hi.data(), hl.data(), n,
+    ctx->h_first_bad[i] = first_bad_event(ht.data(), hs.data(), hi.data(), hl.data(),
+                                          tb->ev_tool ? hk.data() : nullptr, n,
                                           (uint32_t)(tb->sess_offset[i + 1] - tb->sess_offset[i]));
   }
   rc = ctx->hip(hipMemcpyAsync(ctx->at<uint64_t>(ctx->L.first_bad), ctx->h_first_bad.data(),
@@ -391,6 +403,28 @@ int unison_hazard_counts(void* hip_stream, const uint32_t* turns, uint32_t n, ui
   if ((!turns && n) || !d_out || !n_out) return UNISON_E_INVALID;
   hipError_t e = launch_hazard_counts(turns, n, d_out, n_out, reinterpret_cast<hipStream_t>(hip_stream));
   return e == hipSuccess ? UNISON_OK : UNISON_E_HIP;
+}
+
+int unison_eta_fit(void* hip_stream, uint64_t n_events, const uint64_t* ev_t_ns, const uint32_t* ev_info,
+                   const uint32_t* ev_tool, const uint64_t* ev_next_ns, uint64_t* mean_out) {
+  if (!mean_out || (n_events && (!ev_t_ns || !ev_info || !ev_next_ns))) return UNISON_E_INVALID;
+  hipError_t e = launch_eta_fit(n_events, ev_t_ns, ev_info, ev_tool, ev_next_ns, mean_out,
+                                reinterpret_cast<hipStream_t>(hip_stream));
+  return e == hipSuccess ? UNISON_OK : UNISON_E_HIP;
+}
+
+int unison_set_eta(unison_ctx* ctx, uint32_t trace, const uint64_t* mean) {
+  if (!ctx || !mean) return UNISON_E_INVALID;
+  UNISON_LIVE(ctx);
+  if (!ctx->traces_loaded) return ctx->fail(UNISON_E_NOT_READY, "load traces before ETA tables");
+  if (trace >= ctx->dims.n_traces) return ctx->fail(UNISON_E_INVALID, "trace %u >= n_traces", trace);
+  int rc = ctx->hip(hipMemcpyAsync(ctx->at<uint64_t>(ctx->L.eta) + (size_t)trace * UNISON_ETA_CLASSES,
+                                   mean, sizeof(uint64_t) * UNISON_ETA_CLASSES,
+                                   hipMemcpyDeviceToDevice, ctx->stream),
+                    "copy ETA table");
+  if (rc) return rc;
+  ctx->eta_set[trace] = 1;
+  return UNISON_OK;
 }
 
 int unison_set_hazard(unison_ctx* ctx, uint32_t lut, const uint32_t* d, const uint32_t* n) {
@@ -419,7 +453,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
     if (p.dual_sync > UNISON_DUAL_GAP || (p.dual_sync && !ctx->dims.views))
       return ctx->fail(UNISON_E_INVALID, "parameter row %u: dual_sync %u (dims.views = %u)", i,
                        p.dual_sync, ctx->dims.views);
-    if (p.policy > UNISON_POLICY_BELADY || p.tide > 1 || p.score_mode > 1 || p.hazard_online > 1 ||
+    if (p.policy > UNISON_POLICY_ETA || p.tide > 1 || p.score_mode > 1 || p.hazard_online > 1 ||
         p.lut >= ctx->dims.n_luts || p.trace >= ctx->dims.n_traces || p.b_h < 1 || p.b_h > 16 ||
         p.b_g < 1 || p.b_g > 64 || p.tau_ns < 1 || p.n_slots < 1 || p.dma_B_per_us < 1 ||
         !(p.penalty_us >= 0.0f) || std::isinf(p.penalty_us) || !std::isfinite(p.t_s_ns_per_B) ||
@@ -502,8 +536,13 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
     return ctx->fail(UNISON_E_NOT_READY, "traces and parameters must be set before a run");
   for (const auto& p : ctx->h_params)
     if (!ctx->lut_set[p.lut]) return ctx->fail(UNISON_E_NOT_READY, "hazard table %u not set", p.lut);
-  if (policy_override != UNISON_POLICY_PARAMS && policy_override > UNISON_POLICY_BELADY)
+  if (policy_override != UNISON_POLICY_PARAMS && policy_override > UNISON_POLICY_ETA)
     return ctx->fail(UNISON_E_INVALID, "policy %u", policy_override);
+  for (const auto& p : ctx->h_params) {
+    const uint32_t pol = policy_override == UNISON_POLICY_PARAMS ? p.policy : policy_override;
+    if (pol == UNISON_POLICY_ETA && !ctx->eta_set[p.trace])
+      return ctx->fail(UNISON_E_NOT_READY, "ETA table of trace %u not set", p.trace);
+  }
   if (flags & ~(UNISON_RUN_CONTINUE | UNISON_RUN_LOG | UNISON_RUN_LOG_VICTIM))
     return ctx->fail(UNISON_E_INVALID, "flags");
   if ((flags & UNISON_RUN_CONTINUE) && !ctx->ran)
@@ -519,6 +558,8 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   a.ev_info = ctx->tb.ev_info;
   a.ev_len = ctx->tb.ev_len;
   a.ev_next = ctx->tb.ev_next_ns;
+  a.ev_tool = ctx->tb.ev_tool;
+  a.eta = ctx->at<uint64_t>(ctx->L.eta);
   a.sess_kvb = ctx->tb.sess_kvb;
   a.lut_d = ctx->at<uint32_t>(ctx->L.lut_d);
   a.lut_n = ctx->at<uint32_t>(ctx->L.lut_n);

@@ -139,9 +139,12 @@ struct Pol {
   static constexpr bool spear = POL == kSpear;
   static constexpr bool fixed = spear && SMODE == 1;
   static constexpr bool belady = POL == kBelady;
+  static constexpr bool eta = POL == kEta;
+  // the key is the session's next arrival: true (Belady) or predicted (ETA)
+  static constexpr bool nextkey = belady || eta;
   static constexpr bool timeout = POL == kTimeout;
   static constexpr bool recency = POL == kLru || POL == kTimeout;
-  static constexpr bool has_inf = spear || belady;
+  static constexpr bool has_inf = spear || nextkey;
   static constexpr uint64_t inf_key = (spear && !fixed) ? 0x7F800000ull : ~0ull;
 };
 
@@ -159,6 +162,7 @@ struct KeyCtx {
   uint64_t p_z;
   bool pack44;          // times fit 44 bits and ids 20 bits: recency / Belady keys pack
   uint32_t online_cap;  // completions an online table still may count; 0: fixed table
+  const uint64_t* eta;  // the trace's ETA table: expected wait per tool class, ns (global)
 };
 
 // Adds a completed session of Tn turns to the counts (n(t) += 1 for t < Tn,
@@ -211,7 +215,7 @@ __device__ __forceinline__ uint64_t key_of(const KeyCtx& K, uint32_t meta, uint3
       const float s = spear_f32(__uint_as_float(hz), g, K.P);
       return done ? 0x7F800000ull : (uint64_t)__float_as_uint(s);
     }
-  } else if constexpr (PT::belady) {
+  } else if constexpr (PT::nextkey) {
     return next;
   } else {
     return ~0ull - last;
@@ -286,7 +290,7 @@ struct RegTable {
     e.len = bcast(len, sid);
     e.kvb = bcast(kvb, sid);
     e.last = bcast(last, sid);
-    e.next = PT::belady ? bcast(next, sid) : ~0ull;
+    e.next = PT::nextkey ? bcast(next, sid) : ~0ull;
     return e;
   }
   __device__ __forceinline__ void read_size(uint32_t sid, uint64_t& size, uint32_t& m) const {
@@ -312,7 +316,7 @@ struct RegTable {
       const bool w = mine && js == (uint32_t)j;
       meta[j] = w ? m : meta[j];
       last[j] = w ? t : last[j];
-      if constexpr (PT::belady) next[j] = w ? nx : next[j];
+      if constexpr (PT::nextkey) next[j] = w ? nx : next[j];
     }
   }
 
@@ -327,7 +331,7 @@ struct RegTable {
       if constexpr (PT::fixed) gq[j] = w ? e.gq : gq[j];
       len[j] = w ? e.len : len[j];
       last[j] = w ? e.last : last[j];
-      if constexpr (PT::belady) next[j] = w ? e.next : next[j];
+      if constexpr (PT::nextkey) next[j] = w ? e.next : next[j];
     }
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) {
@@ -368,7 +372,8 @@ struct RegTable {
       return PT::fixed ? k : k << 32;
     } else {
       constexpr uint64_t kCap = (1ull << 44) - 1;
-      if (K.pack44) {
+      // predicted returns (ETA) may pass 2^44: they compare unpacked
+      if ((PT::recency || PT::belady) && K.pack44) {
         uint64_t k44;
         if constexpr (PT::belady) k44 = nextv < kCap ? nextv : kCap;
         else k44 = kCap - lastv;
@@ -379,7 +384,7 @@ struct RegTable {
   }
   __device__ __forceinline__ uint64_t packed_key_at(const KeyCtx& K, int j) const {
     return packed_key(K, meta[j], hz[j], g[j], PT::fixed ? gq[j] : 0ull, PT::recency ? last[j] : 0ull,
-                      PT::belady ? next[j] : 0ull);
+                      PT::nextkey ? next[j] : 0ull);
   }
   __device__ __forceinline__ void rescore_all(const KeyCtx& K) {
 #pragma unroll
@@ -394,7 +399,7 @@ struct RegTable {
     const bool mine = lane == sid % G;
     const uint64_t k = packed_key(K, pick(meta, js), pick(hz, js), pick(g, js),
                                   PT::fixed ? pick(gq, js) : 0ull, PT::recency ? pick(last, js) : 0ull,
-                                  PT::belady ? pick(next, js) : 0ull);
+                                  PT::nextkey ? pick(next, js) : 0ull);
 #pragma unroll
     for (int j = 0; j < EPL; ++j) pk[j] = (mine && js == (uint32_t)j) ? k : pk[j];
   }
@@ -568,11 +573,11 @@ struct MemTable {
   // the integer gap EMA (fixed-point score), the next arrival (Belady) or
   // the last event time (LRU, timeout).
   __device__ __forceinline__ static uint64_t aux_pick(uint64_t q, uint64_t l, uint64_t n) {
-    return PT::fixed ? q : PT::belady ? n : PT::recency ? l : 0ull;
+    return PT::fixed ? q : PT::nextkey ? n : PT::recency ? l : 0ull;
   }
   __device__ __forceinline__ uint64_t aux_table(uint32_t i) const {
     if constexpr (PT::fixed) return gq[i];
-    else if constexpr (PT::belady) return next[i];
+    else if constexpr (PT::nextkey) return next[i];
     else if constexpr (PT::recency) return last[i];
     else return 0ull;
   }
@@ -679,7 +684,7 @@ struct MemTable {
     e.len = uni32(len[sid]);
     e.kvb = uni32(kvb[sid]);
     e.last = uni64(last[sid]);
-    e.next = PT::belady ? uni64(next[sid]) : ~0ull;
+    e.next = PT::nextkey ? uni64(next[sid]) : ~0ull;
     __syncthreads();
     return e;
   }
@@ -703,7 +708,7 @@ struct MemTable {
     w_sid = kNone;
     store_meta(sid, m);
     last[sid] = t;
-    if constexpr (PT::belady) next[sid] = nx;
+    if constexpr (PT::nextkey) next[sid] = nx;
   }
   // Every thread stores the same values, so each thread's later loads see
   // them; reads end with a barrier and each event starts with one, so no wave
@@ -718,7 +723,7 @@ struct MemTable {
     if constexpr (PT::fixed) gq[sid] = e.gq;
     len[sid] = e.len;
     last[sid] = e.last;
-    if constexpr (PT::belady) next[sid] = e.next;
+    if constexpr (PT::nextkey) next[sid] = e.next;
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) {
     note(sid, m, 0ull, false, 0ull, false);
@@ -851,7 +856,7 @@ struct MemTable {
     const uint32_t m = (uint32_t)x;
     const float gv = __uint_as_float((uint32_t)(x >> 32));
     return key_of<POL, SMODE>(K, m, hazard_of<POL, SMODE>(K, m), gv, PT::fixed ? q[i] : 0ull,
-                              PT::recency ? l[i] : 0ull, PT::belady ? n[i] : 0ull);
+                              PT::recency ? l[i] : 0ull, PT::nextkey ? n[i] : 0ull);
   }
 
   // f(i, x, aux, k) for each resident entry i of this thread: x its live
@@ -1174,17 +1179,20 @@ struct TraceView {
   const uint32_t* info;
   const uint32_t* len;
   const uint64_t* next;
+  const uint32_t* tool;  // or null: every gap is tool class 0
   uint64_t n_ev;
   uint32_t n_sess;
 };
 
 struct Ev {
   uint64_t t;
-  uint32_t sid, info, len;
+  uint32_t sid, info, len, tool;
   uint64_t next;
 };
 
-template <bool NEXT>
+// The event record; the next arrival only where the key reads it (Belady),
+// the tool class only where it predicts one (ETA).
+template <bool NEXT, bool TOOL>
 __device__ __forceinline__ Ev load_ev(const TraceView& tr, uint64_t e) {
   Ev v;
   v.t = tr.t[e];
@@ -1192,6 +1200,7 @@ __device__ __forceinline__ Ev load_ev(const TraceView& tr, uint64_t e) {
   v.info = tr.info[e];
   v.len = tr.len[e];
   v.next = NEXT ? tr.next[e] : ~0ull;
+  v.tool = (TOOL && tr.tool) ? tr.tool[e] : 0u;
   return v;
 }
 
@@ -1212,20 +1221,25 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& e_io, uint64_t end) {
   using PT = Pol<POL, SMODE>;
   uint64_t e = e_io;
-  Ev cur = load_ev<PT::belady>(tr, e);
+  Ev cur = load_ev<PT::belady, PT::eta>(tr, e);
   // victim-digest weight of event e, (2e + 1) * 0x9e3779b97f4a7c15, stepped per event
   constexpr uint64_t kGolden = 0x9e3779b97f4a7c15ull;
   uint64_t vw = (2ull * e + 1ull) * kGolden;
   for (; e < end; ++e) {
     // the next event's record is in flight while this one is processed
-    const Ev nxt = load_ev<PT::belady>(tr, e + 1 < end ? e + 1 : e);
+    const Ev nxt = load_ev<PT::belady, PT::eta>(tr, e + 1 < end ? e + 1 : e);
     T.event_begin();
     const uint64_t now = UNI ? uni64(cur.t) : cur.t;
     const uint32_t sid = UNI ? uni32(cur.sid) : cur.sid;
     const uint32_t info = UNI ? uni32(cur.info) : cur.info;
     const uint32_t kind = info >> 24, turn = info & 0xFFFFFFu;
     const uint32_t cur_len = UNI ? uni32(cur.len) : cur.len;
-    const uint64_t cur_next = (UNI && PT::belady) ? uni64(cur.next) : cur.next;
+    uint64_t cur_next = (UNI && PT::belady) ? uni64(cur.next) : cur.next;
+    if constexpr (PT::eta) {
+      // the predicted return: gap onset + the expected wait of the gap's tool class
+      const uint32_t tool = UNI ? uni32(cur.tool) : cur.tool;
+      if (kind == kGapStart) cur_next = sat_add(now, K.eta[tool < kEtaClasses ? tool : 0u]);
+    }
     const uint32_t ev = (uint32_t)e;
 
     // timeout policy: TTL timers that fired since the previous event
@@ -1598,7 +1612,7 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
   const uint64_t sb = a.sess_off[P.trace];
   const uint32_t n_sess = (uint32_t)(a.sess_off[P.trace + 1] - sb);
   const TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb,
-                     ee - eb, n_sess};
+                     a.ev_tool ? a.ev_tool + eb : nullptr, ee - eb, n_sess};
   const size_t tb = (size_t)sim * a.max_sessions;
   const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
 
@@ -1616,7 +1630,7 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
     if constexpr (PT::fixed) T.gq[j] = ld ? a.t_gq[tb + s] : 0ull;
     T.len[j] = ld ? a.t_len[tb + s] : 0u;
     T.last[j] = ld ? a.t_last[tb + s] : 0ull;
-    if constexpr (PT::belady) T.next[j] = ld ? a.t_next[tb + s] : ~0ull;
+    if constexpr (PT::nextkey) T.next[j] = ld ? a.t_next[tb + s] : ~0ull;
     T.hz[j] = hazard_of<POL, SMODE>(K, T.meta[j]);
   }
   T.rescore_all(K);  // a resumed table's keys; a fresh table's are never read before its writes
@@ -1652,7 +1666,7 @@ __device__ __forceinline__ void regs_run(const SimArgs& a, uint32_t sim, uint32_
       if constexpr (PT::fixed) a.t_gq[tb + s] = T.gq[j];
       a.t_len[tb + s] = T.len[j];
       a.t_last[tb + s] = T.last[j];
-      if constexpr (PT::belady) a.t_next[tb + s] = T.next[j];
+      if constexpr (PT::nextkey) a.t_next[tb + s] = T.next[j];
     }
   }
   store_hazard(a, P, sim, K, lane, G);
@@ -1680,7 +1694,8 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
   const unison_sim_params P = a.params[simc];
   const uint32_t lambda = (1u << P.b_h) - 1u;
   const KeyCtx K{s_hf[grp], s_hq[grp], s_hd[grp], s_hn[grp], P.penalty_us, lambda, P.p_z,
-                 a.time44 != 0, P.hazard_online ? P.online_sessions : 0u};
+                 a.time44 != 0, P.hazard_online ? P.online_sessions : 0u,
+                 a.eta + (size_t)P.trace * kEtaClasses};
   load_hazard(a, P, simc, K, lane, G);
   __syncthreads();
   if (!live) return;
@@ -1691,7 +1706,8 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
       break;
     case kLru: regs_run<G, EPL, kLru, 0>(a, sim, lane, P, K); break;
     case kTimeout: regs_run<G, EPL, kTimeout, 0>(a, sim, lane, P, K); break;
-    default: regs_run<G, EPL, kBelady, 0>(a, sim, lane, P, K); break;
+    case kBelady: regs_run<G, EPL, kBelady, 0>(a, sim, lane, P, K); break;
+    default: regs_run<G, EPL, kEta, 0>(a, sim, lane, P, K); break;
   }
 }
 
@@ -1708,7 +1724,7 @@ __device__ __forceinline__ void block_run(const SimArgs& a, uint32_t sim, const 
   const uint64_t sb = a.sess_off[P.trace];
   const uint32_t n_sess = (uint32_t)(a.sess_off[P.trace + 1] - sb);
   const TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb,
-                     ee - eb, n_sess};
+                     a.ev_tool ? a.ev_tool + eb : nullptr, ee - eb, n_sess};
   const size_t tb = (size_t)sim * a.max_sessions;
   const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
 
@@ -1859,7 +1875,7 @@ __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   const unison_sim_params P = a.params[sim];
   const uint32_t lambda = (1u << P.b_h) - 1u;
   const KeyCtx K{s_hf, s_hq, s_hd, s_hn, P.penalty_us, lambda, P.p_z, a.time44 != 0,
-                 P.hazard_online ? P.online_sessions : 0u};
+                 P.hazard_online ? P.online_sessions : 0u, a.eta + (size_t)P.trace * kEtaClasses};
   load_hazard(a, P, sim, K, threadIdx.x, BLOCK);
   __syncthreads();
   switch (sim_policy(a, P)) {
@@ -1869,7 +1885,8 @@ __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
       break;
     case kLru: block_run<BLOCK, kLru, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
     case kTimeout: block_run<BLOCK, kTimeout, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
-    default: block_run<BLOCK, kBelady, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
+    case kBelady: block_run<BLOCK, kBelady, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
+    default: block_run<BLOCK, kEta, 0, IN_LDS, VIEWS>(a, sim, P, K, s_red, s_tab); break;
   }
 }
 
@@ -1893,6 +1910,68 @@ __global__ __launch_bounds__(256) void hazard_counts_kernel(const uint32_t* turn
       d_out[t] = s_end[t];
     }
   }
+}
+
+// The ETA table fitted on one trace: per tool class, the mean (floor) of next
+// arrival - gap onset over the class's gap onsets that have a next arrival.
+// One workgroup; each thread sums its events per class in 128 bits.
+__global__ __launch_bounds__(256) void eta_fit_kernel(uint64_t n, const uint64_t* t,
+                                                      const uint32_t* info, const uint32_t* tool,
+                                                      const uint64_t* next, uint64_t* mean) {
+  __shared__ uint64_t s_lo[4][kEtaClasses], s_hi[4][kEtaClasses], s_cnt[4][kEtaClasses];
+  uint64_t lo[kEtaClasses], hi[kEtaClasses], cnt[kEtaClasses];
+#pragma unroll
+  for (uint32_t c = 0; c < kEtaClasses; ++c) lo[c] = hi[c] = cnt[c] = 0;
+  for (uint64_t e = threadIdx.x; e < n; e += 256) {
+    const uint64_t nx = next[e];
+    const uint64_t te = t[e];
+    const uint32_t c = tool ? tool[e] : 0u;
+    const bool ok = (info[e] >> 24) == kGapStart && nx != ~0ull && nx >= te && c < kEtaClasses;
+    const uint64_t g = ok ? nx - te : 0ull;
+#pragma unroll
+    for (uint32_t k = 0; k < kEtaClasses; ++k) {
+      const bool mine = ok && c == k;
+      const uint64_t add = mine ? g : 0ull;
+      const uint64_t s = lo[k] + add;
+      hi[k] += s < lo[k] ? 1ull : 0ull;
+      lo[k] = s;
+      cnt[k] += mine ? 1ull : 0ull;
+    }
+  }
+  // sum over the wavefront, then over the four wavefronts
+#pragma unroll
+  for (uint32_t k = 0; k < kEtaClasses; ++k) {
+    for (int m = 1; m < 64; m <<= 1) {
+      const uint64_t olo = __shfl_xor(lo[k], m), ohi = __shfl_xor(hi[k], m);
+      const uint64_t s = lo[k] + olo;
+      hi[k] += ohi + (s < lo[k] ? 1ull : 0ull);
+      lo[k] = s;
+      cnt[k] += __shfl_xor(cnt[k], m);
+    }
+    if ((threadIdx.x & 63u) == 0) {
+      s_lo[threadIdx.x >> 6][k] = lo[k];
+      s_hi[threadIdx.x >> 6][k] = hi[k];
+      s_cnt[threadIdx.x >> 6][k] = cnt[k];
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < kEtaClasses) {
+    const uint32_t k = threadIdx.x;
+    unsigned __int128 sum = 0;
+    uint64_t c = 0;
+    for (int w = 0; w < 4; ++w) {
+      sum += ((unsigned __int128)s_hi[w][k] << 64) | s_lo[w][k];
+      c += s_cnt[w][k];
+    }
+    const unsigned __int128 q = c ? sum / c : 0;
+    mean[k] = q > (unsigned __int128)~0ull ? ~0ull : (uint64_t)q;
+  }
+}
+
+hipError_t launch_eta_fit(uint64_t n, const uint64_t* t, const uint32_t* info, const uint32_t* tool,
+                          const uint64_t* next, uint64_t* mean, hipStream_t stream) {
+  hipLaunchKernelGGL(eta_fit_kernel, dim3(1), dim3(256), 0, stream, n, t, info, tool, next, mean);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------ launchers

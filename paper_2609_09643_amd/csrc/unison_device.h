@@ -24,7 +24,8 @@ constexpr uint32_t kNone = 0xFFFFFFFFu;
 constexpr uint32_t kLut = 51;  // t = 0..50, eq. (hazard)
 
 enum : uint32_t { kArrive = 0, kGapStart = 1, kDone = 2 };
-enum : uint32_t { kSpear = 0, kLru = 1, kTimeout = 2, kBelady = 3 };
+enum : uint32_t { kSpear = 0, kLru = 1, kTimeout = 2, kBelady = 3, kEta = 4 };
+constexpr uint32_t kEtaClasses = UNISON_ETA_CLASSES;
 enum : uint32_t { kTierNone = 0, kTierSram = 1, kTierHbm = 2 };
 enum : uint32_t { kUnseen = 0, kServing = 1, kGap = 2, kDoneP = 3 };
 enum : uint32_t { kOpEvict = 1, kOpExpire = 2, kOpBypass = 3, kOpPromote = 4, kOpSwap = 5,
@@ -182,6 +183,8 @@ struct SimArgs {
   const uint32_t* ev_info;
   const uint32_t* ev_len;
   const uint64_t* ev_next;
+  const uint32_t* ev_tool;   // tool class per event, or null (all class 0)
+  const uint64_t* eta;       // [n_traces][kEtaClasses] expected wait per tool class, ns
   const uint32_t* sess_kvb;
   const uint32_t* lut_d;   // [n_luts][51]
   const uint32_t* lut_n;

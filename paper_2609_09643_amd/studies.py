@@ -64,7 +64,7 @@ def dual_table(c, meta):
 
 
 def component_table(c, meta):
-    """Per component (LRU, LRU+TIDE, SPEAR, SPEAR+TIDE): hit rate and prefill
+    """Per component (LRU, LRU+TIDE, SPEAR, SPEAR+TIDE, ETA, ETA+TIDE): hit rate and prefill
     reduction averaged over traces and envelopes, AMAT relative to LRU as a
     geometric mean of per-cell ratios, and the prefetch accuracy of the
     TIDE arms over all their moves."""

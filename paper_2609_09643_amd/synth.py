@@ -18,7 +18,16 @@ Event encoding (the binary trace format both implementations read):
   info     uint32  kind << 24 | turn  (kind 0 ARRIVE, 1 GAP_START, 2 DONE)
   length   uint32  ARRIVE: resident KV length of the new turn in tokens, else 0
   next_ns  uint64  GAP_START: time of the session's next ARRIVE, else 2^64-1
+  tool     uint32  GAP_START: the tool class of the gap that starts (0..4), else 0
 Per session: kvb (uint32) KV bytes per token; turns (uint32) its turn count.
+
+Tool classes.  A tool gap belongs to one of TOOL_CLASSES classes whose
+medians spread around the gap distribution's median; a user wait is class
+USER_CLASS.  The label of each drawn tool gap is sampled from its posterior
+under that mixture (class c has log-median ln m + TOOL_OFFSETS[c] and log-
+spread TOOL_SIGMA_W), with a generator seeded from the trace generator's
+state without drawing from it, so labelling changes none of the trace's
+other values.  The labels feed the tool-type arrival-table baseline (ETA).
 """
 from __future__ import annotations
 
@@ -28,8 +37,16 @@ from typing import List, Optional
 import numpy as np
 
 KIND_ARRIVE, KIND_GAP_START, KIND_DONE = 0, 1, 2
-POLICY_SPEAR, POLICY_LRU, POLICY_TIMEOUT, POLICY_BELADY = 0, 1, 2, 3
-POLICY_NAMES = ("spear_tide", "lru", "timeout", "belady")
+POLICY_SPEAR, POLICY_LRU, POLICY_TIMEOUT, POLICY_BELADY, POLICY_ETA = 0, 1, 2, 3, 4
+POLICY_NAMES = ("spear_tide", "lru", "timeout", "belady", "eta")
+# Tool-class labels of gaps: four tool classes around the tool-wait median and
+# one class for user waits.  Offsets of the class log-medians (spread a, 3a
+# around it with 1.25 a^2 + TOOL_SIGMA_W^2 = 1, the tool gaps' log-variance).
+TOOL_SIGMA_W = 0.6
+TOOL_OFFSETS = (-1.0733, -0.3578, 0.3578, 1.0733)
+TOOL_CLASSES = len(TOOL_OFFSETS)
+USER_CLASS = TOOL_CLASSES
+ETA_CLASSES = 16                  # table entries of the ETA baseline
 U64_MAX = np.uint64(0xFFFFFFFFFFFFFFFF)
 KIB, MIB, GIB = 1024, 1024 ** 2, 1024 ** 3
 NS = 1_000_000_000
@@ -58,6 +75,11 @@ class Trace:
     next_ns: np.ndarray
     kvb: np.ndarray
     turns: np.ndarray
+    tool: Optional[np.ndarray] = None   # per event (GAP_START: tool class), or None: all 0
+
+    def __post_init__(self):
+        if self.tool is None:
+            self.tool = np.zeros(self.t_ns.shape[0], np.uint32)
 
     @property
     def n_events(self) -> int:
@@ -77,7 +99,7 @@ class Trace:
 
     def prefix(self, n: int) -> "Trace":
         return Trace(self.t_ns[:n], self.sid[:n], self.info[:n], self.length[:n],
-                     self.next_ns[:n], self.kvb, self.turns)
+                     self.next_ns[:n], self.kvb, self.turns, self.tool[:n])
 
 
 @dataclass
@@ -108,12 +130,50 @@ def gaps_single(rng, n):
     return _lognormal_s(rng, 2.0, 1.0, n, lo=1e-3)
 
 
+def _gaps_single_parts(rng, n):
+    return gaps_single(rng, n), np.zeros(n, bool)
+
+
+gaps_single.parts = _gaps_single_parts
+gaps_single.tool_median_s = 2.0
+
+
+def _gaps_mixture_parts(rng, n):
+    tool = _lognormal_s(rng, 4.0, 1.0, n, lo=0.5, hi=60.0)
+    user = _lognormal_s(rng, 30.0, 1.0, n, lo=5.0, hi=300.0)
+    is_tool = rng.random(n) < 0.8
+    return np.where(is_tool, tool, user), ~is_tool
+
+
 def gaps_mixture(rng, n):
     """80 % tool waits lognormal(ln 4 s, 1) in [0.5, 60] s, 20 % user waits
     lognormal(ln 30 s, 1) in [5, 300] s."""
-    tool = _lognormal_s(rng, 4.0, 1.0, n, lo=0.5, hi=60.0)
-    user = _lognormal_s(rng, 30.0, 1.0, n, lo=5.0, hi=300.0)
-    return np.where(rng.random(n) < 0.8, tool, user)
+    return _gaps_mixture_parts(rng, n)[0]
+
+
+gaps_mixture.parts = _gaps_mixture_parts
+gaps_mixture.tool_median_s = 4.0
+
+
+def label_tools(lrng, gaps_s, is_user, tool_median_s):
+    """Tool class of each gap: USER_CLASS for user waits; for tool waits a
+    draw from the posterior over the TOOL_CLASSES classes (equal priors,
+    class log-medians ln(tool_median_s) + TOOL_OFFSETS, log-spread
+    TOOL_SIGMA_W) given the gap."""
+    x = np.log(np.maximum(gaps_s, 1e-9)) - np.log(tool_median_s)
+    d = x[:, None] - np.asarray(TOOL_OFFSETS)[None, :]
+    w = np.exp(-0.5 * (d / TOOL_SIGMA_W) ** 2 - np.max(-0.5 * (d / TOOL_SIGMA_W) ** 2, axis=1,
+                                                         keepdims=True))
+    cdf = np.cumsum(w / w.sum(axis=1, keepdims=True), axis=1)
+    u = lrng.random(gaps_s.shape[0])
+    cls = np.minimum((u[:, None] > cdf).sum(axis=1), TOOL_CLASSES - 1)
+    return np.where(is_user, USER_CLASS, cls).astype(np.uint32)
+
+
+def _side_generator(rng):
+    """A generator seeded from rng's current state, without drawing from rng."""
+    st = int(rng.bit_generator.state["state"]["state"])
+    return np.random.Generator(np.random.PCG64([st & (2 ** 64 - 1), st >> 64, 0x7001]))
 
 
 def service_times(rng, n):
@@ -153,7 +213,12 @@ def build_trace(rng, turns, first_arrival_s, gap_fn, kvb, grow_lo=200, grow_hi=2
     k = np.arange(total, dtype=np.int64) - starts[owner]
 
     svc_ns = np.rint(service_times(rng, total) * NS).astype(np.int64)
-    gap_ns = np.rint(gap_fn(rng, total) * NS).astype(np.int64)
+    parts = getattr(gap_fn, "parts", None)
+    if parts is not None:
+        gap_s, is_user = parts(rng, total)
+    else:
+        gap_s, is_user = gap_fn(rng, total), None
+    gap_ns = np.rint(gap_s * NS).astype(np.int64)
     gap_ns[k == 0] = 0
     grow = rng.integers(grow_lo, grow_hi + 1, total).astype(np.int64)
     first_ns = np.rint(np.asarray(first_arrival_s) * NS).astype(np.int64)
@@ -173,6 +238,13 @@ def build_trace(rng, turns, first_arrival_s, gap_fn, kvb, grow_lo=200, grow_hi=2
     next_arrive = np.empty(total, dtype=np.int64)
     next_arrive[:-1] = arrive[1:]
     next_arrive[-1] = -1
+    # tool class of the gap that follows turn k (the gap before turn k + 1)
+    if is_user is not None:
+        cls = label_tools(_side_generator(rng), gap_s, is_user, gap_fn.tool_median_s)
+    else:
+        cls = np.zeros(total, np.uint32)
+    next_cls = np.zeros(total, np.uint32)
+    next_cls[:-1] = cls[1:]
 
     n_ev = 2 * total
     t = np.empty(n_ev, dtype=np.int64)
@@ -188,6 +260,8 @@ def build_trace(rng, turns, first_arrival_s, gap_fn, kvb, grow_lo=200, grow_hi=2
     kind[1::2] = np.where(last, KIND_DONE, KIND_GAP_START)
     ln[0::2] = length
     nxt[1::2] = np.where(last, -1, next_arrive)
+    tool = np.zeros(n_ev, dtype=np.int64)
+    tool[1::2] = np.where(last, 0, next_cls)
     rank = np.where(kind == KIND_ARRIVE, 1, 0)  # at equal times: ends before arrivals
     order = np.lexsort((sid, rank, t))
     nxt_u = nxt[order].astype(np.uint64)
@@ -200,6 +274,7 @@ def build_trace(rng, turns, first_arrival_s, gap_fn, kvb, grow_lo=200, grow_hi=2
         next_ns=nxt_u,
         kvb=np.asarray(kvb, dtype=np.uint32),
         turns=turns.astype(np.uint32),
+        tool=tool[order].astype(np.uint32),
     )
 
 
@@ -225,6 +300,8 @@ def default_params(n):
 
 
 def set_policy(p, policy, tide=None):
+    """TIDE is on by default for SPEAR and Belady, off for the recency, timeout
+    and ETA baselines."""
     p["policy"] = policy
     p["tide"] = (1 if policy in (POLICY_SPEAR, POLICY_BELADY) else 0) if tide is None else tide
 
@@ -534,9 +611,10 @@ def attainment_workload(traces=None, envelope=FIDELITY_ENVELOPES[0], points=None
 # Six SRAM/HBM envelopes (tokens at 128 KiB) along the axes of Table VI.
 ABLATION_ENVELOPES = ((10_000, 30_000), (10_000, 50_000), (10_000, 100_000), (10_000, 200_000),
                       (20_000, 50_000), (40_000, 50_000))
-# scoring x tiering: (policy, tide)
+# scoring x tiering: (policy, tide); the tool-type arrival table (ETA) is the
+# third evictor, with and without TIDE
 COMPONENTS = (("lru", POLICY_LRU, 0), ("lru+tide", POLICY_LRU, 1), ("spear", POLICY_SPEAR, 0),
-              ("spear+tide", POLICY_SPEAR, 1))
+              ("spear+tide", POLICY_SPEAR, 1), ("eta", POLICY_ETA, 0), ("eta+tide", POLICY_ETA, 1))
 ASE_SLOTS = (4, 8, 16, 32, 64, 128, 256)
 STUDY_META_DTYPE = np.dtype([("trace", np.uint32), ("envelope", np.uint32), ("arm", np.uint32)])
 
@@ -568,7 +646,8 @@ def dual_ablation(traces=None, envelope=FIDELITY_ENVELOPES[0]):
 
 def component_ablation(traces=None, envelopes=ABLATION_ENVELOPES):
     """Scoring x tiering (the ablation beside Table IV): LRU, LRU+TIDE, SPEAR,
-    SPEAR+TIDE (arm = index in COMPONENTS) per trace and envelope."""
+    SPEAR+TIDE, ETA, ETA+TIDE (arm = index in COMPONENTS) per trace and
+    envelope."""
     traces = fidelity_traces() if traces is None else traces
     cells = [(ti, env, ei, a, {"policy": pol, "tide": tide})
              for ti in range(len(traces)) for ei, env in enumerate(envelopes)

@@ -18,6 +18,7 @@ UNISON_OK, E_INVALID, E_BAD_TRACE, E_CAPACITY, E_HIP, E_NOT_READY = 0, -1, -2, -
 POLICY_PARAMS = 0xFF
 RUN_CONTINUE, RUN_LOG = 1, 2
 LUT_LEN = 51
+ETA_CLASSES = 16
 U64_MAX = 0xFFFFFFFFFFFFFFFF
 
 
@@ -60,7 +61,8 @@ class TraceBatch(C.Structure):
     _fields_ = [("n_traces", C.c_uint32), ("pad0", C.c_uint32),
                 ("ev_offset", C.POINTER(C.c_uint64)), ("sess_offset", C.POINTER(C.c_uint64)),
                 ("ev_t_ns", C.c_void_p), ("ev_sid", C.c_void_p), ("ev_info", C.c_void_p),
-                ("ev_len", C.c_void_p), ("ev_next_ns", C.c_void_p), ("sess_kvb", C.c_void_p)]
+                ("ev_len", C.c_void_p), ("ev_next_ns", C.c_void_p), ("sess_kvb", C.c_void_p),
+                ("ev_tool", C.c_void_p)]
 
 
 _lib = None
@@ -81,6 +83,8 @@ def lib():
             "unison_load_traces": [vp, C.POINTER(TraceBatch)],
             "unison_hazard_counts": [vp, vp, u32, vp, vp],
             "unison_set_hazard": [vp, u32, vp, vp],
+            "unison_eta_fit": [vp, u64, vp, vp, vp, vp, vp],
+            "unison_set_eta": [vp, u32, vp],
             "unison_set_params": [vp, C.POINTER(SimParams)],
             "unison_run": [vp, u32, u32, u64],
             "unison_read_counters": [vp, vp, u32, u32],
@@ -176,6 +180,7 @@ class Simulator:
         self.d_len = _dev(cat("length"), np.uint32)
         self.d_next = _dev(cat("next_ns"), np.uint64)
         self.d_kvb = _dev(cat("kvb"), np.uint32)
+        self.d_tool = _dev(cat("tool"), np.uint32)
         self.n_sims = workload.n_sims
         self.log_cap = int(log_cap)
         max_sess = max(t.n_sessions for t in traces)
@@ -212,7 +217,17 @@ class Simulator:
                                              self.d_info.data_ptr())
         tb.ev_len, tb.ev_next_ns, tb.sess_kvb = (self.d_len.data_ptr(), self.d_next.data_ptr(),
                                                  self.d_kvb.data_ptr())
+        tb.ev_tool = self.d_tool.data_ptr()
         _check(L.unison_load_traces(self.ctx, C.byref(tb)), self.ctx)
+        # the ETA table of each trace, fitted on the GPU from the trace's own gaps
+        self.d_eta = torch.zeros((len(traces), ETA_CLASSES), dtype=torch.int64, device="cuda")
+        for i, tr in enumerate(traces):
+            b, n = int(ev_off[i]), int(tr.n_events)
+            _check(L.unison_eta_fit(_stream(), n, C.c_void_p(self.d_t.data_ptr() + 8 * b),
+                                    C.c_void_p(self.d_info.data_ptr() + 4 * b),
+                                    C.c_void_p(self.d_tool.data_ptr() + 4 * b),
+                                    C.c_void_p(self.d_next.data_ptr() + 8 * b), _ptr(self.d_eta[i])))
+            _check(L.unison_set_eta(self.ctx, i, _ptr(self.d_eta[i])), self.ctx)
         # hazard tables: counted on the GPU from each population, or given counts
         self.d_lut_d = torch.zeros((len(workload.lut_pops), LUT_LEN), dtype=torch.int32, device="cuda")
         self.d_lut_n = torch.zeros_like(self.d_lut_d)
@@ -246,6 +261,17 @@ class Simulator:
     def run(self, policy=POLICY_PARAMS, flags=0, max_events=None):
         me = U64_MAX if max_events is None else int(max_events)
         _check(lib().unison_run(self.ctx, policy, flags, me), self.ctx)
+
+    def set_eta(self, trace, table):
+        """Installs an ETA table (ns per tool class) for a trace in place of
+        the one fitted on it."""
+        t = _dev(np.asarray(table, np.uint64), np.uint64)
+        self.d_eta[trace].copy_(t)
+        _check(lib().unison_set_eta(self.ctx, trace, _ptr(self.d_eta[trace])), self.ctx)
+
+    def eta_table(self, trace):
+        """The ETA table fitted on the GPU for a trace (ns per tool class)."""
+        return _host(self.d_eta[trace], np.uint64)
 
     def counters(self, check=True):
         out = np.zeros(self.n_sims, COUNTERS_DTYPE)

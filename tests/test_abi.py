@@ -75,4 +75,4 @@ def test_struct_layouts_match_header():
     assert C.sizeof(U.SimParams) == 128
     assert U.COUNTERS_DTYPE.itemsize == 25 * 8
     assert U.RECORD_DTYPE.itemsize == 16
-    assert C.sizeof(U.TraceBatch) == 8 + 8 * 8
+    assert C.sizeof(U.TraceBatch) == 8 + 9 * 8

@@ -1,0 +1,95 @@
+"""GPU parity of the ETA baseline (tool-type arrival table) against the
+oracle: the table fitted on the GPU, the hand-worked trace on every kernel
+variant, and ETA (with and without TIDE) on the sweep, the paper-scale trace
+and a large-table prefix."""
+import sys
+
+import numpy as np
+import pytest
+
+import eta_cases
+import oracle
+from paper_2609_09643_amd import synth
+from parity import compare_counters, oracle_counters, oracle_log, same_log
+
+pytestmark = pytest.mark.gpu
+
+VARIANTS = (None, 0, 1, 2, 3, 4, 5, 7, 8, 9, 10, 11, 12)
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def Sim(*a, **k):
+    from paper_2609_09643_amd.unison import Simulator
+    return Simulator(*a, **k)
+
+
+def subset(w, sims):
+    return synth.Workload(w.name, w.traces, w.lut_pops, w.params[np.asarray(sims)].copy(),
+                          w.flat_luts)
+
+
+def test_eta_tables_fitted_on_the_gpu():
+    traces = [synth.c2_paper_scale().traces[0], synth.tiny_trace(3),
+              synth.c4_large(n_traces=1).traces[0]]
+    w = synth.Workload("eta_fit", traces, [t.turns for t in traces], synth.default_params(1))
+    s = Sim(w)
+    for i, tr in enumerate(traces):
+        got, want = s.eta_table(i), oracle.eta_table(tr)
+        assert np.array_equal(got, want), (i, got, want)
+        assert int(want[:4].min()) > 0 and int(want[5:].max()) == 0   # classes 0..3 tool, 4 user
+
+
+@pytest.mark.parametrize("policy", ["eta", "belady"])
+def test_predicted_and_true_returns_disagree_on_every_variant(policy):
+    tr, rows, want = eta_cases.predicted_and_true_returns_disagree()
+    p = rows(synth.POLICY_ETA if policy == "eta" else synth.POLICY_BELADY)
+    w = synth.Workload("eta_hand", [tr], [None], p, flat_luts=[(0, 0, 1)])
+    want_log, (req, miss, hits) = want[policy]
+    for v in VARIANTS:
+        say("eta hand case, %s, variant %s" % (policy, v))
+        s = Sim(w, log_cap=64, variant=v)
+        s.set_eta(0, eta_cases.ETA_TABLE)
+        s.run(flags=2)
+        c = s.counters()[0]
+        got = [(int(r["ev"]), int(r["op"]), int(r["a"]), int(r["b"])) for r in s.log(0)]
+        assert got == want_log, (policy, v)
+        assert (int(c["requests"]), int(c["miss"]), int(c["hit_hbm"])) == (req, miss, hits)
+        s.close()
+
+
+@pytest.mark.parametrize("tide", [0, 1])
+def test_eta_on_a_sweep_subset(tide):
+    c3 = synth.c3_sweep(policies=(synth.POLICY_ETA,))
+    w = subset(c3, list(range(0, c3.n_sims, 7)))
+    w.params["tide"] = tide
+    say("eta sweep subset: %d sims, tide %d" % (w.n_sims, tide))
+    for v in (None, 9, 12, 3):
+        s = Sim(w, variant=v)
+        s.run()
+        compare_counters(s.counters(), oracle_counters(w), label="eta sweep variant %s" % v)
+
+
+def test_eta_on_the_paper_scale_trace():
+    w = synth.c2_paper_scale()
+    w.params["policy"] = synth.POLICY_ETA
+    w.params["tide"] = [0, 1, 0, 1]
+    say("eta c2: 4 sims x %d events" % w.traces[0].n_events)
+    s = Sim(w, log_cap=1 << 17)
+    s.run(flags=2)
+    compare_counters(s.counters(), oracle_counters(w), label="eta c2")
+    assert same_log(s.log(1), oracle_log(w, 1, log_cap=1 << 17)), "eta+tide c2 log"
+
+
+def test_eta_on_a_large_table_prefix():
+    w = synth.c4_large(n_traces=1)
+    ww = subset(w, [0, 1])
+    ww.params["policy"] = synth.POLICY_ETA
+    ww.params["tide"] = [0, 1]
+    say("eta c4: 2 sims, 8,000 events")
+    s = Sim(ww)
+    s.run(max_events=5000)
+    s.run(flags=1, max_events=3000)
+    compare_counters(s.counters(), oracle_counters(ww, max_events=8000), label="eta c4 prefix")

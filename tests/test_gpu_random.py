@@ -42,7 +42,7 @@ def random_rows(rng, n_traces, per_trace, n_luts):
     for ti in range(n_traces):
         for _ in range(per_trace):
             p = synth.default_params(1)
-            pol = int(rng.integers(0, 4))
+            pol = int(rng.integers(0, 5))
             synth.set_policy(p, pol, tide=int(rng.integers(0, 2)))
             p["trace"] = ti
             p["lut"] = int(rng.integers(0, n_luts))

@@ -33,17 +33,19 @@ def test_dual_table_shifts():
 
 
 def test_component_table():
-    meta = np.zeros(4, synth.STUDY_META_DTYPE)
-    meta[:] = [(0, 0, a) for a in range(4)]
+    n_arms = len(synth.COMPONENTS)
+    meta = np.zeros(n_arms, synth.STUDY_META_DTYPE)
+    meta[:] = [(0, 0, a) for a in range(n_arms)]
     c = counters([dict(requests=10, hit_hbm=2, amat_sum_ns=100.0, tokens_total=10, tokens_computed=9)]
                  + [dict(requests=10, hit_hbm=4, amat_sum_ns=50.0, tokens_total=10, tokens_computed=5,
-                         promote=4, swap=0, prefetch_hits=1)] * 3)
+                         promote=4, swap=0, prefetch_hits=1)] * (n_arms - 1))
     t = studies.component_table(c, meta)
     assert t["lru"]["amat_over_lru"] == 1.0 and t["lru"]["prefetch_accuracy"] is None
     assert t["spear+tide"]["amat_over_lru"] == pytest.approx(0.5)
     assert t["lru+tide"]["prefetch_accuracy"] == 0.25
     assert t["spear"]["prefetch_accuracy"] is None          # no TIDE, no prefetch
     assert t["spear+tide"]["hr"] == pytest.approx(0.4) and t["lru"]["prered"] == pytest.approx(0.1)
+    assert t["eta"]["prefetch_accuracy"] is None and t["eta+tide"]["prefetch_accuracy"] == 0.25
 
 
 def test_ase_is_one_where_every_metric_peaks():

@@ -5,10 +5,10 @@ from paper_2609_09643_amd.synth import (KIND_ARRIVE, KIND_DONE, KIND_GAP_START, 
                                          Trace, default_params)
 
 
-def trace_from_events(events, n_sessions, kvb=1):
+def trace_from_events(events, n_sessions, kvb=1, tools=None):
     """events: list of (t_ns, sid, kind, turn, length) in trace order.  The
     next_ns column of each GAP_START is filled from the session's next
-    ARRIVE."""
+    ARRIVE.  tools: optional tool class per event (read at gap onsets)."""
     ev = list(events)
     n = len(ev)
     t = np.array([e[0] for e in ev], dtype=np.uint64)
@@ -28,7 +28,8 @@ def trace_from_events(events, n_sessions, kvb=1):
         if kind[i] == KIND_ARRIVE and sid[i] < n_sessions:
             turns[sid[i]] = max(turns[sid[i]], turn[i] + 1)
     kv = np.full(n_sessions, kvb, dtype=np.uint32) if np.isscalar(kvb) else np.asarray(kvb, np.uint32)
-    return Trace(t, sid, (kind << 24) | turn, length, nxt, kv, turns)
+    tool = None if tools is None else np.asarray(tools, dtype=np.uint32)
+    return Trace(t, sid, (kind << 24) | turn, length, nxt, kv, turns, tool)
 
 
 def trace_from_requests(reqs, n_sessions, length=1, kvb=1, dt=10):
