@@ -321,7 +321,7 @@ def section_fmt(torch):
     envelope) cells of whole-trace SPEAR+TIDE replays plus the fp32
     reference, and ranking fidelity on 7,265 snapshots of 64 sessions."""
     from paper_2609_09643_amd import fidelity, synth
-    fmts = synth.format_grid()
+    fmts = synth.format_grid_dividers()
     w, meta = synth.format_sweep(formats=fmts)
     t0 = time.perf_counter()
     c, d_hr, d_am, cells = fidelity.run_trajectories(w, meta, fmts)
@@ -333,20 +333,30 @@ def section_fmt(torch):
     torch.cuda.synchronize()
     t_rank = time.perf_counter() - t0
     rows = []
-    for f, (bh, bg, tau) in enumerate(fmts):
+    for f, (bh, bg, tau, wb) in enumerate(fmts):
         worst = float(np.nanmax(np.abs(d_hr[f])))
-        rows.append({"format": [bh, bg, tau], "worst_hr_drift_pp": round(worst, 4),
+        rows.append({"format": [bh, bg, tau], "divider": "exact" if wb == 0 else "recip%d" % wb,
+                     "worst_hr_drift_pp": round(worst, 4),
                      "mean_hr_drift_pp": round(float(np.nanmean(np.abs(d_hr[f]))), 4),
                      "mean_amat_drift_pct": round(float(np.nanmean(d_am[f])), 4),
                      "mean_tau_b": round(rank[f][0], 6), "top1": round(rank[f][2], 4),
                      "passes": bool(worst <= fidelity.HR_GATE_PP and rank[f][2] >= fidelity.TOP1_GATE)})
-    locked = rows[fmts.index(synth.LOCKED_FORMAT)]
-    return {"workload": "format sweep: 27 formats + fp32 x 18 cells (6 traces, 1,415 sessions, "
-                        "33,596 turns; 3 envelopes), %d simulations; ranking on %d x %d snapshots"
-                        % (w.n_sims, rs.n_snap, rs.n_per),
+    locked = rows[fmts.index(synth.LOCKED_FORMAT + (0,))]
+    by_div = {}
+    for r in rows:
+        by_div.setdefault(r["divider"], []).append(r)
+    return {"workload": "format sweep: 27 (b_h, b_g, tau) points x %d divider types (exact, "
+                        "reciprocal tables of %s fraction bits) + fp32 x 18 cells (6 traces, 1,415 "
+                        "sessions, 33,596 turns; 3 envelopes), %d simulations; ranking on %d x %d "
+                        "snapshots" % (len(synth.FORMAT_DIVIDERS),
+                                       "/".join(str(x) for x in synth.FORMAT_DIVIDERS[1:]),
+                                       w.n_sims, rs.n_snap, rs.n_per),
             "trajectory_s": t_traj, "events_per_s": float(c["events"].sum()) / t_traj,
             "ranking_s": t_rank, "locked": locked,
-            "passing": [r["format"] for r in rows if r["passes"]], "formats": rows}
+            "by_divider": {k: {"passing": sum(r["passes"] for r in v), "points": len(v),
+                               "locked_point": next(r for r in v if r["format"] == list(synth.LOCKED_FORMAT))}
+                           for k, v in by_div.items()},
+            "passing": [r["format"] + [r["divider"]] for r in rows if r["passes"]], "formats": rows}
 
 
 def section_online(torch):

@@ -148,7 +148,10 @@ typedef struct {
   uint32_t dual_sync;      /* UNISON_DUAL_*: one live register file (0), or the dual design of
                               eq. (stale) whose eviction and TIDE engines decide from private
                               copies refreshed at the given points */
-  uint32_t pad0;
+  uint32_t recip_bits;     /* score_mode 1: 0 divides eq. (t1) by sigma_q exactly; W in 1..32
+                              multiplies by floor(2^W / sigma_q + 1/2) instead and shifts right
+                              by W (a reciprocal table of depth Lambda: the divider-type axis of
+                              the format sweep) */
 } unison_sim_params;
 
 /* Per-simulation results. */
@@ -333,11 +336,14 @@ int unison_score_fp32(void* hip_stream, uint32_t n, const uint8_t* turn, const f
                       float penalty_us, float* out);
 
 /* eq. (hq), eq. (survq), eq. (t1), eq. (t2), eq. (scoreq) with b_s = 64:
- * out[i] = 2^64-1 if done[i], else sat64(floor(gq Lambda / sigma_q) +
- * floor((Lambda - sigma_q) P_Z / Lambda)), Lambda = 2^b_h - 1. */
+ * out[i] = 2^64-1 if done[i], else sat64(T1 + floor((Lambda - sigma_q) P_Z /
+ * Lambda)), Lambda = 2^b_h - 1, with T1 = floor(gq Lambda / sigma_q) for
+ * recip_bits = 0 (exact divider), else T1 = floor(gq Lambda r / 2^W) with
+ * r = floor(2^W / sigma_q + 1/2) and W = recip_bits <= 32 (reciprocal
+ * table). */
 int unison_score_fixed(void* hip_stream, uint32_t n, const uint8_t* turn, const uint64_t* gq,
                        const uint8_t* done, const uint32_t* lut_d, const uint32_t* lut_n,
-                       uint32_t b_h, uint64_t p_z, uint64_t* out);
+                       uint32_t b_h, uint64_t p_z, uint32_t recip_bits, uint64_t* out);
 
 /* Kendall tau-b pair counts per snapshot (Sec. VI-F): counts[s][5] =
  * {concordant, discordant, tied in x only, tied in y only, tied in both}

@@ -50,7 +50,7 @@ class Params(C.Structure):
         ("t_p_ns_per_tok", C.c_double), ("penalty_us", C.c_float), ("b_h", C.c_uint32),
         ("b_g", C.c_uint32), ("hazard_online", C.c_uint32), ("online_sessions", C.c_uint32),
         ("pad0", C.c_uint32), ("tau_ns", C.c_uint64), ("p_z", C.c_uint64),
-        ("dual_sync", C.c_uint32), ("pad1", C.c_uint32),
+        ("dual_sync", C.c_uint32), ("recip_bits", C.c_uint32),
     ]
 
 
@@ -123,7 +123,7 @@ def load_library(path):
     L.orc_lut_q.argtypes = [u32p, u32p, C.c_uint32, u64p]
     L.orc_score_f32.argtypes = [C.c_uint32, u8p, f32p, u8p, f32p, C.c_float, f32p]
     L.orc_score_fixed.argtypes = [C.c_uint32, u8p, u64p, u8p, u64p, C.c_uint32,
-                                  C.c_uint64, u64p]
+                                  C.c_uint64, C.c_uint32, u64p]
     L.orc_ema_replay.argtypes = [C.c_uint32, C.c_uint32, u64p, u8p, C.c_uint32,
                                  C.c_uint64, f32p, u64p]
     L.orc_kendall.argtypes = [C.c_uint32, C.c_uint32, f32p, u64p, u32p, u64p, u8p]
@@ -188,12 +188,14 @@ def score_f32(turn, g, done, d, n, penalty):
     return out
 
 
-def score_fixed(turn, gq, done, d, n, b_h, p_z):
+def score_fixed(turn, gq, done, d, n, b_h, p_z, recip_bits=0):
+    """Fixed-point scores; recip_bits 0: exact divider in eq. (t1), else a
+    reciprocal table with that many fraction bits."""
     turn, gq, done = _c(turn, np.uint8), _c(gq, np.uint64), _c(done, np.uint8)
     hq = lut_q(d, n, b_h)
     out = np.zeros(turn.shape[0], np.uint64)
     lib().orc_score_fixed(turn.shape[0], _p(turn, C.c_uint8), _p(gq, C.c_uint64),
-                          _p(done, C.c_uint8), _p(hq, C.c_uint64), b_h, p_z,
+                          _p(done, C.c_uint8), _p(hq, C.c_uint64), b_h, p_z, recip_bits,
                           _p(out, C.c_uint64))
     return out
 
@@ -257,7 +259,7 @@ def params_struct(row):
     for name, _ in Params._fields_:
         if name.startswith("pad"):
             continue
-        v = row[name]
+        v = row[name] if name in row.dtype.names else 0
         setattr(p, name, float(v) if name.startswith("t_") or name == "penalty_us" else int(v))
     return p
 

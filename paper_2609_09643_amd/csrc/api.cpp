@@ -38,7 +38,8 @@ hipError_t launch_score_fp32(uint32_t n, const uint8_t* turn, const float* g, co
                              hipStream_t s);
 hipError_t launch_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
                               const uint8_t* done, const uint32_t* d, const uint32_t* nn,
-                              uint32_t b_h, uint64_t p_z, uint64_t* out, hipStream_t s);
+                              uint32_t b_h, uint64_t p_z, uint32_t recip_bits, uint64_t* out,
+                              hipStream_t s);
 hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const float* x,
                           const uint64_t* y, const uint32_t* idx, uint64_t* counts, uint8_t* top1,
                           hipStream_t s);
@@ -456,6 +457,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
     if (p.policy > UNISON_POLICY_ETA || p.tide > 1 || p.score_mode > 1 || p.hazard_online > 1 ||
         p.lut >= ctx->dims.n_luts || p.trace >= ctx->dims.n_traces || p.b_h < 1 || p.b_h > 16 ||
         p.b_g < 1 || p.b_g > 64 || p.tau_ns < 1 || p.n_slots < 1 || p.dma_B_per_us < 1 ||
+        p.recip_bits > 32 ||
         !(p.penalty_us >= 0.0f) || std::isinf(p.penalty_us) || !std::isfinite(p.t_s_ns_per_B) ||
         !std::isfinite(p.t_h_ns_per_B) || !std::isfinite(p.t_p_ns_per_tok))
       return ctx->fail(UNISON_E_INVALID, "parameter row %u out of range", i);
@@ -724,10 +726,10 @@ int unison_score_fp32(void* hip_stream, uint32_t n, const uint8_t* turn, const f
 
 int unison_score_fixed(void* hip_stream, uint32_t n, const uint8_t* turn, const uint64_t* gq,
                        const uint8_t* done, const uint32_t* lut_d, const uint32_t* lut_n,
-                       uint32_t b_h, uint64_t p_z, uint64_t* out) {
+                       uint32_t b_h, uint64_t p_z, uint32_t recip_bits, uint64_t* out) {
   if (n && (!turn || !gq || !done || !out)) return UNISON_E_INVALID;
-  if (!lut_d || !lut_n || b_h < 1 || b_h > 16) return UNISON_E_INVALID;
-  return launch_score_fixed(n, turn, gq, done, lut_d, lut_n, b_h, p_z, out,
+  if (!lut_d || !lut_n || b_h < 1 || b_h > 16 || recip_bits > 32) return UNISON_E_INVALID;
+  return launch_score_fixed(n, turn, gq, done, lut_d, lut_n, b_h, p_z, recip_bits, out,
                             reinterpret_cast<hipStream_t>(hip_stream)) == hipSuccess
              ? UNISON_OK
              : UNISON_E_HIP;

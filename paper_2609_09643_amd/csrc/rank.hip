@@ -52,7 +52,8 @@ __global__ __launch_bounds__(256) void score_fixed_kernel(uint32_t n, const uint
                                                           const uint64_t* gq, const uint8_t* done,
                                                           const uint32_t* lut_d,
                                                           const uint32_t* lut_n, uint32_t b_h,
-                                                          uint64_t p_z, uint64_t* out) {
+                                                          uint64_t p_z, uint32_t recip_bits,
+                                                          uint64_t* out) {
   __shared__ uint32_t hq[52];
   const uint32_t lambda = (1u << b_h) - 1u;
   if (threadIdx.x < kLut) hq[threadIdx.x] = hazard_q(lut_d[threadIdx.x], lut_n[threadIdx.x], lambda);
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(256) void score_fixed_kernel(uint32_t n, const uint
   const uint32_t i = blockIdx.x * 256u + threadIdx.x;
   if (i >= n) return;
   const uint32_t t = turn[i] < 50u ? turn[i] : 50u;
-  const uint64_t s = spear_fixed(hq[t], gq[i], lambda, p_z);
+  const uint64_t s = spear_fixed(hq[t], gq[i], lambda, p_z, recip_bits);
   out[i] = done[i] ? ~0ull : s;
 }
 
@@ -596,10 +597,11 @@ hipError_t launch_score_fp32(uint32_t n, const uint8_t* turn, const float* g, co
 
 hipError_t launch_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
                               const uint8_t* done, const uint32_t* d, const uint32_t* nn,
-                              uint32_t b_h, uint64_t p_z, uint64_t* out, hipStream_t s) {
+                              uint32_t b_h, uint64_t p_z, uint32_t recip_bits, uint64_t* out,
+                              hipStream_t s) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(score_fixed_kernel, dim3((n + 255) / 256), dim3(256), 0, s, n, turn, gq, done,
-                     d, nn, b_h, p_z, out);
+                     d, nn, b_h, p_z, recip_bits, out);
   return hipGetLastError();
 }
 

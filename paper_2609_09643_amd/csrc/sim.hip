@@ -163,6 +163,7 @@ struct KeyCtx {
   bool pack44;          // times fit 44 bits and ids 20 bits: recency / Belady keys pack
   uint32_t online_cap;  // completions an online table still may count; 0: fixed table
   const uint64_t* eta;  // the trace's ETA table: expected wait per tool class, ns (global)
+  uint32_t recip_bits;  // eq. (t1) by a reciprocal of this many fraction bits; 0: exact
 };
 
 // Adds a completed session of Tn turns to the counts (n(t) += 1 for t < Tn,
@@ -209,7 +210,7 @@ __device__ __forceinline__ uint64_t key_of(const KeyCtx& K, uint32_t meta, uint3
   if constexpr (PT::spear) {
     const bool done = meta_phase(meta) == kDoneP;
     if constexpr (PT::fixed) {
-      const uint64_t s = spear_fixed(hz, gq, K.lambda, K.p_z);
+      const uint64_t s = spear_fixed(hz, gq, K.lambda, K.p_z, K.recip_bits);
       return done ? ~0ull : s;
     } else {
       const float s = spear_f32(__uint_as_float(hz), g, K.P);
@@ -1695,7 +1696,7 @@ __global__ __launch_bounds__(256) void sim_regs_kernel(SimArgs a) {
   const uint32_t lambda = (1u << P.b_h) - 1u;
   const KeyCtx K{s_hf[grp], s_hq[grp], s_hd[grp], s_hn[grp], P.penalty_us, lambda, P.p_z,
                  a.time44 != 0, P.hazard_online ? P.online_sessions : 0u,
-                 a.eta + (size_t)P.trace * kEtaClasses};
+                 a.eta + (size_t)P.trace * kEtaClasses, P.recip_bits};
   load_hazard(a, P, simc, K, lane, G);
   __syncthreads();
   if (!live) return;
@@ -1875,7 +1876,8 @@ __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   const unison_sim_params P = a.params[sim];
   const uint32_t lambda = (1u << P.b_h) - 1u;
   const KeyCtx K{s_hf, s_hq, s_hd, s_hn, P.penalty_us, lambda, P.p_z, a.time44 != 0,
-                 P.hazard_online ? P.online_sessions : 0u, a.eta + (size_t)P.trace * kEtaClasses};
+                 P.hazard_online ? P.online_sessions : 0u, a.eta + (size_t)P.trace * kEtaClasses,
+                 P.recip_bits};
   load_hazard(a, P, sim, K, threadIdx.x, BLOCK);
   __syncthreads();
   switch (sim_policy(a, P)) {

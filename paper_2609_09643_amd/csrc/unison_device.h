@@ -137,13 +137,20 @@ __device__ __forceinline__ float spear_f32(float h, float g, float P) {
 }
 
 // eq. (survq), eq. (t1), eq. (t2), eq. (scoreq) for a live session, b_s = 64.
+// recip_bits = W > 0: eq. (t1) multiplies by the reciprocal r = floor(2^W /
+// sigma_q + 1/2) -- the entry a table of depth Lambda would hold, computed
+// here -- and shifts right by W.
 __device__ __forceinline__ uint64_t spear_fixed(uint32_t hq, uint64_t gq, uint32_t lambda,
-                                                uint64_t p_z) {
+                                                uint64_t p_z, uint32_t recip_bits) {
   uint32_t eps_q = (lambda + 50u) / 100u;  // floor(Lambda/100 + 1/2)
   uint32_t sigma = lambda - hq;
   if (sigma < eps_q) sigma = eps_q;
   uint64_t t1, t2;
-  if (gq < (1ull << 47)) {
+  if (recip_bits) {
+    const uint64_t r = ((2ull << recip_bits) + sigma) / (2ull * sigma);
+    const unsigned __int128 q = ((unsigned __int128)gq * lambda * r) >> recip_bits;
+    t1 = q > (unsigned __int128)~0ull ? ~0ull : (uint64_t)q;
+  } else if (gq < (1ull << 47)) {
     t1 = (gq * lambda) / sigma;
   } else {
     unsigned __int128 q = ((unsigned __int128)gq * lambda) / sigma;

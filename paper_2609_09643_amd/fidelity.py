@@ -93,9 +93,11 @@ def ranking_fidelity(rs, formats, penalty_us=5e8):
     g, _ = U.ema_replay(gaps, nh)
     x = U.score_fp32(turn, g, done, d, n, penalty_us)
     out = []
-    for bh, bg, tau in formats:
+    for fmt in formats:
+        bh, bg, tau = fmt[:3]
+        w = fmt[3] if len(fmt) > 3 else 0
         _, gq = U.ema_replay(gaps, nh, bg, tau)
-        y = U.score_fixed(turn, gq, done, d, n, bh, int(round(penalty_us * 1000 / tau)))
+        y = U.score_fixed(turn, gq, done, d, n, bh, int(round(penalty_us * 1000 / tau)), w)
         counts, top1 = U.kendall(x, y, idx)
         cnt = U._host(counts, np.uint64)
         t1 = top1.cpu().numpy()
@@ -114,10 +116,12 @@ def sweep(traces=None, rs=None, formats=None, penalty_us=5e8):
     _, d_hr, d_am, cells = run_trajectories(w, meta, formats)
     rank = ranking_fidelity(synth.fidelity_snapshots() if rs is None else rs, formats, penalty_us)
     rows = []
-    for f, (bh, bg, tau) in enumerate(formats):
+    for f, fmt in enumerate(formats):
+        bh, bg, tau = fmt[:3]
         worst = float(np.nanmax(np.abs(d_hr[f])))
         mtau, ptau, top1 = rank[f]
         rows.append({"b_h": bh, "b_g": bg, "tau_ns": tau,
+                     "divider": "exact" if len(fmt) < 4 or fmt[3] == 0 else "recip%d" % fmt[3],
                      "worst_hr_drift_pp": worst, "mean_hr_drift_pp": float(np.nanmean(np.abs(d_hr[f]))),
                      "mean_amat_drift_pct": float(np.nanmean(d_am[f])),
                      "mean_tau_b": mtau, "pooled_tau_b": ptau, "top1": top1,

@@ -61,7 +61,7 @@ SIM_PARAMS_DTYPE = np.dtype([
     ("t_s_ns_per_B", np.float64), ("t_h_ns_per_B", np.float64),
     ("t_p_ns_per_tok", np.float64), ("penalty_us", np.float32),
     ("b_h", np.uint32), ("b_g", np.uint32), ("tau_ns", np.uint64), ("p_z", np.uint64),
-    ("dual_sync", np.uint32),
+    ("dual_sync", np.uint32), ("recip_bits", np.uint32),
 ])
 DUAL_NONE, DUAL_EVERY, DUAL_EIGHT, DUAL_GAP = 0, 1, 2, 3
 
@@ -474,6 +474,10 @@ FORMAT_BH = (8, 10, 12)
 FORMAT_BG = (24, 32, 64)
 FORMAT_TAU_NS = (1, 1000, 1_000_000)
 LOCKED_FORMAT = (12, 32, 1000)
+# The divider type of eq. (t1): 0 is the exact divider; W > 0 a reciprocal
+# table of depth Lambda whose entries hold W fraction bits (the entry width is
+# not given: it is swept).
+FORMAT_DIVIDERS = (0, 12, 16, 20, 24)
 
 # Six traces of 128..496 sessions, 1,415 sessions and 33,596 turns in all
 # (Sec. V-A); three capacity envelopes of Table VI in tokens at 128 KiB/token:
@@ -486,6 +490,12 @@ FIDELITY_TURNS = 33_596
 def format_grid():
     """The 27 (b_h, b_g, tau_ns) points of the format sweep."""
     return [(bh, bg, tau) for bh in FORMAT_BH for bg in FORMAT_BG for tau in FORMAT_TAU_NS]
+
+
+def format_grid_dividers(dividers=FORMAT_DIVIDERS):
+    """The sweep with its divider-type axis: (b_h, b_g, tau_ns, W) for every
+    grid point and divider (W = 0 exact, else reciprocal-table bits)."""
+    return [(bh, bg, tau, w) for (bh, bg, tau) in format_grid() for w in dividers]
 
 
 def fix_total(rng, t, total, lo=1):
@@ -528,7 +538,9 @@ def format_sweep(traces=None, envelopes=FIDELITY_ENVELOPES, formats=None, penalt
     """SPEAR+TIDE on every (trace, envelope) cell, once with the fp32 score
     and once per fixed-point format.  Returns the workload and, per
     simulation, its (trace, envelope, format index; -1 for fp32).  P_Z is the
-    penalty in units of tau: P_Z = P / tau (eq. (lock))."""
+    penalty in units of tau: P_Z = P / tau (eq. (lock)).  A format is (b_h,
+    b_g, tau_ns) with the exact divider, or (b_h, b_g, tau_ns, W) with W the
+    reciprocal table's fraction bits (0: exact)."""
     traces = fidelity_traces() if traces is None else traces
     formats = format_grid() if formats is None else list(formats)
     rows, meta = [], []
@@ -547,9 +559,10 @@ def format_sweep(traces=None, envelopes=FIDELITY_ENVELOPES, formats=None, penalt
         p[r]["cap_hbm_B"] = h_tok * 128 * KIB
         p[r]["penalty_us"] = np.float32(penalty_us)
         if fi >= 0:
-            bh, bg, tau = formats[fi]
+            bh, bg, tau = formats[fi][:3]
             p[r]["score_mode"] = 1
             p[r]["b_h"], p[r]["b_g"], p[r]["tau_ns"] = bh, bg, tau
+            p[r]["recip_bits"] = formats[fi][3] if len(formats[fi]) > 3 else 0
             p[r]["p_z"] = int(round(penalty_us * 1000 / tau))
         m[r] = (ti, ei, fi)
     w = Workload("format_sweep", list(traces), [tr.turns for tr in traces], p)

@@ -42,7 +42,7 @@ class SimParams(C.Structure):
         ("t_s_ns_per_B", C.c_double), ("t_h_ns_per_B", C.c_double),
         ("t_p_ns_per_tok", C.c_double), ("penalty_us", C.c_float), ("b_h", C.c_uint32),
         ("b_g", C.c_uint32), ("online_sessions", C.c_uint32), ("tau_ns", C.c_uint64),
-        ("p_z", C.c_uint64), ("dual_sync", C.c_uint32), ("pad0", C.c_uint32),
+        ("p_z", C.c_uint64), ("dual_sync", C.c_uint32), ("recip_bits", C.c_uint32),
     ]
 
 
@@ -93,7 +93,7 @@ def lib():
             "unison_read_hazard": [vp, u32, vp, vp],
             "unison_ema_replay": [vp, u32, u32, vp, vp, u32, u64, vp, vp],
             "unison_score_fp32": [vp, u32, vp, vp, vp, vp, vp, C.c_float, vp],
-            "unison_score_fixed": [vp, u32, vp, vp, vp, vp, vp, u32, u64, vp],
+            "unison_score_fixed": [vp, u32, vp, vp, vp, vp, vp, u32, u64, u32, vp],
             "unison_kendall": [vp, u32, u32, u64, vp, vp, vp, vp, vp],
             "unison_debug_force_variant": [vp, i32],
             "unison_debug_cache_slots": [vp, i32],
@@ -349,11 +349,12 @@ def score_fp32(turn_dev, g_dev, done_dev, d_dev, n_dev, penalty_us):
     return out
 
 
-def score_fixed(turn_dev, gq_dev, done_dev, d_dev, n_dev, b_h=12, p_z=500_000_000):
+def score_fixed(turn_dev, gq_dev, done_dev, d_dev, n_dev, b_h=12, p_z=500_000_000, recip_bits=0):
     torch = _torch()
     out = torch.empty(turn_dev.numel(), dtype=torch.int64, device="cuda")
     _check(lib().unison_score_fixed(_stream(), int(turn_dev.numel()), _ptr(turn_dev), _ptr(gq_dev),
-                                    _ptr(done_dev), _ptr(d_dev), _ptr(n_dev), b_h, p_z, _ptr(out)))
+                                    _ptr(done_dev), _ptr(d_dev), _ptr(n_dev), b_h, p_z, recip_bits,
+                                    _ptr(out)))
     return out
 
 

@@ -62,7 +62,9 @@ def test_host_side_validation(lib):
     assert lib.unison_kendall(None, 1, 5000, 5000, C.c_void_p(8), C.c_void_p(8), None,
                               C.c_void_p(8), C.c_void_p(8)) == U.E_INVALID
     assert lib.unison_score_fixed(None, 1, C.c_void_p(8), C.c_void_p(8), C.c_void_p(8),
-                                  C.c_void_p(8), C.c_void_p(8), 17, 0, C.c_void_p(8)) == U.E_INVALID
+                                  C.c_void_p(8), C.c_void_p(8), 17, 0, 0, C.c_void_p(8)) == U.E_INVALID
+    assert lib.unison_score_fixed(None, 1, C.c_void_p(8), C.c_void_p(8), C.c_void_p(8),
+                                  C.c_void_p(8), C.c_void_p(8), 12, 0, 33, C.c_void_p(8)) == U.E_INVALID
     assert lib.unison_strerror(U.E_BAD_TRACE) == b"trace breaks the event format"
     assert lib.unison_debug_cache_slots(ctx, -2) == U.E_INVALID
     assert lib.unison_debug_cache_slots(ctx, 0) == 0 and lib.unison_debug_cache_slots(ctx, -1) == 0

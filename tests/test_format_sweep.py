@@ -19,6 +19,32 @@ def test_grid_has_27_distinct_points_and_the_locked_one():
     assert {p[2] for p in g} == {1, 1000, 1_000_000}
 
 
+def test_divider_axis_crosses_every_point_with_every_divider():
+    g = synth.format_grid_dividers()
+    assert len(g) == 27 * len(synth.FORMAT_DIVIDERS) and len(set(g)) == len(g)
+    assert synth.LOCKED_FORMAT + (0,) in g
+    w, meta = synth.format_sweep(traces=synth.fidelity_traces()[:1], formats=g)
+    fixed = meta["fmt"] >= 0
+    assert np.all(w.params["recip_bits"][~fixed] == 0)
+    assert [int(r) for r in w.params["recip_bits"][fixed][:len(g)]] == [f[3] for f in g]
+
+
+def test_reciprocal_divider_trajectories_are_consistent():
+    """The oracle replays a whole trace with the reciprocal-table divider at
+    each width: the counts that the trace fixes hold, and at W = 32 the
+    decisions equal the exact divider's on this trace (every reciprocal then
+    sits within 2^-33 of 1 / sigma_q)."""
+    tr = synth.fidelity_traces()[0]
+    fmts = [(12, 32, 1000, w) for w in (0, 12, 24, 32)]
+    w, meta = synth.format_sweep(traces=[tr], envelopes=synth.FIDELITY_ENVELOPES[:1], formats=fmts)
+    res, _ = oracle.run_workload(w)
+    req = int(tr.turns.sum())
+    for r in res:
+        assert r["requests"] == req == r["hit_sram"] + r["hit_hbm"] + r["miss"]
+    exact, w32 = res[1], res[4]
+    assert exact["digest"] == w32["digest"] and exact["victim_digest"] == w32["victim_digest"]
+
+
 def test_fidelity_traces_match_the_corpus_totals():
     trs = synth.fidelity_traces()
     assert [t.n_sessions for t in trs] == list(synth.FIDELITY_SESSIONS)

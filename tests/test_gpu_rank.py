@@ -70,6 +70,18 @@ def test_score_fixed_exact(U, rs, b_h, p_z):
     assert np.array_equal(U._host(out, np.uint64), want)
 
 
+@pytest.mark.parametrize("b_h,recip", [(12, 12), (12, 16), (12, 24), (16, 32), (8, 20), (10, 1)])
+def test_score_fixed_reciprocal_divider_exact(U, rs, b_h, recip):
+    d, n = oracle.hazard_counts(rs.lut_pop)
+    _, gq = oracle.ema_replay(rs.gaps_ns, rs.n_hist)
+    gq = gq.copy()
+    gq[:64] = np.uint64(2 ** 64 - 1) - np.arange(64, dtype=np.uint64)   # saturating products
+    out = U.score_fixed(dev(U, rs.turn), dev(U, gq, np.uint64), dev(U, rs.done),
+                        dev(U, d, np.uint32), dev(U, n, np.uint32), b_h, 500_000_000, recip)
+    want = oracle.score_fixed(rs.turn, gq, rs.done, d, n, b_h, 500_000_000, recip_bits=recip)
+    assert np.array_equal(U._host(out, np.uint64), want)
+
+
 @pytest.mark.parametrize("n_per", [2, 3, 64, 65, 255, 257, 1000])
 def test_kendall_small_with_ties(U, n_per):
     rng = np.random.default_rng(n_per)

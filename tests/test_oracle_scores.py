@@ -194,3 +194,60 @@ def test_f32_lut_is_ratio_of_counts():
     hf = oracle.lut_f32(d, n)
     assert np.all(np.abs(hf - d / n) <= 2.0 ** -24 * (d / n))
     assert oracle.lut_f32(*flat(0, 0))[0] == 0.0
+
+
+# ---------------------------------------------- reciprocal-table divider
+# The sweep's other divider type: eq. (t1) multiplies by r[sigma_q] =
+# floor(2^W / sigma_q + 1/2), read from a table of depth Lambda, and shifts
+# right by W.  Worked by hand for the (g_q = 2e6, h = 1/24) example above,
+# where sigma_q = 3924 and the exact T1 is 2,087,155:
+#   W = 16: 65,536 / 3924 = 16.70  -> r = 17;
+#           T1 = floor(2e6 * 4095 * 17 / 65,536) = floor(2,124,481.2) = 2,124,481
+#   W = 24: 16,777,216 / 3924 = 4275.54 -> r = 4276;
+#           T1 = floor(8.19e9 * 4276 / 16,777,216) = floor(2,087,380.9) = 2,087,380
+
+def test_reciprocal_divider_worked_example():
+    d, n = flat(1, 24)
+    for w, t1 in ((16, 2_124_481), (24, 2_087_380)):
+        out = oracle.score_fixed([5], [2_000_000], [0], d, n, B_H, P_Z, recip_bits=w)
+        assert int(out[0]) == t1 + 20_879_120, w
+
+
+def test_reciprocal_divider_is_exact_on_powers_of_two():
+    """sigma_q = 2048 (h_q = 2047, from d/n = 2047/4095) divides 2^W: the
+    stored reciprocal is exact and so is T1."""
+    d, n = flat(2047, 4095)
+    assert oracle.lut_q(d, n, B_H)[0] == 2047
+    g = np.array([0, 1, 999, 2_000_000, 2 ** 40 + 3], np.uint64)
+    exact = oracle.score_fixed(np.zeros(5), g, np.zeros(5), d, n, B_H, P_Z)
+    for w in (12, 16, 24):
+        lut = oracle.score_fixed(np.zeros(5), g, np.zeros(5), d, n, B_H, P_Z, recip_bits=w)
+        assert lut.tolist() == exact.tolist(), w
+
+
+@pytest.mark.parametrize("w", [8, 12, 16, 20, 24, 32])
+def test_reciprocal_divider_error_bound(w):
+    """|r - 2^W / sigma| <= 1/2, so |T1_lut - T1_exact| <= g_q Lambda / 2^(W+1) + 1
+    (the two floors add at most 1): checked on random gaps and every sigma_q
+    the hazard counts reach, at b_h = 8, 12 and 16; T2 is the same in both."""
+    rng = np.random.default_rng(w)
+    for b_h in (8, 12, 16):
+        lam = 2 ** b_h - 1
+        for _ in range(20):
+            nn = int(rng.integers(1, 500))
+            dd = int(rng.integers(0, nn + 1))
+            d, n = flat(dd, nn)
+            g = rng.integers(0, 2 ** 36, 64, dtype=np.uint64)
+            exact = oracle.score_fixed(np.zeros(64), g, np.zeros(64), d, n, b_h, 0)
+            lut = oracle.score_fixed(np.zeros(64), g, np.zeros(64), d, n, b_h, 0, recip_bits=w)
+            bound = g.astype(object) * lam / 2 ** (w + 1) + 1
+            diff = np.abs(lut.astype(object) - exact.astype(object))
+            assert all(x <= b for x, b in zip(diff, bound)), (b_h, dd, nn)
+
+
+def test_reciprocal_divider_off_is_the_exact_score():
+    d, n = flat(1, 24)
+    g = np.array([0, 7, 2_000_000], np.uint64)
+    a = oracle.score_fixed([0, 3, 9], g, [0, 0, 0], d, n, B_H, P_Z)
+    b = oracle.score_fixed([0, 3, 9], g, [0, 0, 0], d, n, B_H, P_Z, recip_bits=0)
+    assert a.tolist() == b.tolist()
