@@ -98,7 +98,7 @@ extern "C" {
 
 typedef struct unison_ctx unison_ctx;
 
-/* Register-file organisation (Sec. III-D, eq. (rf), eq. (stale)): the unified
+/* Register-file organisation (Sec. IV-B, eq. (rf), eq. (stale)): the unified
  * file, or two private copies -- the eviction engine's and TIDE's -- that are
  * overwritten with the live file after every request and gap onset, after every
  * 8th request, or at gap onsets only. */
@@ -140,7 +140,8 @@ typedef struct {
   double t_h_ns_per_B;     /* HBM read cost t_h */
   double t_p_ns_per_tok;   /* prefill cost t_p */
   float penalty_us;        /* completion penalty P of eq. (esp), >= 0, microseconds */
-  uint32_t b_h;            /* hazard bits b_h, 1..16 */
+  uint32_t b_h;            /* hazard bits b_h, 6..16 (below 6, floor(eps Lambda + 1/2) = 0 and
+                              sigma_q of eq. (survq) can reach 0, where eq. (t1) is undefined) */
   uint32_t b_g;            /* gap register bits b_g, 1..64 */
   uint32_t online_sessions; /* completions an online table counts (hazard_online = 1) */
   uint64_t tau_ns;         /* gap time divisor tau, >= 1 */

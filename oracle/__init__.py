@@ -122,6 +122,7 @@ def load_library(path):
     L.orc_lut_f32.argtypes = [u32p, u32p, f32p]
     L.orc_lut_q.argtypes = [u32p, u32p, C.c_uint32, u64p]
     L.orc_score_f32.argtypes = [C.c_uint32, u8p, f32p, u8p, f32p, C.c_float, f32p]
+    L.orc_score_fixed.restype = C.c_int
     L.orc_score_fixed.argtypes = [C.c_uint32, u8p, u64p, u8p, u64p, C.c_uint32,
                                   C.c_uint64, C.c_uint32, u64p]
     L.orc_ema_replay.argtypes = [C.c_uint32, C.c_uint32, u64p, u8p, C.c_uint32,
@@ -194,9 +195,11 @@ def score_fixed(turn, gq, done, d, n, b_h, p_z, recip_bits=0):
     turn, gq, done = _c(turn, np.uint8), _c(gq, np.uint64), _c(done, np.uint8)
     hq = lut_q(d, n, b_h)
     out = np.zeros(turn.shape[0], np.uint64)
-    lib().orc_score_fixed(turn.shape[0], _p(turn, C.c_uint8), _p(gq, C.c_uint64),
-                          _p(done, C.c_uint8), _p(hq, C.c_uint64), b_h, p_z, recip_bits,
-                          _p(out, C.c_uint64))
+    rc = lib().orc_score_fixed(turn.shape[0], _p(turn, C.c_uint8), _p(gq, C.c_uint64),
+                               _p(done, C.c_uint8), _p(hq, C.c_uint64), b_h, p_z, recip_bits,
+                               _p(out, C.c_uint64))
+    if rc != 0:
+        raise ValueError("b_h %d or recip_bits %d out of range" % (b_h, recip_bits))
     return out
 
 

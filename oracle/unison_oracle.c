@@ -288,14 +288,19 @@ void orc_score_f32(uint32_t n, const uint8_t* turn, const float* g, const uint8_
 }
 
 /* The fixed-point scores of n sessions; recip_bits 0: exact divider, else the
- * reciprocal table of that many fraction bits. */
-void orc_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
-                     const uint8_t* done, const uint64_t* hq, uint32_t b_h, uint64_t p_z,
-                     uint32_t recip_bits, uint64_t* out) {
+ * reciprocal table of that many fraction bits.  b_h must be 6..32 (below 6,
+ * floor(eps Lambda + 1/2) = 0 and sigma_q can be 0, where eq. (t1) is not
+ * defined).  Returns ORC_OK or ORC_E_INVALID. */
+int orc_score_fixed(uint32_t n, const uint8_t* turn, const uint64_t* gq,
+                    const uint8_t* done, const uint64_t* hq, uint32_t b_h, uint64_t p_z,
+                    uint32_t recip_bits, uint64_t* out) {
+  if (b_h < 6 || b_h > 32 || recip_bits > 32) return ORC_E_INVALID;
   uint64_t* r = recip_bits ? recip_table((1ULL << b_h) - 1, recip_bits) : NULL;
+  if (recip_bits && !r) return ORC_E_INVALID;
   for (uint32_t i = 0; i < n; i++)
     out[i] = spear_fixed(turn[i], gq[i], done[i], hq, b_h, p_z, r, recip_bits);
   free(r);
+  return ORC_OK;
 }
 
 /* ----------------------------------------------------------- EMA updates */
@@ -636,7 +641,7 @@ int orc_run(const orc_params* p, uint64_t n_events, const uint64_t* ev_t,
             const uint32_t* ev_tool, const uint64_t* eta_mean) {
   if (!p || !out || p->policy > P_ETA || (p->policy == P_ETA && !eta_mean) ||
       p->dma_B_per_us == 0 || p->n_slots == 0 ||
-      p->tau_ns == 0 || p->b_h < 1 || p->b_h > 32 || p->b_g < 1 || p->b_g > 64 || p->dual_sync > 3 ||
+      p->tau_ns == 0 || p->b_h < 6 || p->b_h > 32 || p->b_g < 1 || p->b_g > 64 || p->dual_sync > 3 ||
       p->recip_bits > 32 ||
       !(p->penalty_us >= 0.0f))
     return ORC_E_INVALID;

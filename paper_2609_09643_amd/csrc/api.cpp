@@ -455,7 +455,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
       return ctx->fail(UNISON_E_INVALID, "parameter row %u: dual_sync %u (dims.views = %u)", i,
                        p.dual_sync, ctx->dims.views);
     if (p.policy > UNISON_POLICY_ETA || p.tide > 1 || p.score_mode > 1 || p.hazard_online > 1 ||
-        p.lut >= ctx->dims.n_luts || p.trace >= ctx->dims.n_traces || p.b_h < 1 || p.b_h > 16 ||
+        p.lut >= ctx->dims.n_luts || p.trace >= ctx->dims.n_traces || p.b_h < 6 || p.b_h > 16 ||
         p.b_g < 1 || p.b_g > 64 || p.tau_ns < 1 || p.n_slots < 1 || p.dma_B_per_us < 1 ||
         p.recip_bits > 32 ||
         !(p.penalty_us >= 0.0f) || std::isinf(p.penalty_us) || !std::isfinite(p.t_s_ns_per_B) ||
@@ -728,7 +728,7 @@ int unison_score_fixed(void* hip_stream, uint32_t n, const uint8_t* turn, const 
                        const uint8_t* done, const uint32_t* lut_d, const uint32_t* lut_n,
                        uint32_t b_h, uint64_t p_z, uint32_t recip_bits, uint64_t* out) {
   if (n && (!turn || !gq || !done || !out)) return UNISON_E_INVALID;
-  if (!lut_d || !lut_n || b_h < 1 || b_h > 16 || recip_bits > 32) return UNISON_E_INVALID;
+  if (!lut_d || !lut_n || b_h < 6 || b_h > 16 || recip_bits > 32) return UNISON_E_INVALID;
   return launch_score_fixed(n, turn, gq, done, lut_d, lut_n, b_h, p_z, recip_bits, out,
                             reinterpret_cast<hipStream_t>(hip_stream)) == hipSuccess
              ? UNISON_OK

@@ -75,9 +75,13 @@ __device__ __forceinline__ uint64_t sat_mul(uint64_t a, uint64_t b) {
 // s / 10 rounded to nearest even, as the IEEE division gives it.  Between
 // 2^-64 and 2^64 the quotient comes from one product and one residual step:
 // q0 = s * 0.1f, r = s - 10 * q0 (exact in one fma), q = q0 + r * 0.1f (one
-// fma).  An exhaustive comparison over every finite float shows this equal to
-// the division from 2^-125 upwards; outside the window (zero, for one) the
-// division itself runs.  Gap EMAs stay below 2^36 us.
+// fma) -- Markstein's correction step (P. Markstein, IBM J. Res. Dev. 34(1),
+// 1990) applied to division by a divisor known in advance, the setting of
+// Brisebarre, Muller and Raina (IEEE Trans. Computers 53(8), 2004).  Rather
+// than rely on the theorem's hypotheses, an exhaustive comparison over every
+// finite float shows this equal to the division from 2^-125 upwards; outside
+// the window (zero, for one) the division itself runs.  Gap EMAs stay below
+// 2^36 us.
 __device__ __forceinline__ float div10(float s) {
   if (s >= 0x1p-64f && s <= 0x1p64f) {
     const float q0 = s * 0.1f;

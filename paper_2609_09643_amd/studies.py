@@ -1,5 +1,5 @@
 """Policy studies on the batched simulation: the unified-versus-dual register
-file ablation (Sec. III-D, Table V), the scoring x tiering ablation with
+file ablation (Sec. IV-B, Table V), the scoring x tiering ablation with
 prefetch accuracy, and Agent Serving Effectiveness over the session capacity
 (eq. (ase)).  Each study is one launch of libunison; this module turns the
 counters into the paper's rates.

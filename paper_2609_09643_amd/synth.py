@@ -648,7 +648,7 @@ def _study_rows(traces, cells):
 
 
 def dual_ablation(traces=None, envelope=FIDELITY_ENVELOPES[0]):
-    """Sec. III-D / Table V: SPEAR+TIDE with the unified register file (arm 0)
+    """Sec. IV-B / Table V: SPEAR+TIDE with the unified register file (arm 0)
     and with dual copies refreshed after every request and gap (1), every 8
     requests (2) or at gap onsets (3), per trace."""
     traces = fidelity_traces() if traces is None else traces

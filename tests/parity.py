@@ -3,8 +3,9 @@ import numpy as np
 
 import oracle
 
-# Floating-point counters are sums in event order on both sides; 1e-6 relative
-# is the agreed bound (they agree exactly when both sides round identically).
+# Floating-point counters: the oracle adds one f64 product per request in event
+# order, the GPU rounds the products of exact integer totals once at the end.
+# Both are the same real-valued sums; 1e-6 relative is the agreed bound.
 FLOAT_FIELDS = ("amat_sum_ns", "ttft_sum_ns")
 REL_TOL = 1e-6
 
