@@ -36,13 +36,13 @@ def random_trace(rng, n_sess):
                              grow_lo=int(rng.integers(1, 200)), grow_hi=int(rng.integers(200, 3000)))
 
 
-def random_rows(rng, n_traces, per_trace, n_luts):
+def random_rows(rng, n_traces, per_trace, n_luts, n_policies=5):
     formats = synth.format_grid()
     rows = []
     for ti in range(n_traces):
         for _ in range(per_trace):
             p = synth.default_params(1)
-            pol = int(rng.integers(0, 5))
+            pol = int(rng.integers(0, n_policies))
             synth.set_policy(p, pol, tide=int(rng.integers(0, 2)))
             p["trace"] = ti
             p["lut"] = int(rng.integers(0, n_luts))
@@ -63,13 +63,15 @@ def random_rows(rng, n_traces, per_trace, n_luts):
     return np.array(rows, dtype=synth.SIM_PARAMS_DTYPE)
 
 
-def batch(seed, lo, hi, n_traces=24, per_trace=12):
+def batch(seed, lo, hi, n_traces=24, per_trace=12, n_policies=5):
+    """A randomised batch; n_policies = 4 draws the rows as before the ETA
+    baseline existed (the batches the retired variant ran on)."""
     rng = np.random.Generator(np.random.PCG64(seed))
     sizes = np.clip(np.floor(np.exp(rng.uniform(np.log(lo), np.log(hi + 1), n_traces))), lo, hi).astype(int)
     traces = [random_trace(rng, int(n)) for n in sizes]
     # the traces' own tables, a flat table and one fitted elsewhere
     pops = [t.turns for t in traces] + [None, synth.hazard_population(seed + 7, 128)]
-    rows = random_rows(rng, len(traces), per_trace, len(pops))
+    rows = random_rows(rng, len(traces), per_trace, len(pops), n_policies)
     flat = len(traces)
     return synth.Workload("random_%d" % seed, traces, pops, rows, flat_luts=[(flat,) + synth.FLAT_COUNTS])
 
