@@ -19,10 +19,11 @@
 #include "unison_device.h"
 
 namespace unison {
-hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream, int force_variant,
-                      int force_cache_slots);
+hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, uint64_t max_slots, hipStream_t stream,
+                      int force_variant, int force_cache_slots);
 uint32_t sim_variant_capacity(int v);
-int sim_auto_variant(uint32_t max_sess);
+int sim_auto_variant(uint32_t max_sess, uint64_t max_slots);
+bool sim_variant_slots_ok(int v, uint64_t max_slots);
 uint32_t sim_variant_lanes(int v);
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
                                 hipStream_t stream);
@@ -177,6 +178,7 @@ struct unison_ctx {
   bool time44 = false;  // every trace time is below 2^44 - 1 ns
   bool dual = false;    // some row uses the dual register-file design
   uint32_t max_sess_batch = 0;
+  uint64_t max_slots_batch = 0;  // largest N_sess of the parameter rows
   int force_variant = -1;
   int force_cache_slots = -1;  // test hook: resident-cache slots of the streamed tables
   // the register-table kernels' lane-group -> simulation map (slot_map)
@@ -449,6 +451,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
   UNISON_LIVE(ctx);
   if (!ctx->traces_loaded) return ctx->fail(UNISON_E_NOT_READY, "load traces before parameters");
   uint32_t max_sess = 0;
+  uint64_t max_slots = 0;
   for (uint32_t i = 0; i < ctx->dims.n_sims; ++i) {
     const unison_sim_params& p = params[i];
     if (p.dual_sync > UNISON_DUAL_GAP || (p.dual_sync && !ctx->dims.views))
@@ -463,6 +466,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
       return ctx->fail(UNISON_E_INVALID, "parameter row %u out of range", i);
     const uint64_t ns = ctx->h_sess_off[p.trace + 1] - ctx->h_sess_off[p.trace];
     max_sess = std::max<uint32_t>(max_sess, (uint32_t)ns);
+    max_slots = std::max<uint64_t>(max_slots, p.n_slots);
   }
   ctx->h_params.assign(params, params + ctx->dims.n_sims);
   ctx->dual = false;
@@ -475,6 +479,7 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params) {
   rc = ctx->hip(hipStreamSynchronize(ctx->stream), "synchronise after parameters");
   if (rc) return rc;
   ctx->max_sess_batch = max_sess;
+  ctx->max_slots_batch = max_slots;
   ctx->params_set = true;
   ctx->params_gen++;
   return UNISON_OK;
@@ -592,8 +597,11 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   if (v >= 0 && (sim_variant_capacity(v) == 0 || sim_variant_capacity(v) < ctx->max_sess_batch))
     return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds %u sessions < %u", v,
                      sim_variant_capacity(v), ctx->max_sess_batch);
+  if (v >= 0 && !sim_variant_slots_ok(v, ctx->max_slots_batch))
+    return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds N_sess up to 512, not %llu", v,
+                     (unsigned long long)ctx->max_slots_batch);
   if (v < 0) {
-    v = sim_auto_variant(ctx->max_sess_batch);
+    v = sim_auto_variant(ctx->max_sess_batch, ctx->max_slots_batch);
     if (sim_variant_capacity(v) < ctx->max_sess_batch)
       return ctx->fail(UNISON_E_CAPACITY, "%u sessions exceed every kernel variant (largest %u)",
                        ctx->max_sess_batch, sim_variant_capacity(v));
@@ -608,7 +616,9 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
       a.n_slots = ctx->n_slots;
     }
   }
-  int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->stream, v, ctx->force_cache_slots), "launch simulation");
+  int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->max_slots_batch, ctx->stream, v,
+                               ctx->force_cache_slots),
+                    "launch simulation");
   if (rc == UNISON_OK) ctx->ran = true;
   return rc;
 }

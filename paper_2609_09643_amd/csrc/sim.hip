@@ -239,6 +239,102 @@ struct Entry {
   uint64_t next;
 };
 
+struct TraceView {
+  const uint64_t* t;
+  const uint32_t* sid;
+  const uint32_t* info;
+  const uint32_t* len;
+  const uint64_t* next;
+  const uint32_t* tool;  // or null: every gap is tool class 0
+  uint64_t n_ev;
+  uint32_t n_sess;
+};
+
+struct Ev {
+  uint64_t t;
+  uint32_t sid, info, len, tool;
+  uint64_t next;
+};
+
+// The event record; the next arrival only where the key reads it (Belady),
+// the tool class only where it predicts one (ETA).
+template <bool NEXT, bool TOOL>
+__device__ __forceinline__ Ev load_ev(const TraceView& tr, uint64_t e) {
+  Ev v;
+  v.t = tr.t[e];
+  v.sid = tr.sid[e];
+  v.info = tr.info[e];
+  v.len = tr.len[e];
+  v.next = NEXT ? tr.next[e] : ~0ull;
+  v.tool = (TOOL && tr.tool) ? tr.tool[e] : 0u;
+  return v;
+}
+
+// Event records one event ahead: the next record's loads are in flight while
+// the current event is processed.
+template <bool NEXT, bool TOOL>
+struct AheadReader {
+  const TraceView& tr;
+  uint64_t end;
+  Ev cur;
+  __device__ __forceinline__ AheadReader(const TraceView& t, uint64_t e, uint64_t end_)
+      : tr(t), end(end_), cur(load_ev<NEXT, TOOL>(t, e)) {}
+  __device__ __forceinline__ Ev take(uint64_t e) {
+    const Ev c = cur;
+    cur = load_ev<NEXT, TOOL>(tr, e + 1 < end ? e + 1 : e);
+    return c;
+  }
+};
+
+// Event records 64 at a time for a lone wavefront: lane l holds event base + l
+// of the current window and of the next, whose loads are issued a whole
+// window ahead; an event's fields are read out of its lane.
+template <bool NEXT, bool TOOL>
+struct WindowReader {
+  const TraceView& tr;
+  uint64_t end, base;
+  uint32_t lane;
+  uint64_t ct, cn, nt, nn;
+  uint32_t csid, cinfo, clen, ctool, nsid, ninfo, nlen, ntool;
+  __device__ __forceinline__ void load(uint64_t b, uint64_t& t, uint32_t& sid, uint32_t& info,
+                                       uint32_t& len, uint64_t& nx, uint32_t& tool) const {
+    const uint64_t e = b + lane;
+    const bool ok = e < end;
+    const uint64_t i = ok ? e : (end ? end - 1 : 0);
+    t = tr.t[i];
+    sid = tr.sid[i];
+    info = tr.info[i];
+    len = tr.len[i];
+    nx = NEXT ? tr.next[i] : ~0ull;
+    tool = (TOOL && tr.tool) ? tr.tool[i] : 0u;
+  }
+  __device__ __forceinline__ WindowReader(const TraceView& t, uint64_t e, uint64_t end_)
+      : tr(t), end(end_), base(e), lane(threadIdx.x & 63u) {
+    load(base, ct, csid, cinfo, clen, cn, ctool);
+    load(base + 64, nt, nsid, ninfo, nlen, nn, ntool);
+  }
+  __device__ __forceinline__ static uint64_t lane64(uint64_t v, int k) {
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), k) << 32) |
+           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, k);
+  }
+  __device__ __forceinline__ Ev take(uint64_t e) {
+    if (e - base >= 64) {
+      ct = nt; csid = nsid; cinfo = ninfo; clen = nlen; cn = nn; ctool = ntool;
+      base += 64;
+      load(base + 64, nt, nsid, ninfo, nlen, nn, ntool);
+    }
+    const int k = (int)(e - base);
+    Ev v;
+    v.t = lane64(ct, k);
+    v.sid = (uint32_t)__builtin_amdgcn_readlane((int)csid, k);
+    v.info = (uint32_t)__builtin_amdgcn_readlane((int)cinfo, k);
+    v.len = (uint32_t)__builtin_amdgcn_readlane((int)clen, k);
+    v.next = NEXT ? lane64(cn, k) : ~0ull;
+    v.tool = TOOL ? (uint32_t)__builtin_amdgcn_readlane((int)ctool, k) : 0u;
+    return v;
+  }
+};
+
 // ------------------------------------------------------------ tables
 
 // Most resident-cache slots per thread of the streamed-table kernels.
@@ -251,6 +347,8 @@ struct RegTable {
   // Gap onsets reduce their scan victim and TIDE's candidates separately:
   // fusing the three reductions made this kernel slower (0.518 vs 0.498 ms).
   static constexpr bool kFuseGap = false;
+  template <bool N, bool T>
+  using Reader = AheadReader<N, T>;
   uint32_t lane;
   uint32_t meta[EPL];
   float g[EPL];
@@ -515,6 +613,8 @@ struct MemTable {
   // A gap onset's scan and TIDE's first candidates share one pass and one
   // barrier (the dual design scans different copies for the two engines).
   static constexpr bool kFuseGap = !VIEWS;
+  template <bool N, bool T>
+  using Reader = AheadReader<N, T>;
   uint64_t* mg;
   uint64_t* gq;
   uint32_t* len;
@@ -1018,6 +1118,279 @@ struct MemTable {
   }
 };
 
+// Residents in registers, table in LDS, one wavefront per simulation.  Every
+// session's entry stays in LDS (as in the LDS-resident MemTable), and each
+// resident also occupies a VGPR slot of the wavefront -- its session id, meta,
+// size and key -- kept current wherever the engine writes an entry.  Residents
+// never exceed N_sess (eq. (cap)), so SPL slots per lane hold them all while
+// N_sess <= 64 SPL: every scan and TIDE selection is then a reduction over the
+// slots alone, with no table memory touched, and an event reads only its own
+// session's entry.  The single wavefront's LDS accesses are in program order,
+// so no barrier is needed anywhere.
+template <int SPL, uint32_t POL, uint32_t SMODE>
+struct SlotTable {
+  using PT = Pol<POL, SMODE>;
+  static constexpr bool kViews = false;
+  static constexpr bool kFuseGap = true;
+  template <bool N, bool T>
+  using Reader = WindowReader<N, T>;  // events come 64 to a window, one per lane
+  uint64_t* mg;
+  uint64_t* gq;
+  uint32_t* len;
+  uint32_t* kvb;
+  uint64_t* last;
+  uint64_t* next;
+  uint32_t lane;
+  KeyCtx kc;
+  uint32_t ssid[SPL];   // kNone: free
+  uint32_t smeta[SPL];
+  uint64_t skey[SPL];
+  uint64_t ssize[SPL];
+  // the entry of the latest write(): its key and KV bytes per token
+  uint32_t w_sid;
+  uint64_t w_key;
+  uint32_t w_kvb;
+
+  __device__ __forceinline__ uint64_t key_from(uint32_t m, float g, uint64_t q, uint64_t l,
+                                               uint64_t n) const {
+    return key_of<POL, SMODE>(kc, m, hazard_of<POL, SMODE>(kc, m), g, q, l, n);
+  }
+  // the key of entry i from its fields in LDS (per lane)
+  __device__ __forceinline__ uint64_t key_at(uint32_t i) const {
+    const uint64_t x = mg[i];
+    return key_from((uint32_t)x, __uint_as_float((uint32_t)(x >> 32)), PT::fixed ? gq[i] : 0ull,
+                    PT::recency ? last[i] : 0ull, PT::nextkey ? next[i] : ~0ull);
+  }
+
+  template <class T>
+  __device__ __forceinline__ static T pick(const T (&a)[SPL], uint32_t j) {
+    T v = a[0];
+#pragma unroll
+    for (int k = 1; k < SPL; ++k) v = j == (uint32_t)k ? a[k] : v;
+    return v;
+  }
+  // The slot (j, lane l) holding sid; false if sid is not resident.
+  __device__ __forceinline__ bool find(uint32_t sid, uint32_t& j, uint32_t& l) const {
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const uint64_t b = __builtin_amdgcn_ballot_w64(ssid[k] == sid);
+      if (b) {
+        j = (uint32_t)k;
+        l = (uint32_t)__builtin_ctzll(b);
+        return true;
+      }
+    }
+    return false;
+  }
+  __device__ __forceinline__ void put(uint32_t j, uint32_t l, uint32_t sid, uint32_t m,
+                                      uint64_t key, uint64_t size) {
+    const bool mine = lane == l;
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const bool w = mine && j == (uint32_t)k;
+      ssid[k] = w ? sid : ssid[k];
+      smeta[k] = w ? m : smeta[k];
+      skey[k] = w ? key : skey[k];
+      ssize[k] = w ? size : ssize[k];
+    }
+  }
+  __device__ __forceinline__ void set_slot_meta(uint32_t j, uint32_t l, uint32_t m) {
+    const bool mine = lane == l;
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) smeta[k] = (mine && j == (uint32_t)k) ? m : smeta[k];
+  }
+  __device__ __forceinline__ void set_slot_key(uint32_t j, uint32_t l, uint32_t m, uint64_t key) {
+    const bool mine = lane == l;
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const bool w = mine && j == (uint32_t)k;
+      smeta[k] = w ? m : smeta[k];
+      skey[k] = w ? key : skey[k];
+    }
+  }
+  // A resident enters the first free slot.
+  __device__ __forceinline__ void insert(uint32_t sid, uint32_t m, uint64_t key, uint64_t size) {
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const uint64_t b = __builtin_amdgcn_ballot_w64(ssid[k] == kNone);
+      if (b) {
+        put((uint32_t)k, (uint32_t)__builtin_ctzll(b), sid, m, key, size);
+        return;
+      }
+    }
+  }
+  // Meta word m of entry sid: LDS, and the resident set it implies.
+  __device__ __forceinline__ void meta_to(uint32_t sid, uint32_t m) {
+    if (lane == 0) reinterpret_cast<uint32_t*>(mg + sid)[0] = m;
+    uint32_t j, l;
+    const bool res = find(sid, j, l);
+    const bool now = meta_tier(m) != kTierNone;
+    if (res && !now) {
+      put(j, l, kNone, 0u, 0ull, 0ull);
+    } else if (res) {
+      set_slot_meta(j, l, m);
+    } else if (now) {
+      uint64_t key, size;
+      if (sid == w_sid) {
+        key = w_key;
+        size = (uint64_t)uni32(len[sid]) * w_kvb;
+      } else {
+        key = uni64(key_at(sid));
+        size = (uint64_t)uni32(len[sid]) * uni32(kvb[sid]);
+      }
+      insert(sid, m, key, size);
+    }
+  }
+
+  __device__ __forceinline__ void event_begin() {}
+  __device__ __forceinline__ void grow(uint32_t) {}
+
+  __device__ __forceinline__ Entry read(uint32_t sid) const {
+    Entry e;
+    const uint64_t x = uni64(mg[sid]);
+    e.meta = (uint32_t)x;
+    e.g = __uint_as_float((uint32_t)(x >> 32));
+    e.gq = PT::fixed ? uni64(gq[sid]) : 0ull;
+    e.len = uni32(len[sid]);
+    e.kvb = uni32(kvb[sid]);
+    e.last = uni64(last[sid]);
+    e.next = PT::nextkey ? uni64(next[sid]) : ~0ull;
+    return e;
+  }
+  __device__ __forceinline__ void read_size(uint32_t sid, uint64_t& size, uint32_t& m) const {
+    uint32_t j, l;
+    if (find(sid, j, l)) {
+      const uint64_t sz = pick(ssize, j);
+      size = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(sz >> 32), (int)l) << 32) |
+             (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)sz, (int)l);
+      m = (uint32_t)__builtin_amdgcn_readlane((int)pick(smeta, j), (int)l);
+    } else {
+      m = uni32((uint32_t)mg[sid]);
+      size = (uint64_t)uni32(len[sid]) * uni32(kvb[sid]);
+    }
+  }
+  __device__ __forceinline__ void read_end(uint32_t sid, Entry& e) const {
+    const uint64_t x = uni64(mg[sid]);
+    e.meta = (uint32_t)x;
+    e.g = __uint_as_float((uint32_t)(x >> 32));
+    e.gq = PT::fixed ? uni64(gq[sid]) : 0ull;
+  }
+  __device__ __forceinline__ void write_end(uint32_t sid, const Entry& e, uint64_t t, uint64_t nx) {
+    if (lane == 0) {
+      reinterpret_cast<uint32_t*>(mg + sid)[0] = e.meta;
+      last[sid] = t;
+      if constexpr (PT::nextkey) next[sid] = nx;
+    }
+    w_sid = kNone;
+    uint32_t j, l;
+    if (find(sid, j, l)) set_slot_key(j, l, e.meta, key_from(e.meta, e.g, e.gq, t, nx));
+  }
+  __device__ __forceinline__ void write(uint32_t sid, const Entry& e) {
+    if (lane == 0) {
+      mg[sid] = (uint64_t)e.meta | ((uint64_t)__float_as_uint(e.g) << 32);
+      if constexpr (PT::fixed) gq[sid] = e.gq;
+      len[sid] = e.len;
+      last[sid] = e.last;
+      if constexpr (PT::nextkey) next[sid] = e.next;
+    }
+    w_sid = sid;
+    w_key = key_from(e.meta, e.g, e.gq, e.last, e.next);
+    w_kvb = e.kvb;
+    uint32_t j, l;
+    if (find(sid, j, l)) set_slot_key(j, l, e.meta, w_key);
+  }
+  __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) { meta_to(sid, m); }
+  __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
+    if (lane == 0) len[sid] = l;
+    meta_to(sid, m);
+  }
+  __device__ __forceinline__ void set_turn(uint32_t, uint32_t, const KeyCtx&) {}
+  __device__ __forceinline__ void scan(const KeyCtx&, uint32_t) {}
+
+  __device__ __forceinline__ static Cand uniform(const Cand& c) { return Cand{uni64(c.key), uni32(c.sid)}; }
+
+  template <bool MAX>
+  __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx&) const {
+    Cand c = MAX ? cand_none_max() : cand_none_min();
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const uint32_t m = smeta[k];
+      const bool ok = ssid[k] != kNone && meta_phase(m) != kServing &&
+                      (tier == 0 || meta_tier(m) == tier);
+      const bool take = ok && (MAX ? max_better(skey[k], ssid[k], c.key, c.sid)
+                                   : min_better(skey[k], ssid[k], c.key, c.sid));
+      c.key = take ? skey[k] : c.key;
+      c.sid = take ? ssid[k] : c.sid;
+    }
+    return uniform(reduce_group<64, MAX>(c));
+  }
+  __device__ __forceinline__ Cand argmax_first(const KeyCtx& K) const { return select<true>(0, K); }
+  __device__ __forceinline__ void select_pd(const KeyCtx&, Cand& p, Cand& d) const {
+    Cand cp = cand_none_min(), cd = cand_none_max();
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const uint32_t m = smeta[k];
+      const bool ev = ssid[k] != kNone && meta_phase(m) != kServing;
+      const bool tp = ev && meta_tier(m) == kTierHbm && min_better(skey[k], ssid[k], cp.key, cp.sid);
+      const bool td = ev && meta_tier(m) == kTierSram && max_better(skey[k], ssid[k], cd.key, cd.sid);
+      cp.key = tp ? skey[k] : cp.key;
+      cp.sid = tp ? ssid[k] : cp.sid;
+      cd.key = td ? skey[k] : cd.key;
+      cd.sid = td ? ssid[k] : cd.sid;
+    }
+    p = uniform(reduce_group<64, false>(cp));
+    d = uniform(reduce_group<64, true>(cd));
+  }
+  __device__ __forceinline__ void scan3(const KeyCtx&, Cand& v, Cand& p, Cand& d) const {
+    Cand cv = cand_none_max(), cp = cand_none_min(), cd = cand_none_max();
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const uint32_t m = smeta[k];
+      const bool ev = ssid[k] != kNone && meta_phase(m) != kServing;
+      const bool tv = ev && max_better(skey[k], ssid[k], cv.key, cv.sid);
+      const bool tp = ev && meta_tier(m) == kTierHbm && min_better(skey[k], ssid[k], cp.key, cp.sid);
+      const bool td = ev && meta_tier(m) == kTierSram && max_better(skey[k], ssid[k], cd.key, cd.sid);
+      cv.key = tv ? skey[k] : cv.key;
+      cv.sid = tv ? ssid[k] : cv.sid;
+      cp.key = tp ? skey[k] : cp.key;
+      cp.sid = tp ? ssid[k] : cp.sid;
+      cd.key = td ? skey[k] : cd.key;
+      cd.sid = td ? ssid[k] : cd.sid;
+    }
+    v = uniform(reduce_group<64, true>(cv));
+    p = uniform(reduce_group<64, false>(cp));
+    d = uniform(reduce_group<64, true>(cd));
+  }
+
+  // Online hazard table: add the completed session, then rescore every resident.
+  __device__ __forceinline__ bool hazard_open(const KeyCtx& K) const {
+    return uni32(K.hn[0]) < K.online_cap;
+  }
+  __device__ __forceinline__ void hazard_add(const KeyCtx& K, uint32_t Tn) {
+    hazard_add_counts(K, Tn, lane, 64);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int k = 0; k < SPL; ++k)
+      if (ssid[k] != kNone) skey[k] = key_at(ssid[k]);
+    w_sid = kNone;
+  }
+
+  // Smallest evictable resident idle for longer than ttl (timeout: key = 2^64 - 1 - last).
+  __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) const {
+    const uint64_t thr = idle_threshold(now, ttl);
+    uint32_t c = kNone;
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      const bool ok = ssid[k] != kNone && meta_phase(smeta[k]) != kServing && (~0ull - skey[k]) < thr;
+      c = ok && ssid[k] < c ? ssid[k] : c;
+    }
+    if (__builtin_amdgcn_ballot_w64(c != kNone) == 0) return kNone;
+    return uni32(reduce_min32<64, 1>(c));
+  }
+};
+
 // ------------------------------------------------------------- the engine
 
 struct Scalars {
@@ -1174,37 +1547,6 @@ __device__ __forceinline__ void emit(Cnt& C, Scalars& S, const LogSink& L, uint3
   }
 }
 
-struct TraceView {
-  const uint64_t* t;
-  const uint32_t* sid;
-  const uint32_t* info;
-  const uint32_t* len;
-  const uint64_t* next;
-  const uint32_t* tool;  // or null: every gap is tool class 0
-  uint64_t n_ev;
-  uint32_t n_sess;
-};
-
-struct Ev {
-  uint64_t t;
-  uint32_t sid, info, len, tool;
-  uint64_t next;
-};
-
-// The event record; the next arrival only where the key reads it (Belady),
-// the tool class only where it predicts one (ETA).
-template <bool NEXT, bool TOOL>
-__device__ __forceinline__ Ev load_ev(const TraceView& tr, uint64_t e) {
-  Ev v;
-  v.t = tr.t[e];
-  v.sid = tr.sid[e];
-  v.info = tr.info[e];
-  v.len = tr.len[e];
-  v.next = NEXT ? tr.next[e] : ~0ull;
-  v.tool = (TOOL && tr.tool) ? tr.tool[e] : 0u;
-  return v;
-}
-
 template <class Tab>
 __device__ __forceinline__ void release(Tab& T, Scalars& S, uint32_t sid) {
   uint64_t size;
@@ -1222,13 +1564,12 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& e_io, uint64_t end) {
   using PT = Pol<POL, SMODE>;
   uint64_t e = e_io;
-  Ev cur = load_ev<PT::belady, PT::eta>(tr, e);
+  typename Tab::template Reader<PT::belady, PT::eta> rd(tr, e, end);
   // victim-digest weight of event e, (2e + 1) * 0x9e3779b97f4a7c15, stepped per event
   constexpr uint64_t kGolden = 0x9e3779b97f4a7c15ull;
   uint64_t vw = (2ull * e + 1ull) * kGolden;
   for (; e < end; ++e) {
-    // the next event's record is in flight while this one is processed
-    const Ev nxt = load_ev<PT::belady, PT::eta>(tr, e + 1 < end ? e + 1 : e);
+    const Ev cur = rd.take(e);
     T.event_begin();
     const uint64_t now = UNI ? uni64(cur.t) : cur.t;
     const uint32_t sid = UNI ? uni32(cur.sid) : cur.sid;
@@ -1496,7 +1837,6 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       }
     }
     C.events++;
-    cur = nxt;
   }
   e_io = e;
 }
@@ -1892,6 +2232,136 @@ __global__ __launch_bounds__(BLOCK) void sim_block_kernel(SimArgs a) {
   }
 }
 
+// ------------------------------------------------- slot-table kernel
+
+// One wavefront per simulation: the table in LDS, the residents in SPL VGPR
+// slots per lane (SlotTable), events 64 to a window.
+template <int SPL, uint32_t POL, uint32_t SMODE>
+__device__ __forceinline__ void slot_run(const SimArgs& a, uint32_t sim, const unison_sim_params& P,
+                                         const KeyCtx& K, uint64_t* s_tab) {
+  const uint32_t lane = threadIdx.x;
+  const uint64_t eb = a.ev_off[P.trace], ee = a.ev_off[P.trace + 1];
+  const uint64_t sb = a.sess_off[P.trace];
+  const uint32_t n_sess = (uint32_t)(a.sess_off[P.trace + 1] - sb);
+  const TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb,
+                     a.ev_tool ? a.ev_tool + eb : nullptr, ee - eb, n_sess};
+  const size_t tb = (size_t)sim * a.max_sessions;
+  const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
+
+  SlotTable<SPL, POL, SMODE> T;
+  const uint32_t n = n_sess;
+  T.mg = s_tab;
+  T.last = s_tab + n;
+  T.gq = s_tab + 2 * (size_t)n;
+  T.next = s_tab + 3 * (size_t)n;
+  uint32_t* s32 = reinterpret_cast<uint32_t*>(s_tab + 4 * (size_t)n);
+  T.len = s32;
+  T.kvb = s32 + n;
+  T.lane = lane;
+  T.kc = K;
+  T.w_sid = kNone;
+  T.w_key = 0;
+  T.w_kvb = 0;
+#pragma unroll
+  for (int k = 0; k < SPL; ++k) {
+    T.ssid[k] = kNone;
+    T.smeta[k] = 0;
+    T.skey[k] = 0;
+    T.ssize[k] = 0;
+  }
+  for (uint32_t i = lane; i < n; i += 64) {
+    T.mg[i] = cont ? a.t_mg[tb + i] : 0ull;
+    T.last[i] = cont ? a.t_last[tb + i] : 0ull;
+    T.gq[i] = cont ? a.t_gq[tb + i] : 0ull;
+    T.next[i] = cont ? a.t_next[tb + i] : ~0ull;
+    T.len[i] = cont ? a.t_len[tb + i] : 0u;
+    T.kvb[i] = a.sess_kvb[sb + i];
+  }
+  __syncthreads();
+  // a resumed table's residents take slots
+  if (cont) {
+    for (uint32_t base = 0; base < n; base += 64) {
+      const uint32_t i = base + lane;
+      const uint32_t ic = i < n ? i : 0u;  // lanes past the table read entry 0
+      const bool res = i < n && meta_tier((uint32_t)T.mg[ic]) != kTierNone;
+      const uint64_t key = T.key_at(ic);
+      const uint64_t size = (uint64_t)T.len[ic] * T.kvb[ic];
+      const uint32_t m = (uint32_t)T.mg[ic];
+      for (uint64_t bits = __builtin_amdgcn_ballot_w64(res); bits; bits &= bits - 1u) {
+        const int l = __builtin_ctzll(bits);
+        T.insert(base + (uint32_t)l, (uint32_t)__builtin_amdgcn_readlane((int)m, l),
+                 WindowReader<false, false>::lane64(key, l), WindowReader<false, false>::lane64(size, l));
+      }
+    }
+  }
+
+  Scalars S;
+  Cnt C;
+  uint64_t next_event = 0;
+  if (cont) {
+    load_scalars(a.state[sim], S);
+    C = cnt_from(a.counters[sim]);
+    next_event = a.state[sim].next_event;
+  } else {
+    S = Scalars{};
+    C = cnt_from(unison_counters{});
+  }
+  if (S.hi > n_sess) S.hi = n_sess;
+  if (P.dual_sync || P.n_slots > 64u * SPL) C.error = ~0ull;  // the launcher picks a kernel that holds it
+  pin_vgpr(S);
+  pin_vgpr(C);
+  const bool log_on = (a.flags & UNISON_RUN_LOG) && a.log_cap;
+  const LogSink L{log_on, log_on ? a.log + (size_t)sim * a.log_cap : nullptr, a.log_cap, lane == 0,
+                  log_on && (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
+  if (C.error == 0) {
+    unison_sim_params Pv = P;
+    pin_vgpr(Pv);
+    run_events<POL, SMODE, true>(T, Pv, K, tr, S, C, L, next_event, a.max_events,
+                                 a.first_bad[P.trace]);
+  }
+  __syncthreads();
+  for (uint32_t i = lane; i < n; i += 64) {
+    a.t_mg[tb + i] = T.mg[i];
+    a.t_last[tb + i] = T.last[i];
+    a.t_gq[tb + i] = T.gq[i];
+    a.t_next[tb + i] = T.next[i];
+    a.t_len[tb + i] = T.len[i];
+  }
+  store_hazard(a, P, sim, K, lane, 64);
+  if (lane == 0) {
+    finish_costs(S, P, C);
+    store_scalars(a.state[sim], S, next_event);
+    a.counters[sim] = cnt_to(C);
+  }
+}
+
+template <int SPL>
+__global__ __launch_bounds__(64) void sim_slot_kernel(SimArgs a) {
+  __shared__ float s_hf[52];
+  __shared__ uint32_t s_hq[52];
+  __shared__ uint32_t s_hd[52];
+  __shared__ uint32_t s_hn[52];
+  extern __shared__ uint64_t s_tab[];
+  const uint32_t sim = blockIdx.x;
+  const unison_sim_params P = a.params[sim];
+  const uint32_t lambda = (1u << P.b_h) - 1u;
+  const KeyCtx K{s_hf, s_hq, s_hd, s_hn, P.penalty_us, lambda, P.p_z, a.time44 != 0,
+                 P.hazard_online ? P.online_sessions : 0u, a.eta + (size_t)P.trace * kEtaClasses,
+                 P.recip_bits};
+  load_hazard(a, P, sim, K, threadIdx.x, 64);
+  __syncthreads();
+  switch (sim_policy(a, P)) {
+    case kSpear:
+      if (P.score_mode) slot_run<SPL, kSpear, 1>(a, sim, P, K, s_tab);
+      else slot_run<SPL, kSpear, 0>(a, sim, P, K, s_tab);
+      break;
+    case kLru: slot_run<SPL, kLru, 0>(a, sim, P, K, s_tab); break;
+    case kTimeout: slot_run<SPL, kTimeout, 0>(a, sim, P, K, s_tab); break;
+    case kBelady: slot_run<SPL, kBelady, 0>(a, sim, P, K, s_tab); break;
+    default: slot_run<SPL, kEta, 0>(a, sim, P, K, s_tab); break;
+  }
+}
+
 // eq. (hazard) counts over a population of turn counts.
 __global__ __launch_bounds__(256) void hazard_counts_kernel(const uint32_t* turns, uint32_t n,
                                                             uint32_t* d_out, uint32_t* n_out) {
@@ -1990,12 +2460,14 @@ struct Variant {
 // faulted the GPU on a randomised batch without a cause found.
 constexpr Variant kVariants[] = {{16, 1}, {64, 1}, {64, 4}, {0, 0}, {4, 4},
                                  {8, 2},  {-1, 0}, {16, 4}, {32, 8}, {0, 1}, {0, 0}, {0, 0},
-                                 {0, 1}};
+                                 {0, 1},  {0, 2}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kBlock = 256;
 constexpr int kLdsVariant = 9;
 constexpr int kLdsWaveVariant = 12;  // the table in LDS, one wavefront per simulation
 constexpr int kDualVariant = 11;  // streamed, 512 threads, with the dual design's copies
+constexpr int kSlotVariant = 13;  // the table in LDS, residents in VGPR slots, one wavefront
+constexpr uint64_t kSlotMaxResidents = 512;  // 8 slots per lane
 constexpr uint32_t kLdsBytesPerSession = 4 * 8 + 2 * 4;  // mg, last, gq, next; len, kvb
 
 // LDS of the workgroup kernels' residency bits: one bit per session, in whole
@@ -2024,6 +2496,7 @@ static uint32_t block_of(int v) { return v == 10 || v == kDualVariant ? 512u : (
 uint32_t sim_variant_capacity(int v) {
   if (v < 0 || v >= kNumVariants) return 0;
   const uint32_t lim = lds_limit();
+  if (v == kSlotVariant) return lim / kLdsBytesPerSession;  // the table alone
   if (v == kLdsVariant || v == kLdsWaveVariant) {
     // the table and its residency bits
     uint32_t n = lim / kLdsBytesPerSession;
@@ -2052,12 +2525,19 @@ uint32_t sim_variant_lanes(int v) {
 // to its capacity (one wavefront per simulation, which needs no workgroup
 // barriers: C2 163 vs 169 ms with 256 threads), then the 512-thread streamed
 // table.
-int sim_auto_variant(uint32_t max_sess) {
+int sim_auto_variant(uint32_t max_sess, uint64_t max_slots) {
   if (max_sess <= 16) return 5;
   if (max_sess <= 64) return 7;
   if (max_sess <= 256) return 8;
+  if (max_sess <= sim_variant_capacity(kSlotVariant) && max_slots <= kSlotMaxResidents)
+    return kSlotVariant;
   if (max_sess <= sim_variant_capacity(kLdsWaveVariant)) return kLdsWaveVariant;
   return 10;
+}
+
+// Whether a variant can run simulations whose N_sess reaches max_slots.
+bool sim_variant_slots_ok(int v, uint64_t max_slots) {
+  return v != kSlotVariant || max_slots <= kSlotMaxResidents;
 }
 
 // The streamed-table kernels' resident cache: slots per thread of 8 + 8 + 8
@@ -2086,10 +2566,24 @@ static void launch_regs(const SimArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((sim_regs_kernel<G, EPL>), dim3(blocks), dim3(256), 0, stream, a);
 }
 
-hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream,
-                      int force_variant, int force_cache_slots) {
-  const int v = force_variant >= 0 ? force_variant : sim_auto_variant(max_sess_in_batch);
+template <int SPL>
+static void launch_slots(const SimArgs& a, uint32_t max_sess_in_batch, hipStream_t stream) {
+  const uint32_t n = max_sess_in_batch ? max_sess_in_batch : 1;
+  hipLaunchKernelGGL((sim_slot_kernel<SPL>), dim3(a.n_sims), dim3(64), (size_t)n * kLdsBytesPerSession,
+                     stream, a);
+}
+
+hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, uint64_t max_slots,
+                      hipStream_t stream, int force_variant, int force_cache_slots) {
+  const int v = force_variant >= 0 ? force_variant : sim_auto_variant(max_sess_in_batch, max_slots);
   switch (v) {
+    case kSlotVariant:
+      if (max_slots <= 64) launch_slots<1>(a, max_sess_in_batch, stream);
+      else if (max_slots <= 128) launch_slots<2>(a, max_sess_in_batch, stream);
+      else if (max_slots <= 256) launch_slots<4>(a, max_sess_in_batch, stream);
+      else if (max_slots <= kSlotMaxResidents) launch_slots<8>(a, max_sess_in_batch, stream);
+      else return hipErrorInvalidValue;
+      break;
     case 0: launch_regs<16, 1>(a, stream); break;
     case 1: launch_regs<64, 1>(a, stream); break;
     case 2: launch_regs<64, 4>(a, stream); break;

@@ -176,6 +176,25 @@ def test_random_large_batch_on_the_retired_variant():
     compare_counters(s.counters(), oracle_counters(w), label="random large variant 6")
 
 
+@pytest.mark.parametrize("name", sorted(BATCHES))
+def test_random_batches_on_the_slot_kernel(name):
+    """The slot kernel holds residents in VGPR slots sized by N_sess (at
+    most 512): the batches with N_sess capped there, in one launch and split
+    by CONTINUE."""
+    seed, lo, hi, _ = BATCHES[name]
+    w = batch(seed, lo, hi)
+    w.params["n_slots"] = np.minimum(w.params["n_slots"], 512)
+    want = oracle_counters(w)
+    say("random %s on the slot kernel: %d sims" % (name, w.n_sims))
+    s = Sim(w, variant=13)
+    s.run()
+    compare_counters(s.counters(), want, label="random %s slot kernel" % name)
+    longest = max(t.n_events for t in w.traces)
+    s.run(max_events=max(1, longest // 5))
+    s.run(flags=1)
+    compare_counters(s.counters(), want, label="random %s slot kernel split" % name)
+
+
 def test_random_dual_rows():
     w = batch(74, 1, 120, n_traces=6, per_trace=8)
     rng = np.random.Generator(np.random.PCG64(75))

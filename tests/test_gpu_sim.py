@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 RETIRED = pytest.mark.skip(reason="variant 6 (64 x 24) is retired: one of its launches faulted "
                                   "the GPU on a randomised batch and no cause was found; the "
                                   "library refuses it (test_retired_variant_is_refused)")
-VARIANTS = (0, 1, 2, 3, 4, 5, pytest.param(6, marks=RETIRED), 7, 8, 9, 10, 11, 12)
+VARIANTS = (0, 1, 2, 3, 4, 5, pytest.param(6, marks=RETIRED), 7, 8, 9, 10, 11, 12, 13)
 
 
 def say(*a):
@@ -88,7 +88,7 @@ def test_c3_decision_logs(c3):
         assert same_log(s.log(k), oracle_log(c3, i)), "c3 sim %d log" % i
 
 
-@pytest.mark.parametrize("variant", [None, 3, 9, 12, 10])
+@pytest.mark.parametrize("variant", [None, 3, 9, 12, 10, 13])
 def test_continue_matches_single_run(c3, c3_want, variant):
     sims = list(range(5, c3.n_sims, 61))
     w = subset(c3, sims)
@@ -112,13 +112,38 @@ def test_determinism(c3):
     assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
 
 
-def test_c2_paper_scale():
+@pytest.mark.parametrize("variant", [None, 12, 13])
+def test_c2_paper_scale(variant):
     w = synth.c2_paper_scale()
-    say("c2: 4 sims x %d events" % w.traces[0].n_events)
-    s = Sim(w, log_cap=1 << 17)
+    say("c2: 4 sims x %d events, variant %s" % (w.traces[0].n_events, variant))
+    s = Sim(w, log_cap=1 << 17, variant=variant)
     s.run(flags=2)
-    compare_counters(s.counters(), oracle_counters(w), label="c2")
+    compare_counters(s.counters(), oracle_counters(w), label="c2 variant %s" % variant)
     assert same_log(s.log(0), oracle_log(w, 0, log_cap=1 << 17)), "c2 SPEAR log"
+
+
+@pytest.mark.parametrize("slots", [64, 65, 200, 512])
+def test_c2_on_the_slot_kernel_at_each_slot_width(slots):
+    """The slot kernel sizes its VGPR slots by the largest N_sess (1, 2, 4 or
+    8 per lane); every width, across a CONTINUE, against the oracle."""
+    w = synth.c2_paper_scale()
+    w.params["n_slots"] = slots
+    say("c2 slot kernel: N_sess %d" % slots)
+    s = Sim(w, variant=13)
+    n = w.traces[0].n_events
+    s.run(max_events=n // 3)
+    s.run(flags=1)
+    compare_counters(s.counters(), oracle_counters(w), label="c2 slots %d" % slots)
+
+
+def test_slot_kernel_refuses_more_than_512_slots():
+    from paper_2609_09643_amd.unison import E_CAPACITY, UnisonError
+    w = synth.c2_paper_scale()
+    w.params["n_slots"] = 513
+    s = Sim(w, variant=13)
+    with pytest.raises(UnisonError) as e:
+        s.run()
+    assert e.value.code == E_CAPACITY
 
 
 def test_c4_large_live_set_prefix():

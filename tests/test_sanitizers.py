@@ -219,9 +219,10 @@ FATBIN_DEFINITION
 }
 
 namespace unison {
-hipError_t launch_sim(const SimArgs&, uint32_t, hipStream_t, int, int) { return hipSuccess; }
-uint32_t sim_variant_capacity(int v) { return v >= 0 && v <= 12 && v != 6 ? (1u << 20) : 0u; }
-int sim_auto_variant(uint32_t n) { return n <= 16 ? 5 : 10; }
+hipError_t launch_sim(const SimArgs&, uint32_t, uint64_t, hipStream_t, int, int) { return hipSuccess; }
+uint32_t sim_variant_capacity(int v) { return v >= 0 && v <= 13 && v != 6 ? (1u << 20) : 0u; }
+int sim_auto_variant(uint32_t n, uint64_t) { return n <= 16 ? 5 : 10; }
+bool sim_variant_slots_ok(int v, uint64_t s) { return v != 13 || s <= 512; }
 uint32_t sim_variant_lanes(int v) { return v == 5 ? 8u : 0u; }
 hipError_t launch_hazard_counts(const uint32_t*, uint32_t, uint32_t*, uint32_t*, hipStream_t) {
   return hipSuccess;
