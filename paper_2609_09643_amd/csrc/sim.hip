@@ -111,6 +111,55 @@ __device__ __forceinline__ Cand reduce_group(Cand c) {
   return c;
 }
 
+// Whole-wavefront max (MAX) or min of a 32-bit value, uniform: a DPP
+// butterfly inside each row of 16 lanes, then the four row results compared
+// in scalar registers (no cross-row permute through the LDS crossbar).
+template <bool MAX>
+__device__ __forceinline__ uint32_t ext32(uint32_t a, uint32_t b) {
+  return MAX ? (a > b ? a : b) : (a < b ? a : b);
+}
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_ext32(uint32_t v) {
+  v = ext32<MAX>(v, xchg<1>(v));
+  v = ext32<MAX>(v, xchg<2>(v));
+  v = ext32<MAX>(v, xchg<4>(v));
+  v = ext32<MAX>(v, xchg<8>(v));
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+  const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+  return ext32<MAX>(ext32<MAX>(r0, r1), ext32<MAX>(r2, r3));
+}
+// One phase of a lexicographic wavefront reduction over N words per lane:
+// the best word M among the active ones; with NARROW, a word stays active
+// only where it equals M, so the next phase breaks the ties.
+template <bool MAX, bool NARROW, int N>
+__device__ __forceinline__ uint32_t lex_phase(const uint32_t (&w)[N], bool (&act)[N]) {
+  uint32_t v = MAX ? 0u : ~0u;
+#pragma unroll
+  for (int k = 0; k < N; ++k) v = act[k] ? ext32<MAX>(v, w[k]) : v;
+  const uint32_t m = wave_ext32<MAX>(v);
+  if constexpr (NARROW) {
+#pragma unroll
+    for (int k = 0; k < N; ++k) act[k] = act[k] && w[k] == m;
+  }
+  return m;
+}
+
+// Sum mod 2^64 over the wavefront; every lane ends with it.
+__device__ __forceinline__ uint64_t wave_sum64_step(uint64_t v, uint32_t lo, uint32_t hi) {
+  return v + (((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
+  v = wave_sum64_step(v, xchg<1>((uint32_t)v), xchg<1>((uint32_t)(v >> 32)));
+  v = wave_sum64_step(v, xchg<2>((uint32_t)v), xchg<2>((uint32_t)(v >> 32)));
+  v = wave_sum64_step(v, xchg<4>((uint32_t)v), xchg<4>((uint32_t)(v >> 32)));
+  v = wave_sum64_step(v, xchg<8>((uint32_t)v), xchg<8>((uint32_t)(v >> 32)));
+  v = wave_sum64_step(v, xchg<16>((uint32_t)v), xchg<16>((uint32_t)(v >> 32)));
+  v = wave_sum64_step(v, xchg<32>((uint32_t)v), xchg<32>((uint32_t)(v >> 32)));
+  return v;
+}
+
 // Pins a value to a vector register.  A workgroup-per-simulation kernel keeps
 // its long-lived per-simulation state (pool usage, counters) there: held in
 // scalar registers it would exceed them and spill on every event.
@@ -130,6 +179,15 @@ __device__ __forceinline__ uint32_t uni32(uint32_t v) {
 }
 __device__ __forceinline__ uint64_t uni64(uint64_t v) {
   return ((uint64_t)uni32((uint32_t)(v >> 32)) << 32) | uni32((uint32_t)v);
+}
+// A condition every lane of the wavefront evaluates alike (UNI), as a scalar
+// branch condition: values pinned to vector registers would otherwise make
+// the compiler treat the branch as divergent (exec masking, merges of every
+// live value at the join).
+template <bool UNI>
+__device__ __forceinline__ bool uc(bool c) {
+  if constexpr (UNI) return __builtin_amdgcn_ballot_w64(c) != 0ull;
+  else return c;
 }
 
 // ------------------------------------------------------------ keys
@@ -347,6 +405,7 @@ struct RegTable {
   // Gap onsets reduce their scan victim and TIDE's candidates separately:
   // fusing the three reductions made this kernel slower (0.518 vs 0.498 ms).
   static constexpr bool kFuseGap = false;
+  static constexpr bool kLaneDigest = false;
   template <bool N, bool T>
   using Reader = AheadReader<N, T>;
   uint32_t lane;
@@ -613,6 +672,7 @@ struct MemTable {
   // A gap onset's scan and TIDE's first candidates share one pass and one
   // barrier (the dual design scans different copies for the two engines).
   static constexpr bool kFuseGap = !VIEWS;
+  static constexpr bool kLaneDigest = false;
   template <bool N, bool T>
   using Reader = AheadReader<N, T>;
   uint64_t* mg;
@@ -1132,6 +1192,8 @@ struct SlotTable {
   using PT = Pol<POL, SMODE>;
   static constexpr bool kViews = false;
   static constexpr bool kFuseGap = true;
+  // Digest terms are queued one per lane and hashed 64 at a time.
+  static constexpr bool kLaneDigest = true;
   template <bool N, bool T>
   using Reader = WindowReader<N, T>;  // events come 64 to a window, one per lane
   uint64_t* mg;
@@ -1146,10 +1208,17 @@ struct SlotTable {
   uint32_t smeta[SPL];
   uint64_t skey[SPL];
   uint64_t ssize[SPL];
-  // the entry of the latest write(): its key and KV bytes per token
+  // the entry of the latest write(): its key, KV bytes per token and length
   uint32_t w_sid;
   uint64_t w_key;
-  uint32_t w_kvb;
+  uint32_t w_kvb, w_len;
+  // Queued digest terms.  Record j of the current batch sits in lane j (event,
+  // op, a, b); q_sum is the lane's sum of hashed records.  The scan victim of
+  // event v_e0 + j sits in lane j; v_sum is the lane's sum of weighted victims.
+  uint32_t q_ev, q_op, q_a, q_b, q_n;
+  uint64_t q_sum;
+  uint32_t v_sid, v_n;
+  uint64_t v_e0, v_sum;
 
   __device__ __forceinline__ uint64_t key_from(uint32_t m, float g, uint64_t q, uint64_t l,
                                                uint64_t n) const {
@@ -1233,7 +1302,7 @@ struct SlotTable {
       uint64_t key, size;
       if (sid == w_sid) {
         key = w_key;
-        size = (uint64_t)uni32(len[sid]) * w_kvb;
+        size = (uint64_t)w_len * w_kvb;
       } else {
         key = uni64(key_at(sid));
         size = (uint64_t)uni32(len[sid]) * uni32(kvb[sid]);
@@ -1244,6 +1313,52 @@ struct SlotTable {
 
   __device__ __forceinline__ void event_begin() {}
   __device__ __forceinline__ void grow(uint32_t) {}
+
+  __device__ __forceinline__ void queue_init() {
+    q_ev = q_op = q_a = q_b = 0u;
+    q_n = 0u;
+    q_sum = 0ull;
+    v_sid = 0u;
+    v_n = 0u;
+    v_e0 = 0ull;
+    v_sum = 0ull;
+  }
+  __device__ __forceinline__ void flush_records() {
+    if (lane < q_n) q_sum += rec_hash(q_ev, q_op, q_a, q_b);
+    q_n = 0u;
+  }
+  __device__ __forceinline__ void queue_record(uint32_t ev, uint32_t op, uint32_t a, uint32_t b) {
+    const bool mine = lane == q_n;
+    q_ev = mine ? ev : q_ev;
+    q_op = mine ? op : q_op;
+    q_a = mine ? a : q_a;
+    q_b = mine ? b : q_b;
+    if (++q_n == 64u) flush_records();
+  }
+  // The victim digest weighs event e's victim id + 1 by (2e + 1) * 0x9e3779b97f4a7c15.
+  __device__ __forceinline__ void flush_victims() {
+    if (lane < v_n) {
+      const uint64_t e = v_e0 + lane;
+      v_sum += ((uint64_t)v_sid + 1u) * ((2ull * e + 1ull) * 0x9e3779b97f4a7c15ull);
+    }
+    v_n = 0u;
+  }
+  // Events reach the queue in order, one victim each.
+  __device__ __forceinline__ void queue_victim(uint64_t e, uint32_t sid) {
+    if (v_n == 0u) v_e0 = e;
+    v_sid = lane == v_n ? sid : v_sid;
+    if (++v_n == 64u) flush_victims();
+  }
+  // Every queued term, summed over the wavefront mod 2^64: the record digest
+  // and the victim digest still to add.
+  __device__ __forceinline__ void drain(uint64_t& digest, uint64_t& victim_digest) {
+    flush_records();
+    flush_victims();
+    digest = uni64(wave_sum64(q_sum));
+    victim_digest = uni64(wave_sum64(v_sum));
+    q_sum = 0ull;
+    v_sum = 0ull;
+  }
 
   __device__ __forceinline__ Entry read(uint32_t sid) const {
     Entry e;
@@ -1296,70 +1411,136 @@ struct SlotTable {
     w_sid = sid;
     w_key = key_from(e.meta, e.g, e.gq, e.last, e.next);
     w_kvb = e.kvb;
+    w_len = e.len;
     uint32_t j, l;
     if (find(sid, j, l)) set_slot_key(j, l, e.meta, w_key);
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) { meta_to(sid, m); }
   __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
     if (lane == 0) len[sid] = l;
+    if (sid == w_sid) w_len = l;
     meta_to(sid, m);
   }
   __device__ __forceinline__ void set_turn(uint32_t, uint32_t, const KeyCtx&) {}
   __device__ __forceinline__ void scan(const KeyCtx&, uint32_t) {}
 
-  __device__ __forceinline__ static Cand uniform(const Cand& c) { return Cand{uni64(c.key), uni32(c.sid)}; }
+  // Candidates reduce as one 64-bit word where the key allows: an fp32 score
+  // above the id (complemented for argmax, so ties go to the smaller id), or a
+  // time below 2^44 above a 20-bit id; other keys reduce as (key, id) pairs.
+  // 0 and 2^64 - 1 stay free as the empty values (ids stay far below 2^20 - 1:
+  // the table is LDS-resident).
+  static constexpr uint64_t kCap44 = (1ull << 44) - 1;
+  __device__ __forceinline__ int pack_mode() const {
+    if constexpr (PT::spear && !PT::fixed) return 1;
+    if constexpr (PT::recency || PT::belady) return kc.pack44 ? 2 : 0;
+    return 0;
+  }
+  template <bool MAX>
+  __device__ __forceinline__ static uint64_t pack(int mode, uint64_t key, uint32_t sid) {
+    if (mode == 1) return (key << 32) | (MAX ? 0xFFFFFFFFu - sid : sid);
+    uint64_t k44;
+    if constexpr (PT::belady) k44 = key < kCap44 ? key : kCap44;
+    else k44 = key & kCap44;  // recency: key = 2^64 - 1 - last, last below 2^44 - 1
+    return (k44 << 20) | (MAX ? 0xFFFFFu - sid : sid);
+  }
+  template <bool MAX>
+  __device__ __forceinline__ static Cand unpack(int mode, uint64_t c) {
+    const bool none = MAX ? c == 0ull : c == ~0ull;
+    if (mode == 1) {
+      const uint32_t lo = (uint32_t)c;
+      return Cand{c >> 32, none ? kNone : (MAX ? 0xFFFFFFFFu - lo : lo)};
+    }
+    const uint32_t lo = (uint32_t)c & 0xFFFFFu;
+    const uint64_t k44 = c >> 20;
+    uint64_t key;
+    if constexpr (PT::belady) key = k44 == kCap44 ? ~0ull : k44;
+    else key = k44 | ~kCap44;
+    return Cand{key, none ? kNone : (MAX ? 0xFFFFFu - lo : lo)};
+  }
+  __device__ __forceinline__ bool eligible(int k, uint32_t tier) const {
+    const uint32_t m = smeta[k];
+    return ssid[k] != kNone && meta_phase(m) != kServing && (tier == 0 || meta_tier(m) == tier);
+  }
+
+  // Up to three reductions over the slots side by side: argmax over tier ta
+  // (A), argmin over tier tb (B), argmax over tier tc (C).  Each compares its
+  // candidates as a string of 32-bit words, most significant first -- the
+  // packed key's two halves, or a wide key's two halves and then the id -- one
+  // wavefront max / min per word.  The id enters complemented for argmax, so
+  // both directions break ties towards the smaller id, and an id word never
+  // equals the empty value: no candidate leaves it at 0 (argmax) or at
+  // 2^32 - 1 (argmin).
+  template <bool A, bool B, bool C>
+  __device__ __forceinline__ void reduce3(uint32_t ta, uint32_t tb, uint32_t tc, Cand& ra, Cand& rb,
+                                          Cand& rc) const {
+    const int mode = pack_mode();
+    bool aa[SPL], ab[SPL], ac[SPL];
+    uint32_t hi[SPL], lox[SPL], lon[SPL], idx[SPL], idn[SPL];
+#pragma unroll
+    for (int k = 0; k < SPL; ++k) {
+      aa[k] = A && eligible(k, ta);
+      ab[k] = B && eligible(k, tb);
+      ac[k] = C && eligible(k, tc);
+      const uint64_t key = skey[k];
+      const uint32_t sid = ssid[k];
+      idx[k] = ~sid;
+      idn[k] = sid;
+      if (mode == 1) {
+        hi[k] = (uint32_t)key;
+        lox[k] = ~sid;
+        lon[k] = sid;
+      } else if (mode == 2) {
+        uint64_t k44;
+        if constexpr (PT::belady) k44 = key < kCap44 ? key : kCap44;
+        else k44 = key & kCap44;  // recency: key = 2^64 - 1 - last, last below 2^44 - 1
+        hi[k] = (uint32_t)(k44 >> 12);
+        const uint32_t base = (uint32_t)k44 << 20;
+        lox[k] = base | (0xFFFFFu - sid);
+        lon[k] = base | sid;
+      } else {
+        hi[k] = (uint32_t)(key >> 32);
+        lox[k] = (uint32_t)key;
+        lon[k] = (uint32_t)key;
+      }
+    }
+    uint32_t a0 = 0, a1 = 0, a2 = 0, b0 = 0, b1 = 0, b2 = 0, c0 = 0, c1 = 0, c2 = 0;
+    if (A) a0 = lex_phase<true, true>(hi, aa);
+    if (B) b0 = lex_phase<false, true>(hi, ab);
+    if (C) c0 = lex_phase<true, true>(hi, ac);
+    if (mode) {
+      if (A) a1 = lex_phase<true, false>(lox, aa);
+      if (B) b1 = lex_phase<false, false>(lon, ab);
+      if (C) c1 = lex_phase<true, false>(lox, ac);
+      if (A) ra = unpack<true>(mode, ((uint64_t)a0 << 32) | a1);
+      if (B) rb = unpack<false>(mode, ((uint64_t)b0 << 32) | b1);
+      if (C) rc = unpack<true>(mode, ((uint64_t)c0 << 32) | c1);
+      return;
+    }
+    if (A) a1 = lex_phase<true, true>(lox, aa);
+    if (B) b1 = lex_phase<false, true>(lon, ab);
+    if (C) c1 = lex_phase<true, true>(lox, ac);
+    if (A) a2 = lex_phase<true, false>(idx, aa);
+    if (B) b2 = lex_phase<false, false>(idn, ab);
+    if (C) c2 = lex_phase<true, false>(idx, ac);
+    if (A) ra = Cand{((uint64_t)a0 << 32) | a1, a2 == 0u ? kNone : ~a2};
+    if (B) rb = Cand{((uint64_t)b0 << 32) | b1, b2};
+    if (C) rc = Cand{((uint64_t)c0 << 32) | c1, c2 == 0u ? kNone : ~c2};
+  }
 
   template <bool MAX>
   __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx&) const {
-    Cand c = MAX ? cand_none_max() : cand_none_min();
-#pragma unroll
-    for (int k = 0; k < SPL; ++k) {
-      const uint32_t m = smeta[k];
-      const bool ok = ssid[k] != kNone && meta_phase(m) != kServing &&
-                      (tier == 0 || meta_tier(m) == tier);
-      const bool take = ok && (MAX ? max_better(skey[k], ssid[k], c.key, c.sid)
-                                   : min_better(skey[k], ssid[k], c.key, c.sid));
-      c.key = take ? skey[k] : c.key;
-      c.sid = take ? ssid[k] : c.sid;
-    }
-    return uniform(reduce_group<64, MAX>(c));
+    Cand r, unused;
+    if constexpr (MAX) reduce3<true, false, false>(tier, 0, 0, r, unused, unused);
+    else reduce3<false, true, false>(0, tier, 0, unused, r, unused);
+    return r;
   }
   __device__ __forceinline__ Cand argmax_first(const KeyCtx& K) const { return select<true>(0, K); }
   __device__ __forceinline__ void select_pd(const KeyCtx&, Cand& p, Cand& d) const {
-    Cand cp = cand_none_min(), cd = cand_none_max();
-#pragma unroll
-    for (int k = 0; k < SPL; ++k) {
-      const uint32_t m = smeta[k];
-      const bool ev = ssid[k] != kNone && meta_phase(m) != kServing;
-      const bool tp = ev && meta_tier(m) == kTierHbm && min_better(skey[k], ssid[k], cp.key, cp.sid);
-      const bool td = ev && meta_tier(m) == kTierSram && max_better(skey[k], ssid[k], cd.key, cd.sid);
-      cp.key = tp ? skey[k] : cp.key;
-      cp.sid = tp ? ssid[k] : cp.sid;
-      cd.key = td ? skey[k] : cd.key;
-      cd.sid = td ? ssid[k] : cd.sid;
-    }
-    p = uniform(reduce_group<64, false>(cp));
-    d = uniform(reduce_group<64, true>(cd));
+    Cand unused;
+    reduce3<false, true, true>(0, kTierHbm, kTierSram, unused, p, d);
   }
   __device__ __forceinline__ void scan3(const KeyCtx&, Cand& v, Cand& p, Cand& d) const {
-    Cand cv = cand_none_max(), cp = cand_none_min(), cd = cand_none_max();
-#pragma unroll
-    for (int k = 0; k < SPL; ++k) {
-      const uint32_t m = smeta[k];
-      const bool ev = ssid[k] != kNone && meta_phase(m) != kServing;
-      const bool tv = ev && max_better(skey[k], ssid[k], cv.key, cv.sid);
-      const bool tp = ev && meta_tier(m) == kTierHbm && min_better(skey[k], ssid[k], cp.key, cp.sid);
-      const bool td = ev && meta_tier(m) == kTierSram && max_better(skey[k], ssid[k], cd.key, cd.sid);
-      cv.key = tv ? skey[k] : cv.key;
-      cv.sid = tv ? ssid[k] : cv.sid;
-      cp.key = tp ? skey[k] : cp.key;
-      cp.sid = tp ? ssid[k] : cp.sid;
-      cd.key = td ? skey[k] : cd.key;
-      cd.sid = td ? ssid[k] : cd.sid;
-    }
-    v = uniform(reduce_group<64, true>(cv));
-    p = uniform(reduce_group<64, false>(cp));
-    d = uniform(reduce_group<64, true>(cd));
+    reduce3<true, true, true>(0, kTierHbm, kTierSram, v, p, d);
   }
 
   // Online hazard table: add the completed session, then rescore every resident.
@@ -1531,9 +1712,11 @@ struct LogSink {
   bool victims;        // also record each event's scan result
 };
 
-__device__ __forceinline__ void emit(Cnt& C, Scalars& S, const LogSink& L, uint32_t ev, uint32_t op,
-                                     uint32_t a, uint32_t b) {
-  C.digest += rec_hash(ev, op, a, b);
+template <class Tab>
+__device__ __forceinline__ void emit(Tab& T, Cnt& C, Scalars& S, const LogSink& L, uint32_t ev,
+                                     uint32_t op, uint32_t a, uint32_t b) {
+  if constexpr (Tab::kLaneDigest) T.queue_record(ev, op, a, b);
+  else C.digest += rec_hash(ev, op, a, b);
   if (L.on) {
     if (L.lead && S.log_len < L.cap) {
       unison_record r;
@@ -1589,7 +1772,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       for (;;) {
         const uint32_t v = T.first_idle(now, P.ttl_ns);
         if (v == kNone) break;
-        emit(C, S, L, ev, kOpExpire, v, kNone);
+        emit(T, C, S, L, ev, kOpExpire, v, kNone);
         C.expire++;
         release(T, S, v);
       }
@@ -1612,7 +1795,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       } else {
         const uint64_t gap = now - x.last;  // eq. (gap)
         // only SPEAR keys and TIDE budgets read the gap EMA
-        if (PT::spear || PT::belady || P.tide) x.g = ema_f32(x.g, gap);
+        if (PT::spear || PT::belady || uc<UNI>(P.tide != 0)) x.g = ema_f32(x.g, gap);
         if constexpr (PT::fixed) x.gq = ema_int(x.gq, gap, P.b_g, P.tau_ns);
       }
       x.meta = make_meta(kServing, tier0, turn);
@@ -1648,7 +1831,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
     Cand v0, p0, d0;
     bool have_pd = false;
     if constexpr (Tab::kFuseGap) {
-      if (kind == kGapStart && P.tide) {
+      if (kind == kGapStart && uc<UNI>(P.tide != 0)) {
         T.scan3(K, v0, p0, d0);
         have_pd = true;
       } else {
@@ -1658,8 +1841,12 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       v0 = T.argmax_first(K);
     }
     // odd weight per event: a different victim at any one event changes the sum
-    C.victim_digest += ((uint64_t)v0.sid + 1u) * vw;
-    vw += 2ull * kGolden;
+    if constexpr (Tab::kLaneDigest) {
+      T.queue_victim(e, v0.sid);
+    } else {
+      C.victim_digest += ((uint64_t)v0.sid + 1u) * vw;
+      vw += 2ull * kGolden;
+    }
     if (L.victims) {
       if (L.lead && S.log_len < L.cap) L.rec[S.log_len] = unison_record{ev, kOpVictim, v0.sid, kNone};
       S.log_len++;
@@ -1703,8 +1890,8 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       const uint64_t size = ln * kb;
       const uint32_t pref = tier0 == kTierHbm ? kTierHbm : kTierSram;
       const uint32_t other = pref == kTierSram ? kTierHbm : kTierSram;
-      if (size > P.cap_sram_B && size > P.cap_hbm_B) {
-        emit(C, S, L, ev, kOpBypass, sid, kNone);
+      if (uc<UNI>(size > P.cap_sram_B && size > P.cap_hbm_B)) {
+        emit(T, C, S, L, ev, kOpBypass, sid, kNone);
         C.bypass++;
       } else {
         bool first = true;
@@ -1714,12 +1901,12 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
           const bool fit_h = slot && S.used_h + size <= P.cap_hbm_B;
           const bool fit_p = pref == kTierSram ? fit_s : fit_h;
           const bool fit_o = pref == kTierSram ? fit_h : fit_s;
-          if (fit_p || fit_o) {
+          if (uc<UNI>(fit_p || fit_o)) {
             const uint32_t t = fit_p ? pref : other;
             if (t == kTierSram) S.used_s += size; else S.used_h += size;
             S.n_res++;
             T.set_meta(sid, with_tier(x.meta, t));
-            emit(C, S, L, ev, kOpPlace, sid, t);
+            emit(T, C, S, L, ev, kOpPlace, sid, t);
             break;
           }
           // the event's own scan result is the first victim: the arriving
@@ -1741,22 +1928,26 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
             }
           }
           if (v.sid == kNone) {
-            emit(C, S, L, ev, kOpBypass, sid, kNone);
+            emit(T, C, S, L, ev, kOpBypass, sid, kNone);
             C.bypass++;
             break;
           }
-          emit(C, S, L, ev, kOpEvict, v.sid, kNone);
+          emit(T, C, S, L, ev, kOpEvict, v.sid, kNone);
           C.evict++;
           release(T, S, v.sid);
         }
       }
     } else if (kind == kGapStart) {
-      if (P.tide && now >= S.dma_free_at) {
+      if (uc<UNI>(P.tide && now >= S.dma_free_at)) {
         // eq. (budget) / eq. (budgetq): Delta is the session's gap EMA in us
         uint64_t delta_us;
         if constexpr (PT::fixed) {
-          const unsigned __int128 d = ((unsigned __int128)x.gq * P.tau_ns) / 1000u;
-          delta_us = d > (unsigned __int128)~0ull ? ~0ull : (uint64_t)d;
+          if (x.gq < (1ull << 32) && P.tau_ns < (1ull << 32)) {
+            delta_us = (x.gq * P.tau_ns) / 1000u;
+          } else {
+            const unsigned __int128 d = ((unsigned __int128)x.gq * P.tau_ns) / 1000u;
+            delta_us = d > (unsigned __int128)~0ull ? ~0ull : (uint64_t)d;
+          }
         } else {
           delta_us = (uint64_t)x.g;
         }
@@ -1786,13 +1977,13 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
           uint64_t sp;
           uint32_t mp;
           T.read_size(p.sid, sp, mp);
-          if (S.used_s + sp <= P.cap_sram_B && sp <= left) {
+          if (uc<UNI>(S.used_s + sp <= P.cap_sram_B && sp <= left)) {
             S.used_h -= sp;
             S.used_s += sp;
             T.set_meta(p.sid, with_tier(mp, kTierSram) | kPrefetched);
             left -= sp;
             moved += sp;
-            emit(C, S, L, ev, kOpPromote, p.sid, kNone);
+            emit(T, C, S, L, ev, kOpPromote, p.sid, kNone);
             C.promote++;
             C.prom_diff += live_p != p.sid ? 1u : 0u;
             continue;
@@ -1803,23 +1994,20 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
           T.read_size(d.sid, sd, md);
           const bool legal = p.key < d.key && sp <= left && sd <= left - sp &&
                              S.used_s - sd + sp <= P.cap_sram_B && S.used_h - sp + sd <= P.cap_hbm_B;
-          if (!legal) break;
+          if (!uc<UNI>(legal)) break;
           S.used_s = S.used_s - sd + sp;
           S.used_h = S.used_h - sp + sd;
           T.set_meta(p.sid, with_tier(mp, kTierSram) | kPrefetched);
           T.set_meta(d.sid, with_tier(md, kTierHbm));
           left -= sp + sd;
           moved += sp + sd;
-          emit(C, S, L, ev, kOpSwap, p.sid, d.sid);
+          emit(T, C, S, L, ev, kOpSwap, p.sid, d.sid);
           C.swap++;
           C.prom_diff += live_p != p.sid ? 1u : 0u;
         }
-        if (moved) {
+        if (uc<UNI>(moved != 0)) {
           // DMA busy for ceil(moved * 1000 / B) ns
-          const unsigned __int128 ns =
-              ((unsigned __int128)moved * 1000u + P.dma_B_per_us - 1u) / P.dma_B_per_us;
-          const unsigned __int128 fin = (unsigned __int128)now + ns;
-          S.dma_free_at = fin > (unsigned __int128)~0ull ? ~0ull : (uint64_t)fin;
+          S.dma_free_at = sat_add(now, dma_ns(moved, P.dma_B_per_us));
         }
         C.dma_bytes += moved;
       }
@@ -2262,6 +2450,8 @@ __device__ __forceinline__ void slot_run(const SimArgs& a, uint32_t sim, const u
   T.w_sid = kNone;
   T.w_key = 0;
   T.w_kvb = 0;
+  T.w_len = 0;
+  T.queue_init();
 #pragma unroll
   for (int k = 0; k < SPL; ++k) {
     T.ssid[k] = kNone;
@@ -2318,6 +2508,10 @@ __device__ __forceinline__ void slot_run(const SimArgs& a, uint32_t sim, const u
     pin_vgpr(Pv);
     run_events<POL, SMODE, true>(T, Pv, K, tr, S, C, L, next_event, a.max_events,
                                  a.first_bad[P.trace]);
+    uint64_t dg, vd;
+    T.drain(dg, vd);
+    C.digest += dg;
+    C.victim_digest += vd;
   }
   __syncthreads();
   for (uint32_t i = lane; i < n; i += 64) {

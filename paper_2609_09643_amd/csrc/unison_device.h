@@ -67,6 +67,16 @@ __device__ __forceinline__ uint64_t sat_add(uint64_t a, uint64_t b) {
   return s < a ? ~0ull : s;
 }
 
+// DMA busy time of `bytes` at b bytes/us: ceil(bytes * 1000 / b) ns, b > 0.
+// Below 2^53 both the numerator and the divisor fit 64 bits (the quotient
+// then needs no 128-bit division, which the compiler expands into a
+// bit-serial loop); larger values take the 128-bit form, saturated.
+__device__ __forceinline__ uint64_t dma_ns(uint64_t bytes, uint64_t b) {
+  if (bytes < (1ull << 53) && b < (1ull << 53)) return (bytes * 1000u + b - 1u) / b;
+  const unsigned __int128 q = ((unsigned __int128)bytes * 1000u + b - 1u) / b;
+  return q > (unsigned __int128)~0ull ? ~0ull : (uint64_t)q;
+}
+
 // a * b saturated to 2^64 - 1.
 __device__ __forceinline__ uint64_t sat_mul(uint64_t a, uint64_t b) {
   return __umul64hi(a, b) ? ~0ull : a * b;
