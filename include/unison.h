@@ -293,10 +293,13 @@ int unison_set_params(unison_ctx* ctx, const unison_sim_params* params);
  * reads, such as the gap EMA of LRU or timeout without TIDE, is not kept).
  * policy_override is a UNISON_POLICY_* value applied to all simulations, or
  * UNISON_POLICY_PARAMS.  A batch with a dual-design row runs on the copies'
- * kernel (variant 11).  Tables above the LDS-resident size run on workgroup
- * kernels that keep one bit of LDS per session (the residency bits their
- * scans visit): 128 KiB at UNISON_MAX_SESSIONS; the LDS left holds up to 8
- * resident-cache slots of 28 B per thread.  Asynchronous.
+ * kernel (variant 11).  Tables above the LDS-resident size run, while no
+ * simulation can hold more than 4,096 residents (min(N_sess, sessions)), on
+ * one wavefront per simulation with the residents in 24-byte LDS slots
+ * (variant 14); otherwise on workgroup kernels that keep one bit of LDS per
+ * session (the residency bits their scans visit): 128 KiB at
+ * UNISON_MAX_SESSIONS; the LDS left holds up to 8 resident-cache slots of
+ * 28 B per thread.  Asynchronous.
  * Errors: UNISON_E_NOT_READY (also: an ETA simulation whose trace has no ETA
  * table), UNISON_E_INVALID (also: a register-table
  * variant forced on a batch with a dual-design row), UNISON_E_CAPACITY (the
@@ -367,14 +370,18 @@ int unison_kendall(void* hip_stream, uint32_t n_snap, uint32_t n_per, uint64_t n
 int unison_read_hazard(unison_ctx* ctx, uint32_t sim, uint32_t* d_out, uint32_t* n_out);
 
 /* Test hook: pins the simulation kernel variant (-1 = chosen by the largest
- * trace; register tables of lanes x sessions per lane 0: 16 x 1, 1: 64 x 1,
- * 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 7: 16 x 4, 8: 32 x 8 (6 is retired); one
- * workgroup per simulation with the table 3: streamed from the workspace by
- * 256 threads, 10: by 512 threads, 9: held in LDS (256 threads), 12: held in
- * LDS by one wavefront, 11: streamed by 512 threads with the dual design's
- * copies -- the only variant for a batch with
- * a dual-design row).  A variant too small for the traces, or an unknown id,
- * makes unison_run return UNISON_E_CAPACITY. */
+ * trace and the largest resident count; register tables of lanes x sessions
+ * per lane 0: 16 x 1, 1: 64 x 1, 2: 64 x 4, 4: 4 x 4, 5: 8 x 2, 7: 16 x 4,
+ * 8: 32 x 8 (6 is retired); one workgroup per simulation with the table 3:
+ * streamed from the workspace by 256 threads, 10: by 512 threads, 9: held in
+ * LDS (256 threads), 12: held in LDS by one wavefront, 11: streamed by 512
+ * threads with the dual design's copies -- the only variant for a batch with
+ * a dual-design row; one wavefront per simulation with 13: the table in LDS
+ * and the residents in 1 to 8 vector-register slots per lane (at most 512
+ * residents), 14: the table in the workspace and the residents in LDS slots
+ * (at most 4,096 residents)).  A variant too small for the traces or their
+ * resident counts, or an unknown id, makes unison_run return
+ * UNISON_E_CAPACITY. */
 int unison_debug_force_variant(unison_ctx* ctx, int variant);
 
 /* Test hook: at most `slots` resident-cache slots per thread for the streamed

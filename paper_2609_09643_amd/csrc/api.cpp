@@ -24,6 +24,7 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, uint64_t max
 uint32_t sim_variant_capacity(int v);
 int sim_auto_variant(uint32_t max_sess, uint64_t max_slots);
 bool sim_variant_slots_ok(int v, uint64_t max_slots);
+uint64_t sim_variant_max_slots(int v);
 uint32_t sim_variant_lanes(int v);
 hipError_t launch_hazard_counts(const uint32_t* turns, uint32_t n, uint32_t* d, uint32_t* nn,
                                 hipStream_t stream);
@@ -59,7 +60,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // Workspace layout; offsets in bytes from the workspace base.
 struct Layout {
   size_t params, ev_off, first_bad, sess_off, lut_d, lut_n, eta, state, counters, hcount, mg, gq, len,
-      last, next, views, log, slots, scratch, total;
+      last, next, slot, views, log, slots, scratch, total;
 };
 
 bool make_layout(const unison_dims& d, Layout& L) {
@@ -85,6 +86,7 @@ bool make_layout(const unison_dims& d, Layout& L) {
   L.len = take(sizeof(uint32_t) * entries);
   L.last = take(sizeof(uint64_t) * entries);
   L.next = take(sizeof(uint64_t) * entries);
+  L.slot = take(sizeof(uint32_t) * entries);
   L.views = take(d.views ? sizeof(uint64_t) * 8 * entries : 0);
   L.log = take(sizeof(unison_record) * (size_t)d.log_cap * d.n_sims);
   // register-table lane groups -> simulations: at most one partly filled
@@ -577,6 +579,7 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   a.t_len = ctx->at<uint32_t>(ctx->L.len);
   a.t_last = ctx->at<uint64_t>(ctx->L.last);
   a.t_next = ctx->at<uint64_t>(ctx->L.next);
+  a.t_slot = ctx->at<uint32_t>(ctx->L.slot);
   a.log = ctx->dims.log_cap ? ctx->at<unison_record>(ctx->L.log) : nullptr;
   a.hcount = ctx->at<uint32_t>(ctx->L.hcount);
   a.views = ctx->dims.views ? ctx->at<uint64_t>(ctx->L.views) : nullptr;
@@ -597,11 +600,13 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
   if (v >= 0 && (sim_variant_capacity(v) == 0 || sim_variant_capacity(v) < ctx->max_sess_batch))
     return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds %u sessions < %u", v,
                      sim_variant_capacity(v), ctx->max_sess_batch);
-  if (v >= 0 && !sim_variant_slots_ok(v, ctx->max_slots_batch))
-    return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds N_sess up to 512, not %llu", v,
-                     (unsigned long long)ctx->max_slots_batch);
+  // residents never exceed min(N_sess, sessions) of a simulation
+  const uint64_t max_res = std::min<uint64_t>(ctx->max_slots_batch, ctx->max_sess_batch);
+  if (v >= 0 && !sim_variant_slots_ok(v, max_res))
+    return ctx->fail(UNISON_E_CAPACITY, "forced kernel variant %d holds up to %llu residents, not %llu", v,
+                     (unsigned long long)sim_variant_max_slots(v), (unsigned long long)max_res);
   if (v < 0) {
-    v = sim_auto_variant(ctx->max_sess_batch, ctx->max_slots_batch);
+    v = sim_auto_variant(ctx->max_sess_batch, max_res);
     if (sim_variant_capacity(v) < ctx->max_sess_batch)
       return ctx->fail(UNISON_E_CAPACITY, "%u sessions exceed every kernel variant (largest %u)",
                        ctx->max_sess_batch, sim_variant_capacity(v));
@@ -616,7 +621,7 @@ int unison_run(unison_ctx* ctx, uint32_t policy_override, uint32_t flags, uint64
       a.n_slots = ctx->n_slots;
     }
   }
-  int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, ctx->max_slots_batch, ctx->stream, v,
+  int rc = ctx->hip(launch_sim(a, ctx->max_sess_batch, max_res, ctx->stream, v,
                                ctx->force_cache_slots),
                     "launch simulation");
   if (rc == UNISON_OK) ctx->ran = true;

@@ -375,6 +375,13 @@ struct WindowReader {
     return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), k) << 32) |
            (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, k);
   }
+  // Session id of event e, the event after the one take() returned last (at
+  // the end of the trace, the last event's: the window repeats it).
+  __device__ __forceinline__ uint32_t peek_sid(uint64_t e) const {
+    const uint64_t k = e - base;
+    return k < 64 ? (uint32_t)__builtin_amdgcn_readlane((int)csid, (int)k)
+                  : (uint32_t)__builtin_amdgcn_readlane((int)nsid, (int)(k - 64));
+  }
   __device__ __forceinline__ Ev take(uint64_t e) {
     if (e - base >= 64) {
       ct = nt; csid = nsid; cinfo = ninfo; clen = nlen; cn = nn; ctool = ntool;
@@ -406,6 +413,10 @@ struct RegTable {
   // fusing the three reductions made this kernel slower (0.518 vs 0.498 ms).
   static constexpr bool kFuseGap = false;
   static constexpr bool kLaneDigest = false;
+  static constexpr bool kPrefetch = false;
+  struct Pf {};
+  __device__ __forceinline__ Pf prefetch_issue(uint32_t) { return Pf{}; }
+  __device__ __forceinline__ void prefetch_land(const Pf&) {}
   template <bool N, bool T>
   using Reader = AheadReader<N, T>;
   uint32_t lane;
@@ -673,6 +684,10 @@ struct MemTable {
   // barrier (the dual design scans different copies for the two engines).
   static constexpr bool kFuseGap = !VIEWS;
   static constexpr bool kLaneDigest = false;
+  static constexpr bool kPrefetch = false;
+  struct Pf {};
+  __device__ __forceinline__ Pf prefetch_issue(uint32_t) { return Pf{}; }
+  __device__ __forceinline__ void prefetch_land(const Pf&) {}
   template <bool N, bool T>
   using Reader = AheadReader<N, T>;
   uint64_t* mg;
@@ -1178,6 +1193,66 @@ struct MemTable {
   }
 };
 
+// Digest terms of a table whose engine runs on one wavefront, queued one per
+// lane and hashed 64 at a time.  Record j of the current batch sits in lane j
+// (event, op, a, b); q_sum is the lane's sum of hashed records.  The scan
+// victim of event v_e0 + j sits in lane j; v_sum is the lane's sum of weighted
+// victims.
+struct LaneQueue {
+  uint32_t lane;
+  uint32_t q_ev, q_op, q_a, q_b, q_n;
+  uint64_t q_sum;
+  uint32_t v_sid, v_n;
+  uint64_t v_e0, v_sum;
+
+  __device__ __forceinline__ void queue_init() {
+    q_ev = q_op = q_a = q_b = 0u;
+    q_n = 0u;
+    q_sum = 0ull;
+    v_sid = 0u;
+    v_n = 0u;
+    v_e0 = 0ull;
+    v_sum = 0ull;
+  }
+  __device__ __forceinline__ void flush_records() {
+    if (lane < q_n) q_sum += rec_hash(q_ev, q_op, q_a, q_b);
+    q_n = 0u;
+  }
+  __device__ __forceinline__ void queue_record(uint32_t ev, uint32_t op, uint32_t a, uint32_t b) {
+    const bool mine = lane == q_n;
+    q_ev = mine ? ev : q_ev;
+    q_op = mine ? op : q_op;
+    q_a = mine ? a : q_a;
+    q_b = mine ? b : q_b;
+    if (++q_n == 64u) flush_records();
+  }
+  // The victim digest weighs event e's victim id + 1 by (2e + 1) * 0x9e3779b97f4a7c15.
+  __device__ __forceinline__ void flush_victims() {
+    if (lane < v_n) {
+      const uint64_t e = v_e0 + lane;
+      v_sum += ((uint64_t)v_sid + 1u) * ((2ull * e + 1ull) * 0x9e3779b97f4a7c15ull);
+    }
+    v_n = 0u;
+  }
+  // Events reach the queue in order, one victim each.
+  __device__ __forceinline__ void queue_victim(uint64_t e, uint32_t sid) {
+    if (v_n == 0u) v_e0 = e;
+    v_sid = lane == v_n ? sid : v_sid;
+    if (++v_n == 64u) flush_victims();
+  }
+  // Every queued term, summed over the wavefront mod 2^64: the record digest
+  // and the victim digest still to add.
+  __device__ __forceinline__ void drain(uint64_t& digest, uint64_t& victim_digest) {
+    flush_records();
+    flush_victims();
+    digest = uni64(wave_sum64(q_sum));
+    victim_digest = uni64(wave_sum64(v_sum));
+    q_sum = 0ull;
+    v_sum = 0ull;
+  }
+
+};
+
 // Residents in registers, table in LDS, one wavefront per simulation.  Every
 // session's entry stays in LDS (as in the LDS-resident MemTable), and each
 // resident also occupies a VGPR slot of the wavefront -- its session id, meta,
@@ -1188,12 +1263,16 @@ struct MemTable {
 // session's entry.  The single wavefront's LDS accesses are in program order,
 // so no barrier is needed anywhere.
 template <int SPL, uint32_t POL, uint32_t SMODE>
-struct SlotTable {
+struct SlotTable : LaneQueue {
   using PT = Pol<POL, SMODE>;
   static constexpr bool kViews = false;
   static constexpr bool kFuseGap = true;
   // Digest terms are queued one per lane and hashed 64 at a time.
   static constexpr bool kLaneDigest = true;
+  static constexpr bool kPrefetch = false;
+  struct Pf {};
+  __device__ __forceinline__ Pf prefetch_issue(uint32_t) { return Pf{}; }
+  __device__ __forceinline__ void prefetch_land(const Pf&) {}
   template <bool N, bool T>
   using Reader = WindowReader<N, T>;  // events come 64 to a window, one per lane
   uint64_t* mg;
@@ -1202,7 +1281,6 @@ struct SlotTable {
   uint32_t* kvb;
   uint64_t* last;
   uint64_t* next;
-  uint32_t lane;
   KeyCtx kc;
   uint32_t ssid[SPL];   // kNone: free
   uint32_t smeta[SPL];
@@ -1212,13 +1290,6 @@ struct SlotTable {
   uint32_t w_sid;
   uint64_t w_key;
   uint32_t w_kvb, w_len;
-  // Queued digest terms.  Record j of the current batch sits in lane j (event,
-  // op, a, b); q_sum is the lane's sum of hashed records.  The scan victim of
-  // event v_e0 + j sits in lane j; v_sum is the lane's sum of weighted victims.
-  uint32_t q_ev, q_op, q_a, q_b, q_n;
-  uint64_t q_sum;
-  uint32_t v_sid, v_n;
-  uint64_t v_e0, v_sum;
 
   __device__ __forceinline__ uint64_t key_from(uint32_t m, float g, uint64_t q, uint64_t l,
                                                uint64_t n) const {
@@ -1313,52 +1384,6 @@ struct SlotTable {
 
   __device__ __forceinline__ void event_begin() {}
   __device__ __forceinline__ void grow(uint32_t) {}
-
-  __device__ __forceinline__ void queue_init() {
-    q_ev = q_op = q_a = q_b = 0u;
-    q_n = 0u;
-    q_sum = 0ull;
-    v_sid = 0u;
-    v_n = 0u;
-    v_e0 = 0ull;
-    v_sum = 0ull;
-  }
-  __device__ __forceinline__ void flush_records() {
-    if (lane < q_n) q_sum += rec_hash(q_ev, q_op, q_a, q_b);
-    q_n = 0u;
-  }
-  __device__ __forceinline__ void queue_record(uint32_t ev, uint32_t op, uint32_t a, uint32_t b) {
-    const bool mine = lane == q_n;
-    q_ev = mine ? ev : q_ev;
-    q_op = mine ? op : q_op;
-    q_a = mine ? a : q_a;
-    q_b = mine ? b : q_b;
-    if (++q_n == 64u) flush_records();
-  }
-  // The victim digest weighs event e's victim id + 1 by (2e + 1) * 0x9e3779b97f4a7c15.
-  __device__ __forceinline__ void flush_victims() {
-    if (lane < v_n) {
-      const uint64_t e = v_e0 + lane;
-      v_sum += ((uint64_t)v_sid + 1u) * ((2ull * e + 1ull) * 0x9e3779b97f4a7c15ull);
-    }
-    v_n = 0u;
-  }
-  // Events reach the queue in order, one victim each.
-  __device__ __forceinline__ void queue_victim(uint64_t e, uint32_t sid) {
-    if (v_n == 0u) v_e0 = e;
-    v_sid = lane == v_n ? sid : v_sid;
-    if (++v_n == 64u) flush_victims();
-  }
-  // Every queued term, summed over the wavefront mod 2^64: the record digest
-  // and the victim digest still to add.
-  __device__ __forceinline__ void drain(uint64_t& digest, uint64_t& victim_digest) {
-    flush_records();
-    flush_victims();
-    digest = uni64(wave_sum64(q_sum));
-    victim_digest = uni64(wave_sum64(v_sum));
-    q_sum = 0ull;
-    v_sum = 0ull;
-  }
 
   __device__ __forceinline__ Entry read(uint32_t sid) const {
     Entry e;
@@ -1568,6 +1593,557 @@ struct SlotTable {
       c = ok && ssid[k] < c ? ssid[k] : c;
     }
     if (__builtin_amdgcn_ballot_w64(c != kNone) == 0) return kNone;
+    return uni32(reduce_min32<64, 1>(c));
+  }
+};
+
+// One wavefront per simulation for tables too large for LDS.  The session
+// table stays in the workspace; the residents (at most 64 * rows of them,
+// bounded by N_sess, eq. (cap)) sit in LDS slots [0, n_res): slot s holds
+// (key, session id, meta) and the KV bytes, and belongs to lane s % 64.  For
+// each of the three reductions the engine asks for -- argmax over every
+// evictable resident (the scan victim), argmin over the evictable HBM
+// residents and argmax over the evictable SRAM residents (TIDE's candidates,
+// eq. (promote), eq. (demote)) -- each lane keeps the best of its own slots,
+// kept current as slots change.  A lane whose best left or got worse marks
+// that reduction dirty and rescans its slots before the next one, so every
+// reduction is one wavefront reduction over the lanes' bests, with the
+// decisions of a full scan.  A departing resident's slot takes the last
+// slot's resident, whose slot index the table records.  The next event's
+// session entry is loaded one event ahead, and every write to that entry is
+// applied to the loaded copy too.  Lane 0 issues every table write and every
+// uniform read takes lane 0's value, so the single wavefront sees its own
+// writes in program order.
+template <uint32_t POL, uint32_t SMODE>
+struct WideTable : LaneQueue {
+  using PT = Pol<POL, SMODE>;
+  static constexpr bool kViews = false;
+  static constexpr bool kFuseGap = true;
+  static constexpr bool kLaneDigest = true;
+  static constexpr bool kPrefetch = true;
+  template <bool N, bool T>
+  using Reader = WindowReader<N, T>;
+  // the session table (workspace)
+  uint64_t* mg;
+  uint64_t* gq;
+  uint32_t* len;
+  uint64_t* last;
+  uint64_t* next;
+  const uint32_t* kvb;
+  uint32_t* slot;     // slot of each resident session
+  KeyCtx kc;
+  // residents (LDS), column by lane: slot s (lane s % 64, row s / 64) at
+  // index (s % 64) * rows + s / 64, so that one lane's slots are contiguous
+  uint4* rec;         // (key low, key high, session id, meta)
+  uint64_t* rsize;    // KV bytes
+  uint32_t rows;      // slots per lane (capacity / 64)
+  uint32_t n_res;     // slots in use (uniform)
+  __device__ __forceinline__ uint32_t at(uint32_t s) const { return (s & 63u) * rows + (s >> 6); }
+  // per-lane bests of the lane's slots: 0 argmax (any tier), 1 argmin (HBM),
+  // 2 argmax (SRAM); bsid kNone: none
+  uint64_t bkey[3];
+  uint32_t bsid[3], bslot[3];
+  uint32_t dirty;     // bit t: best t must be rebuilt from the lane's slots
+  // the latest winners of each reduction and their slots (uniform)
+  uint32_t cw_sid[3], cw_slot[3];
+  // the event's session and its slot (kNone: not resident)
+  uint32_t e_sid, e_slot;
+  // the entry of the latest write(): its key, KV bytes per token and length
+  uint32_t w_sid;
+  uint64_t w_key;
+  uint32_t w_kvb, w_len;
+  // The next event's entry: loaded while the current event runs, written
+  // into LDS staging (with the writes made to it meanwhile, kept in patch
+  // registers; pfp: which fields) once the current event is done, and read
+  // from there by its event.
+  uint32_t pf_sid;
+  uint64_t* stage;    // LDS: mg, gq, last, next, len | kvb << 32, slot
+  uint32_t pfp;
+  uint64_t pp_mg, pp_gq, pp_last, pp_next;
+  uint32_t pp_meta, pp_len, pp_slot;
+  enum : uint32_t { kPMg = 1, kPMeta = 2, kPGq = 4, kPLen = 8, kPLast = 16, kPNext = 32, kPSlot = 64 };
+
+  __device__ __forceinline__ uint64_t key_from(uint32_t m, float g, uint64_t q, uint64_t l,
+                                               uint64_t n) const {
+    return key_of<POL, SMODE>(kc, m, hazard_of<POL, SMODE>(kc, m), g, q, l, n);
+  }
+  // The key of entry i from its fields in the table (uniform).
+  __device__ __forceinline__ uint64_t key_at(uint32_t i) const {
+    const uint64_t x = uni64(mg[i]);
+    return key_from((uint32_t)x, __uint_as_float((uint32_t)(x >> 32)), PT::fixed ? uni64(gq[i]) : 0ull,
+                    PT::recency ? uni64(last[i]) : 0ull, PT::nextkey ? uni64(next[i]) : ~0ull);
+  }
+  // Opens a path that reads the table: the compiler may not hoist those
+  // loads above the branch that guards them (they would then run, and be
+  // waited for, on the usual path that needs no table read).
+  __device__ __forceinline__ static void cold() { asm volatile("" : : : "memory"); }
+  __device__ __forceinline__ static uint64_t rkey(const uint4& r) {
+    return ((uint64_t)r.y << 32) | r.x;
+  }
+  // Whether a resident with meta m takes part in reduction t.
+  template <int t>
+  __device__ __forceinline__ static bool takes(uint32_t m) {
+    if (meta_phase(m) == kServing) return false;
+    if constexpr (t == 0) return true;
+    else if constexpr (t == 1) return meta_tier(m) == kTierHbm;
+    else return meta_tier(m) == kTierSram;
+  }
+  template <int t>
+  __device__ __forceinline__ static bool better(uint64_t ka, uint32_t sa, uint64_t kb, uint32_t sb) {
+    return t == 1 ? min_better(ka, sa, kb, sb) : max_better(ka, sa, kb, sb);
+  }
+
+  // Lane s % 64 takes slot s's new resident (sid, meta m, key) into best t.
+  template <int t>
+  __device__ __forceinline__ void note_t(bool mine, uint32_t s, uint32_t sid, uint32_t m, uint64_t key) {
+    const bool clean = (dirty & (1u << t)) == 0u;
+    const bool have = bsid[t] != kNone;
+    const bool was = have && bslot[t] == s;
+    const bool in = takes<t>(m);
+    // the slot was the best: it stays so unless it left or got worse
+    const bool keep = was && in && !better<t>(bkey[t], bsid[t], key, sid);
+    const bool gain = !was && in && (!have || better<t>(key, sid, bkey[t], bsid[t]));
+    const bool take = mine && clean && (keep || gain);
+    bkey[t] = take ? key : bkey[t];
+    bsid[t] = take ? sid : bsid[t];
+    bslot[t] = take ? s : bslot[t];
+    dirty |= (mine && clean && was && !keep) ? (1u << t) : 0u;
+  }
+  __device__ __forceinline__ void note(uint32_t s, uint32_t sid, uint32_t m, uint64_t key) {
+    const bool mine = lane == (s & 63u);
+    note_t<0>(mine, s, sid, m, key);
+    note_t<1>(mine, s, sid, m, key);
+    note_t<2>(mine, s, sid, m, key);
+  }
+  // Lane s % 64 loses slot s: a best held there must be rebuilt.
+  __device__ __forceinline__ void gone(uint32_t s) {
+    const bool mine = lane == (s & 63u);
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      dirty |= (mine && bsid[t] != kNone && bslot[t] == s) ? (1u << t) : 0u;
+  }
+  // Rebuilds the dirty bests.  A few dirty lanes are rebuilt one after the
+  // other by the whole wavefront (one LDS read and one wavefront reduction
+  // each); many (after a hazard table change) each walk their own slots.
+  __device__ __forceinline__ void rescan() {
+    const uint64_t dl = __builtin_amdgcn_ballot_w64(dirty != 0u);
+    if (dl == 0ull) return;
+    if (__builtin_popcountll(dl) <= 4) {
+      for (uint64_t bits = dl; bits; bits &= bits - 1u) {
+        const uint32_t l = (uint32_t)__builtin_ctzll(bits);
+        const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)dirty, (int)l);
+        const uint32_t s = l + 64u * lane;
+        const bool valid = s < n_res;       // then lane < rows
+        const uint4 rr = rec[l * rows + (valid ? lane : 0u)];
+        const uint4 r = valid ? rr : make_uint4(0u, 0u, kNone, 0u);
+        if (d & 1u) rebuild<0>(l, r, s, valid);
+        if (d & 2u) rebuild<1>(l, r, s, valid);
+        if (d & 4u) rebuild<2>(l, r, s, valid);
+      }
+      dirty = 0u;
+      return;
+    }
+    const uint32_t d = dirty;
+    const bool any0 = __builtin_amdgcn_ballot_w64((d & 1u) != 0u) != 0ull;
+    const bool any1 = __builtin_amdgcn_ballot_w64((d & 2u) != 0u) != 0ull;
+    const bool any2 = __builtin_amdgcn_ballot_w64((d & 4u) != 0u) != 0ull;
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+      const bool r = (d >> t) & 1u;
+      bsid[t] = r ? kNone : bsid[t];
+      bkey[t] = r ? (t == 1 ? ~0ull : 0ull) : bkey[t];
+    }
+    const uint32_t n = n_res;
+    for (uint32_t base = 0; base < n; base += 256u) {
+      uint4 r[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t sk = base + 64u * k + lane;
+        r[k] = make_uint4(0u, 0u, kNone, 0u);
+        if (d != 0u && sk < n) r[k] = rec[at(sk)];
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t sk = base + 64u * k + lane;
+        if (any0) rescan_one<0>(d, sk, r[k]);
+        if (any1) rescan_one<1>(d, sk, r[k]);
+        if (any2) rescan_one<2>(d, sk, r[k]);
+      }
+    }
+    dirty = 0u;
+  }
+  template <int t>
+  __device__ __forceinline__ void rescan_one(uint32_t d, uint32_t s, const uint4& r) {
+    const uint64_t key = rkey(r);
+    const bool take = ((d >> t) & 1u) && r.z != kNone && takes<t>(r.w) &&
+                      (bsid[t] == kNone || better<t>(key, r.z, bkey[t], bsid[t]));
+    bkey[t] = take ? key : bkey[t];
+    bsid[t] = take ? r.z : bsid[t];
+    bslot[t] = take ? s : bslot[t];
+  }
+
+  // The best of one candidate per lane (act: the lane has one) by reduction
+  // t's order: its key, id and position.  The candidates compare as strings
+  // of 32-bit words, as the slot table's do: an fp32 score and the id; a
+  // time below 2^44 packed above a 20-bit id; else the key's two halves and
+  // the id (complemented for argmax, so ties go to the smaller id).  Every
+  // phase keeps only the lanes still equal, so the one lane left holds the
+  // winner.
+  template <int t>
+  __device__ __forceinline__ Cand wave_pick(bool in, uint64_t key, uint32_t sid, uint32_t pos,
+                                            uint32_t& pos_out) const {
+    constexpr bool MAX = t != 1;
+    bool act[1] = {in};
+    uint32_t w0[1], w1[1], w2[1];
+    if (PT::spear && !PT::fixed) {
+      w0[0] = (uint32_t)key;
+      w1[0] = MAX ? ~sid : sid;
+      lex_phase<MAX, true>(w0, act);
+      lex_phase<MAX, true>(w1, act);
+    } else if ((PT::recency || PT::belady) && kc.pack44) {
+      constexpr uint64_t kCap44 = (1ull << 44) - 1;
+      uint64_t k44;
+      if constexpr (PT::belady) k44 = key < kCap44 ? key : kCap44;
+      else k44 = key & kCap44;  // recency: key = 2^64 - 1 - last, last below 2^44 - 1
+      w0[0] = (uint32_t)(k44 >> 12);
+      w1[0] = ((uint32_t)k44 << 20) | (MAX ? 0xFFFFFu - sid : sid);
+      lex_phase<MAX, true>(w0, act);
+      lex_phase<MAX, true>(w1, act);
+    } else {
+      w0[0] = (uint32_t)(key >> 32);
+      w1[0] = (uint32_t)key;
+      w2[0] = MAX ? ~sid : sid;
+      lex_phase<MAX, true>(w0, act);
+      lex_phase<MAX, true>(w1, act);
+      lex_phase<MAX, true>(w2, act);
+    }
+    const uint64_t b = __builtin_amdgcn_ballot_w64(act[0]);
+    Cand c = MAX ? cand_none_max() : cand_none_min();
+    pos_out = kNone;
+    if (b != 0ull) {
+      const int l = __builtin_ctzll(b);
+      c.key = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(key >> 32), l) << 32) |
+              (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)key, l);
+      c.sid = (uint32_t)__builtin_amdgcn_readlane((int)sid, l);
+      pos_out = (uint32_t)__builtin_amdgcn_readlane((int)pos, l);
+    }
+    return c;
+  }
+  // Reduction t over the lanes' bests: the winner, and its slot recorded.
+  template <int t>
+  __device__ __forceinline__ Cand reduce_t() {
+    uint32_t s;
+    const Cand c = wave_pick<t>(bsid[t] != kNone, bkey[t], bsid[t], bslot[t], s);
+    cw_sid[t] = c.sid;
+    cw_slot[t] = s;
+    return c;
+  }
+  // Rebuilds lane l's best t from its slots, the whole wavefront at once:
+  // lane k reads slot l + 64 k (lane l's slots sit side by side in LDS).
+  template <int t>
+  __device__ __forceinline__ void rebuild(uint32_t l, const uint4& r, uint32_t s, bool valid) {
+    uint32_t pos;
+    const bool in = valid && takes<t>(r.w);
+    const Cand c = wave_pick<t>(in, rkey(r), r.z, s, pos);
+    const bool mine = lane == l;
+    bkey[t] = mine ? c.key : bkey[t];
+    bsid[t] = mine ? c.sid : bsid[t];
+    bslot[t] = mine ? pos : bslot[t];
+  }
+  // The slot of resident sid, kNone if sid is not resident.
+  __device__ __forceinline__ uint32_t find(uint32_t sid) const {
+    // Matching winners hold the same slot, so their slots combine by OR.  (A
+    // select between two members would let the compiler load from a selected
+    // member address, which keeps the whole table object in scratch memory.)
+    const bool h0 = sid == cw_sid[0], h1 = sid == cw_sid[1], h2 = sid == cw_sid[2];
+    const uint32_t c = (h0 ? cw_slot[0] : 0u) | (h1 ? cw_slot[1] : 0u) | (h2 ? cw_slot[2] : 0u);
+    if (sid == e_sid) return e_slot;
+    if (h0 || h1 || h2) return c;
+    uint32_t s;
+    if (sid == pf_sid && (pfp & kPSlot)) {
+      s = pp_slot;
+    } else {
+      cold();
+      s = uni32(slot[sid]);
+    }
+    if (s < n_res && uni32(rec[at(s)].z) == sid) return s;
+    return kNone;
+  }
+  // Records that sid now sits in slot s (kNone: it left).
+  __device__ __forceinline__ void moved_to(uint32_t sid, uint32_t s) {
+    if (s != kNone && lane == 0) slot[sid] = s;
+    if (sid == pf_sid && s != kNone) {
+      pfp |= kPSlot;
+      pp_slot = s;
+    }
+    if (sid == e_sid) e_slot = s;
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+      cw_slot[t] = sid == cw_sid[t] ? s : cw_slot[t];
+      cw_sid[t] = (sid == cw_sid[t] && s == kNone) ? kNone : cw_sid[t];
+    }
+  }
+  __device__ __forceinline__ void put(uint32_t s, uint32_t sid, uint32_t m, uint64_t key) {
+    if (lane == 0) rec[at(s)] = make_uint4((uint32_t)key, (uint32_t)(key >> 32), sid, m);
+    note(s, sid, m, key);
+  }
+  __device__ __forceinline__ void insert(uint32_t sid, uint32_t m, uint64_t key, uint64_t size) {
+    const uint32_t s = n_res++;
+    if (lane == 0) rsize[at(s)] = size;
+    put(s, sid, m, key);
+    moved_to(sid, s);
+  }
+  // Resident sid leaves slot s; the last slot's resident takes its place.
+  __device__ __forceinline__ void remove(uint32_t sid, uint32_t s) {
+    const uint32_t l = n_res - 1u;
+    gone(s);
+    moved_to(sid, kNone);
+    if (l != s) {
+      gone(l);
+      const uint4 r = rec[at(l)];
+      const uint64_t z = rsize[at(l)];
+      const uint4 u = make_uint4(uni32(r.x), uni32(r.y), uni32(r.z), uni32(r.w));
+      const uint64_t zu = uni64(z);
+      if (lane == 0) rsize[at(s)] = zu;
+      n_res = l;
+      put(s, u.z, u.w, rkey(u));
+      moved_to(u.z, s);
+    } else {
+      n_res = l;
+    }
+  }
+  // Meta word m of entry sid: the table, and the resident set it implies.
+  __device__ __forceinline__ void meta_to(uint32_t sid, uint32_t m) {
+    const uint32_t s = find(sid);
+    if (lane == 0) reinterpret_cast<uint32_t*>(mg + sid)[0] = m;
+    if (sid == pf_sid) patch_meta(m);
+    const bool now = meta_tier(m) != kTierNone;
+    if (s != kNone && !now) {
+      remove(sid, s);
+    } else if (s != kNone) {
+      const uint4 r = rec[at(s)];
+      const uint64_t key = uni64(((uint64_t)r.y << 32) | r.x);
+      put(s, sid, m, key);   // a tier or flag change: the key stays
+    } else if (now) {
+      uint64_t key, size;
+      if (sid == w_sid) {
+        key = w_key;
+        size = (uint64_t)w_len * w_kvb;
+      } else {
+        cold();
+        key = key_at(sid);
+        size = (uint64_t)uni32(len[sid]) * uni32(kvb[sid]);
+      }
+      insert(sid, m, key, size);
+    }
+  }
+
+  __device__ __forceinline__ void event_begin() {}
+  __device__ __forceinline__ void grow(uint32_t) {}
+  __device__ __forceinline__ void patch_meta(uint32_t m) {
+    if (pfp & kPMg) {
+      pp_mg = (pp_mg & 0xFFFFFFFF00000000ull) | m;
+    } else {
+      pfp |= kPMeta;
+      pp_meta = m;
+    }
+  }
+  // The next event's entry as loaded from the table.
+  struct Pf {
+    uint64_t mg, gq, last, next;
+    uint32_t len, kvb, slot;
+  };
+  __device__ __forceinline__ Pf prefetch_issue(uint32_t sid) {
+    pf_sid = sid;
+    pfp = 0u;
+    Pf v;
+    v.mg = mg[sid];
+    v.gq = PT::fixed ? gq[sid] : 0ull;
+    v.len = len[sid];
+    v.last = last[sid];
+    v.next = PT::nextkey ? next[sid] : ~0ull;
+    v.kvb = kvb[sid];
+    v.slot = slot[sid];
+    return v;
+  }
+  // After the current event: the entry as loaded into the staging area.
+  __device__ __forceinline__ void prefetch_land(const Pf& v) {
+    if (lane == 0) {
+      stage[0] = v.mg;
+      stage[1] = v.gq;
+      stage[2] = v.last;
+      stage[3] = v.next;
+      stage[4] = (uint64_t)v.len | ((uint64_t)v.kvb << 32);
+      stage[5] = v.slot;
+    }
+  }
+  // The event's session entry: when it was loaded ahead, the staged copy with
+  // every write made to the entry since its load.
+  __device__ __forceinline__ Entry read(uint32_t sid) {
+    uint64_t x, q, la, nx, lk;
+    uint32_t s;
+    if (uc<true>(sid == pf_sid)) {
+      x = uni64(stage[0]);
+      q = uni64(stage[1]);
+      la = uni64(stage[2]);
+      nx = uni64(stage[3]);
+      lk = uni64(stage[4]);
+      s = uni32((uint32_t)stage[5]);
+      if (pfp & kPMg) x = pp_mg;
+      if (pfp & kPMeta) x = (x & 0xFFFFFFFF00000000ull) | pp_meta;
+      if (pfp & kPGq) q = pp_gq;
+      if (pfp & kPLast) la = pp_last;
+      if (pfp & kPNext) nx = pp_next;
+      if (pfp & kPLen) lk = (lk & 0xFFFFFFFF00000000ull) | pp_len;
+      if (pfp & kPSlot) s = pp_slot;
+    } else {
+      // made uniform inside the branch, so that only this path waits for the loads
+      cold();
+      x = uni64(mg[sid]);
+      q = PT::fixed ? uni64(gq[sid]) : 0ull;
+      la = uni64(last[sid]);
+      nx = PT::nextkey ? uni64(next[sid]) : ~0ull;
+      lk = uni64((uint64_t)len[sid] | ((uint64_t)kvb[sid] << 32));
+      s = uni32(slot[sid]);
+    }
+    pf_sid = kNone;
+    Entry e;
+    e.meta = (uint32_t)x;
+    e.g = __uint_as_float((uint32_t)(x >> 32));
+    e.gq = q;
+    e.len = (uint32_t)lk;
+    e.kvb = (uint32_t)(lk >> 32);
+    e.last = la;
+    e.next = nx;
+    e_sid = sid;
+    e_slot = meta_tier(e.meta) != kTierNone ? s : kNone;
+    return e;
+  }
+  __device__ __forceinline__ void read_size(uint32_t sid, uint64_t& size, uint32_t& m) const {
+    const uint32_t s = find(sid);
+    if (s != kNone) {
+      size = uni64(rsize[at(s)]);
+      m = uni32(rec[at(s)].w);
+    } else {
+      cold();
+      m = uni32((uint32_t)mg[sid]);
+      size = (uint64_t)uni32(len[sid]) * uni32(kvb[sid]);
+    }
+  }
+  __device__ __forceinline__ void read_end(uint32_t sid, Entry& e) {
+    const Entry f = read(sid);
+    e.meta = f.meta;
+    e.g = f.g;
+    e.gq = f.gq;
+  }
+  __device__ __forceinline__ void write_end(uint32_t sid, const Entry& e, uint64_t t, uint64_t nx) {
+    if (lane == 0) {
+      reinterpret_cast<uint32_t*>(mg + sid)[0] = e.meta;
+      last[sid] = t;
+      if constexpr (PT::nextkey) next[sid] = nx;
+    }
+    if (sid == pf_sid) {
+      patch_meta(e.meta);
+      pfp |= kPLast | (PT::nextkey ? kPNext : 0u);
+      pp_last = t;
+      pp_next = nx;
+    }
+    w_sid = kNone;
+    const uint32_t s = find(sid);
+    if (s != kNone) put(s, sid, e.meta, key_from(e.meta, e.g, e.gq, t, nx));
+  }
+  __device__ __forceinline__ void write(uint32_t sid, const Entry& e) {
+    const uint64_t x = (uint64_t)e.meta | ((uint64_t)__float_as_uint(e.g) << 32);
+    if (lane == 0) {
+      mg[sid] = x;
+      if constexpr (PT::fixed) gq[sid] = e.gq;
+      len[sid] = e.len;
+      last[sid] = e.last;
+      if constexpr (PT::nextkey) next[sid] = e.next;
+    }
+    if (sid == pf_sid) {
+      pfp = (pfp & kPSlot) | kPMg | kPGq | kPLen | kPLast | kPNext;
+      pp_mg = x;
+      pp_gq = e.gq;
+      pp_len = e.len;
+      pp_last = e.last;
+      pp_next = e.next;
+    }
+    w_sid = sid;
+    w_key = key_from(e.meta, e.g, e.gq, e.last, e.next);
+    w_kvb = e.kvb;
+    w_len = e.len;
+    const uint32_t s = find(sid);
+    if (s != kNone) put(s, sid, e.meta, w_key);
+  }
+  __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) { meta_to(sid, m); }
+  __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
+    if (lane == 0) len[sid] = l;
+    if (sid == pf_sid) {
+      pfp |= kPLen;
+      pp_len = l;
+    }
+    if (sid == w_sid) w_len = l;
+    meta_to(sid, m);
+  }
+  __device__ __forceinline__ void set_turn(uint32_t, uint32_t, const KeyCtx&) {}
+  __device__ __forceinline__ void scan(const KeyCtx&, uint32_t) {}
+
+  template <bool MAX>
+  __device__ __forceinline__ Cand select(uint32_t tier, const KeyCtx&) {
+    rescan();
+    if constexpr (MAX) {
+      if (tier == kTierSram) return reduce_t<2>();
+      return reduce_t<0>();
+    } else {
+      return reduce_t<1>();
+    }
+  }
+  __device__ __forceinline__ Cand argmax_first(const KeyCtx& K) { return select<true>(0, K); }
+  __device__ __forceinline__ void select_pd(const KeyCtx&, Cand& p, Cand& d) {
+    rescan();
+    p = reduce_t<1>();
+    d = reduce_t<2>();
+  }
+  __device__ __forceinline__ void scan3(const KeyCtx&, Cand& v, Cand& p, Cand& d) {
+    rescan();
+    v = reduce_t<0>();
+    p = reduce_t<1>();
+    d = reduce_t<2>();
+  }
+
+  // Online hazard table: add the completed session, then rescore every resident.
+  __device__ __forceinline__ bool hazard_open(const KeyCtx& K) const {
+    return uni32(K.hn[0]) < K.online_cap;
+  }
+  __device__ __forceinline__ void hazard_add(const KeyCtx& K, uint32_t Tn) {
+    hazard_add_counts(K, Tn, lane, 64);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (uint32_t s = 0; s < n_res; ++s) {
+      const uint32_t sid = uni32(rec[at(s)].z);
+      const uint32_t m = uni32(rec[at(s)].w);
+      put(s, sid, m, key_at(sid));
+    }
+    dirty = 7u;
+    w_sid = kNone;
+  }
+
+  // Smallest evictable resident idle for longer than ttl (timeout: key = 2^64 - 1 - last).
+  __device__ __forceinline__ uint32_t first_idle(uint64_t now, uint64_t ttl) {
+    const uint64_t thr = idle_threshold(now, ttl);
+    rescan();
+    // the oldest evictable resident decides whether any timer fired
+    const Cand o = reduce_t<0>();
+    if (o.sid == kNone || ~0ull - o.key >= thr) return kNone;
+    uint32_t c = kNone;
+    const uint32_t n = n_res;
+    for (uint32_t s = lane; s < n; s += 64u) {
+      const uint4 r = rec[at(s)];
+      const bool ok = meta_phase(r.w) != kServing && (~0ull - rkey(r)) < thr;
+      c = ok && r.z < c ? r.z : c;
+    }
     return uni32(reduce_min32<64, 1>(c));
   }
 };
@@ -1816,6 +2392,12 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
       if (kind == kDone && K.online_cap && T.hazard_open(K)) T.hazard_add(K, meta_turn(x.meta) + 1u);
     }
 
+    // a table that loads entries ahead: the next event's session
+    // (also after the last event, where the window holds the last event's
+    // session again: a load that nothing reads, but no branch to join)
+    typename Tab::Pf pf{};
+    if constexpr (Tab::kPrefetch) pf = T.prefetch_issue(rd.peek_sid(e + 1));
+
     // the register-file scan: every table entry is scored; its argmax over
     // evictable residents is this event's victim index
     C.score_evals += S.n_table;
@@ -1831,7 +2413,9 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
     Cand v0, p0, d0;
     bool have_pd = false;
     if constexpr (Tab::kFuseGap) {
-      if (kind == kGapStart && uc<UNI>(P.tide != 0)) {
+      // TIDE's candidates are wanted only when the pass will run (the DMA
+      // engine is idle at this gap onset)
+      if (kind == kGapStart && uc<UNI>(P.tide && now >= S.dma_free_at)) {
         T.scan3(K, v0, p0, d0);
         have_pd = true;
       } else {
@@ -2024,6 +2608,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
         if (uni32(sync ? 1u : 0u)) T.sync_views();
       }
     }
+    if constexpr (Tab::kPrefetch) T.prefetch_land(pf);
     C.events++;
   }
   e_io = e;
@@ -2497,7 +3082,9 @@ __device__ __forceinline__ void slot_run(const SimArgs& a, uint32_t sim, const u
     C = cnt_from(unison_counters{});
   }
   if (S.hi > n_sess) S.hi = n_sess;
-  if (P.dual_sync || P.n_slots > 64u * SPL) C.error = ~0ull;  // the launcher picks a kernel that holds it
+  // residents never exceed min(N_sess, sessions): the launcher picks a kernel that holds them
+  const uint64_t max_res = P.n_slots < n_sess ? P.n_slots : n_sess;
+  if (P.dual_sync || max_res > 64u * SPL) C.error = ~0ull;
   pin_vgpr(S);
   pin_vgpr(C);
   const bool log_on = (a.flags & UNISON_RUN_LOG) && a.log_cap;
@@ -2553,6 +3140,156 @@ __global__ __launch_bounds__(64) void sim_slot_kernel(SimArgs a) {
     case kTimeout: slot_run<SPL, kTimeout, 0>(a, sim, P, K, s_tab); break;
     case kBelady: slot_run<SPL, kBelady, 0>(a, sim, P, K, s_tab); break;
     default: slot_run<SPL, kEta, 0>(a, sim, P, K, s_tab); break;
+  }
+}
+
+// ------------------------------------------------- wide-table kernel
+
+// One wavefront per simulation: the table in the workspace, the residents in
+// LDS slots (WideTable), events 64 to a window.  LDS: cap slots of 24 bytes.
+constexpr uint32_t kWideSlotBytes = sizeof(uint4) + sizeof(uint64_t);
+constexpr uint32_t kWideStageBytes = 6 * sizeof(uint64_t);
+
+template <uint32_t POL, uint32_t SMODE>
+__device__ __forceinline__ void wide_run(const SimArgs& a, uint32_t sim, const unison_sim_params& P,
+                                         const KeyCtx& K, uint64_t* s_tab, uint32_t cap) {
+  const uint32_t lane = threadIdx.x;
+  const uint64_t eb = a.ev_off[P.trace], ee = a.ev_off[P.trace + 1];
+  const uint64_t sb = a.sess_off[P.trace];
+  const uint32_t n_sess = (uint32_t)(a.sess_off[P.trace + 1] - sb);
+  const TraceView tr{a.ev_t + eb, a.ev_sid + eb, a.ev_info + eb, a.ev_len + eb, a.ev_next + eb,
+                     a.ev_tool ? a.ev_tool + eb : nullptr, ee - eb, n_sess};
+  const size_t tb = (size_t)sim * a.max_sessions;
+  const bool cont = (a.flags & UNISON_RUN_CONTINUE) != 0;
+
+  WideTable<POL, SMODE> T;
+  T.mg = a.t_mg + tb;
+  T.gq = a.t_gq + tb;
+  T.len = a.t_len + tb;
+  T.last = a.t_last + tb;
+  T.next = a.t_next + tb;
+  T.kvb = a.sess_kvb + sb;
+  T.slot = a.t_slot + tb;
+  T.kc = K;
+  T.rec = reinterpret_cast<uint4*>(s_tab);
+  T.rsize = reinterpret_cast<uint64_t*>(T.rec + cap);
+  T.rows = cap / 64u;
+  T.lane = lane;
+  T.n_res = 0;
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    T.bkey[t] = t == 1 ? ~0ull : 0ull;
+    T.bsid[t] = kNone;
+    T.bslot[t] = 0;
+    T.cw_sid[t] = kNone;
+    T.cw_slot[t] = kNone;
+  }
+  T.dirty = 0;
+  T.e_sid = kNone;
+  T.e_slot = kNone;
+  T.w_sid = kNone;
+  T.w_key = 0;
+  T.w_kvb = 0;
+  T.w_len = 0;
+  T.pf_sid = kNone;
+  T.stage = T.rsize + cap;
+  T.pfp = 0;
+  T.pp_mg = T.pp_gq = T.pp_last = T.pp_next = 0;
+  T.pp_meta = T.pp_len = T.pp_slot = 0;
+  T.queue_init();
+
+  Scalars S;
+  Cnt C;
+  uint64_t next_event = 0;
+  if (cont) {
+    load_scalars(a.state[sim], S);
+    C = cnt_from(a.counters[sim]);
+    next_event = a.state[sim].next_event;
+  } else {
+    S = Scalars{};
+    C = cnt_from(unison_counters{});
+  }
+  if (S.hi > n_sess) S.hi = n_sess;
+  // residents never exceed min(N_sess, sessions): the launcher picks a kernel that holds them
+  const uint64_t max_res = P.n_slots < n_sess ? P.n_slots : n_sess;
+  if (P.dual_sync || max_res > cap) C.error = ~0ull;
+
+  if (!cont) {
+    for (uint32_t i = lane; i < n_sess; i += 64) {
+      T.mg[i] = 0;
+      T.gq[i] = 0;
+      T.len[i] = 0;
+      T.last[i] = 0;
+      T.next[i] = ~0ull;
+    }
+  }
+  __syncthreads();
+  // a resumed table's residents take slots, in session order
+  if (cont && C.error == 0) {
+    for (uint32_t base = 0; base < n_sess; base += 64) {
+      const uint32_t i = base + lane;
+      const uint32_t ic = i < n_sess ? i : 0u;  // lanes past the table read entry 0
+      const uint64_t x = T.mg[ic];
+      const bool res = i < n_sess && meta_tier((uint32_t)x) != kTierNone;
+      for (uint64_t bits = __builtin_amdgcn_ballot_w64(res); bits; bits &= bits - 1u) {
+        const uint32_t sid = base + (uint32_t)__builtin_ctzll(bits);
+        if (T.n_res >= cap) {
+          C.error = ~0ull;
+          break;
+        }
+        const uint32_t m = uni32((uint32_t)T.mg[sid]);
+        T.insert(sid, m, T.key_at(sid), (uint64_t)uni32(T.len[sid]) * uni32(T.kvb[sid]));
+      }
+    }
+    __syncthreads();
+  }
+  pin_vgpr(S);
+  pin_vgpr(C);
+  const bool log_on = (a.flags & UNISON_RUN_LOG) && a.log_cap;
+  const LogSink L{log_on, log_on ? a.log + (size_t)sim * a.log_cap : nullptr, a.log_cap, lane == 0,
+                  log_on && (a.flags & UNISON_RUN_LOG_VICTIM) != 0};
+  if (C.error == 0) {
+    unison_sim_params Pv = P;
+    pin_vgpr(Pv);
+    run_events<POL, SMODE, true>(T, Pv, K, tr, S, C, L, next_event, a.max_events,
+                                 a.first_bad[P.trace]);
+    uint64_t dg, vd;
+    T.drain(dg, vd);
+    C.digest += dg;
+    C.victim_digest += vd;
+  }
+  __syncthreads();
+  store_hazard(a, P, sim, K, lane, 64);
+  if (lane == 0) {
+    finish_costs(S, P, C);
+    store_scalars(a.state[sim], S, next_event);
+    a.counters[sim] = cnt_to(C);
+  }
+}
+
+__global__ __launch_bounds__(64) void sim_wide_kernel(SimArgs a, uint32_t cap) {
+  __shared__ float s_hf[52];
+  __shared__ uint32_t s_hq[52];
+  __shared__ uint32_t s_hd[52];
+  __shared__ uint32_t s_hn[52];
+  extern __shared__ uint64_t s_tab[];
+  const uint32_t sim = blockIdx.x;
+  const unison_sim_params P = a.params[sim];
+  const uint32_t lambda = (1u << P.b_h) - 1u;
+  const KeyCtx K{s_hf, s_hq, s_hd, s_hn, P.penalty_us, lambda, P.p_z, a.time44 != 0,
+                 P.hazard_online ? P.online_sessions : 0u, a.eta + (size_t)P.trace * kEtaClasses,
+                 P.recip_bits};
+  load_hazard(a, P, sim, K, threadIdx.x, 64);
+  __syncthreads();
+  switch (sim_policy(a, P)) {
+    case kSpear:
+      if (P.score_mode) wide_run<kSpear, 1>(a, sim, P, K, s_tab, cap);
+      else wide_run<kSpear, 0>(a, sim, P, K, s_tab, cap);
+      break;
+    case kLru: wide_run<kLru, 0>(a, sim, P, K, s_tab, cap); break;
+    case kTimeout: wide_run<kTimeout, 0>(a, sim, P, K, s_tab, cap); break;
+    case kBelady: wide_run<kBelady, 0>(a, sim, P, K, s_tab, cap); break;
+    default: wide_run<kEta, 0>(a, sim, P, K, s_tab, cap); break;
   }
 }
 
@@ -2654,7 +3391,7 @@ struct Variant {
 // faulted the GPU on a randomised batch without a cause found.
 constexpr Variant kVariants[] = {{16, 1}, {64, 1}, {64, 4}, {0, 0}, {4, 4},
                                  {8, 2},  {-1, 0}, {16, 4}, {32, 8}, {0, 1}, {0, 0}, {0, 0},
-                                 {0, 1},  {0, 2}};
+                                 {0, 1},  {0, 2},  {0, 3}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kBlock = 256;
 constexpr int kLdsVariant = 9;
@@ -2662,6 +3399,8 @@ constexpr int kLdsWaveVariant = 12;  // the table in LDS, one wavefront per simu
 constexpr int kDualVariant = 11;  // streamed, 512 threads, with the dual design's copies
 constexpr int kSlotVariant = 13;  // the table in LDS, residents in VGPR slots, one wavefront
 constexpr uint64_t kSlotMaxResidents = 512;  // 8 slots per lane
+constexpr int kWideVariant = 14;  // the table in the workspace, residents in LDS slots, one wavefront
+constexpr uint64_t kWideMaxResidents = 4096;  // 96 KiB of slots
 constexpr uint32_t kLdsBytesPerSession = 4 * 8 + 2 * 4;  // mg, last, gq, next; len, kvb
 
 // LDS of the workgroup kernels' residency bits: one bit per session, in whole
@@ -2691,6 +3430,7 @@ uint32_t sim_variant_capacity(int v) {
   if (v < 0 || v >= kNumVariants) return 0;
   const uint32_t lim = lds_limit();
   if (v == kSlotVariant) return lim / kLdsBytesPerSession;  // the table alone
+  if (v == kWideVariant) return UNISON_MAX_SESSIONS;  // the table stays in the workspace
   if (v == kLdsVariant || v == kLdsWaveVariant) {
     // the table and its residency bits
     uint32_t n = lim / kLdsBytesPerSession;
@@ -2723,16 +3463,21 @@ int sim_auto_variant(uint32_t max_sess, uint64_t max_slots) {
   if (max_sess <= 16) return 5;
   if (max_sess <= 64) return 7;
   if (max_sess <= 256) return 8;
-  if (max_sess <= sim_variant_capacity(kSlotVariant) && max_slots <= kSlotMaxResidents)
-    return kSlotVariant;
+  if (max_sess <= sim_variant_capacity(kSlotVariant) && max_slots <= 256) return kSlotVariant;
   if (max_sess <= sim_variant_capacity(kLdsWaveVariant)) return kLdsWaveVariant;
+  if (max_slots <= kWideMaxResidents) return kWideVariant;
   return 10;
 }
 
-// Whether a variant can run simulations whose N_sess reaches max_slots.
-bool sim_variant_slots_ok(int v, uint64_t max_slots) {
-  return v != kSlotVariant || max_slots <= kSlotMaxResidents;
+// Largest N_sess a variant holds (UNISON_MAX_SESSIONS: no limit of its own).
+uint64_t sim_variant_max_slots(int v) {
+  if (v == kSlotVariant) return kSlotMaxResidents;
+  if (v == kWideVariant) return kWideMaxResidents;
+  return UNISON_MAX_SESSIONS;
 }
+
+// Whether a variant can run simulations whose N_sess reaches max_slots.
+bool sim_variant_slots_ok(int v, uint64_t max_slots) { return max_slots <= sim_variant_max_slots(v); }
 
 // The streamed-table kernels' resident cache: slots per thread of 8 + 8 + 8
 // + 4 bytes each, after the residency bits; as many as the LDS left by the bits
@@ -2778,6 +3523,13 @@ hipError_t launch_sim(const SimArgs& a, uint32_t max_sess_in_batch, uint64_t max
       else if (max_slots <= kSlotMaxResidents) launch_slots<8>(a, max_sess_in_batch, stream);
       else return hipErrorInvalidValue;
       break;
+    case kWideVariant: {
+      if (max_slots > kWideMaxResidents) return hipErrorInvalidValue;
+      const uint32_t cap = (uint32_t)((max_slots ? max_slots : 1) + 63) / 64u * 64u;
+      hipLaunchKernelGGL(sim_wide_kernel, dim3(a.n_sims), dim3(64),
+                         (size_t)cap * kWideSlotBytes + kWideStageBytes, stream, a, cap);
+      break;
+    }
     case 0: launch_regs<16, 1>(a, stream); break;
     case 1: launch_regs<64, 1>(a, stream); break;
     case 2: launch_regs<64, 4>(a, stream); break;

@@ -216,6 +216,7 @@ struct SimArgs {
   uint32_t* t_len;
   uint64_t* t_last;
   uint64_t* t_next;
+  uint32_t* t_slot;        // wide-table kernel: the LDS slot of each resident session
   unison_record* log;
   uint32_t* hcount;        // [n_sims][2][51] hazard counts d, n at the end of a launch
   uint64_t* views;         // dual design: [n_sims][2 copies][4 fields][max_sessions], or null

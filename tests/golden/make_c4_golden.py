@@ -1,6 +1,6 @@
 """Writes c4_prefix.json: the oracle's counters (both decision digests
 included) for two simulations of the large-live-set workload (65,536
-sessions, 160 KiB per token, SRAM 512 MiB, HBM 288 GiB, N_sess = 65,536)
+sessions, 160 KiB per token, SRAM 512 MiB, HBM 288 GiB, N_sess = 4,096)
 after the first 100,000, 200,000, 300,000 and 400,000 events of its first
 trace.  By 400,000 events about 63,000 sessions have arrived and the register
 file holds about 57,000 entries.

@@ -14,7 +14,7 @@ from parity import compare_counters, oracle_counters, oracle_log, same_log
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = (None, 0, 1, 2, 3, 4, 5, 7, 8, 9, 10, 11, 12, 13)
+VARIANTS = (None, 0, 1, 2, 3, 4, 5, 7, 8, 9, 10, 11, 12, 13, 14)
 
 
 def say(*a):
@@ -66,7 +66,7 @@ def test_eta_on_a_sweep_subset(tide):
     w = subset(c3, list(range(0, c3.n_sims, 7)))
     w.params["tide"] = tide
     say("eta sweep subset: %d sims, tide %d" % (w.n_sims, tide))
-    for v in (None, 9, 12, 3, 13):
+    for v in (None, 9, 12, 3, 13, 14):
         s = Sim(w, variant=v)
         s.run()
         compare_counters(s.counters(), oracle_counters(w), label="eta sweep variant %s" % v)

@@ -55,7 +55,7 @@ def check(s, w, label, max_events=None):
             "%s sim %d: hazard counts differ" % (label, i)
 
 
-@pytest.mark.parametrize("variant", [None, 0, 4, 7, 3, 9, 12, 10, 13])
+@pytest.mark.parametrize("variant", [None, 0, 4, 7, 3, 9, 12, 10, 13, 14])
 def test_c3_online_tables(variant):
     c3 = synth.c3_sweep()
     w = online(c3, list(range(0, c3.n_sims, 97)))
@@ -87,7 +87,7 @@ def test_paper_shaped_trace_online_all_policies_and_both_scores():
     assert np.array_equal(gd, d) and np.array_equal(gn, n)
 
 
-@pytest.mark.parametrize("variant", [None, 9, 12, 13])
+@pytest.mark.parametrize("variant", [None, 9, 12, 13, 14])
 def test_online_table_survives_continue(variant):
     tr = synth.fidelity_traces()[1]
     w0 = synth.format_sweep(traces=[tr], envelopes=synth.FIDELITY_ENVELOPES[:1],

@@ -195,6 +195,24 @@ def test_random_batches_on_the_slot_kernel(name):
     compare_counters(s.counters(), want, label="random %s slot kernel split" % name)
 
 
+@pytest.mark.parametrize("name", sorted(BATCHES))
+def test_random_batches_on_the_wide_kernel(name):
+    """The wide-table kernel (table in the workspace, residents in LDS slots,
+    the next entry loaded one event ahead): every batch, in one launch and
+    split by CONTINUE."""
+    seed, lo, hi, _ = BATCHES[name]
+    w = batch(seed, lo, hi)
+    want = oracle_counters(w)
+    say("random %s on the wide kernel: %d sims" % (name, w.n_sims))
+    s = Sim(w, variant=14)
+    s.run()
+    compare_counters(s.counters(), want, label="random %s wide kernel" % name)
+    longest = max(t.n_events for t in w.traces)
+    s.run(max_events=max(1, longest // 7))
+    s.run(flags=1)
+    compare_counters(s.counters(), want, label="random %s wide kernel split" % name)
+
+
 def test_random_dual_rows():
     w = batch(74, 1, 120, n_traces=6, per_trace=8)
     rng = np.random.Generator(np.random.PCG64(75))

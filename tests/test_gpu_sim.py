@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 RETIRED = pytest.mark.skip(reason="variant 6 (64 x 24) is retired: one of its launches faulted "
                                   "the GPU on a randomised batch and no cause was found; the "
                                   "library refuses it (test_retired_variant_is_refused)")
-VARIANTS = (0, 1, 2, 3, 4, 5, pytest.param(6, marks=RETIRED), 7, 8, 9, 10, 11, 12, 13)
+VARIANTS = (0, 1, 2, 3, 4, 5, pytest.param(6, marks=RETIRED), 7, 8, 9, 10, 11, 12, 13, 14)
 
 
 def say(*a):
@@ -88,7 +88,7 @@ def test_c3_decision_logs(c3):
         assert same_log(s.log(k), oracle_log(c3, i)), "c3 sim %d log" % i
 
 
-@pytest.mark.parametrize("variant", [None, 3, 9, 12, 10, 13])
+@pytest.mark.parametrize("variant", [None, 3, 9, 12, 10, 13, 14])
 def test_continue_matches_single_run(c3, c3_want, variant):
     sims = list(range(5, c3.n_sims, 61))
     w = subset(c3, sims)
@@ -112,7 +112,7 @@ def test_determinism(c3):
     assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
 
 
-@pytest.mark.parametrize("variant", [None, 12, 13])
+@pytest.mark.parametrize("variant", [None, 12, 13, 14])
 def test_c2_paper_scale(variant):
     w = synth.c2_paper_scale()
     say("c2: 4 sims x %d events, variant %s" % (w.traces[0].n_events, variant))
@@ -136,6 +136,19 @@ def test_c2_on_the_slot_kernel_at_each_slot_width(slots):
     compare_counters(s.counters(), oracle_counters(w), label="c2 slots %d" % slots)
 
 
+def test_wide_kernel_refuses_more_than_4096_residents():
+    """The wide-table kernel holds up to 4,096 residents in LDS slots; a batch
+    whose N_sess and sessions both pass that runs elsewhere or is refused."""
+    from paper_2609_09643_amd.unison import E_CAPACITY, UnisonError
+    w = synth.c4_large(n_traces=1)
+    ww = subset(w, [0])
+    ww.params["n_slots"] = 4097
+    s = Sim(ww, variant=14)
+    with pytest.raises(UnisonError) as e:
+        s.run(max_events=10)
+    assert e.value.code == E_CAPACITY
+
+
 def test_slot_kernel_refuses_more_than_512_slots():
     from paper_2609_09643_amd.unison import E_CAPACITY, UnisonError
     w = synth.c2_paper_scale()
@@ -146,13 +159,14 @@ def test_slot_kernel_refuses_more_than_512_slots():
     assert e.value.code == E_CAPACITY
 
 
-def test_c4_large_live_set_prefix():
+@pytest.mark.parametrize("variant", [None, 10])
+def test_c4_large_live_set_prefix(variant):
     w = synth.c4_large(n_traces=1)
     sims = [0, 3]
     ww = subset(w, sims)
     n1, n2 = 6000, 9000
-    say("c4: %d sims, 65,536 sessions, prefixes %d / %d events" % (len(sims), n1, n2))
-    s = Sim(ww)
+    say("c4: %d sims, 65,536 sessions, prefixes %d / %d events, variant %s" % (len(sims), n1, n2, variant))
+    s = Sim(ww, variant=variant)
     s.run(max_events=n1)
     compare_counters(s.counters(), oracle_counters(ww, max_events=n1), label="c4 prefix")
     s.run(flags=1, max_events=n2 - n1)
@@ -173,7 +187,8 @@ def test_c4_longer_prefix_in_the_timed_configuration():
     compare_counters(s.counters(), oracle_counters(ww, max_events=40_000), label="c4 40k")
 
 
-def test_c4_golden_prefix_in_the_timed_configuration():
+@pytest.mark.parametrize("variant", [None, 10])
+def test_c4_golden_prefix_in_the_timed_configuration(variant):
     """The 65,536-session trace on the kernel the bench times, resumed by
     CONTINUE to 100,000, 200,000, 300,000 and 400,000 events, against the
     oracle's counters and both decision digests at each point
@@ -188,10 +203,10 @@ def test_c4_golden_prefix_in_the_timed_configuration():
     w = G.workload()
     assert G.trace_sha(w.traces[0]) == gold["trace_sha256"], "the C4 generator changed"
     ww = subset(w, gold["sims"])
-    s = Sim(ww)
+    s = Sim(ww, variant=variant)
     done = 0
     for n in gold["checkpoints"]:
-        say("c4 golden: %d sims to event %d" % (len(gold["sims"]), n))
+        say("c4 golden: %d sims to event %d, variant %s" % (len(gold["sims"]), n, variant))
         s.run(flags=1 if done else 0, max_events=n - done)
         done = n
         compare_counters(s.counters(), gold["counters"][str(n)], label="c4 golden %d" % n)

@@ -10,7 +10,7 @@ from paper_2609_09643_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = (None, 0, 1, 2, 3, 4, 5, 7, 8, 9, 10, 11, 12, 13)
+VARIANTS = (None, 0, 1, 2, 3, 4, 5, 7, 8, 9, 10, 11, 12, 13, 14)
 
 
 def say(*a):

@@ -220,9 +220,10 @@ FATBIN_DEFINITION
 
 namespace unison {
 hipError_t launch_sim(const SimArgs&, uint32_t, uint64_t, hipStream_t, int, int) { return hipSuccess; }
-uint32_t sim_variant_capacity(int v) { return v >= 0 && v <= 13 && v != 6 ? (1u << 20) : 0u; }
+uint32_t sim_variant_capacity(int v) { return v >= 0 && v <= 14 && v != 6 ? (1u << 20) : 0u; }
 int sim_auto_variant(uint32_t n, uint64_t) { return n <= 16 ? 5 : 10; }
-bool sim_variant_slots_ok(int v, uint64_t s) { return v != 13 || s <= 512; }
+uint64_t sim_variant_max_slots(int v) { return v == 13 ? 512u : v == 14 ? 4096u : (1u << 20); }
+bool sim_variant_slots_ok(int v, uint64_t s) { return s <= sim_variant_max_slots(v); }
 uint32_t sim_variant_lanes(int v) { return v == 5 ? 8u : 0u; }
 hipError_t launch_hazard_counts(const uint32_t*, uint32_t, uint32_t*, uint32_t*, hipStream_t) {
   return hipSuccess;
