@@ -335,7 +335,7 @@ struct AheadReader {
   const TraceView& tr;
   uint64_t end;
   Ev cur;
-  __device__ __forceinline__ AheadReader(const TraceView& t, uint64_t e, uint64_t end_)
+  __device__ __forceinline__ AheadReader(const TraceView& t, uint64_t e, uint64_t end_, void*)
       : tr(t), end(end_), cur(load_ev<NEXT, TOOL>(t, e)) {}
   __device__ __forceinline__ Ev take(uint64_t e) {
     const Ev c = cur;
@@ -366,7 +366,7 @@ struct WindowReader {
     nx = NEXT ? tr.next[i] : ~0ull;
     tool = (TOOL && tr.tool) ? tr.tool[i] : 0u;
   }
-  __device__ __forceinline__ WindowReader(const TraceView& t, uint64_t e, uint64_t end_)
+  __device__ __forceinline__ WindowReader(const TraceView& t, uint64_t e, uint64_t end_, void*)
       : tr(t), end(end_), base(e), lane(threadIdx.x & 63u) {
     load(base, ct, csid, cinfo, clen, cn, ctool);
     load(base + 64, nt, nsid, ninfo, nlen, nn, ntool);
@@ -400,6 +400,73 @@ struct WindowReader {
   }
 };
 
+// Events through a window in LDS (one wavefront): events [base, base + 128)
+// of the trace, reloaded 64 further on every 64 events, so that the event
+// after the current one is always there.  An event is read back from LDS as
+// uniform values; the window's registers hold no load in flight across
+// events (a load still in flight across the loop would be waited for at
+// every event, with every table store the wavefront issued).
+template <bool NEXT, bool TOOL>
+struct LdsWindowReader {
+  static constexpr uint32_t kWin = 128;
+  static constexpr uint32_t kBytes = kWin * (2 * sizeof(uint64_t) + 4 * sizeof(uint32_t));
+  const TraceView& tr;
+  uint64_t end, base;
+  uint32_t lane;
+  uint64_t* wt;
+  uint64_t* wn;
+  uint32_t* wsid;
+  uint32_t* winfo;
+  uint32_t* wlen;
+  uint32_t* wtool;
+  __device__ __forceinline__ void fill() {
+#pragma unroll
+    for (uint32_t h = 0; h < kWin; h += 64) {
+      const uint64_t e = base + h + lane;
+      const uint64_t i = e < end ? e : end - 1;  // end > 0: a reader exists only for events
+      const uint64_t t = tr.t[i];
+      const uint32_t sid = tr.sid[i], info = tr.info[i], len = tr.len[i];
+      const uint64_t nx = NEXT ? tr.next[i] : ~0ull;
+      const uint32_t tool = (TOOL && tr.tool) ? tr.tool[i] : 0u;
+      wt[h + lane] = t;
+      wn[h + lane] = nx;
+      wsid[h + lane] = sid;
+      winfo[h + lane] = info;
+      wlen[h + lane] = len;
+      wtool[h + lane] = tool;
+    }
+  }
+  __device__ __forceinline__ LdsWindowReader(const TraceView& t, uint64_t e, uint64_t end_, void* w)
+      : tr(t), end(end_), base(e), lane(threadIdx.x & 63u) {
+    wt = reinterpret_cast<uint64_t*>(w);
+    wn = wt + kWin;
+    wsid = reinterpret_cast<uint32_t*>(wn + kWin);
+    winfo = wsid + kWin;
+    wlen = winfo + kWin;
+    wtool = wlen + kWin;
+    fill();
+  }
+  // Session id of event e, the event after the one take() returned last.
+  __device__ __forceinline__ uint32_t peek_sid(uint64_t e) const {
+    return uni32(wsid[(uint32_t)(e - base)]);
+  }
+  __device__ __forceinline__ Ev take(uint64_t e) {
+    if (e - base >= 64) {
+      base += 64;
+      fill();
+    }
+    const uint32_t k = (uint32_t)(e - base);
+    Ev v;
+    v.t = uni64(wt[k]);
+    v.sid = uni32(wsid[k]);
+    v.info = uni32(winfo[k]);
+    v.len = uni32(wlen[k]);
+    v.next = NEXT ? uni64(wn[k]) : ~0ull;
+    v.tool = TOOL ? uni32(wtool[k]) : 0u;
+    return v;
+  }
+};
+
 // ------------------------------------------------------------ tables
 
 // Most resident-cache slots per thread of the streamed-table kernels.
@@ -414,6 +481,7 @@ struct RegTable {
   static constexpr bool kFuseGap = false;
   static constexpr bool kLaneDigest = false;
   static constexpr bool kPrefetch = false;
+  __device__ __forceinline__ void* window() const { return nullptr; }
   struct Pf {};
   __device__ __forceinline__ Pf prefetch_issue(uint32_t) { return Pf{}; }
   __device__ __forceinline__ void prefetch_land(const Pf&) {}
@@ -685,6 +753,7 @@ struct MemTable {
   static constexpr bool kFuseGap = !VIEWS;
   static constexpr bool kLaneDigest = false;
   static constexpr bool kPrefetch = false;
+  __device__ __forceinline__ void* window() const { return nullptr; }
   struct Pf {};
   __device__ __forceinline__ Pf prefetch_issue(uint32_t) { return Pf{}; }
   __device__ __forceinline__ void prefetch_land(const Pf&) {}
@@ -1270,6 +1339,7 @@ struct SlotTable : LaneQueue {
   // Digest terms are queued one per lane and hashed 64 at a time.
   static constexpr bool kLaneDigest = true;
   static constexpr bool kPrefetch = false;
+  __device__ __forceinline__ void* window() const { return nullptr; }
   struct Pf {};
   __device__ __forceinline__ Pf prefetch_issue(uint32_t) { return Pf{}; }
   __device__ __forceinline__ void prefetch_land(const Pf&) {}
@@ -1599,21 +1669,20 @@ struct SlotTable : LaneQueue {
 
 // One wavefront per simulation for tables too large for LDS.  The session
 // table stays in the workspace; the residents (at most 64 * rows of them,
-// bounded by N_sess, eq. (cap)) sit in LDS slots [0, n_res): slot s holds
-// (key, session id, meta) and the KV bytes, and belongs to lane s % 64.  For
-// each of the three reductions the engine asks for -- argmax over every
-// evictable resident (the scan victim), argmin over the evictable HBM
-// residents and argmax over the evictable SRAM residents (TIDE's candidates,
-// eq. (promote), eq. (demote)) -- each lane keeps the best of its own slots,
-// kept current as slots change.  A lane whose best left or got worse marks
-// that reduction dirty and rescans its slots before the next one, so every
-// reduction is one wavefront reduction over the lanes' bests, with the
-// decisions of a full scan.  A departing resident's slot takes the last
-// slot's resident, whose slot index the table records.  The next event's
-// session entry is loaded one event ahead, and every write to that entry is
-// applied to the loaded copy too.  Lane 0 issues every table write and every
-// uniform read takes lane 0's value, so the single wavefront sees its own
-// writes in program order.
+// bounded by N_sess, eq. (cap)) sit in LDS slots: slot s holds (key, session
+// id, meta) and the KV bytes, and belongs to lane s % 64; the table records
+// each resident's slot.  For each of the three reductions the engine asks
+// for -- argmax over every evictable resident (the scan victim), argmin over
+// the evictable HBM residents and argmax over the evictable SRAM residents
+// (TIDE's candidates, eq. (promote), eq. (demote)) -- each lane keeps the
+// best of its own slots, kept current as slots change.  A lane whose best
+// left or got worse marks that reduction dirty, and before the next one the
+// whole wavefront rebuilds it from that lane's slots; so every reduction is
+// one wavefront reduction over the lanes' bests, with the decisions of a
+// full scan.  The next event's session entry is loaded one event ahead, and
+// every write to that entry is applied to the loaded copy too.  Lane 0
+// issues every table write and every uniform read takes lane 0's value, so
+// the single wavefront sees its own writes in program order.
 template <uint32_t POL, uint32_t SMODE>
 struct WideTable : LaneQueue {
   using PT = Pol<POL, SMODE>;
@@ -1622,7 +1691,9 @@ struct WideTable : LaneQueue {
   static constexpr bool kLaneDigest = true;
   static constexpr bool kPrefetch = true;
   template <bool N, bool T>
-  using Reader = WindowReader<N, T>;
+  using Reader = LdsWindowReader<N, T>;
+  void* win;          // LDS: the event window
+  __device__ __forceinline__ void* window() const { return win; }
   // the session table (workspace)
   uint64_t* mg;
   uint64_t* gq;
@@ -1633,19 +1704,27 @@ struct WideTable : LaneQueue {
   uint32_t* slot;     // slot of each resident session
   KeyCtx kc;
   // residents (LDS), column by lane: slot s (lane s % 64, row s / 64) at
-  // index (s % 64) * rows + s / 64, so that one lane's slots are contiguous
+  // index (s % 64) * rows + s / 64, so that one lane's slots are contiguous.
+  // A resident keeps its slot until it leaves; a new one takes a free slot of
+  // the next lane round the wavefront that has one.
   uint4* rec;         // (key low, key high, session id, meta)
   uint64_t* rsize;    // KV bytes
   uint32_t rows;      // slots per lane (capacity / 64)
-  uint32_t n_res;     // slots in use (uniform)
+  uint32_t n_res;     // residents (uniform)
+  uint64_t used;      // per lane: bit j set when slot j * 64 + lane holds a resident
+  uint32_t cur;       // the lane the next search for a free slot starts at (uniform)
+  uint32_t top;       // rows [0, top) have held residents (uniform)
   __device__ __forceinline__ uint32_t at(uint32_t s) const { return (s & 63u) * rows + (s >> 6); }
   // per-lane bests of the lane's slots: 0 argmax (any tier), 1 argmin (HBM),
   // 2 argmax (SRAM); bsid kNone: none
   uint64_t bkey[3];
   uint32_t bsid[3], bslot[3];
   uint32_t dirty;     // bit t: best t must be rebuilt from the lane's slots
-  // the latest winners of each reduction and their slots (uniform)
+  // the latest winners of each reduction, their slots and keys (uniform)
   uint32_t cw_sid[3], cw_slot[3];
+  uint64_t cw_key[3];
+  // the latest session first_idle returned, and its slot
+  uint32_t ci_sid, ci_slot;
   // the event's session and its slot (kNone: not resident)
   uint32_t e_sid, e_slot;
   // the entry of the latest write(): its key, KV bytes per token and length
@@ -1677,6 +1756,10 @@ struct WideTable : LaneQueue {
   // loads above the branch that guards them (they would then run, and be
   // waited for, on the usual path that needs no table read).
   __device__ __forceinline__ static void cold() { asm volatile("" : : : "memory"); }
+  __device__ __forceinline__ static uint64_t lane64(uint64_t v, int l) {
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l) << 32) |
+           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  }
   __device__ __forceinline__ static uint64_t rkey(const uint4& r) {
     return ((uint64_t)r.y << 32) | r.x;
   }
@@ -1733,7 +1816,8 @@ struct WideTable : LaneQueue {
         const uint32_t l = (uint32_t)__builtin_ctzll(bits);
         const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)dirty, (int)l);
         const uint32_t s = l + 64u * lane;
-        const bool valid = s < n_res;       // then lane < rows
+        const uint64_t ul = lane64(used, (int)l);
+        const bool valid = lane < top && ((ul >> lane) & 1ull);   // then lane < rows
         const uint4 rr = rec[l * rows + (valid ? lane : 0u)];
         const uint4 r = valid ? rr : make_uint4(0u, 0u, kNone, 0u);
         if (d & 1u) rebuild<0>(l, r, s, valid);
@@ -1753,18 +1837,17 @@ struct WideTable : LaneQueue {
       bsid[t] = r ? kNone : bsid[t];
       bkey[t] = r ? (t == 1 ? ~0ull : 0ull) : bkey[t];
     }
-    const uint32_t n = n_res;
-    for (uint32_t base = 0; base < n; base += 256u) {
+    for (uint32_t j0 = 0; j0 < top; j0 += 4u) {
       uint4 r[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const uint32_t sk = base + 64u * k + lane;
+        const uint32_t j = j0 + (uint32_t)k;
         r[k] = make_uint4(0u, 0u, kNone, 0u);
-        if (d != 0u && sk < n) r[k] = rec[at(sk)];
+        if (d != 0u && j < top && ((used >> j) & 1ull)) r[k] = rec[lane * rows + j];
       }
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const uint32_t sk = base + 64u * k + lane;
+        const uint32_t sk = (j0 + (uint32_t)k) * 64u + lane;
         if (any0) rescan_one<0>(d, sk, r[k]);
         if (any1) rescan_one<1>(d, sk, r[k]);
         if (any2) rescan_one<2>(d, sk, r[k]);
@@ -1836,6 +1919,7 @@ struct WideTable : LaneQueue {
     const Cand c = wave_pick<t>(bsid[t] != kNone, bkey[t], bsid[t], bslot[t], s);
     cw_sid[t] = c.sid;
     cw_slot[t] = s;
+    cw_key[t] = c.key;
     return c;
   }
   // Rebuilds lane l's best t from its slots, the whole wavefront at once:
@@ -1859,6 +1943,7 @@ struct WideTable : LaneQueue {
     const uint32_t c = (h0 ? cw_slot[0] : 0u) | (h1 ? cw_slot[1] : 0u) | (h2 ? cw_slot[2] : 0u);
     if (sid == e_sid) return e_slot;
     if (h0 || h1 || h2) return c;
+    if (sid == ci_sid) return ci_slot;
     uint32_t s;
     if (sid == pf_sid && (pfp & kPSlot)) {
       s = pp_slot;
@@ -1866,7 +1951,10 @@ struct WideTable : LaneQueue {
       cold();
       s = uni32(slot[sid]);
     }
-    if (s < n_res && uni32(rec[at(s)].z) == sid) return s;
+    // the table's slot field is current only while the session is resident
+    if (s < 64u * rows && ((lane64(used, (int)(s & 63u)) >> (s >> 6)) & 1ull) &&
+        uni32(rec[at(s)].z) == sid)
+      return s;
     return kNone;
   }
   // Records that sid now sits in slot s (kNone: it left).
@@ -1882,35 +1970,35 @@ struct WideTable : LaneQueue {
       cw_slot[t] = sid == cw_sid[t] ? s : cw_slot[t];
       cw_sid[t] = (sid == cw_sid[t] && s == kNone) ? kNone : cw_sid[t];
     }
+    if (sid == ci_sid) ci_sid = kNone;
   }
   __device__ __forceinline__ void put(uint32_t s, uint32_t sid, uint32_t m, uint64_t key) {
     if (lane == 0) rec[at(s)] = make_uint4((uint32_t)key, (uint32_t)(key >> 32), sid, m);
     note(s, sid, m, key);
   }
+  // A new resident takes the first free slot of the first lane from cur on
+  // that has one (there is one: residents never exceed the slots).
   __device__ __forceinline__ void insert(uint32_t sid, uint32_t m, uint64_t key, uint64_t size) {
-    const uint32_t s = n_res++;
+    const uint64_t rowmask = rows >= 64u ? ~0ull : ((1ull << rows) - 1ull);
+    const uint64_t fm = __builtin_amdgcn_ballot_w64((~used & rowmask) != 0ull);
+    const uint64_t rot = cur ? ((fm >> cur) | (fm << (64u - cur))) : fm;
+    const uint32_t l = (cur + (uint32_t)__builtin_ctzll(rot)) & 63u;
+    const uint32_t j = (uint32_t)__builtin_ctzll(~lane64(used, (int)l) & rowmask);
+    const uint32_t s = j * 64u + l;
+    used |= lane == l ? (1ull << j) : 0ull;
+    cur = (l + 1u) & 63u;
+    top = j + 1u > top ? j + 1u : top;
+    ++n_res;
     if (lane == 0) rsize[at(s)] = size;
     put(s, sid, m, key);
     moved_to(sid, s);
   }
-  // Resident sid leaves slot s; the last slot's resident takes its place.
+  // Resident sid leaves slot s.
   __device__ __forceinline__ void remove(uint32_t sid, uint32_t s) {
-    const uint32_t l = n_res - 1u;
     gone(s);
     moved_to(sid, kNone);
-    if (l != s) {
-      gone(l);
-      const uint4 r = rec[at(l)];
-      const uint64_t z = rsize[at(l)];
-      const uint4 u = make_uint4(uni32(r.x), uni32(r.y), uni32(r.z), uni32(r.w));
-      const uint64_t zu = uni64(z);
-      if (lane == 0) rsize[at(s)] = zu;
-      n_res = l;
-      put(s, u.z, u.w, rkey(u));
-      moved_to(u.z, s);
-    } else {
-      n_res = l;
-    }
+    used &= lane == (s & 63u) ? ~(1ull << (s >> 6)) : ~0ull;
+    --n_res;
   }
   // Meta word m of entry sid: the table, and the resident set it implies.
   __device__ __forceinline__ void meta_to(uint32_t sid, uint32_t m) {
@@ -1921,9 +2009,14 @@ struct WideTable : LaneQueue {
     if (s != kNone && !now) {
       remove(sid, s);
     } else if (s != kNone) {
-      const uint4 r = rec[at(s)];
-      const uint64_t key = uni64(((uint64_t)r.y << 32) | r.x);
-      put(s, sid, m, key);   // a tier or flag change: the key stays
+      // a tier or flag change: the key stays (a reduction winner's is at hand)
+      const bool h0 = sid == cw_sid[0], h1 = sid == cw_sid[1], h2 = sid == cw_sid[2];
+      uint64_t key = (h0 ? cw_key[0] : 0ull) | (h1 ? cw_key[1] : 0ull) | (h2 ? cw_key[2] : 0ull);
+      if (!(h0 || h1 || h2)) {
+        const uint4 r = rec[at(s)];
+        key = uni64(((uint64_t)r.y << 32) | r.x);
+      }
+      put(s, sid, m, key);
     } else if (now) {
       uint64_t key, size;
       if (sid == w_sid) {
@@ -2121,13 +2214,22 @@ struct WideTable : LaneQueue {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (uint32_t s = 0; s < n_res; ++s) {
-      const uint32_t sid = uni32(rec[at(s)].z);
-      const uint32_t m = uni32(rec[at(s)].w);
-      put(s, sid, m, key_at(sid));
+    // every lane rescores its own residents (their fields from the table)
+    for (uint32_t j = 0; j < top; ++j) {
+      if ((used >> j) & 1ull) {
+        const uint32_t o = lane * rows + j;
+        const uint4 r = rec[o];
+        const uint64_t x = mg[r.z];
+        const uint64_t key =
+            key_from((uint32_t)x, __uint_as_float((uint32_t)(x >> 32)), PT::fixed ? gq[r.z] : 0ull,
+                     PT::recency ? last[r.z] : 0ull, PT::nextkey ? next[r.z] : ~0ull);
+        rec[o] = make_uint4((uint32_t)key, (uint32_t)(key >> 32), r.z, r.w);
+      }
     }
     dirty = 7u;
     w_sid = kNone;
+#pragma unroll
+    for (int t = 0; t < 3; ++t) cw_sid[t] = kNone;   // their keys changed
   }
 
   // Smallest evictable resident idle for longer than ttl (timeout: key = 2^64 - 1 - last).
@@ -2137,14 +2239,22 @@ struct WideTable : LaneQueue {
     // the oldest evictable resident decides whether any timer fired
     const Cand o = reduce_t<0>();
     if (o.sid == kNone || ~0ull - o.key >= thr) return kNone;
-    uint32_t c = kNone;
-    const uint32_t n = n_res;
-    for (uint32_t s = lane; s < n; s += 64u) {
-      const uint4 r = rec[at(s)];
-      const bool ok = meta_phase(r.w) != kServing && (~0ull - rkey(r)) < thr;
-      c = ok && r.z < c ? r.z : c;
+    uint32_t c = kNone, cs = kNone;
+    for (uint32_t j = 0; j < top; ++j) {
+      if ((used >> j) & 1ull) {
+        const uint4 r = rec[lane * rows + j];
+        const bool ok = meta_phase(r.w) != kServing && (~0ull - rkey(r)) < thr;
+        cs = ok && r.z < c ? j * 64u + lane : cs;
+        c = ok && r.z < c ? r.z : c;
+      }
     }
-    return uni32(reduce_min32<64, 1>(c));
+    const uint32_t m = uni32(reduce_min32<64, 1>(c));
+    if (m != kNone) {
+      const uint64_t b = __builtin_amdgcn_ballot_w64(c == m);
+      ci_sid = m;
+      ci_slot = (uint32_t)__builtin_amdgcn_readlane((int)cs, __builtin_ctzll(b));
+    }
+    return m;
   }
 };
 
@@ -2323,7 +2433,7 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& e_io, uint64_t end) {
   using PT = Pol<POL, SMODE>;
   uint64_t e = e_io;
-  typename Tab::template Reader<PT::belady, PT::eta> rd(tr, e, end);
+  typename Tab::template Reader<PT::belady, PT::eta> rd(tr, e, end, T.window());
   // victim-digest weight of event e, (2e + 1) * 0x9e3779b97f4a7c15, stepped per event
   constexpr uint64_t kGolden = 0x9e3779b97f4a7c15ull;
   uint64_t vw = (2ull * e + 1ull) * kGolden;
@@ -3148,7 +3258,7 @@ __global__ __launch_bounds__(64) void sim_slot_kernel(SimArgs a) {
 // One wavefront per simulation: the table in the workspace, the residents in
 // LDS slots (WideTable), events 64 to a window.  LDS: cap slots of 24 bytes.
 constexpr uint32_t kWideSlotBytes = sizeof(uint4) + sizeof(uint64_t);
-constexpr uint32_t kWideStageBytes = 6 * sizeof(uint64_t);
+constexpr uint32_t kWideStageBytes = 6 * sizeof(uint64_t) + LdsWindowReader<true, true>::kBytes;
 
 template <uint32_t POL, uint32_t SMODE>
 __device__ __forceinline__ void wide_run(const SimArgs& a, uint32_t sim, const unison_sim_params& P,
@@ -3176,6 +3286,9 @@ __device__ __forceinline__ void wide_run(const SimArgs& a, uint32_t sim, const u
   T.rows = cap / 64u;
   T.lane = lane;
   T.n_res = 0;
+  T.used = 0;
+  T.cur = 0;
+  T.top = 0;
 #pragma unroll
   for (int t = 0; t < 3; ++t) {
     T.bkey[t] = t == 1 ? ~0ull : 0ull;
@@ -3183,7 +3296,10 @@ __device__ __forceinline__ void wide_run(const SimArgs& a, uint32_t sim, const u
     T.bslot[t] = 0;
     T.cw_sid[t] = kNone;
     T.cw_slot[t] = kNone;
+    T.cw_key[t] = 0;
   }
+  T.ci_sid = kNone;
+  T.ci_slot = kNone;
   T.dirty = 0;
   T.e_sid = kNone;
   T.e_slot = kNone;
@@ -3193,6 +3309,7 @@ __device__ __forceinline__ void wide_run(const SimArgs& a, uint32_t sim, const u
   T.w_len = 0;
   T.pf_sid = kNone;
   T.stage = T.rsize + cap;
+  T.win = T.stage + 6;
   T.pfp = 0;
   T.pp_mg = T.pp_gq = T.pp_last = T.pp_next = 0;
   T.pp_meta = T.pp_len = T.pp_slot = 0;
