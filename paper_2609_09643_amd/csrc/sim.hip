@@ -1876,6 +1876,8 @@ struct WideTable : LaneQueue {
   __device__ __forceinline__ Cand wave_pick(bool in, uint64_t key, uint32_t sid, uint32_t pos,
                                             uint32_t& pos_out) const {
     constexpr bool MAX = t != 1;
+    pos_out = kNone;
+    if (__builtin_amdgcn_ballot_w64(in) == 0ull) return MAX ? cand_none_max() : cand_none_min();
     bool act[1] = {in};
     uint32_t w0[1], w1[1], w2[1];
     if (PT::spear && !PT::fixed) {
@@ -1902,7 +1904,6 @@ struct WideTable : LaneQueue {
     }
     const uint64_t b = __builtin_amdgcn_ballot_w64(act[0]);
     Cand c = MAX ? cand_none_max() : cand_none_min();
-    pos_out = kNone;
     if (b != 0ull) {
       const int l = __builtin_ctzll(b);
       c.key = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(key >> 32), l) << 32) |
