@@ -1727,9 +1727,11 @@ struct WideTable : LaneQueue {
   uint32_t ci_sid, ci_slot;
   // the event's session and its slot (kNone: not resident)
   uint32_t e_sid, e_slot;
-  // the entry of the latest write(): its key, KV bytes per token and length
-  uint32_t w_sid;
-  uint64_t w_key;
+  // the entry of the latest write(): the fields its key reads (the key itself
+  // is computed only if the entry is placed), KV bytes per token and length
+  uint32_t w_sid, w_meta;
+  float w_g;
+  uint64_t w_gq, w_last, w_next;
   uint32_t w_kvb, w_len;
   // The next event's entry: loaded while the current event runs, written
   // into LDS staging (with the writes made to it meanwhile, kept in patch
@@ -2021,7 +2023,7 @@ struct WideTable : LaneQueue {
     } else if (now) {
       uint64_t key, size;
       if (sid == w_sid) {
-        key = w_key;
+        key = key_from(w_meta, w_g, w_gq, w_last, w_next);
         size = (uint64_t)w_len * w_kvb;
       } else {
         cold();
@@ -2164,11 +2166,15 @@ struct WideTable : LaneQueue {
       pp_next = e.next;
     }
     w_sid = sid;
-    w_key = key_from(e.meta, e.g, e.gq, e.last, e.next);
+    w_meta = e.meta;
+    w_g = e.g;
+    w_gq = e.gq;
+    w_last = e.last;
+    w_next = e.next;
     w_kvb = e.kvb;
     w_len = e.len;
     const uint32_t s = find(sid);
-    if (s != kNone) put(s, sid, e.meta, w_key);
+    if (s != kNone) put(s, sid, e.meta, key_from(e.meta, e.g, e.gq, e.last, e.next));
   }
   __device__ __forceinline__ void set_meta(uint32_t sid, uint32_t m) { meta_to(sid, m); }
   __device__ __forceinline__ void set_len_meta(uint32_t sid, uint32_t l, uint32_t m) {
@@ -3305,7 +3311,9 @@ __device__ __forceinline__ void wide_run(const SimArgs& a, uint32_t sim, const u
   T.e_sid = kNone;
   T.e_slot = kNone;
   T.w_sid = kNone;
-  T.w_key = 0;
+  T.w_meta = 0;
+  T.w_g = 0.0f;
+  T.w_gq = T.w_last = T.w_next = 0;
   T.w_kvb = 0;
   T.w_len = 0;
   T.pf_sid = kNone;
