@@ -2436,8 +2436,8 @@ __device__ __forceinline__ void release(Tab& T, Scalars& S, uint32_t sid) {
 
 // Events [e_io, end) of one simulation; e_io ends at end.
 template <uint32_t POL, uint32_t SMODE, bool UNI, class Tab>
-__device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
-                          Scalars& S, Cnt& C, const LogSink& L, uint64_t& e_io, uint64_t end) {
+__device__ __forceinline__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
+                                          Scalars& S, Cnt& C, const LogSink& L, uint64_t& e_io, uint64_t end) {
   using PT = Pol<POL, SMODE>;
   uint64_t e = e_io;
   typename Tab::template Reader<PT::belady, PT::eta> rd(tr, e, end, T.window());
@@ -2739,9 +2739,9 @@ __device__ void run_range(Tab& T, const unison_sim_params& P, const KeyCtx& K, c
 // (found once when the traces are loaded, ~0 if none): the run stops there and
 // reports it, so the loop itself checks nothing.
 template <uint32_t POL, uint32_t SMODE, bool UNI, class Tab>
-__device__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
-                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& next_event,
-                           uint64_t max_events, uint64_t bad_at) {
+__device__ __forceinline__ void run_events(Tab& T, const unison_sim_params& P, const KeyCtx& K, const TraceView& tr,
+                                           Scalars& S, Cnt& C, const LogSink& L, uint64_t& next_event,
+                                           uint64_t max_events, uint64_t bad_at) {
   uint64_t e = next_event;
   uint64_t end = (e >= tr.n_ev || tr.n_ev - e < max_events) ? tr.n_ev : e + max_events;
   const bool stops = bad_at < end;
