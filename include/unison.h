@@ -394,10 +394,14 @@ int unison_debug_cache_slots(unison_ctx* ctx, int slots);
 /* Test hook, host only (no GPU work): the barrier plan of the sorted Kendall
  * path for a snapshot padded to n_pad entries (a power of two, 256..4096).
  * step 0: bitonic pass of stage a (= k) and stride b (= j); step 1: merge
- * level that merges runs of a entries.  Returns 1 when the kernel places a
- * workgroup barrier after that step, 0 when only the wavefront-local fence
- * (the step and the next touch no LDS entry another wavefront touches), or
- * UNISON_E_INVALID for a step the kernel does not take. */
+ * level that merges runs of a entries (a >= 8: shorter runs are merged in
+ * registers).  Bitonic passes run in groups of up to three in registers, one
+ * LDS load before a group's first pass and one store after its last.
+ * Returns 1 when the kernel places a workgroup barrier after that step, 0
+ * when none (the next pass of the group runs in registers) or only the
+ * wavefront-local fence (the step and the next touch no LDS entry another
+ * wavefront touches), or UNISON_E_INVALID for a step the kernel does not
+ * take. */
 int unison_debug_kendall_barrier(uint32_t n_pad, uint32_t step, uint32_t a, uint32_t b);
 
 uint32_t unison_version(void);

@@ -6,9 +6,12 @@
 // workgroup and gather its (x, y) pairs into LDS once.  Small snapshots are
 // classified pair by pair (each thread owns rows i and walks j > i with all
 // lanes of a wave reading the same LDS word, a broadcast); from 256 entries
-// on, a bitonic sort and a counting merge sort (merge path from runs of 8)
-// find the same counts in O(n log^2 n).
+// on, a bitonic sort (its passes in groups of three in registers) and a
+// counting merge sort (runs of 8 inside each thread, merge path above) find
+// the same counts in O(n log^2 n).
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "unison_device.h"
 
@@ -204,22 +207,15 @@ __device__ __forceinline__ uint32_t float_key(uint32_t b) {
 }
 
 
-__device__ __forceinline__ bool pair_less(uint32_t xa, uint64_t ya, uint32_t xb, uint64_t yb) {
-  return xa < xb || (xa == xb && ya < yb);
-}
-
-// Entries per thread and compare-exchanges per thread and pass at the largest
-// snapshot.  Each thread runs its compare-exchanges (and its searches) in
-// lockstep, so their LDS loads are in flight together.
+// Entries per thread at the largest snapshot.
 constexpr uint32_t kSortE = kKendallMax / kSortBlock;
-constexpr uint32_t kSortQ = kSortE / 2;
-// From runs of this width on, the merge levels use merge path (each thread
-// merges its own 8 outputs); narrower runs place each entry by a short
-// binary search.
+// The merge levels use merge path (each thread merges its own 8 outputs)
+// from runs of this width on; the narrower runs are sorted inside each
+// thread's 8 consecutive entries.
 constexpr uint32_t kMergeRun = 8;
-// Merge-path levels store entry i at i + i / 8: a thread's 8 consecutive
-// outputs then start 72 B after its neighbour's, not 64 B, which spreads a
-// wavefront's stores over the LDS banks.
+// Sort and merge buffers store entry i at i + i / 8: a thread's 8 consecutive
+// entries then start 72 B after its neighbour's, not 64 B, and the bitonic
+// groups below spread their accesses over the banks as well.
 __device__ __forceinline__ uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
 // Entries of each sort buffer, the padding included.
 __host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
@@ -232,31 +228,54 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Whether bitonic pass (k, j) is followed by a workgroup barrier.  With
-// strides up to 64 every compare-exchange stays inside the 128 entries that
-// one wavefront owns for each q (t = tid + q * 512), so two such passes in a
-// row need only the wavefront's own in-order LDS accesses between them;
-// passes of longer strides exchange entries across wavefronts and take a
-// workgroup barrier on both sides (the last pass of a stage precedes the
-// first, longest-stride pass of the next).
-__host__ __device__ constexpr bool bitonic_barrier_after(uint32_t k, uint32_t j) {
-  return j >= 128 || (j == 1 && k >= 128);
+// Bitonic passes run in groups, one LDS round trip per group: a thread holds
+// the 8 entries whose indexes differ only in bits b, b+1 and b+2 and runs up
+// to three consecutive passes on them in registers (strides 2^(b+2), 2^(b+1),
+// 2^b).  Stage k = 2^L (L >= 4) splits its passes s = L-1 ... 0 (stride 2^s)
+// from the top: L-1..L-3, L-4..L-6, ...; the last group holds the one to
+// three passes left and uses bits 0..2.  Stages 2, 4 and 8 form one group on
+// each thread's 8 consecutive entries, straight from the gather.
+// A wavefront's 64 threads hold 512 entries: while every bit of a group is
+// below 9, they are its own aligned block of 512 (the thread index fills the
+// other bits from the bottom), so two such groups in a row need only the
+// wavefront's in-order LDS accesses between them.
+constexpr uint32_t kWaveSpanBits = 9;
+__host__ __device__ constexpr uint32_t group_top(uint32_t L, uint32_t s) {
+  return L - 1 - 3 * ((L - 1 - s) / 3);
+}
+__host__ __device__ constexpr uint32_t group_low(uint32_t top) { return top >= 2 ? top - 2 : 0; }
+__host__ __device__ constexpr uint32_t group_high(uint32_t top) { return top >= 2 ? top : 2; }
+__host__ __device__ constexpr uint32_t ilog2(uint32_t v) {
+  uint32_t r = 0;
+  while (v > 1) {
+    v >>= 1;
+    ++r;
+  }
+  return r;
 }
 
-// Whether merge level w (runs of w merged into runs of 2w) is followed by a
-// workgroup barrier.  Levels of runs below 4 keep each entry p = tid + e * 512
-// inside its aligned group of 8, which one wavefront owns.  Merge-path levels
-// after the first keep a thread's outputs and the runs it reads inside one
-// wavefront's 512 consecutive entries (576 padded) while the pair of runs of
-// the next level spans at most 512.  The first merge-path level (w = 8) reads
-// the plain layout that the search levels wrote, and the next level stores
-// padded positions into that same buffer: a wavefront's padded stores there
-// reach past its own 512 plain entries into those its neighbour reads at
-// w = 8, so that step takes the barrier.  Elsewhere entries cross wavefronts,
-// and the last level is followed by the scan of the sorted y.
+// Whether bitonic pass (k, j) of a P-entry sort is followed by a workgroup
+// barrier.  Inside a group the next pass runs in registers; the gathered
+// stages end with the barrier that also publishes the argmax partials; the
+// last group's entries become the merge input only after every wavefront
+// has read its group (the x keys share that buffer).
+__host__ __device__ constexpr bool bitonic_barrier_after(uint32_t P, uint32_t k, uint32_t j) {
+  if (k <= 8) return k == 8 && j == 1;
+  const uint32_t L = ilog2(k), s = ilog2(j);
+  const uint32_t top = group_top(L, s);
+  if (s != group_low(top)) return false;
+  if (s == 0 && k == P) return true;
+  const uint32_t next_high = s > 0 ? group_high(s - 1) : L;
+  return group_high(top) >= kWaveSpanBits || next_high >= kWaveSpanBits;
+}
+
+// Whether merge level w (runs of w merged into runs of 2w, w >= 8) is
+// followed by a workgroup barrier.  A thread's outputs and the pair of runs
+// it reads lie in its wavefront's 512 consecutive entries (576 padded) while
+// a pair of runs spans at most 512, so the barrier is needed only before a
+// level whose pairs of runs are wider, and before the scan of the sorted y.
 __host__ __device__ constexpr bool merge_barrier_after(uint32_t w, uint32_t P) {
-  return !(w < kMergeRun / 2 ||
-           (w > kMergeRun && 4 * w <= (uint32_t)kSortBlock && 2 * w < P));
+  return !(4 * w <= (uint32_t)kSortBlock && 2 * w < P);
 }
 
 __device__ __forceinline__ void level_sync(uint32_t w, uint32_t P) {
@@ -289,36 +308,315 @@ __device__ __forceinline__ void block_max_scan(uint32_t (&v)[kSortE], uint32_t* 
 }
 static_assert(kSortE == 8 && kSortE * kSortBlock == kKendallMax, "8 outputs per thread");
 
+// Compare-exchange of two sort entries, a 64-bit key k and (unless NARROW) a
+// 32-bit tie-breaker r: afterwards a precedes b in (k, r) order when up,
+// follows it otherwise (equal entries are identical).
+template <bool NARROW>
+__device__ __forceinline__ void sort_cx(uint64_t& ka, uint32_t& ra, uint64_t& kb, uint32_t& rb,
+                                        bool up) {
+  const bool b_first = NARROW ? kb < ka : (kb < ka || (kb == ka && rb < ra));
+  if (b_first == up) {
+    const uint64_t tk = ka;
+    ka = kb;
+    kb = tk;
+    if (!NARROW) {
+      const uint32_t tr = ra;
+      ra = rb;
+      rb = tr;
+    }
+  }
+}
+
+// One bitonic pass inside a group: entries c and c + 2^M of the thread's 8.
+template <uint32_t M, bool NARROW>
+__device__ __forceinline__ void sort_pass(uint64_t (&kk)[kSortE], uint32_t (&kr)[kSortE], bool up) {
+#pragma unroll
+  for (uint32_t c = 0; c < kSortE; ++c)
+    if ((c & (1u << M)) == 0)
+      sort_cx<NARROW>(kk[c], kr[c], kk[c | (1u << M)], kr[c | (1u << M)], up);
+}
+
+template <class Y>
+__device__ __forceinline__ void sort_min_max(Y& a, Y& b) {
+  const Y lo = a < b ? a : b;
+  b = a < b ? b : a;
+  a = lo;
+}
+
+// Knight's counts of one snapshot from its gathered entries (thread t holds
+// entries 8t ... 8t+7; x as order-preserving u32 keys): the bitonic sort by
+// (x, y), the ties in x and in both from the sorted runs, the inversions of y
+// in that order counted while it is merge-sorted, the ties in y from the
+// sorted y.  cnt = {discordant, ties in x, ties in y, ties in both}.
+// NARROW: every y of the snapshot other than 2^64 - 1 lies below 2^32 - 1, so
+// y -> (y == 2^64 - 1 ? 2^32 - 1 : y) keeps the order and the ties of y, and
+// (x, y) packs into one 64-bit key; otherwise the key is x with the upper
+// half of y, and the lower half breaks its ties.
+// LDS: two buffers of sort_buf(P) 8-byte entries.  The keys sort in the
+// first (the tie-breakers in the second); the merge sort of y starts in the
+// second and alternates.
+template <bool NARROW>
+__device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
+                                              const uint64_t (&ky)[kSortE], uint32_t P,
+                                              uint32_t n, uint32_t tid, uint64_t* s_dyn,
+                                              uint64_t* s_ek, uint32_t* s_er, uint32_t* s_part,
+                                              uint64_t (&cnt)[4]) {
+  using Y = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
+  uint64_t* s_k = s_dyn;
+  uint32_t* s_r = reinterpret_cast<uint32_t*>(s_dyn + sort_buf(P));
+  const uint32_t i0 = tid * kSortE;
+  const bool active = i0 < P;
+  uint64_t kk[kSortE];
+  uint32_t kr[kSortE];
+#pragma unroll
+  for (uint32_t c = 0; c < kSortE; ++c) {
+    if (NARROW) {
+      kk[c] = ((uint64_t)kx[c] << 32) | (ky[c] == ~0ull ? 0xFFFFFFFFu : (uint32_t)ky[c]);
+      kr[c] = 0;
+    } else {
+      kk[c] = ((uint64_t)kx[c] << 32) | (ky[c] >> 32);
+      kr[c] = (uint32_t)ky[c];
+    }
+  }
+
+  // bitonic sort: stages 2, 4 and 8 on the gathered entries (the direction
+  // of stage k follows bit k of the entry's index)
+#pragma unroll
+  for (uint32_t k = 2; k <= 8; k <<= 1)
+#pragma unroll
+    for (uint32_t j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (uint32_t c = 0; c < kSortE; ++c)
+        if ((c & j) == 0) {
+          const bool up = k == 8 ? (tid & 1u) == 0 : (c & k) == 0;
+          sort_cx<NARROW>(kk[c], kr[c], kk[c | j], kr[c | j], up);
+        }
+  if (active) {
+#pragma unroll
+    for (uint32_t c = 0; c < kSortE; ++c) {
+      s_k[mp_pad(i0 + c)] = kk[c];
+      if (!NARROW) s_r[mp_pad(i0 + c)] = kr[c];
+    }
+  }
+  __syncthreads();
+  // then the grouped passes of stages 16 ... P; the last group keeps the
+  // thread's 8 consecutive sorted entries in registers
+  for (uint32_t L = 4, k = 16; k <= P; ++L, k <<= 1) {
+    for (int top = (int)L - 1; top >= 0; top -= 3) {
+      const uint32_t lo = group_low((uint32_t)top);
+      const uint32_t gb = ((tid >> lo) << (lo + 3)) | (tid & ((1u << lo) - 1u));
+      const bool last = k == P && lo == 0;
+      if (gb < P) {
+#pragma unroll
+        for (uint32_t c = 0; c < kSortE; ++c) {
+          const uint32_t at = mp_pad(gb | (c << lo));
+          kk[c] = s_k[at];
+          kr[c] = NARROW ? 0u : s_r[at];
+        }
+        const bool up = (gb & k) == 0;
+        const uint32_t np = (uint32_t)top - lo + 1;
+        if (np == 3) sort_pass<2, NARROW>(kk, kr, up);
+        if (np >= 2) sort_pass<1, NARROW>(kk, kr, up);
+        sort_pass<0, NARROW>(kk, kr, up);
+        if (!last) {
+#pragma unroll
+          for (uint32_t c = 0; c < kSortE; ++c) {
+            const uint32_t at = mp_pad(gb | (c << lo));
+            s_k[at] = kk[c];
+            if (!NARROW) s_r[at] = kr[c];
+          }
+        }
+      }
+      if (last) break;
+      if (bitonic_barrier_after(P, k, 1u << lo)) __syncthreads();
+      else wave_lds_sync();
+    }
+  }
+  // the entry before the thread's first (the neighbouring thread's last)
+  if ((tid & 63u) == 63u) {
+    s_ek[tid >> 6] = kk[kSortE - 1];
+    s_er[tid >> 6] = kr[kSortE - 1];
+  }
+  __syncthreads();  // every group is read: the tie-breakers' buffer is free
+  uint64_t pk = __shfl_up(kk[kSortE - 1], 1);
+  uint32_t pr = __shfl_up(kr[kSortE - 1], 1);
+  if ((tid & 63u) == 0 && tid > 0) {
+    pk = s_ek[(tid >> 6) - 1];
+    pr = s_er[(tid >> 6) - 1];
+  }
+
+  uint64_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
+  Y* src = reinterpret_cast<Y*>(s_dyn + sort_buf(P));
+  Y* dst = reinterpret_cast<Y*>(s_dyn);
+  // pairs tied in x, and in x and y: each entry counts the earlier entries of
+  // its run; a run starts where the key differs from the one before, and a
+  // max-scan of those starts gives every entry the start of its run
+  {
+    uint32_t sx[kSortE], sxy[kSortE];
+    Y yv[kSortE];
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = i0 + e;
+      const bool ok = i < P;
+      const bool new_x = i == 0 || (kk[e] >> 32) != (pk >> 32);
+      const bool new_xy = new_x || kk[e] != pk || (!NARROW && kr[e] != pr);
+      sx[e] = ok && new_x ? i : 0u;
+      sxy[e] = ok && new_xy ? i : 0u;
+      pk = kk[e];
+      pr = kr[e];
+      if (NARROW) yv[e] = (Y)(uint32_t)kk[e];
+      else yv[e] = (Y)((kk[e] << 32) | kr[e]);
+    }
+    // merge levels of runs 1, 2 and 4 stay inside the thread's 8 entries:
+    // their discordant pairs are the inversions among those 8 y values
+    if (active) {
+#pragma unroll
+      for (uint32_t p = 0; p < kSortE; ++p)
+#pragma unroll
+        for (uint32_t q = p + 1; q < kSortE; ++q) inv += yv[p] > yv[q] ? 1u : 0u;
+      // a 19-comparator sorting network on 8 inputs
+      sort_min_max(yv[0], yv[2]);
+      sort_min_max(yv[1], yv[3]);
+      sort_min_max(yv[4], yv[6]);
+      sort_min_max(yv[5], yv[7]);
+      sort_min_max(yv[0], yv[4]);
+      sort_min_max(yv[1], yv[5]);
+      sort_min_max(yv[2], yv[6]);
+      sort_min_max(yv[3], yv[7]);
+      sort_min_max(yv[0], yv[1]);
+      sort_min_max(yv[2], yv[3]);
+      sort_min_max(yv[4], yv[5]);
+      sort_min_max(yv[6], yv[7]);
+      sort_min_max(yv[2], yv[4]);
+      sort_min_max(yv[3], yv[5]);
+      sort_min_max(yv[1], yv[4]);
+      sort_min_max(yv[3], yv[6]);
+      sort_min_max(yv[1], yv[2]);
+      sort_min_max(yv[3], yv[4]);
+      sort_min_max(yv[5], yv[6]);
+#pragma unroll
+      for (uint32_t e = 0; e < kSortE; ++e) src[mp_pad(i0 + e)] = yv[e];
+    }
+    block_max_scan(sx, s_part, tid);
+    block_max_scan(sxy, s_part, tid);
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = i0 + e;
+      if (i < n) {
+        t_x += i - sx[e];
+        t_xy += i - sxy[e];
+      }
+    }
+  }
+  // merge sort of y in that order from runs of 8 (the scans' barriers
+  // publish them); a right-run entry is discordant with every larger entry of
+  // its left run.  A left-run entry lands after the entries of the right run
+  // below it, a right-run entry after those of the left run at or below it.
+  for (uint32_t w = kMergeRun; w < P; w <<= 1) {
+    // merge path: thread t writes outputs [8t, 8t + 8) of its pair of runs A
+    // (left) and B (right).  A binary search on its diagonal finds how many
+    // of them come from A; then it merges sequentially, A first on equal
+    // values, and each B entry taken adds the A entries still waiting, all of
+    // them larger.
+    if (active) {
+      const uint32_t b0 = i0 & ~(2 * w - 1);
+      const uint32_t d = i0 - b0;
+      auto at = [&](uint32_t k) { return src[mp_pad(k)]; };
+      const uint32_t bb = b0 + w;
+      uint32_t lo = d > w ? d - w : 0u, hi = d < w ? d : w;
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (at(b0 + mid) <= at(bb + d - 1 - mid)) lo = mid + 1;
+        else hi = mid;
+      }
+      uint32_t i = lo, j = d - lo;
+      Y a = i < w ? at(b0 + i) : (Y)0, b = j < w ? at(bb + j) : (Y)0;
+#pragma unroll
+      for (uint32_t e = 0; e < kSortE; ++e) {
+        const bool take_a = i < w && (j >= w || a <= b);
+        dst[mp_pad(i0 + e)] = take_a ? a : b;
+        if (take_a) {
+          ++i;
+          a = i < w ? at(b0 + i) : (Y)0;
+        } else {
+          inv += w - i;
+          ++j;
+          b = j < w ? at(bb + j) : (Y)0;
+        }
+      }
+    }
+    level_sync(w, P);
+    Y* tmp = src;
+    src = dst;
+    dst = tmp;
+  }
+  // pairs tied in y: each entry counts the earlier equal entries of the
+  // sorted y (real entries hold positions [0, n): the padding sorts last)
+  {
+    uint32_t sy[kSortE];
+    Y py = i0 > 0 && i0 < P ? src[mp_pad(i0 - 1)] : (Y)0;
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = i0 + e;
+      const bool ok = i < P;
+      const Y yk = ok ? src[mp_pad(i)] : (Y)0;
+      sy[e] = ok && (i == 0 || yk != py) ? i : 0u;
+      py = yk;
+    }
+    block_max_scan(sy, s_part, tid);
+#pragma unroll
+    for (uint32_t e = 0; e < kSortE; ++e) {
+      const uint32_t i = i0 + e;
+      if (i < n) t_y += i - sy[e];
+    }
+  }
+  cnt[0] = inv;
+  cnt[1] = t_x;
+  cnt[2] = t_y;
+  cnt[3] = t_xy;
+}
+
 __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
                                                                   uint64_t n_x, const float* x,
                                                                   const uint64_t* y,
                                                                   const uint32_t* idx,
                                                                   uint64_t* counts, uint8_t* top1) {
-  // [P] y, then merge buffer A; [P] merge buffer B, which holds the x keys
-  // until the merge sort starts (two buffers of P + P/8 entries, 18 B of LDS
-  // per entry: 72 KiB at 4,096, so two snapshots share a CU)
+  // two buffers of P + P/8 8-byte entries (18 B of LDS per entry with the
+  // padding: 72 KiB at 4,096, so two snapshots share a CU)
   extern __shared__ uint64_t s_dyn[];
-  uint64_t* s_ky = s_dyn;
-  uint64_t* s_yb = s_dyn + sort_buf(P);
-  uint32_t* s_kx = reinterpret_cast<uint32_t*>(s_yb);
   __shared__ uint64_t s_sum[4][kSortBlock / 64];
   __shared__ float s_bx[kSortBlock / 64];
   __shared__ uint32_t s_bxi[kSortBlock / 64], s_byi[kSortBlock / 64];
   __shared__ uint64_t s_by[kSortBlock / 64];
-  __shared__ uint32_t s_bad;
+  __shared__ uint32_t s_bad, s_wide;
   __shared__ uint32_t s_part[kSortBlock / 64];
+  __shared__ uint64_t s_ek[kSortBlock / 64];
+  __shared__ uint32_t s_er[kSortBlock / 64];
   const uint32_t snap = blockIdx.x;
   const uint32_t tid = threadIdx.x;
   const size_t base = (size_t)snap * n_per;
   const uint32_t n = n_per;
 
-  // gather, both argmaxes (ties to the earlier position), padding that sorts last
-  if (tid == 0) s_bad = 0;
+  // gather each thread's 8 consecutive entries into registers, both argmaxes
+  // (ties to the earlier position), padding that sorts last, and whether a y
+  // other than 2^64 - 1 reaches 2^32 - 1
+  if (tid == 0) {
+    s_bad = 0;
+    s_wide = 0;
+  }
   __syncthreads();
   float bx = 0.0f;
   uint32_t bxi = kNone, byi = kNone;
   uint64_t by = 0;
-  for (uint32_t i = tid; i < P; i += kSortBlock) {
+  const uint32_t i0 = tid * kSortE;
+  uint32_t kx[kSortE];
+  uint64_t ky[kSortE];
+  bool wide = false;
+#pragma unroll
+  for (uint32_t c = 0; c < kSortE; ++c) {
+    const uint32_t i = i0 + c;
+    kx[c] = 0xFFFFFFFFu;
+    ky[c] = ~0ull;
     if (i < n) {
       size_t e = idx ? (size_t)idx[base + i] : base + i;
       if (e >= n_x) {
@@ -327,15 +625,14 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
       }
       const float xv = x[e];
       const uint64_t yv = y[e];
-      s_kx[i] = float_key(__float_as_uint(xv));
-      s_ky[i] = yv;
+      kx[c] = float_key(__float_as_uint(xv));
+      ky[c] = yv;
+      wide = wide || (yv != ~0ull && yv >= 0xFFFFFFFFull);
       if (bxi == kNone || fbetter(xv, i, bx, bxi)) { bx = xv; bxi = i; }
       if (byi == kNone || ubetter(yv, i, by, byi)) { by = yv; byi = i; }
-    } else {
-      s_kx[i] = 0xFFFFFFFFu;
-      s_ky[i] = ~0ull;
     }
   }
+  if (wide) s_wide = 1;
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) {
     const float ox = __shfl_xor(bx, m);
@@ -353,194 +650,9 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
   }
   __syncthreads();
 
-  uint64_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
-  // bitonic sort of the P pairs by (x, y); a pass's compare-exchanges touch
-  // disjoint pairs, so each thread loads all of its pairs before storing any
-  for (uint32_t k = 2; k <= P; k <<= 1) {
-    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-      uint32_t ia[kSortQ], xa[kSortQ], xb[kSortQ];
-      uint64_t ya[kSortQ], yb[kSortQ];
-#pragma unroll
-      for (uint32_t q = 0; q < kSortQ; ++q) {
-        const uint32_t t = tid + q * kSortBlock;
-        const uint32_t i = t < (P >> 1) ? ((t & ~(j - 1)) << 1) | (t & (j - 1)) : 0u;
-        ia[q] = t < (P >> 1) ? i : ~0u;
-        xa[q] = s_kx[i];
-        xb[q] = s_kx[i + j];
-        ya[q] = s_ky[i];
-        yb[q] = s_ky[i + j];
-      }
-#pragma unroll
-      for (uint32_t q = 0; q < kSortQ; ++q) {
-        const uint32_t i = ia[q];
-        if (i != ~0u) {
-          const bool up = (i & k) == 0;
-          if (up ? pair_less(xb[q], yb[q], xa[q], ya[q]) : pair_less(xa[q], ya[q], xb[q], yb[q])) {
-            s_kx[i] = xb[q];
-            s_kx[i + j] = xa[q];
-            s_ky[i] = yb[q];
-            s_ky[i + j] = ya[q];
-          }
-        }
-      }
-      if (bitonic_barrier_after(k, j)) __syncthreads();
-      else wave_lds_sync();
-    }
-  }
-  // pairs tied in x, and in x and y: each entry counts the earlier entries of
-  // its run; a run starts where the key differs from the one before, and a
-  // max-scan of those starts gives every entry the start of its run
-  {
-    const uint32_t b = tid * kSortE;
-    uint32_t sx[kSortE], sxy[kSortE];
-    uint32_t px = 0;
-    uint64_t py = 0;
-    if (b > 0 && b < P) {
-      px = s_kx[b - 1];
-      py = s_ky[b - 1];
-    }
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = b + e;
-      const bool ok = i < P;
-      const uint32_t xk = ok ? s_kx[i] : 0u;
-      const uint64_t yk = ok ? s_ky[i] : 0ull;
-      const bool new_x = i == 0 || xk != px;
-      sx[e] = ok && new_x ? i : 0u;
-      sxy[e] = ok && (new_x || yk != py) ? i : 0u;
-      px = xk;
-      py = yk;
-    }
-    block_max_scan(sx, s_part, tid);
-    block_max_scan(sxy, s_part, tid);
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = b + e;
-      if (i < n) {
-        t_x += i - sx[e];
-        t_xy += i - sxy[e];
-      }
-    }
-  }
-  __syncthreads();  // the x keys are read for the last time; buffer B is free
-  // merge sort of y in that order; a right-run entry is discordant with every
-  // larger entry of its left run.  A left-run entry lands after the entries
-  // of the right run below it, a right-run entry after those of the left run
-  // at or below it.
-  uint64_t* src = s_ky;
-  uint64_t* dst = s_yb;
-  uint32_t steps = 1;  // log2(w) + 1 binary-search steps over a run of w
-  for (uint32_t w = 1; w < P; w <<= 1, ++steps) {
-    if (w >= kMergeRun) {
-      // merge path: thread t writes outputs [8t, 8t + 8) of its pair of
-      // runs A (left) and B (right).  A binary search on its diagonal finds
-      // how many of them come from A; then it merges sequentially, A first
-      // on equal values, and each B entry taken adds the A entries still
-      // waiting, all of them larger.
-      const uint32_t o0 = tid * kSortE;
-      if (o0 < P) {
-        const uint32_t b0 = o0 & ~(2 * w - 1);
-        const uint32_t d = o0 - b0;
-        // the first merge-path level reads the plain layout
-        const bool padded = w > kMergeRun;
-        auto at = [&](uint32_t k) { return src[padded ? mp_pad(k) : k]; };
-        const uint32_t bb = b0 + w;
-        uint32_t lo = d > w ? d - w : 0u, hi = d < w ? d : w;
-        while (lo < hi) {
-          const uint32_t mid = (lo + hi) >> 1;
-          if (at(b0 + mid) <= at(bb + d - 1 - mid)) lo = mid + 1;
-          else hi = mid;
-        }
-        uint32_t i = lo, j = d - lo;
-        uint64_t a = i < w ? at(b0 + i) : 0ull, b = j < w ? at(bb + j) : 0ull;
-#pragma unroll
-        for (uint32_t e = 0; e < kSortE; ++e) {
-          const bool take_a = i < w && (j >= w || a <= b);
-          dst[mp_pad(o0 + e)] = take_a ? a : b;
-          if (take_a) {
-            ++i;
-            a = i < w ? at(b0 + i) : 0ull;
-          } else {
-            inv += w - i;
-            ++j;
-            b = j < w ? at(bb + j) : 0ull;
-          }
-        }
-      }
-      level_sync(w, P);
-      uint64_t* tmp = src;
-      src = dst;
-      dst = tmp;
-      continue;
-    }
-    uint32_t lo[kSortE], hi[kSortE], rb[kSortE];
-    uint64_t v[kSortE];
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t p = tid + e * kSortBlock;
-      const bool ok = p < P;
-      const uint32_t b0 = p & ~(2 * w - 1);
-      const bool left = (p - b0) < w;
-      v[e] = ok ? src[p] : 0ull;
-      rb[e] = left ? b0 + w : b0;  // the other run
-      lo[e] = 0;
-      hi[e] = ok ? w : 0u;
-    }
-    for (uint32_t step = 0; step < steps; ++step) {
-#pragma unroll
-      for (uint32_t e = 0; e < kSortE; ++e) {
-        const uint32_t p = tid + e * kSortBlock;
-        const bool left = (p & (2 * w - 1)) < w;
-        const uint32_t m = (lo[e] + hi[e]) >> 1;
-        const bool open = lo[e] < hi[e];
-        const uint64_t a = src[open ? rb[e] + m : 0u];
-        const bool goes_right = left ? a < v[e] : a <= v[e];
-        lo[e] = open && goes_right ? m + 1 : lo[e];
-        hi[e] = open && !goes_right ? m : hi[e];
-      }
-    }
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t p = tid + e * kSortBlock;
-      if (p < P) {
-        const uint32_t b0 = p & ~(2 * w - 1);
-        const uint32_t off = p - b0;
-        if (off < w) {
-          dst[b0 + off + lo[e]] = v[e];
-        } else {
-          dst[b0 + (off - w) + lo[e]] = v[e];
-          inv += w - lo[e];
-        }
-      }
-    }
-    level_sync(w, P);
-    uint64_t* tmp = src;
-    src = dst;
-    dst = tmp;
-  }
-  // pairs tied in y: each entry counts the earlier equal entries of the
-  // sorted y (real entries hold positions [0, n): the padding sorts last)
-  {
-    const uint32_t b = tid * kSortE;
-    uint32_t sy[kSortE];
-    uint64_t py = b > 0 && b < P ? src[mp_pad(b - 1)] : 0ull;
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = b + e;
-      const bool ok = i < P;
-      const uint64_t yk = ok ? src[mp_pad(i)] : 0ull;
-      sy[e] = ok && (i == 0 || yk != py) ? i : 0u;
-      py = yk;
-    }
-    block_max_scan(sy, s_part, tid);
-#pragma unroll
-    for (uint32_t e = 0; e < kSortE; ++e) {
-      const uint32_t i = b + e;
-      if (i < n) t_y += i - sy[e];
-    }
-  }
-
-  uint64_t v[4] = {inv, t_x, t_y, t_xy};
+  uint64_t v[4];
+  if (s_wide) sorted_counts<false>(kx, ky, P, n, tid, s_dyn, s_ek, s_er, s_part, v);
+  else sorted_counts<true>(kx, ky, P, n, tid, s_dyn, s_ek, s_er, s_part, v);
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
 #pragma unroll
@@ -631,10 +743,10 @@ int kendall_barrier_after(uint32_t P, uint32_t step, uint32_t a, uint32_t b) {
   if (P < kKendallSortFrom || P > kKendallMax || (P & (P - 1))) return -1;
   if (step == 0) {  // bitonic pass (k = a, j = b)
     if (a < 2 || a > P || (a & (a - 1)) || b == 0 || b >= a || (b & (b - 1))) return -1;
-    return bitonic_barrier_after(a, b) ? 1 : 0;
+    return bitonic_barrier_after(P, a, b) ? 1 : 0;
   }
-  if (step == 1) {  // merge level w = a
-    if (a == 0 || a >= P || (a & (a - 1))) return -1;
+  if (step == 1) {  // merge level w = a (runs below 8 are merged in registers)
+    if (a < kMergeRun || a >= P || (a & (a - 1))) return -1;
     return merge_barrier_after(a, P) ? 1 : 0;
   }
   return -1;

@@ -135,6 +135,30 @@ def test_kendall_sorted_path_heavy_ties(U, n_per):
     assert np.array_equal(t.cpu().numpy(), ot)
 
 
+@pytest.mark.parametrize("n_per", [300, 4096])
+def test_kendall_sorted_path_at_the_32_bit_key_boundary(U, n_per):
+    """A snapshot packs (x, y) into one 64-bit key only while every y other
+    than 2^64 - 1 lies below 2^32 - 1 (2^64 - 1 then stands in as 2^32 - 1):
+    y values at 2^32 - 2, 2^32 - 1 and 2^32 beside 2^64 - 1, each snapshot on
+    its side of the boundary, with ties in both scores."""
+    rng = np.random.default_rng(7 + n_per)
+    n_snap = 4
+    x = rng.integers(0, 9, (n_snap, n_per)).astype(np.float32)
+    top = np.array([2 ** 32 - 2, 2 ** 32 - 1, 2 ** 32, 2 ** 64 - 1], np.uint64)
+    y = rng.integers(0, 6, (n_snap, n_per)).astype(np.uint64)
+    y[0, ::4] = top[0]                      # narrow: the largest packed value
+    y[0, 1::4] = top[3]
+    y[1, ::4] = top[1]                      # wide: 2^32 - 1 is a real value
+    y[1, 1::4] = top[3]
+    y[2, ::3] = top[2]                      # wide
+    y[2, 1::3] = top[0]
+    y[3, ::5] = top[3]                      # narrow, only the done value above
+    c, t = U.kendall(dev(U, x.ravel()), dev(U, y.ravel(), np.uint64), None, n_snap, n_per)
+    oc, ot = oracle.kendall(x, y)
+    assert np.array_equal(U._host(c, np.uint64), oc)
+    assert np.array_equal(t.cpu().numpy(), ot)
+
+
 def test_kendall_rejects_out_of_range_index(U):
     x = np.arange(10, dtype=np.float32)
     y = np.arange(10, dtype=np.uint64)

@@ -9,7 +9,14 @@ wavefronts may be at any of the steps in between, so within each such
 segment no entry one wavefront writes may be read or written by another.
 This test rebuilds every step's per-wavefront read and write sets from the
 kernel's index maps and checks that rule for every padded size, with the
-barrier plan the library itself reports (unison_debug_kendall_barrier)."""
+barrier plan the library itself reports (unison_debug_kendall_barrier).
+
+The bitonic passes run in groups of up to three in registers: a group loads
+its entries before its first pass and stores them after its last.  The sort
+keys are 8-byte entries of the first buffer (A); the 4-byte tie-breakers of
+the wide form live in the second (B), as do the y values of the first merge
+level, 4 or 8 bytes each by the form.  Accesses are modelled as the 4-byte
+words they touch, so the aliasing between those uses is exact."""
 import os
 
 import pytest
@@ -25,65 +32,104 @@ def mp_pad(i):
     return i + i // 8
 
 
-def bitonic_steps(P):
-    """(('bitonic', k, j), accesses) per pass; accesses[w] = (reads, writes) of
-    wavefront w as sets of (buffer, entry): kx are the 32-bit x keys, A the
-    y keys."""
+def group_top(L, s):
+    return L - 1 - 3 * ((L - 1 - s) // 3)
+
+
+def group_low(top):
+    return top - 2 if top >= 2 else 0
+
+
+def words(buf, i, size):
+    """The 4-byte words of entry i (padded) of a buffer of size-byte entries."""
+    w = size // 4
+    return [(buf, mp_pad(i) * w + k) for k in range(w)]
+
+
+def sort_words(i):
+    """An entry's sort key (A, 8 B) and wide-form tie-breaker (B, 4 B)."""
+    return words("A", i, 8) + words("B", i, 4)
+
+
+def bitonic_steps(P, ysize=8):
+    """(('bitonic', k, j), accesses) per pass, then ('final',): accesses[w] =
+    (reads, writes) of wavefront w as sets of (buffer, word).  Stages 2, 4 and
+    8 run on each thread's 8 consecutive entries from the gather and store
+    them at the end; from stage 16 on, a group with low bit b holds the
+    entries that differ from the thread's base only in bits b..b+2.  The last
+    group keeps its entries; after its barrier they are stored, sorted by y
+    within each thread, as the merge input in B."""
     steps = []
-    k = 2
-    while k <= P:
+    n_w = BLOCK // WAVE
+
+    def empty():
+        return [(set(), set()) for _ in range(n_w)]
+
+    for k in (2, 4, 8):
         j = k // 2
         while j >= 1:
-            acc = [(set(), set()) for _ in range(BLOCK // WAVE)]
-            for t in range(BLOCK):
-                r, wr = acc[t // WAVE]
-                for q in range(PER_T // 2):
-                    tt = t + q * BLOCK
-                    if tt >= P // 2:
+            acc = empty()
+            if k == 8 and j == 1:
+                for t in range(BLOCK):
+                    if t * PER_T >= P:
                         continue
-                    i = ((tt & ~(j - 1)) << 1) | (tt & (j - 1))
-                    for e in (i, i + j):
-                        for buf in ("kx", "A"):
-                            r.add((buf, e))
-                            wr.add((buf, e))
+                    for c in range(PER_T):
+                        for e in sort_words(t * PER_T + c):
+                            acc[t // WAVE][1].add(e)
             steps.append((("bitonic", k, j), acc))
             j //= 2
+    k, L = 16, 4
+    while k <= P:
+        for s in range(L - 1, -1, -1):
+            top = group_top(L, s)
+            lo = group_low(top)
+            acc = empty()
+            first, last = s == top, s == lo
+            for t in range(BLOCK):
+                base = ((t >> lo) << (lo + 3)) | (t & ((1 << lo) - 1))
+                if base >= P:
+                    continue
+                r, wr = acc[t // WAVE]
+                for c in range(PER_T):
+                    for e in sort_words(base | (c << lo)):
+                        if first:
+                            r.add(e)
+                        if last and not (k == P and s == 0):
+                            wr.add(e)
+            steps.append((("bitonic", k, 1 << s), acc))
         k *= 2
+        L += 1
+    acc = empty()
+    for t in range(BLOCK):
+        for c in range(PER_T):
+            i = t * PER_T + c
+            if i < P:
+                acc[t // WAVE][1].update(words("B", i, ysize))
+    steps.append((("final",), acc))
     return steps
 
 
-def merge_steps(P):
-    """(('merge', w), accesses) per merge level.  Level L reads buffer A when L
-    is even (B when odd) and writes the other.  Levels of runs below 8 place
-    entry p = t + 512 e by a binary search in the other run; from 8 on, thread
-    t merges outputs [8t, 8t + 8), reading anywhere in its pair of runs (in
-    the padded layout after the first such level) and storing padded."""
+def merge_steps(P, ysize=8):
+    """(('merge', w), accesses) per merge level from runs of 8 (y values of
+    ysize bytes).  The first
+    level reads B (the per-thread sorted groups), and the levels alternate;
+    thread t merges outputs [8t, 8t + 8), reading anywhere in its pair of
+    runs and storing padded."""
     steps = []
-    w, lvl = 1, 0
+    w, lvl = 8, 0
     while w < P:
-        src, dst = ("A", "B") if lvl % 2 == 0 else ("B", "A")
+        src, dst = ("B", "A") if lvl % 2 == 0 else ("A", "B")
         acc = [(set(), set()) for _ in range(BLOCK // WAVE)]
         for t in range(BLOCK):
             r, wr = acc[t // WAVE]
-            if w < 8:
-                for e in range(PER_T):
-                    p = t + e * BLOCK
-                    if p >= P:
-                        continue
-                    b0 = p & ~(2 * w - 1)
-                    for q in range(b0, b0 + 2 * w):     # own entry and the other run
-                        r.add((src, q))
-                        wr.add((dst, q))                # lands inside the pair of runs
-            else:
-                o0 = t * PER_T
-                if o0 >= P:
-                    continue
-                b0 = o0 & ~(2 * w - 1)
-                pad = (lambda i: mp_pad(i)) if w > 8 else (lambda i: i)
-                for q in range(b0, b0 + 2 * w):
-                    r.add((src, pad(q)))
-                for e in range(PER_T):
-                    wr.add((dst, mp_pad(o0 + e)))
+            o0 = t * PER_T
+            if o0 >= P:
+                continue
+            b0 = o0 & ~(2 * w - 1)
+            for q in range(b0, b0 + 2 * w):
+                r.update(words(src, q, ysize))
+            for e in range(PER_T):
+                wr.update(words(dst, o0 + e, ysize))
         steps.append((("merge", w), acc))
         w *= 2
         lvl += 1
@@ -122,7 +168,9 @@ def lib():
 def plan(lib, P, steps):
     out = []
     for name, _ in steps:
-        if name[0] == "bitonic":
+        if name[0] == "final":
+            b = 1          # the scans of the sorted runs start with workgroup barriers
+        elif name[0] == "bitonic":
             b = lib.unison_debug_kendall_barrier(P, 0, name[1], name[2])
         else:
             b = lib.unison_debug_kendall_barrier(P, 1, name[1], 0)
@@ -132,36 +180,54 @@ def plan(lib, P, steps):
 
 
 @pytest.mark.parametrize("P", SIZES)
-def test_bitonic_passes_share_no_entry_across_wavefronts_between_barriers(lib, P):
-    steps = bitonic_steps(P)
+@pytest.mark.parametrize("ysize", [4, 8])
+def test_bitonic_groups_share_no_entry_across_wavefronts_between_barriers(lib, P, ysize):
+    steps = bitonic_steps(P, ysize)
     bar = plan(lib, P, steps)
-    assert bar[-1], "the last pass is followed by the run-start scan"
-    assert not races(steps, bar)
+    names = [s[0] for s in steps]
+    assert bar[names.index(("bitonic", P, 1))], "the last group is read before the merge input is stored"
+    assert not races(steps, bar), races(steps, bar)[:3]
     assert not all(bar), "the plan should skip some barriers"
 
 
 @pytest.mark.parametrize("P", SIZES)
-def test_merge_levels_share_no_entry_across_wavefronts_between_barriers(lib, P):
-    steps = merge_steps(P)
+@pytest.mark.parametrize("ysize", [4, 8])
+def test_merge_levels_share_no_entry_across_wavefronts_between_barriers(lib, P, ysize):
+    steps = merge_steps(P, ysize)
     bar = plan(lib, P, steps)
     assert bar[-1], "the last level is followed by the scan of the sorted y"
     assert not races(steps, bar), races(steps, bar)[:3]
 
 
-def test_model_flags_a_barrier_taken_out():
-    """The model is not vacuous: dropping the barrier after the first merge-
-    path level (w = 8) of a 4,096-entry snapshot, where the next level's
-    padded stores reach the entries the neighbouring wavefront reads at w = 8,
-    is reported, and so is a plan without any workgroup barrier."""
-    steps = merge_steps(4096)
-    bar = [True] * len(steps)
-    assert not races(steps, bar)
-    names = [s[0] for s in steps]
-    i8 = names.index(("merge", 8))
-    bar[i8] = False
-    found = races(steps, bar)
-    assert found and all(f[0] == i8 + 1 for f in found)
+@pytest.mark.parametrize("ysize", [4, 8])
+def test_whole_plan_shares_no_entry_across_wavefronts_between_barriers(lib, ysize):
+    """Sort and merge as one sequence at 4,096 entries: the tie-breakers share
+    B with the merge input and the later levels, the keys share A with them."""
+    steps = bitonic_steps(4096, ysize) + merge_steps(4096, ysize)
+    assert not races(steps, plan(lib, 4096, steps))
+
+
+def test_model_flags_a_barrier_taken_out(lib):
+    """The model is not vacuous: dropping any one workgroup barrier the
+    library places between groups of cross-wavefront passes, or between merge
+    levels, is reported, and so is a plan without any workgroup barrier."""
+    for steps in (bitonic_steps(4096), merge_steps(4096)):
+        bar = plan(lib, 4096, steps)
+        assert not races(steps, bar)
+        flagged = 0
+        for i in range(len(steps) - 1):
+            if bar[i]:
+                cut = list(bar)
+                cut[i] = False
+                flagged += bool(races(steps, cut))
+        assert flagged >= 3
     assert races(bitonic_steps(1024), [False] * len(bitonic_steps(1024)))
+    # before the merge input is stored, every wavefront must have read its last group
+    steps = bitonic_steps(4096)
+    bar = plan(lib, 4096, steps)
+    names = [s[0] for s in steps]
+    bar[names.index(("bitonic", 4096, 1))] = False
+    assert races(steps, bar)
 
 
 def test_invalid_steps_are_refused(lib):
@@ -169,5 +235,6 @@ def test_invalid_steps_are_refused(lib):
     assert lib.unison_debug_kendall_barrier(100, 1, 8, 0) == E_INVALID      # not a power of two
     assert lib.unison_debug_kendall_barrier(8192, 1, 8, 0) == E_INVALID     # above 4,096
     assert lib.unison_debug_kendall_barrier(1024, 1, 3, 0) == E_INVALID
+    assert lib.unison_debug_kendall_barrier(1024, 1, 4, 0) == E_INVALID     # merged in registers
     assert lib.unison_debug_kendall_barrier(1024, 0, 8, 8) == E_INVALID     # stride >= stage
     assert lib.unison_debug_kendall_barrier(1024, 2, 1, 1) == E_INVALID
