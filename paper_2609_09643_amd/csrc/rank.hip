@@ -216,7 +216,7 @@ constexpr uint32_t kMergeRun = 8;
 // Sort and merge buffers store entry i at i + i / 8: a thread's 8 consecutive
 // entries then start 72 B after its neighbour's, not 64 B, and the bitonic
 // groups below spread their accesses over the banks as well.
-__device__ __forceinline__ uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
+__host__ __device__ constexpr uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
 // Entries of each sort buffer, the padding included.
 __host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
 
@@ -314,16 +314,16 @@ static_assert(kSortE == 8 && kSortE * kSortBlock == kKendallMax, "8 outputs per 
 template <bool NARROW>
 __device__ __forceinline__ void sort_cx(uint64_t& ka, uint32_t& ra, uint64_t& kb, uint32_t& rb,
                                         bool up) {
-  const bool b_first = NARROW ? kb < ka : (kb < ka || (kb == ka && rb < ra));
-  if (b_first == up) {
-    const uint64_t tk = ka;
-    ka = kb;
-    kb = tk;
-    if (!NARROW) {
-      const uint32_t tr = ra;
-      ra = rb;
-      rb = tr;
-    }
+  // selects, not a branch: the lanes of a pass swap independently
+  const bool b_first = NARROW ? kb < ka : ((kb < ka) | ((kb == ka) & (rb < ra)));
+  const bool sw = b_first == up;
+  const uint64_t k0 = sw ? kb : ka, k1 = sw ? ka : kb;
+  ka = k0;
+  kb = k1;
+  if (!NARROW) {
+    const uint32_t r0 = sw ? rb : ra, r1 = sw ? ra : rb;
+    ra = r0;
+    rb = r1;
   }
 }
 
@@ -336,10 +336,88 @@ __device__ __forceinline__ void sort_pass(uint64_t (&kk)[kSortE], uint32_t (&kr)
       sort_cx<NARROW>(kk[c], kr[c], kk[c | (1u << M)], kr[c | (1u << M)], up);
 }
 
-template <class Y>
-__device__ __forceinline__ void sort_min_max(Y& a, Y& b) {
-  const Y lo = a < b ? a : b;
-  b = a < b ? b : a;
+// The thread's entries of the group with low bit lo sit at the padded
+// position of its base plus the padded position of c << lo (the base's bits
+// below lo and those of c << lo never carry into each other).
+__device__ __forceinline__ uint32_t group_base(uint32_t tid, uint32_t lo) {
+  return ((tid >> lo) << (lo + 3)) | (tid & ((1u << lo) - 1u));
+}
+
+// A full group (three passes) with low bit lo >= 1: the offsets are the same
+// for every lane.
+template <bool NARROW>
+__device__ __forceinline__ void sort_group3(uint32_t lo, uint64_t (&kk)[kSortE],
+                                            uint32_t (&kr)[kSortE], uint64_t* s_k,
+                                            uint32_t* s_r, uint32_t tid, uint32_t P, uint32_t k) {
+  const uint32_t gb = group_base(tid, lo);
+  if (gb >= P) return;
+  uint64_t* gk = s_k + mp_pad(gb);
+  uint32_t* gr = s_r + mp_pad(gb);
+#pragma unroll
+  for (uint32_t c = 0; c < kSortE; ++c) {
+    const uint32_t off = __builtin_amdgcn_readfirstlane(mp_pad(c << lo));
+    kk[c] = gk[off];
+    kr[c] = NARROW ? 0u : gr[off];
+  }
+  const bool up = (gb & k) == 0;
+  sort_pass<2, NARROW>(kk, kr, up);
+  sort_pass<1, NARROW>(kk, kr, up);
+  sort_pass<0, NARROW>(kk, kr, up);
+#pragma unroll
+  for (uint32_t c = 0; c < kSortE; ++c) {
+    const uint32_t off = __builtin_amdgcn_readfirstlane(mp_pad(c << lo));
+    gk[off] = kk[c];
+    if (!NARROW) gr[off] = kr[c];
+  }
+}
+
+// The last group of a stage: low bit 0 (the thread's 8 consecutive entries),
+// NP passes.  LAST: the stage-P group that ends the sort keeps its entries in
+// registers.
+template <uint32_t NP, bool NARROW, bool LAST>
+__device__ __forceinline__ void sort_group0(uint64_t (&kk)[kSortE], uint32_t (&kr)[kSortE],
+                                            uint64_t* s_k, uint32_t* s_r, uint32_t tid,
+                                            uint32_t P, uint32_t k) {
+  const uint32_t gb = tid * kSortE;
+  if (gb >= P) return;
+  const uint32_t pb = mp_pad(gb);
+#pragma unroll
+  for (uint32_t c = 0; c < kSortE; ++c) {
+    kk[c] = s_k[pb + c];
+    kr[c] = NARROW ? 0u : s_r[pb + c];
+  }
+  const bool up = (gb & k) == 0;
+  if (NP == 3) sort_pass<2, NARROW>(kk, kr, up);
+  if (NP >= 2) sort_pass<1, NARROW>(kk, kr, up);
+  sort_pass<0, NARROW>(kk, kr, up);
+  if (!LAST) {
+#pragma unroll
+    for (uint32_t c = 0; c < kSortE; ++c) {
+      s_k[pb + c] = kk[c];
+      if (!NARROW) s_r[pb + c] = kr[c];
+    }
+  }
+}
+
+template <bool NARROW, bool LAST>
+__device__ __forceinline__ void sort_group0_at(uint32_t top, uint64_t (&kk)[kSortE],
+                                               uint32_t (&kr)[kSortE], uint64_t* s_k,
+                                               uint32_t* s_r, uint32_t tid, uint32_t P,
+                                               uint32_t k) {
+  if (top == 0) sort_group0<1, NARROW, LAST>(kk, kr, s_k, s_r, tid, P, k);
+  else if (top == 1) sort_group0<2, NARROW, LAST>(kk, kr, s_k, s_r, tid, P, k);
+  else sort_group0<3, NARROW, LAST>(kk, kr, s_k, s_r, tid, P, k);
+}
+
+__device__ __forceinline__ void sort_min_max(uint32_t& a, uint32_t& b) {
+  const uint32_t lo = min(a, b);
+  b = max(a, b);
+  a = lo;
+}
+__device__ __forceinline__ void sort_min_max(uint64_t& a, uint64_t& b) {
+  const bool sw = b < a;
+  const uint64_t lo = sw ? b : a;
+  b = sw ? a : b;
   a = lo;
 }
 
@@ -352,9 +430,10 @@ __device__ __forceinline__ void sort_min_max(Y& a, Y& b) {
 // y -> (y == 2^64 - 1 ? 2^32 - 1 : y) keeps the order and the ties of y, and
 // (x, y) packs into one 64-bit key; otherwise the key is x with the upper
 // half of y, and the lower half breaks its ties.
-// LDS: two buffers of sort_buf(P) 8-byte entries.  The keys sort in the
-// first (the tie-breakers in the second); the merge sort of y starts in the
-// second and alternates.
+// LDS: the keys sort in a buffer of sort_buf(P) 8-byte entries.  NARROW: the
+// merge sort of y then runs in that buffer's two halves (4-byte values);
+// otherwise a second such buffer holds the tie-breakers, and the merge sort
+// of y starts there and alternates between the two.
 template <bool NARROW>
 __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
                                               const uint64_t (&ky)[kSortE], uint32_t P,
@@ -402,33 +481,18 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   // then the grouped passes of stages 16 ... P; the last group keeps the
   // thread's 8 consecutive sorted entries in registers
   for (uint32_t L = 4, k = 16; k <= P; ++L, k <<= 1) {
-    for (int top = (int)L - 1; top >= 0; top -= 3) {
-      const uint32_t lo = group_low((uint32_t)top);
-      const uint32_t gb = ((tid >> lo) << (lo + 3)) | (tid & ((1u << lo) - 1u));
-      const bool last = k == P && lo == 0;
-      if (gb < P) {
-#pragma unroll
-        for (uint32_t c = 0; c < kSortE; ++c) {
-          const uint32_t at = mp_pad(gb | (c << lo));
-          kk[c] = s_k[at];
-          kr[c] = NARROW ? 0u : s_r[at];
-        }
-        const bool up = (gb & k) == 0;
-        const uint32_t np = (uint32_t)top - lo + 1;
-        if (np == 3) sort_pass<2, NARROW>(kk, kr, up);
-        if (np >= 2) sort_pass<1, NARROW>(kk, kr, up);
-        sort_pass<0, NARROW>(kk, kr, up);
-        if (!last) {
-#pragma unroll
-          for (uint32_t c = 0; c < kSortE; ++c) {
-            const uint32_t at = mp_pad(gb | (c << lo));
-            s_k[at] = kk[c];
-            if (!NARROW) s_r[at] = kr[c];
-          }
-        }
-      }
-      if (last) break;
+    uint32_t top = L - 1;
+    for (; top >= 3; top -= 3) {
+      const uint32_t lo = top - 2;
+      sort_group3<NARROW>(lo, kk, kr, s_k, s_r, tid, P, k);
       if (bitonic_barrier_after(P, k, 1u << lo)) __syncthreads();
+      else wave_lds_sync();
+    }
+    if (k == P) {
+      sort_group0_at<NARROW, true>(top, kk, kr, s_k, s_r, tid, P, k);
+    } else {
+      sort_group0_at<NARROW, false>(top, kk, kr, s_k, s_r, tid, P, k);
+      if (bitonic_barrier_after(P, k, 1u)) __syncthreads();
       else wave_lds_sync();
     }
   }
@@ -437,7 +501,7 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
     s_ek[tid >> 6] = kk[kSortE - 1];
     s_er[tid >> 6] = kr[kSortE - 1];
   }
-  __syncthreads();  // every group is read: the tie-breakers' buffer is free
+  __syncthreads();  // every group is read: the merge buffers are free
   uint64_t pk = __shfl_up(kk[kSortE - 1], 1);
   uint32_t pr = __shfl_up(kr[kSortE - 1], 1);
   if ((tid & 63u) == 0 && tid > 0) {
@@ -446,8 +510,8 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   }
 
   uint64_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
-  Y* src = reinterpret_cast<Y*>(s_dyn + sort_buf(P));
-  Y* dst = reinterpret_cast<Y*>(s_dyn);
+  Y* src = NARROW ? reinterpret_cast<Y*>(s_dyn) : reinterpret_cast<Y*>(s_dyn + sort_buf(P));
+  Y* dst = NARROW ? reinterpret_cast<Y*>(s_dyn) + sort_buf(P) : reinterpret_cast<Y*>(s_dyn);
   // pairs tied in x, and in x and y: each entry counts the earlier entries of
   // its run; a run starts where the key differs from the one before, and a
   // max-scan of those starts gives every entry the start of its run
@@ -470,10 +534,12 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
     // merge levels of runs 1, 2 and 4 stay inside the thread's 8 entries:
     // their discordant pairs are the inversions among those 8 y values
     if (active) {
+      uint32_t inv8 = 0;
 #pragma unroll
       for (uint32_t p = 0; p < kSortE; ++p)
 #pragma unroll
-        for (uint32_t q = p + 1; q < kSortE; ++q) inv += yv[p] > yv[q] ? 1u : 0u;
+        for (uint32_t q = p + 1; q < kSortE; ++q) inv8 += yv[p] > yv[q] ? 1u : 0u;
+      inv += inv8;
       // a 19-comparator sorting network on 8 inputs
       sort_min_max(yv[0], yv[2]);
       sort_min_max(yv[1], yv[3]);
@@ -529,21 +595,22 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
         if (at(b0 + mid) <= at(bb + d - 1 - mid)) lo = mid + 1;
         else hi = mid;
       }
-      uint32_t i = lo, j = d - lo;
-      Y a = i < w ? at(b0 + i) : (Y)0, b = j < w ? at(bb + j) : (Y)0;
+      // each step reloads only the run it took from (selects, not a
+      // branch; an index past its run is clamped and its value never used)
+      uint32_t i = lo, j = d - lo, waiting = 0;
+      Y a = at(b0 + min(i, w - 1)), b = at(bb + min(j, w - 1));
 #pragma unroll
       for (uint32_t e = 0; e < kSortE; ++e) {
-        const bool take_a = i < w && (j >= w || a <= b);
+        const bool take_a = (i < w) & ((j >= w) | (a <= b));
         dst[mp_pad(i0 + e)] = take_a ? a : b;
-        if (take_a) {
-          ++i;
-          a = i < w ? at(b0 + i) : (Y)0;
-        } else {
-          inv += w - i;
-          ++j;
-          b = j < w ? at(bb + j) : (Y)0;
-        }
+        waiting += take_a ? 0u : w - i;
+        i += take_a ? 1u : 0u;
+        j += take_a ? 0u : 1u;
+        const Y v = at(take_a ? b0 + min(i, w - 1) : bb + min(j, w - 1));
+        a = take_a ? v : a;
+        b = take_a ? b : v;
       }
+      inv += waiting;
     }
     level_sync(w, P);
     Y* tmp = src;
@@ -576,13 +643,21 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   cnt[3] = t_xy;
 }
 
+// The top-1 value a snapshot keeps between the two launches when its y values
+// need the wide form.
+constexpr uint8_t kWideMark = 254;
+
+// NARROW: every snapshot whose y values pack (see sorted_counts) is counted
+// here with half the LDS, so four snapshots share a CU; the others are left
+// marked in top1.  Otherwise only the marked snapshots are counted.
+template <bool NARROW>
 __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
                                                                   uint64_t n_x, const float* x,
                                                                   const uint64_t* y,
                                                                   const uint32_t* idx,
                                                                   uint64_t* counts, uint8_t* top1) {
-  // two buffers of P + P/8 8-byte entries (18 B of LDS per entry with the
-  // padding: 72 KiB at 4,096, so two snapshots share a CU)
+  // one (NARROW) or two buffers of P + P/8 8-byte entries: 36 or 72 KiB at
+  // 4,096 entries
   extern __shared__ uint64_t s_dyn[];
   __shared__ uint64_t s_sum[4][kSortBlock / 64];
   __shared__ float s_bx[kSortBlock / 64];
@@ -596,6 +671,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
   const uint32_t tid = threadIdx.x;
   const size_t base = (size_t)snap * n_per;
   const uint32_t n = n_per;
+  if (!NARROW && top1[snap] != kWideMark) return;
 
   // gather each thread's 8 consecutive entries into registers, both argmaxes
   // (ties to the earlier position), padding that sorts last, and whether a y
@@ -650,9 +726,12 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
   }
   __syncthreads();
 
+  if (NARROW && __builtin_amdgcn_readfirstlane(s_wide)) {
+    if (tid == 0) top1[snap] = kWideMark;
+    return;
+  }
   uint64_t v[4];
-  if (s_wide) sorted_counts<false>(kx, ky, P, n, tid, s_dyn, s_ek, s_er, s_part, v);
-  else sorted_counts<true>(kx, ky, P, n, tid, s_dyn, s_ek, s_er, s_part, v);
+  sorted_counts<NARROW>(kx, ky, P, n, tid, s_dyn, s_ek, s_er, s_part, v);
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
 #pragma unroll
@@ -728,9 +807,12 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
   } else {
     uint32_t P = 2;
     while (P < n_per) P <<= 1;
-    const size_t lds = (size_t)sort_buf(P) * 2 * sizeof(uint64_t);
-    hipLaunchKernelGGL(kendall_sort_kernel, dim3(n_snap), dim3(kSortBlock), lds, s, n_per, P, n_x,
-                       x, y, idx, counts, top1);
+    // the packed form first; then the snapshots it left marked
+    const size_t lds = (size_t)sort_buf(P) * sizeof(uint64_t);
+    hipLaunchKernelGGL(kendall_sort_kernel<true>, dim3(n_snap), dim3(kSortBlock), lds, s, n_per, P,
+                       n_x, x, y, idx, counts, top1);
+    hipLaunchKernelGGL(kendall_sort_kernel<false>, dim3(n_snap), dim3(kSortBlock), 2 * lds, s, n_per,
+                       P, n_x, x, y, idx, counts, top1);
   }
   return hipGetLastError();
 }

@@ -13,10 +13,11 @@ barrier plan the library itself reports (unison_debug_kendall_barrier).
 
 The bitonic passes run in groups of up to three in registers: a group loads
 its entries before its first pass and stores them after its last.  The sort
-keys are 8-byte entries of the first buffer (A); the 4-byte tie-breakers of
-the wide form live in the second (B), as do the y values of the first merge
-level, 4 or 8 bytes each by the form.  Accesses are modelled as the 4-byte
-words they touch, so the aliasing between those uses is exact."""
+keys are 8-byte entries of the first buffer (A).  In the narrow form (4-byte
+y values) the merge sort then runs in A's two halves; in the wide form the
+4-byte tie-breakers live in a second buffer (B), where the merge sort of the
+8-byte y values starts.  Accesses are modelled as the 4-byte words they
+touch, so the aliasing between those uses is exact."""
 import os
 
 import pytest
@@ -46,9 +47,23 @@ def words(buf, i, size):
     return [(buf, mp_pad(i) * w + k) for k in range(w)]
 
 
-def sort_words(i):
-    """An entry's sort key (A, 8 B) and wide-form tie-breaker (B, 4 B)."""
-    return words("A", i, 8) + words("B", i, 4)
+def sort_words(i, ysize):
+    """An entry's sort key (A, 8 B) and the wide form's tie-breaker (B, 4 B)."""
+    return words("A", i, 8) + (words("B", i, 4) if ysize == 8 else [])
+
+
+def merge_buffers(P, ysize):
+    """(first source, first destination) of the merge levels: entry q of
+    buffer b lies at words(b[0], q + b[1], ysize)."""
+    if ysize == 4:
+        return ("A", 0), ("A", P + P // 8)      # A's two halves
+    return ("B", 0), ("A", 0)
+
+
+def merge_words(buf, q, ysize):
+    name, shift = buf
+    w = ysize // 4
+    return [(name, (shift + (q + q // 8)) * w + k) for k in range(w)]
 
 
 def bitonic_steps(P, ysize=8):
@@ -74,7 +89,7 @@ def bitonic_steps(P, ysize=8):
                     if t * PER_T >= P:
                         continue
                     for c in range(PER_T):
-                        for e in sort_words(t * PER_T + c):
+                        for e in sort_words(t * PER_T + c, ysize):
                             acc[t // WAVE][1].add(e)
             steps.append((("bitonic", k, j), acc))
             j //= 2
@@ -91,7 +106,7 @@ def bitonic_steps(P, ysize=8):
                     continue
                 r, wr = acc[t // WAVE]
                 for c in range(PER_T):
-                    for e in sort_words(base | (c << lo)):
+                    for e in sort_words(base | (c << lo), ysize):
                         if first:
                             r.add(e)
                         if last and not (k == P and s == 0):
@@ -104,21 +119,21 @@ def bitonic_steps(P, ysize=8):
         for c in range(PER_T):
             i = t * PER_T + c
             if i < P:
-                acc[t // WAVE][1].update(words("B", i, ysize))
+                acc[t // WAVE][1].update(merge_words(merge_buffers(P, ysize)[0], i, ysize))
     steps.append((("final",), acc))
     return steps
 
 
 def merge_steps(P, ysize=8):
     """(('merge', w), accesses) per merge level from runs of 8 (y values of
-    ysize bytes).  The first
-    level reads B (the per-thread sorted groups), and the levels alternate;
-    thread t merges outputs [8t, 8t + 8), reading anywhere in its pair of
-    runs and storing padded."""
+    ysize bytes).  The first level reads the per-thread sorted groups, and the
+    levels alternate; thread t merges outputs [8t, 8t + 8), reading anywhere
+    in its pair of runs and storing padded."""
     steps = []
     w, lvl = 8, 0
+    first, second = merge_buffers(P, ysize)
     while w < P:
-        src, dst = ("B", "A") if lvl % 2 == 0 else ("A", "B")
+        src, dst = (first, second) if lvl % 2 == 0 else (second, first)
         acc = [(set(), set()) for _ in range(BLOCK // WAVE)]
         for t in range(BLOCK):
             r, wr = acc[t // WAVE]
@@ -127,9 +142,9 @@ def merge_steps(P, ysize=8):
                 continue
             b0 = o0 & ~(2 * w - 1)
             for q in range(b0, b0 + 2 * w):
-                r.update(words(src, q, ysize))
+                r.update(merge_words(src, q, ysize))
             for e in range(PER_T):
-                wr.update(words(dst, o0 + e, ysize))
+                wr.update(merge_words(dst, o0 + e, ysize))
         steps.append((("merge", w), acc))
         w *= 2
         lvl += 1
