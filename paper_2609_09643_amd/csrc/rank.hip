@@ -3,7 +3,7 @@
 //
 // The scorers are elementwise and HBM-bound (one thread per session, coalesced
 // loads, the hazard table in LDS).  The Kendall kernels give each snapshot one
-// workgroup and gather its (x, y) pairs into LDS once.  Small snapshots are
+// workgroup, which gathers its (x, y) pairs once.  Small snapshots are
 // classified pair by pair (each thread owns rows i and walks j > i with all
 // lanes of a wave reading the same LDS word, a broadcast); from 256 entries
 // on, a bitonic sort (its passes in groups of three in registers) and a
@@ -214,8 +214,8 @@ constexpr uint32_t kSortE = kKendallMax / kSortBlock;
 // thread's 8 consecutive entries.
 constexpr uint32_t kMergeRun = 8;
 // Sort and merge buffers store entry i at i + i / 8: a thread's 8 consecutive
-// entries then start 72 B after its neighbour's, not 64 B, and the bitonic
-// groups below spread their accesses over the banks as well.
+// entries then start 9 entries after its neighbour's, not 8, which spreads a
+// wavefront's accesses over the banks; the bitonic groups below do the same.
 __host__ __device__ constexpr uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
 // Entries of each sort buffer, the padding included.
 __host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
@@ -258,7 +258,7 @@ __host__ __device__ constexpr uint32_t ilog2(uint32_t v) {
 // barrier.  Inside a group the next pass runs in registers; the gathered
 // stages end with the barrier that also publishes the argmax partials; the
 // last group's entries become the merge input only after every wavefront
-// has read its group (the x keys share that buffer).
+// has read its group (the merge buffers reuse the sort's LDS).
 __host__ __device__ constexpr bool bitonic_barrier_after(uint32_t P, uint32_t k, uint32_t j) {
   if (k <= 8) return k == 8 && j == 1;
   const uint32_t L = ilog2(k), s = ilog2(j);
