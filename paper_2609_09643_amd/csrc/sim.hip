@@ -479,6 +479,7 @@ struct RegTable {
   // Gap onsets reduce their scan victim and TIDE's candidates separately:
   // fusing the three reductions made this kernel slower (0.518 vs 0.498 ms).
   static constexpr bool kFuseGap = false;
+  static constexpr bool kDeferD = false;
   static constexpr bool kLaneDigest = false;
   static constexpr bool kPrefetch = false;
   __device__ __forceinline__ void* window() const { return nullptr; }
@@ -751,6 +752,7 @@ struct MemTable {
   // A gap onset's scan and TIDE's first candidates share one pass and one
   // barrier (the dual design scans different copies for the two engines).
   static constexpr bool kFuseGap = !VIEWS;
+  static constexpr bool kDeferD = false;
   static constexpr bool kLaneDigest = false;
   static constexpr bool kPrefetch = false;
   __device__ __forceinline__ void* window() const { return nullptr; }
@@ -1336,6 +1338,7 @@ struct SlotTable : LaneQueue {
   using PT = Pol<POL, SMODE>;
   static constexpr bool kViews = false;
   static constexpr bool kFuseGap = true;
+  static constexpr bool kDeferD = false;
   // Digest terms are queued one per lane and hashed 64 at a time.
   static constexpr bool kLaneDigest = true;
   static constexpr bool kPrefetch = false;
@@ -1688,6 +1691,9 @@ struct WideTable : LaneQueue {
   using PT = Pol<POL, SMODE>;
   static constexpr bool kViews = false;
   static constexpr bool kFuseGap = true;
+  // The gap onset's fused scan leaves TIDE's demotion candidate to the pass,
+  // which selects it only if it gets that far.
+  static constexpr bool kDeferD = true;
   static constexpr bool kLaneDigest = true;
   static constexpr bool kPrefetch = true;
   template <bool N, bool T>
@@ -2209,7 +2215,11 @@ struct WideTable : LaneQueue {
     rescan();
     v = reduce_t<0>();
     p = reduce_t<1>();
-    d = reduce_t<2>();
+    d = Cand{0ull, kNone};  // deferred: select_d
+  }
+  __device__ __forceinline__ Cand select_d(const KeyCtx&) {
+    rescan();
+    return reduce_t<2>();
   }
 
   // Online hazard table: add the completed session, then rescore every resident.
@@ -2657,10 +2667,12 @@ __device__ __forceinline__ void run_range(Tab& T, const unison_sim_params& P, co
         C.tide_passes++;
         if constexpr (Tab::kViews) T.set_src(dual ? 1 : -1);  // TIDE decides from its own copy
         for (;;) {
-          Cand p, d;
+            Cand p, d;
+          bool d_later = false;
           if (have_pd) {
             p = p0;
             d = d0;
+            d_later = Tab::kDeferD;
             have_pd = false;
           } else {
             T.select_pd(K, p, d);  // eq. (promote), eq. (demote)
@@ -2678,6 +2690,12 @@ __device__ __forceinline__ void run_range(Tab& T, const unison_sim_params& P, co
           uint64_t sp;
           uint32_t mp;
           T.read_size(p.sid, sp, mp);
+          // a promotion needs used_s + sp <= C_S, a swap used_s - sd + sp <= C_S
+          // with sd <= used_s (d is in SRAM): neither is legal once sp > C_S,
+          // and the pass can stop before it selects d (taken where d waits)
+          if constexpr (Tab::kDeferD) {
+            if (uc<UNI>(sp > P.cap_sram_B)) break;
+          }
           if (uc<UNI>(S.used_s + sp <= P.cap_sram_B && sp <= left)) {
             S.used_h -= sp;
             S.used_s += sp;
@@ -2688,6 +2706,9 @@ __device__ __forceinline__ void run_range(Tab& T, const unison_sim_params& P, co
             C.promote++;
             C.prom_diff += live_p != p.sid ? 1u : 0u;
             continue;
+          }
+          if constexpr (Tab::kDeferD) {
+            if (d_later) d = T.select_d(K);
           }
           if (d.sid == kNone) break;
           uint64_t sd;
