@@ -479,7 +479,8 @@ struct RegTable {
   // Gap onsets reduce their scan victim and TIDE's candidates separately:
   // fusing the three reductions made this kernel slower (0.518 vs 0.498 ms).
   static constexpr bool kFuseGap = false;
-  static constexpr bool kDeferD = false;
+  // TIDE's demotion candidate is reduced only when the pass needs it.
+  static constexpr bool kDeferD = true;
   static constexpr bool kLaneDigest = false;
   static constexpr bool kPrefetch = false;
   __device__ __forceinline__ void* window() const { return nullptr; }
@@ -708,11 +709,13 @@ struct RegTable {
     return Cand{key, none ? kNone : (MAX ? 0xFFFFFu - lo : lo)};
   }
 
-  // TIDE's two candidates, eq. (promote) and eq. (demote), from one pass.
+  // TIDE's two candidates, eq. (promote) and eq. (demote).
   __device__ __forceinline__ void select_pd(const KeyCtx& K, Cand& p, Cand& d) const {
     p = select<false>(kTierHbm, K);
     d = select<true>(kTierSram, K);
   }
+  __device__ __forceinline__ Cand select_p(const KeyCtx& K) const { return select<false>(kTierHbm, K); }
+  __device__ __forceinline__ Cand select_d(const KeyCtx& K) const { return select<true>(kTierSram, K); }
 
   // Online hazard table: does it still count completions?  Then add one and
   // refresh every entry's hazard value, so the next scan rescores them all.
@@ -2217,6 +2220,10 @@ struct WideTable : LaneQueue {
     p = reduce_t<1>();
     d = Cand{0ull, kNone};  // deferred: select_d
   }
+  __device__ __forceinline__ Cand select_p(const KeyCtx&) {
+    rescan();
+    return reduce_t<1>();
+  }
   __device__ __forceinline__ Cand select_d(const KeyCtx&) {
     rescan();
     return reduce_t<2>();
@@ -2667,15 +2674,20 @@ __device__ __forceinline__ void run_range(Tab& T, const unison_sim_params& P, co
         C.tide_passes++;
         if constexpr (Tab::kViews) T.set_src(dual ? 1 : -1);  // TIDE decides from its own copy
         for (;;) {
-            Cand p, d;
+            // eq. (promote), eq. (demote); a table that defers d reduces it
+          // only when the pass gets past the promotion test
+          Cand p, d;
           bool d_later = false;
           if (have_pd) {
             p = p0;
             d = d0;
             d_later = Tab::kDeferD;
             have_pd = false;
+          } else if constexpr (Tab::kDeferD) {
+            p = T.select_p(K);
+            d_later = true;
           } else {
-            T.select_pd(K, p, d);  // eq. (promote), eq. (demote)
+            T.select_pd(K, p, d);
           }
           if (p.sid == kNone) break;
           uint32_t live_p = p.sid;
