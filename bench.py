@@ -16,8 +16,9 @@ changes, with the decisions of a full rescan.
 The headline kernel is bound by VALU issue along each simulation's event
 chain, so its roofline is the wave64 VALU instruction rate (rocprofv3
 SQ_INSTS_VALU per launch over the HIP-event kernel time) against the chip's
-issue limit; the same launch against the bytes the survey's per-unit figures
-give, and against measured DRAM bytes, is reported beside it.
+issue limit; the same launch against algorithmic bytes (12 or 20 B per
+scanned table entry, 32 B per event), and against measured DRAM bytes, is
+reported beside it.
 
 Prints one JSON line.  Extra sections (the tiny trace, the paper-scale trace,
 the 65,536-session large live set over its whole trace and the ranking-
@@ -508,8 +509,8 @@ def main():
                               "unit": "G wave64 VALU instructions/s", "frac": None,
                               "traffic": traffic,
                               "note": "no VALU count taken on this kernel source"}
-    # the same launch against the survey's algorithmic bytes (12 or 20 B per
-    # scanned entry, 32 B per event): a normalisation, not measured traffic
+    # the same launch against algorithmic bytes (12 or 20 B per scanned
+    # entry, 32 B per event): a normalisation, not measured traffic
     result["algorithmic_bytes_rate"] = {"achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                         "frac": achieved / HBM_PEAK_GBS,
                                         "bytes_per_launch": ab}
