@@ -259,14 +259,20 @@ __host__ __device__ constexpr uint32_t ilog2(uint32_t v) {
 // stages end with the barrier that also publishes the argmax partials; the
 // last group's entries become the merge input only after every wavefront
 // has read its group (the merge buffers reuse the sort's LDS).
+// By group: a full group (top >= 3) is followed by a lower group of the same
+// stage, so it takes the barrier while its own top bit reaches 9; the last
+// group of stage 2^L is followed by the next stage's first group (top L), or
+// ends the sort (stage 2^Lp = P).
+__host__ __device__ constexpr bool group_barrier_after(uint32_t Lp, uint32_t L, uint32_t top) {
+  if (top >= 3) return top >= kWaveSpanBits;
+  return L == Lp || L >= kWaveSpanBits;
+}
 __host__ __device__ constexpr bool bitonic_barrier_after(uint32_t P, uint32_t k, uint32_t j) {
   if (k <= 8) return k == 8 && j == 1;
   const uint32_t L = ilog2(k), s = ilog2(j);
   const uint32_t top = group_top(L, s);
   if (s != group_low(top)) return false;
-  if (s == 0 && k == P) return true;
-  const uint32_t next_high = s > 0 ? group_high(s - 1) : L;
-  return group_high(top) >= kWaveSpanBits || next_high >= kWaveSpanBits;
+  return group_barrier_after(ilog2(P), L, top);
 }
 
 // Whether merge level w (runs of w merged into runs of 2w, w >= 8) is
@@ -346,11 +352,12 @@ __device__ __forceinline__ uint32_t group_base(uint32_t tid, uint32_t lo) {
 // A full group (three passes) with low bit lo >= 1: the offsets are the same
 // for every lane.
 template <bool NARROW>
-__device__ __forceinline__ void sort_group3(uint32_t lo, uint64_t (&kk)[kSortE],
-                                            uint32_t (&kr)[kSortE], uint64_t* s_k,
-                                            uint32_t* s_r, uint32_t tid, uint32_t P, uint32_t k) {
+__device__ __forceinline__ void sort_group3(uint32_t lo, uint64_t* s_k, uint32_t* s_r,
+                                            uint32_t tid, uint32_t P, uint32_t k) {
   const uint32_t gb = group_base(tid, lo);
   if (gb >= P) return;
+  uint64_t kk[kSortE];
+  uint32_t kr[kSortE];
   uint64_t* gk = s_k + mp_pad(gb);
   uint32_t* gr = s_r + mp_pad(gb);
 #pragma unroll
@@ -375,11 +382,22 @@ __device__ __forceinline__ void sort_group3(uint32_t lo, uint64_t (&kk)[kSortE],
 // NP passes.  LAST: the stage-P group that ends the sort keeps its entries in
 // registers.
 template <uint32_t NP, bool NARROW, bool LAST>
-__device__ __forceinline__ void sort_group0(uint64_t (&kk)[kSortE], uint32_t (&kr)[kSortE],
+__device__ __forceinline__ void sort_group0(uint64_t (&ko)[kSortE], uint32_t (&ro)[kSortE],
                                             uint64_t* s_k, uint32_t* s_r, uint32_t tid,
                                             uint32_t P, uint32_t k) {
   const uint32_t gb = tid * kSortE;
-  if (gb >= P) return;
+  if (gb >= P) {
+    if (LAST) {  // no entries: padding values (the caller's earlier ones are dead)
+#pragma unroll
+      for (uint32_t c = 0; c < kSortE; ++c) {
+        ko[c] = ~0ull;
+        ro[c] = ~0u;
+      }
+    }
+    return;
+  }
+  uint64_t kk[kSortE];
+  uint32_t kr[kSortE];
   const uint32_t pb = mp_pad(gb);
 #pragma unroll
   for (uint32_t c = 0; c < kSortE; ++c) {
@@ -395,6 +413,12 @@ __device__ __forceinline__ void sort_group0(uint64_t (&kk)[kSortE], uint32_t (&k
     for (uint32_t c = 0; c < kSortE; ++c) {
       s_k[pb + c] = kk[c];
       if (!NARROW) s_r[pb + c] = kr[c];
+    }
+  } else {
+#pragma unroll
+    for (uint32_t c = 0; c < kSortE; ++c) {
+      ko[c] = kk[c];
+      ro[c] = kr[c];
     }
   }
 }
@@ -421,6 +445,23 @@ __device__ __forceinline__ void sort_min_max(uint64_t& a, uint64_t& b) {
   a = lo;
 }
 
+// The packed form's two merge buffers share the sort's LDS, the second one
+// kMergeGap entries after the first ends: a step may read one entry past a
+// run (a value it never takes), which then never lands on the other buffer.
+constexpr uint32_t kMergeGap = 16;
+
+// A thread's 8 consecutive outputs (aligned to 32 or 64 B) as 16-byte stores.
+__device__ __forceinline__ void store8(uint32_t* p, const uint32_t (&v)[kSortE]) {
+  uint4* q = reinterpret_cast<uint4*>(p);
+  q[0] = make_uint4(v[0], v[1], v[2], v[3]);
+  q[1] = make_uint4(v[4], v[5], v[6], v[7]);
+}
+__device__ __forceinline__ void store8(uint64_t* p, const uint64_t (&v)[kSortE]) {
+  ulonglong2* q = reinterpret_cast<ulonglong2*>(p);
+#pragma unroll
+  for (uint32_t h = 0; h < kSortE / 2; ++h) q[h] = make_ulonglong2(v[2 * h], v[2 * h + 1]);
+}
+
 // Knight's counts of one snapshot from its gathered entries (thread t holds
 // entries 8t ... 8t+7; x as order-preserving u32 keys): the bitonic sort by
 // (x, y), the ties in x and in both from the sorted runs, the inversions of y
@@ -431,9 +472,10 @@ __device__ __forceinline__ void sort_min_max(uint64_t& a, uint64_t& b) {
 // (x, y) packs into one 64-bit key; otherwise the key is x with the upper
 // half of y, and the lower half breaks its ties.
 // LDS: the keys sort in a buffer of sort_buf(P) 8-byte entries.  NARROW: the
-// merge sort of y then runs in that buffer's two halves (4-byte values);
-// otherwise a second such buffer holds the tie-breakers, and the merge sort
-// of y starts there and alternates between the two.
+// merge sort of y then runs in that buffer (two runs of P 4-byte values, the
+// second kMergeGap entries after the first); otherwise a second such buffer
+// holds the tie-breakers, and the merge sort of y starts there and
+// alternates between the two.  The merge buffers hold entry i at i.
 template <bool NARROW>
 __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
                                               const uint64_t (&ky)[kSortE], uint32_t P,
@@ -480,19 +522,19 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   __syncthreads();
   // then the grouped passes of stages 16 ... P; the last group keeps the
   // thread's 8 consecutive sorted entries in registers
+  const uint32_t Lp = 31u - (uint32_t)__builtin_clz(P);
   for (uint32_t L = 4, k = 16; k <= P; ++L, k <<= 1) {
     uint32_t top = L - 1;
     for (; top >= 3; top -= 3) {
-      const uint32_t lo = top - 2;
-      sort_group3<NARROW>(lo, kk, kr, s_k, s_r, tid, P, k);
-      if (bitonic_barrier_after(P, k, 1u << lo)) __syncthreads();
+      sort_group3<NARROW>(top - 2, s_k, s_r, tid, P, k);
+      if (group_barrier_after(Lp, L, top)) __syncthreads();
       else wave_lds_sync();
     }
     if (k == P) {
       sort_group0_at<NARROW, true>(top, kk, kr, s_k, s_r, tid, P, k);
     } else {
       sort_group0_at<NARROW, false>(top, kk, kr, s_k, s_r, tid, P, k);
-      if (bitonic_barrier_after(P, k, 1u)) __syncthreads();
+      if (group_barrier_after(Lp, L, top)) __syncthreads();
       else wave_lds_sync();
     }
   }
@@ -511,7 +553,7 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
 
   uint64_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
   Y* src = NARROW ? reinterpret_cast<Y*>(s_dyn) : reinterpret_cast<Y*>(s_dyn + sort_buf(P));
-  Y* dst = NARROW ? reinterpret_cast<Y*>(s_dyn) + sort_buf(P) : reinterpret_cast<Y*>(s_dyn);
+  Y* dst = NARROW ? reinterpret_cast<Y*>(s_dyn) + P + kMergeGap : reinterpret_cast<Y*>(s_dyn);
   // pairs tied in x, and in x and y: each entry counts the earlier entries of
   // its run; a run starts where the key differs from the one before, and a
   // max-scan of those starts gives every entry the start of its run
@@ -560,8 +602,7 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
       sort_min_max(yv[1], yv[2]);
       sort_min_max(yv[3], yv[4]);
       sort_min_max(yv[5], yv[6]);
-#pragma unroll
-      for (uint32_t e = 0; e < kSortE; ++e) src[mp_pad(i0 + e)] = yv[e];
+      store8(src + i0, yv);
     }
     block_max_scan(sx, s_part, tid);
     block_max_scan(sxy, s_part, tid);
@@ -587,29 +628,37 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
     if (active) {
       const uint32_t b0 = i0 & ~(2 * w - 1);
       const uint32_t d = i0 - b0;
-      auto at = [&](uint32_t k) { return src[mp_pad(k)]; };
-      const uint32_t bb = b0 + w;
+      const Y* run_a = src + b0;
+      const Y* run_b = run_a + w;
       uint32_t lo = d > w ? d - w : 0u, hi = d < w ? d : w;
       while (lo < hi) {
         const uint32_t mid = (lo + hi) >> 1;
-        if (at(b0 + mid) <= at(bb + d - 1 - mid)) lo = mid + 1;
+        if (run_a[mid] <= run_b[d - 1 - mid]) lo = mid + 1;
         else hi = mid;
       }
-      // each step reloads only the run it took from (selects, not a
-      // branch; an index past its run is clamped and its value never used)
-      uint32_t i = lo, j = d - lo, waiting = 0;
-      Y a = at(b0 + min(i, w - 1)), b = at(bb + min(j, w - 1));
+      // Each step takes the smaller head (A's on equal values) and reloads
+      // only the run it took from, by selects rather than a branch.  A run
+      // with no entries left has its head one past its end: that value is
+      // read but never taken.
+      const Y* pa = run_a + lo;
+      const Y* pb = run_b + (d - lo);
+      uint32_t na = w - lo, nb = w - (d - lo), waiting = 0;
+      Y a = *pa, b = *pb;
+      Y out[kSortE];
 #pragma unroll
       for (uint32_t e = 0; e < kSortE; ++e) {
-        const bool take_a = (i < w) & ((j >= w) | (a <= b));
-        dst[mp_pad(i0 + e)] = take_a ? a : b;
-        waiting += take_a ? 0u : w - i;
-        i += take_a ? 1u : 0u;
-        j += take_a ? 0u : 1u;
-        const Y v = at(take_a ? b0 + min(i, w - 1) : bb + min(j, w - 1));
+        const bool take_a = (na != 0) & ((nb == 0) | (a <= b));
+        out[e] = take_a ? a : b;
+        waiting += take_a ? 0u : na;
+        na -= take_a ? 1u : 0u;
+        nb -= take_a ? 0u : 1u;
+        pa += take_a ? 1 : 0;
+        pb += take_a ? 0 : 1;
+        const Y v = *(take_a ? pa : pb);
         a = take_a ? v : a;
         b = take_a ? b : v;
       }
+      store8(dst + i0, out);
       inv += waiting;
     }
     level_sync(w, P);
@@ -621,12 +670,12 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   // sorted y (real entries hold positions [0, n): the padding sorts last)
   {
     uint32_t sy[kSortE];
-    Y py = i0 > 0 && i0 < P ? src[mp_pad(i0 - 1)] : (Y)0;
+    Y py = i0 > 0 && i0 < P ? src[i0 - 1] : (Y)0;
 #pragma unroll
     for (uint32_t e = 0; e < kSortE; ++e) {
       const uint32_t i = i0 + e;
       const bool ok = i < P;
-      const Y yk = ok ? src[mp_pad(i)] : (Y)0;
+      const Y yk = ok ? src[i] : (Y)0;
       sy[e] = ok && (i == 0 || yk != py) ? i : 0u;
       py = yk;
     }
@@ -658,7 +707,7 @@ __global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per
                                                                   uint64_t* counts, uint8_t* top1) {
   // one (NARROW) or two buffers of P + P/8 8-byte entries: 36 or 72 KiB at
   // 4,096 entries
-  extern __shared__ uint64_t s_dyn[];
+  extern __shared__ __attribute__((aligned(16))) uint64_t s_dyn[];
   __shared__ uint64_t s_sum[4][kSortBlock / 64];
   __shared__ float s_bx[kSortBlock / 64];
   __shared__ uint32_t s_bxi[kSortBlock / 64], s_byi[kSortBlock / 64];

@@ -13,11 +13,15 @@ barrier plan the library itself reports (unison_debug_kendall_barrier).
 
 The bitonic passes run in groups of up to three in registers: a group loads
 its entries before its first pass and stores them after its last.  The sort
-keys are 8-byte entries of the first buffer (A).  In the narrow form (4-byte
-y values) the merge sort then runs in A's two halves; in the wide form the
-4-byte tie-breakers live in a second buffer (B), where the merge sort of the
-8-byte y values starts.  Accesses are modelled as the 4-byte words they
-touch, so the aliasing between those uses is exact."""
+keys are 8-byte entries of the first buffer (A), at padded positions.  In the
+narrow form (4-byte y values) the merge sort then runs in A, its two buffers
+of P values 16 entries apart; in the wide form the 4-byte tie-breakers live
+in a second buffer (B), where the merge sort of the 8-byte y values starts.
+The merge buffers are not padded.  Accesses are modelled as the 4-byte words
+they touch, so the aliasing between those uses is exact.  A merge step also
+reads one entry past a run whose entries are all taken, a value it never
+uses; that read lands in the gap or a buffer's unused tail, never on a buffer
+being written (checked by a host model of the step), and is not modelled."""
 import os
 
 import pytest
@@ -52,18 +56,21 @@ def sort_words(i, ysize):
     return words("A", i, 8) + (words("B", i, 4) if ysize == 8 else [])
 
 
+MERGE_GAP = 16
+
+
 def merge_buffers(P, ysize):
     """(first source, first destination) of the merge levels: entry q of
-    buffer b lies at words(b[0], q + b[1], ysize)."""
+    buffer b lies at merge_words(b, q, ysize)."""
     if ysize == 4:
-        return ("A", 0), ("A", P + P // 8)      # A's two halves
+        return ("A", 0), ("A", P + MERGE_GAP)   # both in A, a gap between them
     return ("B", 0), ("A", 0)
 
 
 def merge_words(buf, q, ysize):
     name, shift = buf
     w = ysize // 4
-    return [(name, (shift + (q + q // 8)) * w + k) for k in range(w)]
+    return [(name, (shift + q) * w + k) for k in range(w)]
 
 
 def bitonic_steps(P, ysize=8):
@@ -128,7 +135,7 @@ def merge_steps(P, ysize=8):
     """(('merge', w), accesses) per merge level from runs of 8 (y values of
     ysize bytes).  The first level reads the per-thread sorted groups, and the
     levels alternate; thread t merges outputs [8t, 8t + 8), reading anywhere
-    in its pair of runs and storing padded."""
+    in its pair of runs."""
     steps = []
     w, lvl = 8, 0
     first, second = merge_buffers(P, ysize)
