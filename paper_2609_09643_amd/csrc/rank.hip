@@ -213,9 +213,11 @@ constexpr uint32_t kSortE = kKendallMax / kSortBlock;
 // from runs of this width on; the narrower runs are sorted inside each
 // thread's 8 consecutive entries.
 constexpr uint32_t kMergeRun = 8;
-// Sort and merge buffers store entry i at i + i / 8: a thread's 8 consecutive
-// entries then start 9 entries after its neighbour's, not 8, which spreads a
-// wavefront's accesses over the banks; the bitonic groups below do the same.
+// Sort buffers, and the packed form's merge buffers, store entry i at
+// i + i / 8: a thread's 8 consecutive entries then start 9 entries after its
+// neighbour's, not 8, which spreads a wavefront's accesses over the banks; the
+// bitonic groups below do the same.  In a merge level neighbouring lanes walk
+// their runs about 4 entries apart, which the padding spreads too.
 __host__ __device__ constexpr uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
 // Entries of each sort buffer, the padding included.
 __host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
@@ -446,16 +448,12 @@ __device__ __forceinline__ void sort_min_max(uint64_t& a, uint64_t& b) {
 }
 
 // The packed form's two merge buffers share the sort's LDS, the second one
-// kMergeGap entries after the first ends: a step may read one entry past a
-// run (a value it never takes), which then never lands on the other buffer.
+// kMergeGap 4-byte words after the first ends, and kMergeGap words follow the
+// second: a step may read one entry past a run (a value it never takes),
+// which then lands in a gap, never on the other buffer.
 constexpr uint32_t kMergeGap = 16;
 
-// A thread's 8 consecutive outputs (aligned to 32 or 64 B) as 16-byte stores.
-__device__ __forceinline__ void store8(uint32_t* p, const uint32_t (&v)[kSortE]) {
-  uint4* q = reinterpret_cast<uint4*>(p);
-  q[0] = make_uint4(v[0], v[1], v[2], v[3]);
-  q[1] = make_uint4(v[4], v[5], v[6], v[7]);
-}
+// A thread's 8 consecutive outputs (aligned to 64 B) as 16-byte stores.
 __device__ __forceinline__ void store8(uint64_t* p, const uint64_t (&v)[kSortE]) {
   ulonglong2* q = reinterpret_cast<ulonglong2*>(p);
 #pragma unroll
@@ -472,10 +470,11 @@ __device__ __forceinline__ void store8(uint64_t* p, const uint64_t (&v)[kSortE])
 // (x, y) packs into one 64-bit key; otherwise the key is x with the upper
 // half of y, and the lower half breaks its ties.
 // LDS: the keys sort in a buffer of sort_buf(P) 8-byte entries.  NARROW: the
-// merge sort of y then runs in that buffer (two runs of P 4-byte values, the
-// second kMergeGap entries after the first); otherwise a second such buffer
-// holds the tie-breakers, and the merge sort of y starts there and
-// alternates between the two.  The merge buffers hold entry i at i.
+// merge sort of y then runs in that buffer and the 2 kMergeGap words after it
+// (two buffers of sort_buf(P) 4-byte words holding entry i at i + i / 8, the
+// second kMergeGap words after the first); otherwise a second such buffer of
+// 8-byte entries holds the tie-breakers, and the merge sort of y starts there
+// and alternates between the two, which hold entry i at i.
 template <bool NARROW>
 __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
                                               const uint64_t (&ky)[kSortE], uint32_t P,
@@ -551,9 +550,14 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
     pr = s_er[(tid >> 6) - 1];
   }
 
-  uint64_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
+  // a thread's counts stay below 2^16 at 4,096 entries: ties at most
+  // 8 x 4,095; discordant pairs 28 inside its 8 entries and at most 8 w at
+  // merge level w, 8 x (8 + 16 + ... + 2,048) over the levels
+  uint32_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
   Y* src = NARROW ? reinterpret_cast<Y*>(s_dyn) : reinterpret_cast<Y*>(s_dyn + sort_buf(P));
-  Y* dst = NARROW ? reinterpret_cast<Y*>(s_dyn) + P + kMergeGap : reinterpret_cast<Y*>(s_dyn);
+  Y* dst = NARROW ? reinterpret_cast<Y*>(s_dyn) + sort_buf(P) + kMergeGap : reinterpret_cast<Y*>(s_dyn);
+  // the packed form's merge buffers hold entry q at q + q / 8, the wide form's at q
+  auto mpos = [](uint32_t q) -> uint32_t { return NARROW ? mp_pad(q) : q; };
   // pairs tied in x, and in x and y: each entry counts the earlier entries of
   // its run; a run starts where the key differs from the one before, and a
   // max-scan of those starts gives every entry the start of its run
@@ -602,7 +606,12 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
       sort_min_max(yv[1], yv[2]);
       sort_min_max(yv[3], yv[4]);
       sort_min_max(yv[5], yv[6]);
-      store8(src + i0, yv);
+      if constexpr (NARROW) {
+#pragma unroll
+        for (uint32_t e = 0; e < kSortE; ++e) src[mp_pad(i0) + e] = yv[e];
+      } else {
+        store8(src + i0, yv);
+      }
     }
     block_max_scan(sx, s_part, tid);
     block_max_scan(sxy, s_part, tid);
@@ -628,22 +637,19 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
     if (active) {
       const uint32_t b0 = i0 & ~(2 * w - 1);
       const uint32_t d = i0 - b0;
-      const Y* run_a = src + b0;
-      const Y* run_b = run_a + w;
       uint32_t lo = d > w ? d - w : 0u, hi = d < w ? d : w;
       while (lo < hi) {
         const uint32_t mid = (lo + hi) >> 1;
-        if (run_a[mid] <= run_b[d - 1 - mid]) lo = mid + 1;
+        if (src[mpos(b0 + mid)] <= src[mpos(b0 + w + d - 1 - mid)]) lo = mid + 1;
         else hi = mid;
       }
       // Each step takes the smaller head (A's on equal values) and reloads
       // only the run it took from, by selects rather than a branch.  A run
       // with no entries left has its head one past its end: that value is
       // read but never taken.
-      const Y* pa = run_a + lo;
-      const Y* pb = run_b + (d - lo);
+      uint32_t xa = b0 + lo, xb = b0 + w + (d - lo);
       uint32_t na = w - lo, nb = w - (d - lo), waiting = 0;
-      Y a = *pa, b = *pb;
+      Y a = src[mpos(xa)], b = src[mpos(xb)];
       Y out[kSortE];
 #pragma unroll
       for (uint32_t e = 0; e < kSortE; ++e) {
@@ -652,13 +658,18 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
         waiting += take_a ? 0u : na;
         na -= take_a ? 1u : 0u;
         nb -= take_a ? 0u : 1u;
-        pa += take_a ? 1 : 0;
-        pb += take_a ? 0 : 1;
-        const Y v = *(take_a ? pa : pb);
+        xa += take_a ? 1u : 0u;
+        xb += take_a ? 0u : 1u;
+        const Y v = src[mpos(take_a ? xa : xb)];
         a = take_a ? v : a;
         b = take_a ? b : v;
       }
-      store8(dst + i0, out);
+      if constexpr (NARROW) {
+#pragma unroll
+        for (uint32_t e = 0; e < kSortE; ++e) dst[mp_pad(i0) + e] = out[e];
+      } else {
+        store8(dst + i0, out);
+      }
       inv += waiting;
     }
     level_sync(w, P);
@@ -670,12 +681,12 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   // sorted y (real entries hold positions [0, n): the padding sorts last)
   {
     uint32_t sy[kSortE];
-    Y py = i0 > 0 && i0 < P ? src[i0 - 1] : (Y)0;
+    Y py = i0 > 0 && i0 < P ? src[mpos(i0 - 1)] : (Y)0;
 #pragma unroll
     for (uint32_t e = 0; e < kSortE; ++e) {
       const uint32_t i = i0 + e;
       const bool ok = i < P;
-      const Y yk = ok ? src[i] : (Y)0;
+      const Y yk = ok ? src[mpos(i)] : (Y)0;
       sy[e] = ok && (i == 0 || yk != py) ? i : 0u;
       py = yk;
     }
@@ -700,13 +711,13 @@ constexpr uint8_t kWideMark = 254;
 // here with half the LDS, so four snapshots share a CU; the others are left
 // marked in top1.  Otherwise only the marked snapshots are counted.
 template <bool NARROW>
-__global__ __launch_bounds__(kSortBlock) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
+__global__ __launch_bounds__(kSortBlock, NARROW ? 8 : 4) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
                                                                   uint64_t n_x, const float* x,
                                                                   const uint64_t* y,
                                                                   const uint32_t* idx,
                                                                   uint64_t* counts, uint8_t* top1) {
-  // one (NARROW) or two buffers of P + P/8 8-byte entries: 36 or 72 KiB at
-  // 4,096 entries
+  // one (NARROW, and 2 kMergeGap 4-byte words) or two buffers of P + P/8
+  // 8-byte entries: 36 or 72 KiB at 4,096 entries
   extern __shared__ __attribute__((aligned(16))) uint64_t s_dyn[];
   __shared__ uint64_t s_sum[4][kSortBlock / 64];
   __shared__ float s_bx[kSortBlock / 64];
@@ -858,7 +869,8 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
     while (P < n_per) P <<= 1;
     // the packed form first; then the snapshots it left marked
     const size_t lds = (size_t)sort_buf(P) * sizeof(uint64_t);
-    hipLaunchKernelGGL(kendall_sort_kernel<true>, dim3(n_snap), dim3(kSortBlock), lds, s, n_per, P,
+    hipLaunchKernelGGL(kendall_sort_kernel<true>, dim3(n_snap), dim3(kSortBlock),
+                       lds + 2 * kMergeGap * sizeof(uint32_t), s, n_per, P,
                        n_x, x, y, idx, counts, top1);
     hipLaunchKernelGGL(kendall_sort_kernel<false>, dim3(n_snap), dim3(kSortBlock), 2 * lds, s, n_per,
                        P, n_x, x, y, idx, counts, top1);
