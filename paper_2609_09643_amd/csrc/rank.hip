@@ -213,11 +213,11 @@ constexpr uint32_t kSortE = kKendallMax / kSortBlock;
 // from runs of this width on; the narrower runs are sorted inside each
 // thread's 8 consecutive entries.
 constexpr uint32_t kMergeRun = 8;
-// Sort buffers, and the packed form's merge buffers, store entry i at
-// i + i / 8: a thread's 8 consecutive entries then start 9 entries after its
-// neighbour's, not 8, which spreads a wavefront's accesses over the banks; the
-// bitonic groups below do the same.  In a merge level neighbouring lanes walk
-// their runs about 4 entries apart, which the padding spreads too.
+// Sort and merge buffers store entry i at i + i / 8: a thread's 8
+// consecutive entries then start 9 entries after its neighbour's, not 8,
+// which spreads a wavefront's accesses over the banks; the bitonic groups
+// below do the same.  In a merge level neighbouring lanes walk their runs
+// about 4 entries apart, which the padding spreads too.
 __host__ __device__ constexpr uint32_t mp_pad(uint32_t i) { return i + (i >> 3); }
 // Entries of each sort buffer, the padding included.
 __host__ __device__ __forceinline__ uint32_t sort_buf(uint32_t P) { return P + P / 8; }
@@ -452,13 +452,10 @@ __device__ __forceinline__ void sort_min_max(uint64_t& a, uint64_t& b) {
 // second: a step may read one entry past a run (a value it never takes),
 // which then lands in a gap, never on the other buffer.
 constexpr uint32_t kMergeGap = 16;
+// The wide form's second buffer starts kWideGap 8-byte entries after the
+// first ends, and kWideGap entries follow it, for the same reads.
+constexpr uint32_t kWideGap = 8;
 
-// A thread's 8 consecutive outputs (aligned to 64 B) as 16-byte stores.
-__device__ __forceinline__ void store8(uint64_t* p, const uint64_t (&v)[kSortE]) {
-  ulonglong2* q = reinterpret_cast<ulonglong2*>(p);
-#pragma unroll
-  for (uint32_t h = 0; h < kSortE / 2; ++h) q[h] = make_ulonglong2(v[2 * h], v[2 * h + 1]);
-}
 
 // Knight's counts of one snapshot from its gathered entries (thread t holds
 // entries 8t ... 8t+7; x as order-preserving u32 keys): the bitonic sort by
@@ -471,10 +468,11 @@ __device__ __forceinline__ void store8(uint64_t* p, const uint64_t (&v)[kSortE])
 // half of y, and the lower half breaks its ties.
 // LDS: the keys sort in a buffer of sort_buf(P) 8-byte entries.  NARROW: the
 // merge sort of y then runs in that buffer and the 2 kMergeGap words after it
-// (two buffers of sort_buf(P) 4-byte words holding entry i at i + i / 8, the
-// second kMergeGap words after the first); otherwise a second such buffer of
-// 8-byte entries holds the tie-breakers, and the merge sort of y starts there
-// and alternates between the two, which hold entry i at i.
+// (two buffers of sort_buf(P) 4-byte words, the second kMergeGap words after
+// the first); otherwise a second buffer of sort_buf(P) 8-byte entries,
+// kWideGap entries after the first and followed by kWideGap more, holds the
+// tie-breakers, and the merge sort of y starts there and alternates between
+// the two.  Every merge buffer holds entry i at i + i / 8.
 template <bool NARROW>
 __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
                                               const uint64_t (&ky)[kSortE], uint32_t P,
@@ -483,7 +481,7 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
                                               uint64_t (&cnt)[4]) {
   using Y = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
   uint64_t* s_k = s_dyn;
-  uint32_t* s_r = reinterpret_cast<uint32_t*>(s_dyn + sort_buf(P));
+  uint32_t* s_r = reinterpret_cast<uint32_t*>(s_dyn + sort_buf(P) + kWideGap);
   const uint32_t i0 = tid * kSortE;
   const bool active = i0 < P;
   uint64_t kk[kSortE];
@@ -554,10 +552,8 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   // 8 x 4,095; discordant pairs 28 inside its 8 entries and at most 8 w at
   // merge level w, 8 x (8 + 16 + ... + 2,048) over the levels
   uint32_t inv = 0, t_x = 0, t_xy = 0, t_y = 0;
-  Y* src = NARROW ? reinterpret_cast<Y*>(s_dyn) : reinterpret_cast<Y*>(s_dyn + sort_buf(P));
+  Y* src = NARROW ? reinterpret_cast<Y*>(s_dyn) : reinterpret_cast<Y*>(s_dyn + sort_buf(P) + kWideGap);
   Y* dst = NARROW ? reinterpret_cast<Y*>(s_dyn) + sort_buf(P) + kMergeGap : reinterpret_cast<Y*>(s_dyn);
-  // the packed form's merge buffers hold entry q at q + q / 8, the wide form's at q
-  auto mpos = [](uint32_t q) -> uint32_t { return NARROW ? mp_pad(q) : q; };
   // pairs tied in x, and in x and y: each entry counts the earlier entries of
   // its run; a run starts where the key differs from the one before, and a
   // max-scan of those starts gives every entry the start of its run
@@ -606,12 +602,8 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
       sort_min_max(yv[1], yv[2]);
       sort_min_max(yv[3], yv[4]);
       sort_min_max(yv[5], yv[6]);
-      if constexpr (NARROW) {
 #pragma unroll
-        for (uint32_t e = 0; e < kSortE; ++e) src[mp_pad(i0) + e] = yv[e];
-      } else {
-        store8(src + i0, yv);
-      }
+      for (uint32_t e = 0; e < kSortE; ++e) src[mp_pad(i0) + e] = yv[e];
     }
     block_max_scan(sx, s_part, tid);
     block_max_scan(sxy, s_part, tid);
@@ -640,7 +632,7 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
       uint32_t lo = d > w ? d - w : 0u, hi = d < w ? d : w;
       while (lo < hi) {
         const uint32_t mid = (lo + hi) >> 1;
-        if (src[mpos(b0 + mid)] <= src[mpos(b0 + w + d - 1 - mid)]) lo = mid + 1;
+        if (src[mp_pad(b0 + mid)] <= src[mp_pad(b0 + w + d - 1 - mid)]) lo = mid + 1;
         else hi = mid;
       }
       // Each step takes the smaller head (A's on equal values) and reloads
@@ -649,7 +641,7 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
       // read but never taken.
       uint32_t xa = b0 + lo, xb = b0 + w + (d - lo);
       uint32_t na = w - lo, nb = w - (d - lo), waiting = 0;
-      Y a = src[mpos(xa)], b = src[mpos(xb)];
+      Y a = src[mp_pad(xa)], b = src[mp_pad(xb)];
       Y out[kSortE];
 #pragma unroll
       for (uint32_t e = 0; e < kSortE; ++e) {
@@ -660,16 +652,12 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
         nb -= take_a ? 0u : 1u;
         xa += take_a ? 1u : 0u;
         xb += take_a ? 0u : 1u;
-        const Y v = src[mpos(take_a ? xa : xb)];
+        const Y v = src[mp_pad(take_a ? xa : xb)];
         a = take_a ? v : a;
         b = take_a ? b : v;
       }
-      if constexpr (NARROW) {
 #pragma unroll
-        for (uint32_t e = 0; e < kSortE; ++e) dst[mp_pad(i0) + e] = out[e];
-      } else {
-        store8(dst + i0, out);
-      }
+      for (uint32_t e = 0; e < kSortE; ++e) dst[mp_pad(i0) + e] = out[e];
       inv += waiting;
     }
     level_sync(w, P);
@@ -681,12 +669,12 @@ __device__ __forceinline__ void sorted_counts(const uint32_t (&kx)[kSortE],
   // sorted y (real entries hold positions [0, n): the padding sorts last)
   {
     uint32_t sy[kSortE];
-    Y py = i0 > 0 && i0 < P ? src[mpos(i0 - 1)] : (Y)0;
+    Y py = i0 > 0 && i0 < P ? src[mp_pad(i0 - 1)] : (Y)0;
 #pragma unroll
     for (uint32_t e = 0; e < kSortE; ++e) {
       const uint32_t i = i0 + e;
       const bool ok = i < P;
-      const Y yk = ok ? src[mpos(i)] : (Y)0;
+      const Y yk = ok ? src[mp_pad(i)] : (Y)0;
       sy[e] = ok && (i == 0 || yk != py) ? i : 0u;
       py = yk;
     }
@@ -717,7 +705,7 @@ __global__ __launch_bounds__(kSortBlock, NARROW ? 8 : 4) void kendall_sort_kerne
                                                                   const uint32_t* idx,
                                                                   uint64_t* counts, uint8_t* top1) {
   // one (NARROW, and 2 kMergeGap 4-byte words) or two buffers of P + P/8
-  // 8-byte entries: 36 or 72 KiB at 4,096 entries
+  // 8-byte entries (and 2 kWideGap entries): 36 or 72 KiB at 4,096 entries
   extern __shared__ __attribute__((aligned(16))) uint64_t s_dyn[];
   __shared__ uint64_t s_sum[4][kSortBlock / 64];
   __shared__ float s_bx[kSortBlock / 64];
@@ -872,7 +860,8 @@ hipError_t launch_kendall(uint32_t n_snap, uint32_t n_per, uint64_t n_x, const f
     hipLaunchKernelGGL(kendall_sort_kernel<true>, dim3(n_snap), dim3(kSortBlock),
                        lds + 2 * kMergeGap * sizeof(uint32_t), s, n_per, P,
                        n_x, x, y, idx, counts, top1);
-    hipLaunchKernelGGL(kendall_sort_kernel<false>, dim3(n_snap), dim3(kSortBlock), 2 * lds, s, n_per,
+    hipLaunchKernelGGL(kendall_sort_kernel<false>, dim3(n_snap), dim3(kSortBlock),
+                       2 * lds + 2 * kWideGap * sizeof(uint64_t), s, n_per,
                        P, n_x, x, y, idx, counts, top1);
   }
   return hipGetLastError();

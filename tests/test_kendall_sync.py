@@ -17,8 +17,8 @@ keys are 8-byte entries of the first buffer (A), at padded positions.  In the
 narrow form (4-byte y values) the merge sort then runs in A, its two buffers
 of P padded values 16 words apart; in the wide form the 4-byte tie-breakers
 live in a second buffer (B), where the merge sort of the 8-byte y values
-starts, and those merge buffers are not padded.  Accesses are modelled as the
-4-byte words they touch, so the aliasing between those uses is exact.  A merge step also
+starts.  Every merge buffer is padded.  Accesses are modelled as the 4-byte
+words they touch, so the aliasing between those uses is exact.  A merge step also
 reads one entry past a run whose entries are all taken, a value it never
 uses; that read lands in the gap or a buffer's unused tail, never on a buffer
 being written (checked by a host model of the step), and is not modelled."""
@@ -61,18 +61,16 @@ MERGE_GAP = 16
 
 def merge_buffers(P, ysize):
     """(first source, first destination) of the merge levels, each as (LDS
-    buffer, first entry, padded): entry q of buffer b lies at
-    merge_words(b, q, ysize)."""
-    if ysize == 4:   # both in A, padded, a gap between them
-        return ("A", 0, True), ("A", P + P // 8 + MERGE_GAP, True)
-    return ("B", 0, False), ("A", 0, False)
+    buffer, first entry): entry q of buffer b lies at merge_words(b, q, ysize)."""
+    if ysize == 4:   # both in A, a gap between them
+        return ("A", 0), ("A", P + P // 8 + MERGE_GAP)
+    return ("B", 0), ("A", 0)
 
 
 def merge_words(buf, q, ysize):
-    name, shift, padded = buf
+    name, shift = buf
     w = ysize // 4
-    at = mp_pad(q) if padded else q
-    return [(name, (shift + at) * w + k) for k in range(w)]
+    return [(name, (shift + mp_pad(q)) * w + k) for k in range(w)]
 
 
 def bitonic_steps(P, ysize=8):
