@@ -114,6 +114,34 @@ def test_kendall_ranking_snapshots(U, rs):
     assert np.array_equal(t[sample], ot)
 
 
+def test_kendall_ranking_snapshots_in_the_wide_form(U, rs):
+    """The same snapshots with every fixed-point score other than 2^64 - 1
+    shifted up 33 bits: order and ties are unchanged, so are tau-b's counts
+    and the top-1 flags, but no snapshot packs into one 64-bit key.  Every
+    snapshot must match the packed form's result, and a sample the oracle."""
+    d, n = oracle.hazard_counts(rs.lut_pop)
+    g, gq = oracle.ema_replay(rs.gaps_ns, rs.n_hist)
+    x = oracle.score_f32(rs.turn, g, rs.done, d, n, 5e8)
+    y = oracle.score_fixed(rs.turn, gq, rs.done, d, n, 12, 500_000_000).astype(np.uint64)
+    top = np.uint64(2 ** 64 - 1)
+    assert int(y[y != top].max()) < 2 ** 31
+    yw = np.where(y == top, top, y << np.uint64(33)).astype(np.uint64)
+    ys = yw[rs.idx]
+    assert np.all(((ys != top) & (ys >= np.uint64(2 ** 32))).any(axis=1)), "a snapshot would pack"
+    say("kendall, wide form: %d snapshots x %d" % (rs.n_snap, rs.n_per))
+    idx = dev(U, rs.idx, np.uint32)
+    cn, tn = U.kendall(dev(U, x), dev(U, y, np.uint64), idx)
+    cw, tw = U.kendall(dev(U, x), dev(U, yw, np.uint64), idx)
+    cw = U._host(cw, np.uint64)
+    tw = tw.cpu().numpy()
+    assert np.array_equal(cw, U._host(cn, np.uint64))
+    assert np.array_equal(tw, tn.cpu().numpy())
+    sample = np.arange(3, rs.n_snap, rs.n_snap // 12)
+    oc, ot = oracle.kendall(x, yw, idx=rs.idx[sample])
+    assert np.array_equal(cw[sample], oc)
+    assert np.array_equal(tw[sample], ot)
+
+
 @pytest.mark.parametrize("n_per", [256, 257, 1000, 2048, 4095, 4096])
 def test_kendall_sorted_path_heavy_ties(U, n_per):
     """From 256 entries the counts come from sorting: few distinct values, the
