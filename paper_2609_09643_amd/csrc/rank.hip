@@ -456,7 +456,6 @@ constexpr uint32_t kMergeGap = 16;
 // first ends, and kWideGap entries follow it, for the same reads.
 constexpr uint32_t kWideGap = 8;
 
-
 // Knight's counts of one snapshot from its gathered entries (thread t holds
 // entries 8t ... 8t+7; x as order-preserving u32 keys): the bitonic sort by
 // (x, y), the ties in x and in both from the sorted runs, the inversions of y
@@ -697,13 +696,14 @@ constexpr uint8_t kWideMark = 254;
 
 // NARROW: every snapshot whose y values pack (see sorted_counts) is counted
 // here with half the LDS, so four snapshots share a CU; the others are left
-// marked in top1.  Otherwise only the marked snapshots are counted.
+// marked in top1.  Otherwise only the marked snapshots are counted.  The
+// packed form asks for eight wavefronts per SIMD (at most 64 VGPRs), so that
+// four of its blocks fit a CU as its LDS allows.
 template <bool NARROW>
-__global__ __launch_bounds__(kSortBlock, NARROW ? 8 : 4) void kendall_sort_kernel(uint32_t n_per, uint32_t P,
-                                                                  uint64_t n_x, const float* x,
-                                                                  const uint64_t* y,
-                                                                  const uint32_t* idx,
-                                                                  uint64_t* counts, uint8_t* top1) {
+__global__ __launch_bounds__(kSortBlock, NARROW ? 8 : 4)
+void kendall_sort_kernel(uint32_t n_per, uint32_t P, uint64_t n_x, const float* x,
+                         const uint64_t* y, const uint32_t* idx, uint64_t* counts,
+                         uint8_t* top1) {
   // one (NARROW, and 2 kMergeGap 4-byte words) or two buffers of P + P/8
   // 8-byte entries (and 2 kWideGap entries): 36 or 72 KiB at 4,096 entries
   extern __shared__ __attribute__((aligned(16))) uint64_t s_dyn[];
