@@ -18,10 +18,10 @@ narrow form (4-byte y values) the merge sort then runs in A, its two buffers
 of P padded values 16 words apart; in the wide form the 4-byte tie-breakers
 live in a second buffer (B), where the merge sort of the 8-byte y values
 starts.  Every merge buffer is padded.  Accesses are modelled as the 4-byte
-words they touch, so the aliasing between those uses is exact.  A merge step also
-reads one entry past a run whose entries are all taken, a value it never
-uses; that read lands in the gap or a buffer's unused tail, never on a buffer
-being written (checked by a host model of the step), and is not modelled."""
+words they touch, so the aliasing between those uses is exact.  A merge
+step also reads one entry past a run whose entries are all taken, a value it
+never uses; that read lands in a gap after a buffer, never on a buffer being
+written (test_kendall_merge_model.py replays the step), and is not modelled."""
 import os
 
 import pytest
