@@ -68,29 +68,30 @@ __device__ __forceinline__ bool min_better(uint64_t ka, uint32_t sa, uint64_t kb
 __device__ __forceinline__ Cand cand_none_max() { return Cand{0ull, kNone}; }
 __device__ __forceinline__ Cand cand_none_min() { return Cand{~0ull, kNone}; }
 
+// Max (MAX) or min of a 32-bit value over each aligned group of W lanes;
+// every lane of the group ends with it.
 template <int W, int M, bool MAX>
-__device__ __forceinline__ void reduce_step(Cand& c) {
+__device__ __forceinline__ uint32_t group_ext32(uint32_t v) {
   if constexpr (M < W) {
-    const uint32_t klo = xchg<M>((uint32_t)c.key);
-    const uint32_t khi = xchg<M>((uint32_t)(c.key >> 32));
-    const uint32_t s = xchg<M>(c.sid);
-    const uint64_t k = ((uint64_t)khi << 32) | klo;
-    const bool take = MAX ? max_better(k, s, c.key, c.sid) : min_better(k, s, c.key, c.sid);
-    c.key = take ? k : c.key;
-    c.sid = take ? s : c.sid;
-    reduce_step<W, M * 2, MAX>(c);
+    const uint32_t o = xchg<M>(v);
+    return group_ext32<W, M * 2, MAX>(MAX ? (o > v ? o : v) : (o < v ? o : v));
+  } else {
+    return v;
   }
 }
 
-template <int W, int M, bool MAX>
-__device__ __forceinline__ uint64_t reduce_packed(uint64_t c) {
-  if constexpr (M < W) {
-    const uint64_t o = ((uint64_t)xchg<M>((uint32_t)(c >> 32)) << 32) | xchg<M>((uint32_t)c);
-    c = (MAX ? o > c : o < c) ? o : c;
-    return reduce_packed<W, M * 2, MAX>(c);
-  } else {
-    return c;
-  }
+// Max (MAX) or min of a packed 64-bit value over each aligned group of W
+// lanes, as two 32-bit words, most significant first: the group's best high
+// word, then the best low word among the lanes that hold it (the others enter
+// the empty value).  Each word's step is one max or min with a lane permute,
+// which the compiler folds into one DPP instruction, where a 64-bit step
+// needs two permutes, a compare and two selects.
+template <int W, bool MAX>
+__device__ __forceinline__ uint64_t reduce_words(uint64_t c) {
+  const uint32_t hi = (uint32_t)(c >> 32);
+  const uint32_t h = group_ext32<W, 1, MAX>(hi);
+  const uint32_t lo = hi == h ? (uint32_t)c : (MAX ? 0u : ~0u);
+  return ((uint64_t)h << 32) | group_ext32<W, 1, MAX>(lo);
 }
 
 template <int W, int M>
@@ -104,11 +105,18 @@ __device__ __forceinline__ uint32_t reduce_min32(uint32_t c) {
 }
 
 // Every lane of an aligned group of W lanes ends with the winner (ties to
-// the smaller session id).
+// the smaller session id): the key's two words, most significant first, then
+// the smallest id among the lanes still tied, each over the lanes that hold
+// the best word so far (the others enter the empty value).
 template <int W, bool MAX>
 __device__ __forceinline__ Cand reduce_group(Cand c) {
-  reduce_step<W, 1, MAX>(c);
-  return c;
+  const uint32_t empty = MAX ? 0u : ~0u;
+  const uint32_t khi = (uint32_t)(c.key >> 32), klo = (uint32_t)c.key;
+  const uint32_t h = group_ext32<W, 1, MAX>(khi);
+  const bool tied = khi == h;
+  const uint32_t l = group_ext32<W, 1, MAX>(tied ? klo : empty);
+  const uint32_t s = group_ext32<W, 1, false>(tied && klo == l ? c.sid : ~0u);
+  return Cand{((uint64_t)h << 32) | l, s};
 }
 
 // Whole-wavefront max (MAX) or min of a 32-bit value, uniform: a DPP
@@ -676,7 +684,7 @@ struct RegTable {
       const uint64_t p = pk[j] | (MAX ? (0xFFFFFFFFu - s) : s);
       c = ok && (MAX ? p > c : p < c) ? p : c;
     }
-    c = reduce_packed<G, 1, MAX>(c);
+    c = reduce_words<G, MAX>(c);
     const bool none = MAX ? c == 0ull : c == ~0ull;
     const uint32_t lo = (uint32_t)c;
     return Cand{c >> 32, none ? kNone : (MAX ? 0xFFFFFFFFu - lo : lo)};
@@ -699,7 +707,7 @@ struct RegTable {
       const uint64_t p = pk[j] | (MAX ? (0xFFFFFu - s) : s);
       c = ok && (MAX ? p > c : p < c) ? p : c;
     }
-    c = reduce_packed<G, 1, MAX>(c);
+    c = reduce_words<G, MAX>(c);
     const bool none = MAX ? c == 0ull : c == ~0ull;
     const uint32_t lo = (uint32_t)c & 0xFFFFFu;
     const uint64_t k44 = c >> 20;
